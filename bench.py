@@ -1,0 +1,224 @@
+#!/usr/bin/env python3
+"""Throughput of the LASER decode + confidence-probe hot path on one MI355X.
+
+One step = one chain-of-thought decode token for every request of the batch; every
+`probe_every` steps each request also runs the trial-answer probe (S=8 suffix tokens,
+T=4 trial tokens) and the host takes the load-aware exit decision on its confidence,
+as at an action transition point.  Inputs are synthetic and seeded: random-initialised
+weights of the named shape and pre-filled random KV (stand-ins for the paper's trained
+reasoners and their chains of thought, which are not available here).
+
+Prints one JSON line.  `value` is whole-job decode throughput (tokens/s) with the
+probes and exit decisions inside the timed region.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import math
+import os
+import sys
+import time
+
+HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, published
+PAGE = 16
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=256)
+    ap.add_argument("--warmup", type=int, default=16)
+    ap.add_argument("--workload", default="7B-b1-kv14336")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--profile-only", action="store_true", help="decode loop only (for rocprofv3 runs)")
+    return ap.parse_args()
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU: this build has no multi-GPU path (asked for --gpus {args.gpus})",
+              file=sys.stderr)
+        sys.exit(2)
+    import numpy as np
+    import torch
+
+    from paper_2606_31580_amd import laser as L
+    from paper_2606_31580_amd import synth
+    from paper_2606_31580_amd.configs import WORKLOADS
+
+    wl = WORKLOADS[args.workload]
+    shape = wl.shape
+    dev = torch.device("cuda:0")
+    B = wl.batch
+    S, T = wl.suffix_len, wl.trial_len
+    lens = list(wl.kv_lens) if wl.kv_lens else synth.make_ragged_lengths(B, 3000, 14000)
+    total_steps = args.warmup + args.steps
+    max_pos = max(lens) + 2 * total_steps + S + T + 2 * PAGE
+    max_pos = min(65536, (max_pos + 255) // 256 * 256)
+
+    def log(msg):
+        print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+    log(f"workload {wl.name}: generating weights")
+    weights = synth.make_weights(shape, device=dev)
+    model = L.Model(shape, weights, max_rows=max(B, B * S), max_positions=max_pos)
+    pps = max_pos // PAGE + 1
+    num_pages = sum((n + 2 * total_steps + S + T) // PAGE + 2 for n in lens) + 8
+    kv = L.KVCache(model, num_pages, B, pps)
+    for i, n in enumerate(lens):
+        k0, v0 = synth.make_prefill_kv(shape, n, i, device=dev)
+        kv.add_seq(i, n)
+        kv.import_kv(i, k0, v0)
+        del k0, v0
+    torch.cuda.synchronize()
+    seqs = list(range(B))
+    tokens = synth.make_tokens(B, shape.vocab, 3003).to(dev)
+    nxt = torch.empty(B, dtype=torch.int32, device=dev)
+    pmax = torch.empty(B, device=dev)
+    suffix = synth.make_suffix(S, shape.vocab).to(dev)
+    conf = torch.empty(B, device=dev)
+    argm = torch.empty(B * T, dtype=torch.int32, device=dev)
+    params = L.laser_params_default()
+    load_state = L.laser_load_state(0.0)
+    stream = torch.cuda.current_stream()
+
+    probe_ms = []
+
+    def step(i, timed_probe):
+        L.laser_decode_step(model, kv, seqs, tokens, nxt, pmax)
+        tokens.copy_(nxt)
+        if wl.probe_every and (i + 1) % wl.probe_every == 0:
+            t0 = time.perf_counter()
+            L.laser_probe_confidence(model, kv, seqs, suffix, T, conf, argm)
+            c = conf.cpu().numpy()  # the controller needs the confidence on the host
+            for b in range(B):
+                L.laser_exit_decision(params, load_state, float(c[b]), B, 0, 10)
+            if timed_probe:
+                probe_ms.append((time.perf_counter() - t0) * 1e3)
+
+    log("warmup")
+    for i in range(args.warmup):
+        step(i, False)
+    torch.cuda.synchronize()
+
+    if args.profile_only:
+        for i in range(args.steps):
+            L.laser_decode_step(model, kv, seqs, tokens, nxt, pmax)
+            tokens.copy_(nxt)
+        torch.cuda.synchronize()
+        log("profile loop done")
+        return
+
+    # ---- whole job: decode + probes + host exit decisions
+    model.timing_enable(L.K_GATEUP, True)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record(stream)
+    w0 = time.perf_counter()
+    for i in range(args.steps):
+        step(args.warmup + i, True)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - w0
+    ms_total = e0.elapsed_time(e1)
+    gu_ms, gu_n = model.timing_read(L.K_GATEUP)
+    model.timing_enable(L.K_GATEUP, False)
+    ms_per_step = ms_total / args.steps
+    value = args.steps * B / (ms_total / 1e3)
+    log(f"timed {args.steps} steps: {ms_per_step:.3f} ms/step, {value:.1f} tok/s (wall {wall:.2f}s)")
+
+    # ---- decode only (same cache, no probes)
+    n_dec = min(args.steps, 128)
+    torch.cuda.synchronize()
+    e0.record(stream)
+    for i in range(n_dec):
+        L.laser_decode_step(model, kv, seqs, tokens, nxt, pmax)
+        tokens.copy_(nxt)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    dec_ms = e0.elapsed_time(e1) / n_dec
+
+    # ---- algorithmic bytes
+    es = 2 if shape.dtype == "bf16" else 4
+    ctx = [kv.seq_len(i) for i in seqs]
+    kv_tok = shape.kv_bytes_per_token()
+    step_bytes = shape.weight_bytes() + sum(ctx) * kv_tok + B * kv_tok
+    step_gbs = step_bytes / (dec_ms / 1e3) / 1e9
+    gu_bytes = 2 * shape.d_ffn * shape.d_model * es + B * shape.d_model * 4 + B * shape.d_ffn * 4
+    gu_avg_ms = gu_ms / max(gu_n, 1)
+    gu_gbs = gu_bytes / (gu_avg_ms / 1e3) / 1e9
+
+    traffic = None
+    tf = os.path.join(os.path.dirname(os.path.abspath(__file__)), "profiles", "gateup_traffic.json")
+    src = os.path.join(os.path.dirname(os.path.abspath(__file__)), "paper_2606_31580_amd", "csrc", "gemm.hip")
+    if os.path.exists(tf):
+        rec = json.load(open(tf))
+        cur = hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
+        if rec.get("gemm_hip_sha256_16") == cur and rec.get("workload") == wl.name:
+            traffic = rec.get("bytes_per_launch")
+
+    out = {
+        "metric": "decode tok/s + probe latency, achieved HBM GB/s vs peak, 1 GPU",
+        "value": round(value, 2),
+        "unit": "tok/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16 weights+KV, fp32 activations" if shape.dtype == "bf16" else "f32",
+        "data": "synthetic: random-init weights, seeded pre-filled KV",
+        "config": {"workload": wl.name, "model_shape": shape.name, "batch": B, "kv_lens": lens,
+                   "probe_every": wl.probe_every, "suffix": S, "trials": T},
+        "decode_only_ms_per_step": round(dec_ms, 4),
+        "decode_only_tok_s": round(B / (dec_ms / 1e3), 2),
+        "probe_latency_ms": {"mean": round(float(np.mean(probe_ms)), 3) if probe_ms else None,
+                             "max": round(float(np.max(probe_ms)), 3) if probe_ms else None, "n": len(probe_ms)},
+        "step_hbm": {"bytes": step_bytes, "achieved_GBs": round(step_gbs, 1), "frac_of_peak": round(step_gbs / HBM_PEAK_GBS, 4)},
+        "roofline": {"kernel": "gate/up projection + SwiGLU (k_gemm, EPI_SWIGLU)", "bound": "hbm",
+                     "achieved": round(gu_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(gu_gbs / HBM_PEAK_GBS, 4), "traffic": traffic,
+                     "avg_launch_us": round(gu_avg_ms * 1e3, 2), "launches": gu_n, "bytes_per_launch": gu_bytes},
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(shape, weights, kv, lens, model, dev, log)
+    print(json.dumps(out), flush=True)
+
+
+def cpu_baseline(shape, weights, kv, lens, model, dev, log):
+    """The oracle, as written, timed on this host for one decode token of request 0."""
+    import numpy as np
+    import torch
+    from threadpoolctl import threadpool_info
+
+    from oracle.transformer import DecoderOracle, SeqState
+    from paper_2606_31580_amd import synth
+
+    log("cpu baseline: copying weights and the request's KV to the host")
+    host = {k: synth.to_numpy(v) for k, v in weights.items()}
+    n = kv.seq_len(0)
+    dt = torch.bfloat16 if shape.dtype == "bf16" else torch.float32
+    K = torch.empty((shape.n_layers, n, shape.n_kv_heads, shape.head_dim), dtype=dt, device=dev)
+    V = torch.empty_like(K)
+    kv.export_kv(0, K, V)
+    torch.cuda.synchronize()
+    st = SeqState.from_prefill(shape, synth.to_numpy(K), synth.to_numpy(V), n + 1)
+    del K, V
+    orc = DecoderOracle(shape, host)
+    tok = int(synth.make_tokens(1, shape.vocab, 3004)[0])
+    log("cpu baseline: one oracle decode token")
+    t0 = time.perf_counter()
+    orc.decode_token(st, tok)
+    sec = time.perf_counter() - t0
+    threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    return {"value": round(1.0 / sec, 5), "unit": "tok/s", "cores": threads, "kind": "oracle",
+            "sample": f"1 decode token of request 0 at context {n} (float64 numpy, {sec:.1f} s)"}
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,265 @@
+/*
+ * laser.h -- C ABI of liblaser.so, the MI355X (gfx950) decode + confidence-probe
+ * hot path of LASER (load-aware early exit for reasoning LLMs).
+ *
+ * The paper (Section 3.1, Eq. 1-2) splits a reasoning request into chain-of-thought
+ * chunks separated by action transition points (ATPs).  Generating the chunks is a
+ * token-by-token decode; at each ATP an answer-inducing suffix makes the model emit a
+ * trial answer whose confidence, computed from the token probabilities, is compared
+ * with a threshold.  LASER's contribution (Section 4) is to make that threshold and a
+ * per-request budget depend on the serving load.  This library provides:
+ *
+ *   laser_decode_step        one greedy decode token per request over a paged KV cache
+ *   laser_probe_confidence   the trial-answer probe, returning confidence and argmax ids
+ *   laser_step_mixed         decode for a batch plus probe chunks for a subset, one forward
+ *   laser_exit_decision      the host-side ATP decision (Eq. 5 threshold, Algorithm 1)
+ *   laser_budget             the budget pre-allocation of Eq. 6-8
+ *
+ * Conventions for every function:
+ *   - The return value is a laser_status; LASER_OK (0) on success, a negative code on
+ *     failure.  No C++ exception, abort or exit crosses the ABI.  After a failure,
+ *     laser_last_error() returns a message for the calling thread.
+ *   - Arguments are validated before anything is mutated: a failing call leaves every
+ *     handle, page table and device buffer as it was.
+ *   - Pointers named d_* are device pointers on the model's GPU; every other pointer
+ *     is host memory.  All device memory (weights, workspace, KV pools, block table,
+ *     outputs) is allocated by the caller and only borrowed: the library never frees
+ *     caller memory.  Handles are owned by the caller through create/destroy.
+ *   - `stream` is a hipStream_t passed as void* (NULL = the default stream).  Device
+ *     work is asynchronous on that stream; outputs are valid after the stream is
+ *     synchronised.  Host bookkeeping (lengths, page tables) is updated before the call
+ *     returns.
+ *   - Calls on one model or KV handle must not overlap (no internal locking).
+ */
+#ifndef LASER_H
+#define LASER_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define LASER_ABI_VERSION 1
+
+typedef enum {
+  LASER_OK = 0,
+  LASER_ERR_INVALID_ARG = -1,   /* NULL/out-of-range argument, unknown name, wrong size */
+  LASER_ERR_OUT_OF_PAGES = -2,  /* page pool cannot satisfy an allocation (nothing changed) */
+  LASER_ERR_HIP = -3,           /* a HIP runtime call failed; message from hipGetErrorString */
+  LASER_ERR_UNSUPPORTED = -4,   /* shape or size outside what the kernels handle */
+  LASER_ERR_STATE = -5          /* call out of order (e.g. before finalize, destroyed handle) */
+} laser_status;
+
+typedef enum { LASER_DTYPE_F32 = 0, LASER_DTYPE_BF16 = 1 } laser_dtype;
+
+/* Message of the last failing call on this thread ("" if none).  Owned by the library. */
+const char* laser_last_error(void);
+int laser_abi_version(void);
+
+/* ========================================================================== */
+/* Host controller (Section 4).  Pure host arithmetic, no device access.       */
+/* ========================================================================== */
+
+/* Hyper-parameters.  Defaults (laser_params_default) are the paper's: Section 5.1
+ * (lambda_base .95, L_target 10, beta .04, gamma 1, alpha .3, B_base 10, lambda_min .88,
+ * lambda_max .97, B_min 2) and Section 4.3 (f_min .6, f_max 1.5, p_min 50, p_max 275). */
+typedef struct {
+  double lambda_base, beta, gamma, alpha, L_target, lambda_min, lambda_max;
+  int B_base, B_min;
+  double f_min, f_max;
+  int p_min, p_max;
+} laser_params;
+
+/* The one scalar of controller state (Section 4.4): the EMA-smoothed load L_bar,
+ * initialised to 0 (Algorithm 1). */
+typedef struct {
+  double L_bar;
+} laser_load_state;
+
+enum { LASER_CONTINUE = 0, LASER_EARLY_EXIT = 1, LASER_BUDGET_EXHAUSTED = 2 };
+
+void laser_params_default(laser_params* p);
+
+/* EMA update of Section 4.2: L_bar <- alpha * active_requests + (1 - alpha) * L_bar.
+ * Errors: INVALID_ARG for NULL pointers, active_requests < 0 or alpha outside [0,1]. */
+laser_status laser_ema_update(const laser_params* p, laser_load_state* state, int active_requests);
+
+/* Eq. 5: lambda = lambda_base - beta * tanh(gamma * (L_bar - L_target) / L_target),
+ * clamped to [lambda_min, lambda_max].  Errors: INVALID_ARG for NULL, L_target <= 0 or
+ * lambda_min > lambda_max. */
+laser_status laser_threshold(const laser_params* p, double L_bar, double* lambda_out);
+
+/* Eq. 6-8: B = max(B_min, floor(B_base * f_diff(prompt_len) * f_load(active_requests))),
+ * f_diff = clip(f_min + (prompt_len - p_min)/(p_max - p_min) * (f_max - f_min), f_min, f_max),
+ * f_load = min(1, L_target / max(1, active_requests)).  The floor is of the exact value:
+ * the product is formed in double precision and floored with a 1e-9 guard against
+ * representation error of the decimal parameters.  Errors: INVALID_ARG for NULL,
+ * prompt_len < 0, active_requests < 0, p_max <= p_min, B_min < 1. */
+laser_status laser_budget(const laser_params* p, int prompt_len, int active_requests, int* B_out);
+
+/* The decision after the probe at ATP k_done+1 of a request with budget B_i
+ * (Algorithm 1 loop body): update L_bar with active_requests (the EMA above), compute
+ * lambda (Eq. 5), then EARLY_EXIT if confidence > lambda (strict, Section 3.1);
+ * otherwise the failed-probe count becomes k_done+1 and the decision is
+ * BUDGET_EXHAUSTED if that reaches B_i (force the conclusion), else CONTINUE.
+ * lambda_out may be NULL.  Errors: INVALID_ARG for NULL state/decision_out, k_done < 0,
+ * k_done >= B_i, or a NaN confidence; the state is not updated on error. */
+laser_status laser_exit_decision(const laser_params* p, laser_load_state* state, float confidence,
+                                 int active_requests, int k_done, int B_i, int* decision_out,
+                                 double* lambda_out);
+
+/* ========================================================================== */
+/* Page pool: host bookkeeping of the paged KV cache.                          */
+/* ========================================================================== */
+/* The paper serves from a vLLM-style engine (Section 4.2) without stating a paging
+ * policy.  This pool hands out fixed-size pages by lowest free id; a page is taken when
+ * a token lands at a length that is a multiple of page_size; a sequence added with a
+ * length takes its pages in ascending id order; truncation returns the pages beyond the
+ * kept length.  Every allocation is all-or-nothing (OUT_OF_PAGES leaves the pool as it
+ * was).  Sequence ids are 0 <= seq_id < max_seqs. */
+typedef struct laser_page_pool laser_page_pool;
+
+laser_status laser_pages_create(int num_pages, int page_size, int max_seqs, int max_pages_per_seq,
+                                laser_page_pool** out);
+laser_status laser_pages_add_seq(laser_page_pool* pool, int seq_id, int length);
+laser_status laser_pages_append(laser_page_pool* pool, int seq_id, int n_tokens);
+laser_status laser_pages_truncate(laser_page_pool* pool, int seq_id, int length);
+laser_status laser_pages_free_seq(laser_page_pool* pool, int seq_id);
+/* Copies the page ids of seq_id (in sequence order) to out[0..n-1]; *n_out = n.
+ * INVALID_ARG if cap < n. */
+laser_status laser_pages_table(const laser_page_pool* pool, int seq_id, int32_t* out, int cap, int* n_out);
+laser_status laser_pages_seq_len(const laser_page_pool* pool, int seq_id, int* len_out);
+laser_status laser_pages_num_free(const laser_page_pool* pool, int* n_out);
+laser_status laser_pages_destroy(laser_page_pool* pool);
+
+/* ========================================================================== */
+/* Model                                                                       */
+/* ========================================================================== */
+/* A Qwen2/Llama-style decoder: RMSNorm, grouped-query attention with rotary position
+ * embedding on half-split pairs (i, i + head_dim/2) at angle pos * rope_theta^(-2i/head_dim),
+ * SwiGLU MLP, final RMSNorm, LM head (the embedding when tied_embeddings).
+ * Supported: head_dim in {64, 128}; n_q_heads a multiple of n_kv_heads with
+ * G = n_q_heads/n_kv_heads <= 16; d_model a multiple of 64; d_ffn a multiple of 8;
+ * n_q_heads*head_dim a multiple of 64; dtype F32 or BF16 for every tensor and the KV
+ * cache; max_positions <= 65536. */
+typedef struct {
+  int n_layers, d_model, n_q_heads, n_kv_heads, head_dim, d_ffn, vocab;
+  int tied_embeddings, qkv_bias, dtype;
+  float rope_theta, rms_eps;
+  int max_positions;
+} laser_model_desc;
+
+typedef struct laser_model laser_model;
+
+/* Creates a host handle (no device memory).  Binds to the current HIP device. */
+laser_status laser_model_create(const laser_model_desc* desc, laser_model** out);
+
+/* Borrows a device tensor (row-major, dtype of the model) for the model's lifetime.
+ * Names: "embed" [vocab, d_model]; "lm_head" [vocab, d_model] (untied only);
+ * "final_norm" [d_model]; per layer i, "layers.i.attn_norm" [d], "layers.i.wq"
+ * [hq*hd, d], "layers.i.wk"/"layers.i.wv" [hkv*hd, d], "layers.i.bq" [hq*hd],
+ * "layers.i.bk"/"layers.i.bv" [hkv*hd] (qkv_bias only), "layers.i.wo" [d, hq*hd],
+ * "layers.i.mlp_norm" [d], "layers.i.w_gate"/"layers.i.w_up" [d_ffn, d],
+ * "layers.i.w_down" [d, d_ffn].  INVALID_ARG for an unknown name or a byte size that
+ * does not match; STATE after finalize. */
+laser_status laser_model_set_tensor(laser_model* m, const char* name, const void* d_ptr, size_t bytes);
+
+/* Bytes of device workspace the model needs for forwards of up to max_rows rows
+ * (tokens per forward: batch for decode, S*batch for a probe chunk; 1..64). */
+laser_status laser_workspace_size(const laser_model* m, int max_rows, size_t* bytes);
+
+/* Checks that every tensor is set, lays out the caller's workspace (>= the size above
+ * for max_rows) and fills its constant tables (RoPE cos/sin computed on the host in
+ * double precision) with asynchronous copies on `stream`.  The workspace must stay
+ * allocated until laser_model_destroy. */
+laser_status laser_model_finalize(laser_model* m, int max_rows, void* d_workspace, size_t bytes, void* stream);
+laser_status laser_model_destroy(laser_model* m);
+
+/* ========================================================================== */
+/* KV cache: device pools + page pool                                          */
+/* ========================================================================== */
+/* Device layout (owned by the caller, laid out by the library): K and V pools of
+ * n_layers x num_pages x n_kv_heads blocks; block (layer, page, kv_head) holds 16
+ * positions x head_dim values in the order the attention kernel's matrix-core
+ * operands read them: K element (t, d) at ((d/32*4 + (d%32)/8)*16 + t)*8 + d%8, V element
+ * (t, d) at ((d/16*4 + t/4)*16 + d%16)*4 + t%4 (t = position within the page).  The
+ * block table is int32 [max_seqs][max_pages_per_seq].  Page size is 16. */
+typedef struct laser_kv laser_kv;
+
+laser_status laser_kv_pool_bytes(const laser_model* m, int num_pages, size_t* bytes_per_pool);
+laser_status laser_kv_create(const laser_model* m, int num_pages, int max_seqs, int max_pages_per_seq,
+                             void* d_k_pool, void* d_v_pool, int32_t* d_block_table, laser_kv** out);
+/* Adds seq_id with `length` positions already present (pages allocated, contents
+ * undefined until imported).  OUT_OF_PAGES / INVALID_ARG leave the cache unchanged. */
+laser_status laser_kv_add_seq(laser_kv* kv, int seq_id, int length);
+/* Writes positions 0..length-1 of seq_id from d_k, d_v laid out [n_layers][length]
+ * [n_kv_heads][head_dim] (model dtype; keys already rotated).  length must equal the
+ * sequence's length. */
+laser_status laser_kv_import(laser_kv* kv, int seq_id, const void* d_k, const void* d_v, int length, void* stream);
+/* Inverse of import: gathers all positions of seq_id into [n_layers][len][hkv][hd]. */
+laser_status laser_kv_export(const laser_kv* kv, int seq_id, void* d_k, void* d_v, void* stream);
+laser_status laser_kv_free_seq(laser_kv* kv, int seq_id);
+laser_status laser_kv_seq_len(const laser_kv* kv, int seq_id, int* len_out);
+laser_status laser_kv_page_table(const laser_kv* kv, int seq_id, int32_t* out, int cap, int* n_out);
+laser_status laser_kv_destroy(laser_kv* kv);
+
+/* ========================================================================== */
+/* Hot path                                                                    */
+/* ========================================================================== */
+
+/* Runs n prompt tokens d_tokens[0..n-1] of seq_id at its current length (chunks of at
+ * most max_rows rows), appending their K/V.  d_logits_last (vocab floats or NULL)
+ * receives the last token's logits. */
+laser_status laser_prefill(laser_model* m, laser_kv* kv, int seq_id, const int32_t* d_tokens, int n,
+                           float* d_logits_last, void* stream);
+
+/* One chain-of-thought decode step (the reasoning-chunk generation of Eq. 2): request b
+ * (seq_ids[b], host array) runs token d_tokens[b] at position len(seq_ids[b]), appends its
+ * K/V (taking a page when the length is a multiple of 16) and gets the greedy next token
+ * d_next[b] (lowest index among equal maxima) and the maximum softmax probability
+ * d_max_prob[b] = 1 / sum_j exp(l_j - l_max).  d_logits ([batch][vocab] floats) may be
+ * NULL.  d_next may alias d_tokens.  1 <= batch <= max_rows; seq_ids distinct. */
+laser_status laser_decode_step(laser_model* m, laser_kv* kv, int batch, const int32_t* seq_ids,
+                               const int32_t* d_tokens, int32_t* d_next, float* d_max_prob, float* d_logits,
+                               void* stream);
+
+/* The trial-answer probe at an ATP (Section 3.1): for each request, the S suffix tokens
+ * d_suffix[0..S-1] run at positions L..L+S-1 (L = the request's length), the last one's
+ * distribution gives trial token t_1 and p_1, and each t_j (j < T) is fed back to give
+ * t_{j+1}, p_{j+1}.  d_conf[b] = (p_1 + ... + p_T) / T, d_argmax[b*T + j-1] = t_j, and
+ * d_logits ([batch][T][vocab] or NULL) the trial distributions' logits.  Afterwards every
+ * request's length, page table and cached K/V below its length are as before the call
+ * (the probe's pages are returned to the pool).  Requires S*batch <= max_rows. */
+laser_status laser_probe_confidence(laser_model* m, laser_kv* kv, int batch, const int32_t* seq_ids,
+                                    const int32_t* d_suffix, int S, int T, float* d_conf, int32_t* d_argmax,
+                                    float* d_logits, void* stream);
+
+/* Decode for every request of the batch plus, in the same forward, the probe chunk of
+ * the requests probe_idx[0..n_probe-1] (indices into the batch), taken at their length
+ * after this step's token; the T-1 trial tokens then run as further forwards.  Outputs
+ * as laser_decode_step (d_next, d_max_prob) and laser_probe_confidence (d_conf[i],
+ * d_argmax[i*T + j] for probe i).  Requires batch + S*n_probe <= max_rows. */
+laser_status laser_step_mixed(laser_model* m, laser_kv* kv, int batch, const int32_t* seq_ids,
+                              const int32_t* d_tokens, int32_t* d_next, float* d_max_prob, int n_probe,
+                              const int32_t* probe_idx, const int32_t* d_suffix, int S, int T, float* d_conf,
+                              int32_t* d_argmax, void* stream);
+
+/* ========================================================================== */
+/* Kernel timing (HIP events recorded around every launch of the enabled classes). */
+/* ========================================================================== */
+enum {
+  LASER_K_EMBED = 0, LASER_K_QKV = 1, LASER_K_ATTN = 2, LASER_K_OPROJ = 3,
+  LASER_K_GATEUP = 4, LASER_K_DOWN = 5, LASER_K_LMHEAD = 6, LASER_K_OTHER = 7, LASER_K_NCLASS = 8
+};
+/* Enables (1) or disables (0) event timing of one kernel class; clears its totals. */
+laser_status laser_timing_enable(laser_model* m, int kernel_class, int enable);
+/* Synchronises the recorded events and returns the summed duration (ms) and launch
+ * count of the class since it was enabled or last read, then clears them. */
+laser_status laser_timing_read(laser_model* m, int kernel_class, double* total_ms, int* launches);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* LASER_H */

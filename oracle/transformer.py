@@ -152,15 +152,23 @@ class DecoderOracle:
     defaults to the shape's storage dtype.
     """
 
-    def __init__(self, shape, weights: Mapping[str, np.ndarray], dtype=np.float64, kv_storage: Optional[str] = "auto"):
+    def __init__(self, shape, weights: Mapping[str, np.ndarray], dtype=np.float64, kv_storage: Optional[str] = "auto",
+                 cache_weights: bool = False):
         self.shape = shape
         self.weights = weights
         self.dtype = dtype
         if kv_storage == "auto":
             kv_storage = shape.dtype
         self.kv_storage = kv_storage
+        # cache_weights keeps each tensor's decoded value after first use (memory for speed)
+        self._cache = {} if cache_weights else None
 
     def W(self, name: str) -> np.ndarray:
+        if self._cache is not None:
+            w = self._cache.get(name)
+            if w is None:
+                w = self._cache[name] = as_float64(self.weights[name]).astype(self.dtype, copy=False)
+            return w
         return as_float64(self.weights[name]).astype(self.dtype, copy=False)
 
     def store_kv(self, x: np.ndarray) -> np.ndarray:

@@ -1,0 +1,73 @@
+// Device helpers shared by the gfx950 kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+namespace laser {
+
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
+typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8;
+typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4;
+typedef __attribute__((__vector_size__(4 * sizeof(short)))) short s16x4;
+
+struct bf16_t {
+  uint16_t bits;
+};
+
+__device__ __forceinline__ float bf2f(uint16_t b) { return __uint_as_float(((uint32_t)b) << 16); }
+
+// fp32 -> bf16 bits, round to nearest even (finite inputs).
+__device__ __forceinline__ uint16_t f2bf(float f) {
+  uint32_t u = __float_as_uint(f);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+
+// Split x into bf16 hi + bf16 lo (x - hi, rounded), so hi + lo carries ~16 significand bits.
+__device__ __forceinline__ void split_bf16(float x, uint16_t& hi, uint16_t& lo) {
+  hi = f2bf(x);
+  lo = f2bf(x - bf2f(hi));
+}
+
+__device__ __forceinline__ u32x4 ld_nt16(const void* p) { return __builtin_nontemporal_load((const u32x4*)p); }
+__device__ __forceinline__ u32x2 ld_nt8(const void* p) { return __builtin_nontemporal_load((const u32x2*)p); }
+
+__device__ __forceinline__ float wave_sum(float x) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) x += __shfl_xor(x, off);
+  return x;
+}
+
+// Value of element e of a stored tensor (fp32 or bf16 bits).
+template <class WT>
+__device__ __forceinline__ float ldw(const void* base, size_t e);
+template <>
+__device__ __forceinline__ float ldw<float>(const void* base, size_t e) {
+  return ((const float*)base)[e];
+}
+template <>
+__device__ __forceinline__ float ldw<bf16_t>(const void* base, size_t e) {
+  return bf2f(((const uint16_t*)base)[e]);
+}
+
+// Store a value in the storage type (bf16: round to nearest even).
+template <class WT>
+__device__ __forceinline__ void stw(void* base, size_t e, float v);
+template <>
+__device__ __forceinline__ void stw<float>(void* base, size_t e, float v) {
+  ((float*)base)[e] = v;
+}
+template <>
+__device__ __forceinline__ void stw<bf16_t>(void* base, size_t e, float v) {
+  ((uint16_t*)base)[e] = f2bf(v);
+}
+
+// Offsets of element (t, d) inside a KV page block (16 positions x hd), chosen so that the
+// attention kernel's matrix-core operand loads are contiguous per wave instruction.
+__device__ __forceinline__ int k_block_off(int t, int d) { return (((d >> 5) * 4 + ((d & 31) >> 3)) * 16 + t) * 8 + (d & 7); }
+__device__ __forceinline__ int v_block_off(int t, int d) { return (((d >> 4) * 4 + (t >> 2)) * 16 + (d & 15)) * 4 + (t & 3); }
+
+}  // namespace laser

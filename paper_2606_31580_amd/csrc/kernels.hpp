@@ -1,0 +1,120 @@
+// Internal interface between the host runtime and the gfx950 kernels of liblaser.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+namespace laser {
+
+constexpr int kMaxRows = 64;       // rows (tokens) of one forward
+constexpr int kPage = 16;          // positions per KV page
+constexpr int kMaxBt = 1024;       // block-table updates carried by one plan
+constexpr int kAttnWaves = 4;      // waves per attention workgroup (one split each)
+constexpr int kAttnMaxWG = 64;     // attention workgroups per (group, kv head)
+constexpr int kGemmThreads = 256;  // 4 waves; a GEMM unit covers 64 weight rows
+constexpr int kGroupRows = 64;
+
+// One row of a forward: request slot, position, and where its input token id lives.
+struct RowDesc {
+  int seq, pos, tok_sel, tok_off;  // token = tok_base[tok_sel][tok_off]
+};
+// Rows of one request that share its KV pages in attention (contiguous rows).
+struct GroupDesc {
+  int seq, row0, nrows, npages, pps, nwg;  // pps: pages per wave split; nwg: workgroups
+};
+// LM-head output row: activation row, destination (sel, off) for token / prob / logits.
+struct OutDesc {
+  int row, sel, off, pad;
+};
+struct BtUpdate {
+  int seq, idx, page;
+};
+
+// Everything the kernels of one forward need that changes per call; uploaded once.
+struct Plan {
+  int M, n_groups, n_out, n_bt;
+  RowDesc rows[kMaxRows];
+  GroupDesc groups[kMaxRows];
+  OutDesc outs[kMaxRows];
+  BtUpdate bt[kMaxBt];
+};
+
+struct LmPart {
+  float mx, sum;
+  int idx, pad;
+};
+
+enum Epi { EPI_QKV = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_LMHEAD = 3 };
+
+struct GemmArgs {
+  // weights (row-major [rows][K] in the model dtype)
+  const void* w0;
+  const void* w1;
+  const void* w2;
+  int K, N, n_groups, n_splits, kslice, M;
+  // A operand: fp32 activations [row][ldx]; optional RMSNorm (gain, ss partials)
+  const float* x;
+  int ldx;
+  const void* gain;
+  const float* ss;  // [n_ss][kMaxRows] sums of squares of x rows
+  int n_ss;
+  float eps;
+  int row_map;  // A row m = plan->outs[m].row (LM head)
+  const Plan* plan;
+  // split-K
+  float* part;
+  int* cnt;
+  // EPI_QKV
+  const void* b0;
+  const void* b1;
+  const void* b2;
+  int hq, hkv, hd;
+  const float2* rope;  // [max_positions][hd/2] (cos, sin)
+  float* q_out;        // [M][hq][hd]
+  void* kpool;
+  void* vpool;
+  const int* bt;
+  int max_pps, num_pages, layer;
+  // EPI_RESID
+  float* h;       // [M][N]
+  float* ss_out;  // [N/64][kMaxRows]
+  // EPI_SWIGLU
+  float* act;  // [M][F] (F = N/2 logical pairs)
+  int F;
+  // EPI_LMHEAD
+  float* logits[2];  // [..][vocab] or null
+  int* tok_out[2];
+  float* p_out[2];
+  LmPart* lm_part;  // [n_groups][kMaxRows]
+  int* lm_cnt;
+};
+
+struct AttnArgs {
+  const Plan* plan;
+  const float* q;  // [M][hq][hd]
+  float* o;        // [M][hq][hd]
+  const void* kpool;
+  const void* vpool;
+  const int* bt;
+  int max_pps, num_pages, layer;
+  int hq, hkv, G, max_rows;
+  float scale_log2;
+  float* part;  // [hkv][kAttnMaxWG][max_rows*G][hd]
+  float* ml;    // [hkv][kAttnMaxWG][max_rows*G][2]
+  int* cnt;     // [n_groups][hkv]
+};
+
+// dtype: 0 fp32, 1 bf16.  mode: 1..4 VALU rows per forward, 5..8 MFMA with 1..4 m-tiles.
+size_t gemm_lds_bytes(int dtype, int mode, int kslice, int M);
+hipError_t launch_gemm(int dtype, int mode, int epi, const GemmArgs& a, int grid, hipStream_t s);
+hipError_t launch_attn(int dtype, int hd, int nt, const AttnArgs& a, dim3 grid, hipStream_t s);
+hipError_t launch_embed(int dtype, const Plan* plan, int M, const void* embed, int d, int vocab, const int* tok0,
+                        const int* tok1, float* h, float* ss, int* bt, int max_pps, hipStream_t s);
+hipError_t launch_apply_bt(const Plan* plan, int* bt, int max_pps, hipStream_t s);
+hipError_t launch_kv_copy(int dtype, int to_pool, void* kpool, void* vpool, const int* bt, int max_pps,
+                          int num_pages, int n_layers, int hkv, int hd, int seq, int len, void* k_lin,
+                          void* v_lin, hipStream_t s);
+hipError_t launch_confidence(const float* p, int T, int n, float* conf, hipStream_t s);
+
+}  // namespace laser

@@ -1,0 +1,974 @@
+// Host runtime of liblaser: model / KV handles, workspace layout, forward planning and the
+// hot-path entry points (decode step, confidence probe, mixed step, prefill).
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <mutex>
+#include <new>
+#include <string>
+#include <unordered_set>
+#include <vector>
+
+#include "kernels.hpp"
+#include "laser.h"
+#include "laser_error.h"
+#include "pages.hpp"
+
+using namespace laser;
+
+// ----------------------------------------------------------------------------- errors
+
+static thread_local char g_err[512];
+
+extern "C" laser_status laser_fail(laser_status code, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_err, sizeof(g_err), fmt, ap);
+  va_end(ap);
+  return code;
+}
+extern "C" void laser_clear_error(void) { g_err[0] = 0; }
+extern "C" const char* laser_last_error(void) { return g_err; }
+extern "C" int laser_abi_version(void) { return LASER_ABI_VERSION; }
+
+#define HIP_TRY(expr)                                                                       \
+  do {                                                                                      \
+    hipError_t e_ = (expr);                                                                 \
+    if (e_ != hipSuccess) return laser_fail(LASER_ERR_HIP, "%s: %s", #expr, hipGetErrorString(e_)); \
+  } while (0)
+
+// Live handles: lets destroy/use of a stale handle fail cleanly instead of touching freed memory.
+static std::mutex g_handles_mu;
+static std::unordered_set<const void*> g_handles;
+static void handle_add(const void* p) {
+  std::lock_guard<std::mutex> lk(g_handles_mu);
+  g_handles.insert(p);
+}
+static bool handle_live(const void* p) {
+  std::lock_guard<std::mutex> lk(g_handles_mu);
+  return p && g_handles.count(p);
+}
+static void handle_del(const void* p) {
+  std::lock_guard<std::mutex> lk(g_handles_mu);
+  g_handles.erase(p);
+}
+
+// ----------------------------------------------------------------------------- model
+
+namespace {
+
+struct LayerW {
+  const void *attn_norm, *wq, *wk, *wv, *bq, *bk, *bv, *wo, *mlp_norm, *w_gate, *w_up, *w_down;
+};
+
+constexpr int kRing = 16;   // plan slots (pinned host + device)
+constexpr int kMaxT = 16;   // trial tokens per probe
+constexpr int kTargetUnits = 1024;  // GEMM workgroups aimed for per launch
+constexpr int kTargetAttnWaves = 2048;
+constexpr int kGemmLdsBudget = 48 * 1024;
+
+struct Layout {
+  size_t rope, h, ss, q, o, act, part, cnt, lm_part, lm_cnt, attn_part, attn_ml, attn_cnt, plans, probe_p, tok_buf,
+      p_buf, total;
+  size_t part_floats;
+  int cnt_ints;
+};
+
+struct Timer {
+  bool enabled = false;
+  std::vector<hipEvent_t> ev;  // pairs
+  int used = 0;
+};
+
+}  // namespace
+
+struct laser_model {
+  laser_model_desc desc;
+  int device = 0;
+  int es = 4;  // bytes per stored element
+  const void* embed = nullptr;
+  const void* lm_head = nullptr;
+  const void* final_norm = nullptr;
+  std::vector<LayerW> layers;
+  bool finalized = false;
+  int max_rows = 0;
+  char* ws = nullptr;
+  Layout lay{};
+  Plan* h_plans = nullptr;  // pinned ring
+  hipEvent_t ring_ev[kRing] = {};
+  bool ring_used[kRing] = {};
+  int ring_pos = 0;
+  Timer timers[LASER_K_NCLASS];
+
+  template <class T>
+  T* wsp(size_t off) const { return (T*)(ws + off); }
+};
+
+struct laser_kv {
+  const laser_model* m;
+  PagePool pool;
+  void* kpool;
+  void* vpool;
+  int32_t* bt;
+  std::vector<PageUpdate> pending;  // block-table writes not yet on the device
+  laser_kv(const laser_model* mm, int np, int ms, int mpps, void* k, void* v, int32_t* b)
+      : m(mm), pool(np, kPage, ms, mpps), kpool(k), vpool(v), bt(b) {}
+};
+
+namespace {
+
+static int ceil_div(int a, int b) { return (a + b - 1) / b; }
+static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+static int gemm_mode(int M) { return M <= 4 ? M : 4 + ceil_div(M, 16); }
+
+// Split-K choice for a projection with n_groups 64-row groups, K inputs and M rows.
+static void gemm_plan(int K, int n_groups, int M, int* n_splits, int* kslice) {
+  int kmax = (kGemmLdsBudget / 4 - 64 * M) / M - 8;
+  kmax = std::max(32, kmax & ~31);
+  int splits = ceil_div(K, kmax);
+  const int want = ceil_div(kTargetUnits, n_groups);
+  const int by_width = std::max(1, K / 512);
+  splits = std::max(splits, std::min(want, by_width));
+  int ks = ceil_div(ceil_div(K, splits), 32) * 32;
+  if (ks > kmax) ks = kmax;
+  *kslice = ks;
+  *n_splits = ceil_div(K, ks);
+}
+
+static int groups_qkv(const laser_model_desc& d) { return (d.n_q_heads + 2 * d.n_kv_heads) * d.head_dim / 64; }
+static int groups_gateup(const laser_model_desc& d) { return ceil_div(d.d_ffn, 32); }
+static int groups_resid(const laser_model_desc& d) { return d.d_model / 64; }
+static int groups_lm(const laser_model_desc& d) { return ceil_div(d.vocab, 64); }
+
+static Layout make_layout(const laser_model_desc& d, int max_rows) {
+  Layout L{};
+  const int hd = d.head_dim, G = d.n_q_heads / d.n_kv_heads;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    size_t o = off;
+    off = align256(off + bytes);
+    return o;
+  };
+  // largest split-K partial buffer over the projections and row counts
+  size_t part = 0;
+  int cnt = groups_lm(d) + 1;
+  struct K_ {
+    int K, groups;
+  } ks[5] = {{d.d_model, groups_qkv(d)},
+             {d.n_q_heads * hd, groups_resid(d)},
+             {d.d_model, groups_gateup(d)},
+             {d.d_ffn, groups_resid(d)},
+             {d.d_model, groups_lm(d)}};
+  for (int M = 1; M <= max_rows; ++M)
+    for (auto& k : ks) {
+      int ns, kl;
+      gemm_plan(k.K, k.groups, M, &ns, &kl);
+      if (ns > 1) part = std::max(part, (size_t)k.groups * ns * M * 64);
+      cnt = std::max(cnt, k.groups);
+    }
+  L.part_floats = part;
+  L.cnt_ints = cnt;
+  L.rope = take((size_t)d.max_positions * (hd / 2) * sizeof(float2));
+  L.h = take((size_t)max_rows * d.d_model * 4);
+  L.ss = take((size_t)(d.d_model / 64) * kMaxRows * 4);
+  L.q = take((size_t)max_rows * d.n_q_heads * hd * 4);
+  L.o = take((size_t)max_rows * d.n_q_heads * hd * 4);
+  L.act = take((size_t)max_rows * d.d_ffn * 4);
+  L.part = take(std::max<size_t>(part, 1) * 4);
+  L.cnt = take((size_t)cnt * 4);
+  L.lm_part = take((size_t)groups_lm(d) * kMaxRows * sizeof(LmPart));
+  L.lm_cnt = take(4);
+  L.attn_part = take((size_t)d.n_kv_heads * kAttnMaxWG * max_rows * G * hd * 4);
+  L.attn_ml = take((size_t)d.n_kv_heads * kAttnMaxWG * max_rows * G * 2 * 4);
+  L.attn_cnt = take((size_t)kMaxRows * d.n_kv_heads * 4);
+  L.plans = take((size_t)kRing * sizeof(Plan));
+  L.probe_p = take((size_t)kMaxRows * kMaxT * 4);
+  L.tok_buf = take((size_t)kMaxRows * 4);
+  L.p_buf = take((size_t)kMaxRows * 4);
+  L.total = off;
+  return L;
+}
+
+static laser_status check_desc(const laser_model_desc* d) {
+  if (!d) return laser_fail(LASER_ERR_INVALID_ARG, "desc is NULL");
+  if (d->n_layers < 1 || d->d_model < 64 || d->n_q_heads < 1 || d->n_kv_heads < 1 || d->d_ffn < 8 || d->vocab < 2)
+    return laser_fail(LASER_ERR_INVALID_ARG, "non-positive model dimension");
+  if (d->head_dim != 64 && d->head_dim != 128) return laser_fail(LASER_ERR_UNSUPPORTED, "head_dim must be 64 or 128");
+  if (d->n_q_heads % d->n_kv_heads) return laser_fail(LASER_ERR_UNSUPPORTED, "n_q_heads %% n_kv_heads != 0");
+  if (d->n_q_heads / d->n_kv_heads > 16) return laser_fail(LASER_ERR_UNSUPPORTED, "query group size above 16");
+  if (d->d_model % 64) return laser_fail(LASER_ERR_UNSUPPORTED, "d_model must be a multiple of 64");
+  if (d->d_ffn % 8) return laser_fail(LASER_ERR_UNSUPPORTED, "d_ffn must be a multiple of 8");
+  if ((d->n_q_heads * d->head_dim) % 64) return laser_fail(LASER_ERR_UNSUPPORTED, "n_q_heads*head_dim % 64 != 0");
+  if (d->dtype != LASER_DTYPE_F32 && d->dtype != LASER_DTYPE_BF16) return laser_fail(LASER_ERR_INVALID_ARG, "bad dtype");
+  if (d->max_positions < 16 || d->max_positions > 65536) return laser_fail(LASER_ERR_UNSUPPORTED, "max_positions out of range");
+  if (!(d->rope_theta > 1.0f) || !(d->rms_eps > 0.0f)) return laser_fail(LASER_ERR_INVALID_ARG, "bad rope_theta or rms_eps");
+  return LASER_OK;
+}
+
+static laser_model* model_of(laser_model* m) { return handle_live(m) ? m : nullptr; }
+
+}  // namespace
+
+extern "C" laser_status laser_model_create(const laser_model_desc* desc, laser_model** out) {
+  laser_status st = check_desc(desc);
+  if (st != LASER_OK) return st;
+  if (!out) return laser_fail(LASER_ERR_INVALID_ARG, "out is NULL");
+  laser_model* m = new (std::nothrow) laser_model();
+  if (!m) return laser_fail(LASER_ERR_INVALID_ARG, "allocation failed");
+  m->desc = *desc;
+  m->es = desc->dtype == LASER_DTYPE_BF16 ? 2 : 4;
+  m->layers.assign(desc->n_layers, LayerW{});
+  (void)hipGetDevice(&m->device);
+  handle_add(m);
+  *out = m;
+  return LASER_OK;
+}
+
+extern "C" laser_status laser_model_set_tensor(laser_model* m, const char* name, const void* d_ptr, size_t bytes) {
+  if (!model_of(m)) return laser_fail(LASER_ERR_STATE, "invalid or destroyed model");
+  if (m->finalized) return laser_fail(LASER_ERR_STATE, "model already finalized");
+  if (!name || !d_ptr) return laser_fail(LASER_ERR_INVALID_ARG, "NULL name or pointer");
+  const laser_model_desc& d = m->desc;
+  const size_t es = m->es, D = d.d_model, hq = d.n_q_heads * (size_t)d.head_dim, hk = d.n_kv_heads * (size_t)d.head_dim;
+  const void** slot = nullptr;
+  size_t want = 0;
+  std::string n(name);
+  if (n == "embed") {
+    slot = &m->embed;
+    want = (size_t)d.vocab * D;
+  } else if (n == "lm_head") {
+    if (d.tied_embeddings) return laser_fail(LASER_ERR_INVALID_ARG, "lm_head given for a tied model");
+    slot = &m->lm_head;
+    want = (size_t)d.vocab * D;
+  } else if (n == "final_norm") {
+    slot = &m->final_norm;
+    want = D;
+  } else if (n.rfind("layers.", 0) == 0) {
+    size_t dot = n.find('.', 7);
+    if (dot == std::string::npos) return laser_fail(LASER_ERR_INVALID_ARG, "bad tensor name '%s'", name);
+    int li = -1;
+    try {
+      li = std::stoi(n.substr(7, dot - 7));
+    } catch (...) {
+      li = -1;
+    }
+    if (li < 0 || li >= d.n_layers) return laser_fail(LASER_ERR_INVALID_ARG, "layer index out of range in '%s'", name);
+    std::string f = n.substr(dot + 1);
+    LayerW& L = m->layers[li];
+    struct {
+      const char* nm;
+      const void** p;
+      size_t sz;
+      bool bias;
+    } tab[] = {{"attn_norm", &L.attn_norm, D, false}, {"wq", &L.wq, hq * D, false}, {"wk", &L.wk, hk * D, false},
+               {"wv", &L.wv, hk * D, false},         {"bq", &L.bq, hq, true},       {"bk", &L.bk, hk, true},
+               {"bv", &L.bv, hk, true},              {"wo", &L.wo, D * hq, false},  {"mlp_norm", &L.mlp_norm, D, false},
+               {"w_gate", &L.w_gate, (size_t)d.d_ffn * D, false}, {"w_up", &L.w_up, (size_t)d.d_ffn * D, false},
+               {"w_down", &L.w_down, D * d.d_ffn, false}};
+    for (auto& t : tab)
+      if (f == t.nm) {
+        if (t.bias && !d.qkv_bias) return laser_fail(LASER_ERR_INVALID_ARG, "bias '%s' given for a model without qkv_bias", name);
+        slot = t.p;
+        want = t.sz;
+      }
+  }
+  if (!slot) return laser_fail(LASER_ERR_INVALID_ARG, "unknown tensor name '%s'", name);
+  if (bytes != want * es) return laser_fail(LASER_ERR_INVALID_ARG, "'%s': %zu bytes given, %zu expected", name, bytes, want * es);
+  *slot = d_ptr;
+  return LASER_OK;
+}
+
+extern "C" laser_status laser_workspace_size(const laser_model* m, int max_rows, size_t* bytes) {
+  if (!handle_live(m)) return laser_fail(LASER_ERR_STATE, "invalid or destroyed model");
+  if (!bytes) return laser_fail(LASER_ERR_INVALID_ARG, "bytes is NULL");
+  if (max_rows < 1 || max_rows > kMaxRows) return laser_fail(LASER_ERR_INVALID_ARG, "max_rows must be in [1, %d]", kMaxRows);
+  *bytes = make_layout(m->desc, max_rows).total;
+  return LASER_OK;
+}
+
+extern "C" laser_status laser_model_finalize(laser_model* m, int max_rows, void* d_workspace, size_t bytes, void* stream) {
+  if (!model_of(m)) return laser_fail(LASER_ERR_STATE, "invalid or destroyed model");
+  if (m->finalized) return laser_fail(LASER_ERR_STATE, "model already finalized");
+  if (max_rows < 1 || max_rows > kMaxRows) return laser_fail(LASER_ERR_INVALID_ARG, "max_rows must be in [1, %d]", kMaxRows);
+  const laser_model_desc& d = m->desc;
+  if (!m->embed || !m->final_norm || (!d.tied_embeddings && !m->lm_head))
+    return laser_fail(LASER_ERR_STATE, "embed / final_norm / lm_head not set");
+  for (int i = 0; i < d.n_layers; ++i) {
+    const LayerW& L = m->layers[i];
+    if (!L.attn_norm || !L.wq || !L.wk || !L.wv || !L.wo || !L.mlp_norm || !L.w_gate || !L.w_up || !L.w_down ||
+        (d.qkv_bias && (!L.bq || !L.bk || !L.bv)))
+      return laser_fail(LASER_ERR_STATE, "layer %d has unset tensors", i);
+  }
+  Layout L = make_layout(d, max_rows);
+  if (!d_workspace || bytes < L.total) return laser_fail(LASER_ERR_INVALID_ARG, "workspace of %zu bytes needed", L.total);
+  hipStream_t s = (hipStream_t)stream;
+  // RoPE table: angle pos * theta^(-2i/hd), computed in double precision
+  const int half = d.head_dim / 2;
+  std::vector<float2> rope((size_t)d.max_positions * half);
+  for (int p = 0; p < d.max_positions; ++p)
+    for (int i = 0; i < half; ++i) {
+      const double ang = (double)p * std::pow((double)d.rope_theta, -2.0 * i / d.head_dim);
+      rope[(size_t)p * half + i] = make_float2((float)std::cos(ang), (float)std::sin(ang));
+    }
+  Plan* hp = nullptr;
+  HIP_TRY(hipHostMalloc((void**)&hp, sizeof(Plan) * kRing, hipHostMallocDefault));
+  for (int i = 0; i < kRing; ++i) {
+    hipError_t e = hipEventCreateWithFlags(&m->ring_ev[i], hipEventDisableTiming);
+    if (e != hipSuccess) {
+      for (int j = 0; j < i; ++j) (void)hipEventDestroy(m->ring_ev[j]);
+      (void)hipHostFree(hp);
+      return laser_fail(LASER_ERR_HIP, "hipEventCreate: %s", hipGetErrorString(e));
+    }
+  }
+  char* ws = (char*)d_workspace;
+  HIP_TRY(hipMemcpyAsync(ws + L.rope, rope.data(), rope.size() * sizeof(float2), hipMemcpyHostToDevice, s));
+  HIP_TRY(hipMemsetAsync(ws + L.cnt, 0, (size_t)L.cnt_ints * 4, s));
+  HIP_TRY(hipMemsetAsync(ws + L.lm_cnt, 0, 4, s));
+  HIP_TRY(hipMemsetAsync(ws + L.attn_cnt, 0, (size_t)kMaxRows * d.n_kv_heads * 4, s));
+  HIP_TRY(hipStreamSynchronize(s));  // the host rope table goes out of scope
+  m->ws = ws;
+  m->lay = L;
+  m->h_plans = hp;
+  m->max_rows = max_rows;
+  m->finalized = true;
+  return LASER_OK;
+}
+
+extern "C" laser_status laser_model_destroy(laser_model* m) {
+  if (!model_of(m)) return laser_fail(LASER_ERR_STATE, "invalid or destroyed model");
+  handle_del(m);
+  if (m->finalized) {
+    for (int i = 0; i < kRing; ++i) {
+      if (m->ring_used[i]) (void)hipEventSynchronize(m->ring_ev[i]);
+      (void)hipEventDestroy(m->ring_ev[i]);
+    }
+    (void)hipHostFree(m->h_plans);
+  }
+  for (auto& t : m->timers)
+    for (auto e : t.ev) (void)hipEventDestroy(e);
+  delete m;
+  return LASER_OK;
+}
+
+// ----------------------------------------------------------------------------- KV cache
+
+extern "C" laser_status laser_kv_pool_bytes(const laser_model* m, int num_pages, size_t* bytes_per_pool) {
+  if (!handle_live(m)) return laser_fail(LASER_ERR_STATE, "invalid or destroyed model");
+  if (!bytes_per_pool || num_pages < 1) return laser_fail(LASER_ERR_INVALID_ARG, "bad argument");
+  const laser_model_desc& d = m->desc;
+  *bytes_per_pool = (size_t)d.n_layers * num_pages * d.n_kv_heads * kPage * d.head_dim * m->es;
+  return LASER_OK;
+}
+
+extern "C" laser_status laser_kv_create(const laser_model* m, int num_pages, int max_seqs, int max_pages_per_seq,
+                                        void* d_k_pool, void* d_v_pool, int32_t* d_block_table, laser_kv** out) {
+  if (!handle_live(m)) return laser_fail(LASER_ERR_STATE, "invalid or destroyed model");
+  if (!out || !d_k_pool || !d_v_pool || !d_block_table) return laser_fail(LASER_ERR_INVALID_ARG, "NULL argument");
+  if (num_pages < 1 || max_seqs < 1 || max_pages_per_seq < 1)
+    return laser_fail(LASER_ERR_INVALID_ARG, "sizes must be positive");
+  if ((long long)max_pages_per_seq * kPage > m->desc.max_positions + kPage)
+    return laser_fail(LASER_ERR_INVALID_ARG, "max_pages_per_seq exceeds max_positions");
+  laser_kv* kv = new (std::nothrow) laser_kv(m, num_pages, max_seqs, max_pages_per_seq, d_k_pool, d_v_pool, d_block_table);
+  if (!kv) return laser_fail(LASER_ERR_INVALID_ARG, "allocation failed");
+  handle_add(kv);
+  *out = kv;
+  return LASER_OK;
+}
+
+static laser_kv* kv_of(const laser_kv* kv) { return handle_live(kv) ? const_cast<laser_kv*>(kv) : nullptr; }
+
+extern "C" laser_status laser_kv_add_seq(laser_kv* kv, int seq_id, int length) {
+  if (!kv_of(kv)) return laser_fail(LASER_ERR_STATE, "invalid or destroyed kv");
+  if (length > kv->m->desc.max_positions) return laser_fail(LASER_ERR_INVALID_ARG, "length exceeds max_positions");
+  return (laser_status)kv->pool.add_seq(seq_id, length, &kv->pending);
+}
+
+extern "C" laser_status laser_kv_free_seq(laser_kv* kv, int seq_id) {
+  if (!kv_of(kv)) return laser_fail(LASER_ERR_STATE, "invalid or destroyed kv");
+  return (laser_status)kv->pool.free_seq(seq_id);
+}
+
+extern "C" laser_status laser_kv_seq_len(const laser_kv* kv, int seq_id, int* len_out) {
+  if (!kv_of(kv)) return laser_fail(LASER_ERR_STATE, "invalid or destroyed kv");
+  if (!len_out) return laser_fail(LASER_ERR_INVALID_ARG, "NULL argument");
+  if (!kv->pool.live(seq_id)) return laser_fail(LASER_ERR_INVALID_ARG, "seq_id %d not present", seq_id);
+  *len_out = kv->pool.len(seq_id);
+  return LASER_OK;
+}
+
+extern "C" laser_status laser_kv_page_table(const laser_kv* kv, int seq_id, int32_t* out, int cap, int* n_out) {
+  if (!kv_of(kv)) return laser_fail(LASER_ERR_STATE, "invalid or destroyed kv");
+  if (!out || !n_out) return laser_fail(LASER_ERR_INVALID_ARG, "NULL argument");
+  if (!kv->pool.live(seq_id)) return laser_fail(LASER_ERR_INVALID_ARG, "seq_id %d not present", seq_id);
+  const auto& t = kv->pool.table(seq_id);
+  if ((int)t.size() > cap) return laser_fail(LASER_ERR_INVALID_ARG, "cap %d < %d pages", cap, (int)t.size());
+  for (size_t i = 0; i < t.size(); ++i) out[i] = t[i];
+  *n_out = (int)t.size();
+  return LASER_OK;
+}
+
+extern "C" laser_status laser_kv_destroy(laser_kv* kv) {
+  if (!kv_of(kv)) return laser_fail(LASER_ERR_STATE, "invalid or destroyed kv");
+  handle_del(kv);
+  delete kv;
+  return LASER_OK;
+}
+
+// ----------------------------------------------------------------------------- launches
+
+namespace {
+
+struct Launch {
+  laser_model* m;
+  hipStream_t s;
+};
+
+// Records timing events around a launch of class `cls` when enabled.
+template <class F>
+static hipError_t timed(laser_model* m, int cls, hipStream_t s, F&& f) {
+  Timer& t = m->timers[cls];
+  if (!t.enabled) return f();
+  if ((int)t.ev.size() < 2 * (t.used + 1)) {
+    hipEvent_t a, b;
+    hipError_t e = hipEventCreate(&a);
+    if (e != hipSuccess) return e;
+    e = hipEventCreate(&b);
+    if (e != hipSuccess) return e;
+    t.ev.push_back(a);
+    t.ev.push_back(b);
+  }
+  (void)hipEventRecord(t.ev[2 * t.used], s);
+  hipError_t e = f();
+  (void)hipEventRecord(t.ev[2 * t.used + 1], s);
+  t.used++;
+  return e;
+}
+
+// Copies a plan into the next ring slot (pinned) and on to the device; returns the device copy.
+static laser_status upload_plan(laser_model* m, const Plan& p, hipStream_t s, Plan** d_out) {
+  const int slot = m->ring_pos;
+  m->ring_pos = (m->ring_pos + 1) % kRing;
+  if (m->ring_used[slot]) HIP_TRY(hipEventSynchronize(m->ring_ev[slot]));
+  Plan* hp = m->h_plans + slot;
+  const size_t bytes = offsetof(Plan, bt) + sizeof(BtUpdate) * (size_t)p.n_bt;
+  std::memcpy(hp, &p, bytes);
+  Plan* dp = m->wsp<Plan>(m->lay.plans) + slot;
+  HIP_TRY(hipMemcpyAsync(dp, hp, bytes, hipMemcpyHostToDevice, s));
+  HIP_TRY(hipEventRecord(m->ring_ev[slot], s));
+  m->ring_used[slot] = true;
+  *d_out = dp;
+  return LASER_OK;
+}
+
+// Sends block-table writes that are not part of a forward plan (after add_seq).
+static laser_status flush_pending(laser_kv* kv, laser_model* m, hipStream_t s) {
+  size_t i = 0;
+  while (i < kv->pending.size()) {
+    Plan* p = new (std::nothrow) Plan;
+    if (!p) return laser_fail(LASER_ERR_INVALID_ARG, "allocation failed");
+    p->M = p->n_groups = p->n_out = 0;
+    p->n_bt = 0;
+    while (i < kv->pending.size() && p->n_bt < kMaxBt) {
+      const PageUpdate& u = kv->pending[i++];
+      p->bt[p->n_bt++] = BtUpdate{u.seq, u.idx, u.page};
+    }
+    Plan* dp = nullptr;
+    laser_status st = upload_plan(m, *p, s, &dp);
+    delete p;
+    if (st != LASER_OK) return st;
+    HIP_TRY(launch_apply_bt(dp, kv->bt, kv->pool.max_pages_per_seq(), s));
+  }
+  kv->pending.clear();
+  return LASER_OK;
+}
+
+// Output destinations of a forward's LM head.
+struct Outs {
+  int* tok[2] = {nullptr, nullptr};
+  float* p[2] = {nullptr, nullptr};
+  float* logits[2] = {nullptr, nullptr};
+};
+
+// Fill row groups (contiguous rows of one request) and their attention splits.
+static void plan_groups(const laser_model* m, Plan& p) {
+  const laser_model_desc& d = m->desc;
+  const int G = d.n_q_heads / d.n_kv_heads;
+  const int cap = std::max(1, 64 / G);  // query columns of a group fit 4 MFMA n-tiles
+  p.n_groups = 0;
+  long long units = 0;
+  for (int r = 0; r < p.M;) {
+    int e = r + 1;
+    while (e < p.M && p.rows[e].seq == p.rows[r].seq && e - r < cap) ++e;
+    int maxpos = 0;
+    for (int q = r; q < e; ++q) maxpos = std::max(maxpos, p.rows[q].pos);
+    GroupDesc& g = p.groups[p.n_groups++];
+    g.seq = p.rows[r].seq;
+    g.row0 = r;
+    g.nrows = e - r;
+    g.npages = maxpos / kPage + 1;
+    units += (long long)g.npages * d.n_kv_heads;
+    r = e;
+  }
+  const int base = std::max(1, (int)((units + kTargetAttnWaves - 1) / kTargetAttnWaves));
+  for (int i = 0; i < p.n_groups; ++i) {
+    GroupDesc& g = p.groups[i];
+    g.pps = std::max(base, ceil_div(g.npages, kAttnMaxWG * kAttnWaves));
+    g.nwg = ceil_div(g.npages, kAttnWaves * g.pps);
+  }
+}
+
+static laser_status run_forward(laser_model* m, laser_kv* kv, Plan& p, const int* tok0, const int* tok1, const Outs& outs,
+                                hipStream_t s) {
+  const laser_model_desc& d = m->desc;
+  const Layout& L = m->lay;
+  const int hd = d.head_dim, G = d.n_q_heads / d.n_kv_heads;
+  const int dt = d.dtype == LASER_DTYPE_BF16 ? 1 : 0;
+  const int max_pps = kv->pool.max_pages_per_seq();
+  plan_groups(m, p);
+  Plan* dp = nullptr;
+  laser_status st = upload_plan(m, p, s, &dp);
+  if (st != LASER_OK) return st;
+  float* h = m->wsp<float>(L.h);
+  float* ss = m->wsp<float>(L.ss);
+  HIP_TRY(timed(m, LASER_K_EMBED, s, [&] {
+    return launch_embed(dt, dp, p.M, m->embed, d.d_model, d.vocab, tok0, tok1, h, ss, kv->bt, max_pps, s);
+  }));
+
+  GemmArgs base{};
+  base.plan = dp;
+  base.part = m->wsp<float>(L.part);
+  base.cnt = m->wsp<int>(L.cnt);
+  base.eps = d.rms_eps;
+  base.hq = d.n_q_heads;
+  base.hkv = d.n_kv_heads;
+  base.hd = hd;
+  base.rope = m->wsp<float2>(L.rope);
+  base.q_out = m->wsp<float>(L.q);
+  base.kpool = kv->kpool;
+  base.vpool = kv->vpool;
+  base.bt = kv->bt;
+  base.max_pps = max_pps;
+  base.num_pages = kv->pool.num_pages();
+  base.h = h;
+  base.ss_out = ss;
+  base.act = m->wsp<float>(L.act);
+  base.F = d.d_ffn;
+  base.ss = ss;
+  base.n_ss = d.d_model / 64;
+
+  auto gemm = [&](int cls, int epi, GemmArgs a, int K, int N, int n_groups, int M) -> laser_status {
+    a.K = K;
+    a.N = N;
+    a.n_groups = n_groups;
+    a.M = M;
+    gemm_plan(K, n_groups, M, &a.n_splits, &a.kslice);
+    const int mode = gemm_mode(M);
+    HIP_TRY(timed(m, cls, s, [&] { return launch_gemm(dt, mode, epi, a, n_groups * a.n_splits, s); }));
+    return LASER_OK;
+  };
+
+  AttnArgs aa{};
+  aa.plan = dp;
+  aa.q = m->wsp<float>(L.q);
+  aa.o = m->wsp<float>(L.o);
+  aa.kpool = kv->kpool;
+  aa.vpool = kv->vpool;
+  aa.bt = kv->bt;
+  aa.max_pps = max_pps;
+  aa.num_pages = kv->pool.num_pages();
+  aa.hq = d.n_q_heads;
+  aa.hkv = d.n_kv_heads;
+  aa.G = G;
+  aa.max_rows = m->max_rows;
+  aa.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)hd));
+  aa.part = m->wsp<float>(L.attn_part);
+  aa.ml = m->wsp<float>(L.attn_ml);
+  aa.cnt = m->wsp<int>(L.attn_cnt);
+  int max_nwg = 1, nt = 1;
+  for (int i = 0; i < p.n_groups; ++i) {
+    max_nwg = std::max(max_nwg, p.groups[i].nwg);
+    nt = std::max(nt, ceil_div(p.groups[i].nrows * G, 16));
+  }
+  if (nt == 3) nt = 4;
+  const dim3 agrid(max_nwg, d.n_kv_heads, p.n_groups);
+
+  for (int li = 0; li < d.n_layers; ++li) {
+    const LayerW& W = m->layers[li];
+    GemmArgs a = base;
+    a.w0 = W.wq;
+    a.w1 = W.wk;
+    a.w2 = W.wv;
+    a.b0 = W.bq;
+    a.b1 = W.bk;
+    a.b2 = W.bv;
+    a.x = h;
+    a.ldx = d.d_model;
+    a.gain = W.attn_norm;
+    a.layer = li;
+    st = gemm(LASER_K_QKV, EPI_QKV, a, d.d_model, (d.n_q_heads + 2 * d.n_kv_heads) * hd, groups_qkv(d), p.M);
+    if (st != LASER_OK) return st;
+
+    aa.layer = li;
+    HIP_TRY(timed(m, LASER_K_ATTN, s, [&] { return launch_attn(dt, hd, nt, aa, agrid, s); }));
+
+    a = base;
+    a.w0 = W.wo;
+    a.x = m->wsp<float>(L.o);
+    a.ldx = d.n_q_heads * hd;
+    a.gain = nullptr;
+    st = gemm(LASER_K_OPROJ, EPI_RESID, a, d.n_q_heads * hd, d.d_model, groups_resid(d), p.M);
+    if (st != LASER_OK) return st;
+
+    a = base;
+    a.w0 = W.w_gate;
+    a.w1 = W.w_up;
+    a.x = h;
+    a.ldx = d.d_model;
+    a.gain = W.mlp_norm;
+    st = gemm(LASER_K_GATEUP, EPI_SWIGLU, a, d.d_model, 2 * d.d_ffn, groups_gateup(d), p.M);
+    if (st != LASER_OK) return st;
+
+    a = base;
+    a.w0 = W.w_down;
+    a.x = m->wsp<float>(L.act);
+    a.ldx = d.d_ffn;
+    a.gain = nullptr;
+    st = gemm(LASER_K_DOWN, EPI_RESID, a, d.d_ffn, d.d_model, groups_resid(d), p.M);
+    if (st != LASER_OK) return st;
+  }
+  if (p.n_out > 0) {
+    GemmArgs a = base;
+    a.w0 = d.tied_embeddings ? m->embed : m->lm_head;
+    a.x = h;
+    a.ldx = d.d_model;
+    a.gain = m->final_norm;
+    a.row_map = 1;
+    for (int i = 0; i < 2; ++i) {
+      a.logits[i] = outs.logits[i];
+      a.tok_out[i] = outs.tok[i];
+      a.p_out[i] = outs.p[i];
+    }
+    a.lm_part = m->wsp<LmPart>(L.lm_part);
+    a.lm_cnt = m->wsp<int>(L.lm_cnt);
+    st = gemm(LASER_K_LMHEAD, EPI_LMHEAD, a, d.d_model, d.vocab, groups_lm(d), p.n_out);
+    if (st != LASER_OK) return st;
+  }
+  return LASER_OK;
+}
+
+static laser_status check_ready(laser_model* m, laser_kv* kv) {
+  if (!model_of(m)) return laser_fail(LASER_ERR_STATE, "invalid or destroyed model");
+  if (!m->finalized) return laser_fail(LASER_ERR_STATE, "model not finalized");
+  if (!kv_of(kv)) return laser_fail(LASER_ERR_STATE, "invalid or destroyed kv");
+  if (kv->m != m) return laser_fail(LASER_ERR_INVALID_ARG, "kv cache belongs to another model");
+  return LASER_OK;
+}
+
+// Validates that every (seq, growth) can be satisfied at once: distinct live sequences,
+// positions below max_positions, pages per sequence and free pages in total.
+static laser_status check_growth(laser_model* m, laser_kv* kv, const std::vector<int>& seqs, const std::vector<int>& grow) {
+  std::unordered_set<int> seen;
+  long long need = 0;
+  for (size_t i = 0; i < seqs.size(); ++i) {
+    const int sq = seqs[i];
+    if (!kv->pool.live(sq)) return laser_fail(LASER_ERR_INVALID_ARG, "seq_id %d not present", sq);
+    if (!seen.insert(sq).second) return laser_fail(LASER_ERR_INVALID_ARG, "seq_id %d repeated", sq);
+    const int nl = kv->pool.len(sq) + grow[i];
+    if (nl > m->desc.max_positions) return laser_fail(LASER_ERR_INVALID_ARG, "seq %d would exceed max_positions", sq);
+    if (kv->pool.pages_for(nl) > kv->pool.max_pages_per_seq())
+      return laser_fail(LASER_ERR_INVALID_ARG, "seq %d would exceed max_pages_per_seq", sq);
+    need += kv->pool.pages_needed(sq, grow[i]);
+  }
+  if (need > kv->pool.num_free()) return laser_fail(LASER_ERR_OUT_OF_PAGES, "need %lld pages, %d free", need, kv->pool.num_free());
+  return LASER_OK;
+}
+
+static void push_updates(Plan& p, const std::vector<PageUpdate>& u) {
+  for (const auto& x : u) p.bt[p.n_bt++] = BtUpdate{x.seq, x.idx, x.page};
+}
+
+}  // namespace
+
+extern "C" laser_status laser_kv_import(laser_kv* kv, int seq_id, const void* d_k, const void* d_v, int length, void* stream) {
+  if (!kv_of(kv)) return laser_fail(LASER_ERR_STATE, "invalid or destroyed kv");
+  laser_model* m = const_cast<laser_model*>(kv->m);
+  if (!model_of(m) || !m->finalized) return laser_fail(LASER_ERR_STATE, "model not finalized");
+  if (!d_k || !d_v) return laser_fail(LASER_ERR_INVALID_ARG, "NULL argument");
+  if (!kv->pool.live(seq_id)) return laser_fail(LASER_ERR_INVALID_ARG, "seq_id %d not present", seq_id);
+  if (length != kv->pool.len(seq_id)) return laser_fail(LASER_ERR_INVALID_ARG, "length %d != sequence length %d", length, kv->pool.len(seq_id));
+  hipStream_t s = (hipStream_t)stream;
+  laser_status st = flush_pending(kv, m, s);
+  if (st != LASER_OK) return st;
+  const laser_model_desc& d = m->desc;
+  HIP_TRY(launch_kv_copy(d.dtype == LASER_DTYPE_BF16, 1, kv->kpool, kv->vpool, kv->bt, kv->pool.max_pages_per_seq(),
+                         kv->pool.num_pages(), d.n_layers, d.n_kv_heads, d.head_dim, seq_id, length,
+                         const_cast<void*>(d_k), const_cast<void*>(d_v), s));
+  return LASER_OK;
+}
+
+extern "C" laser_status laser_kv_export(const laser_kv* kvc, int seq_id, void* d_k, void* d_v, void* stream) {
+  laser_kv* kv = kv_of(kvc);
+  if (!kv) return laser_fail(LASER_ERR_STATE, "invalid or destroyed kv");
+  laser_model* m = const_cast<laser_model*>(kv->m);
+  if (!model_of(m) || !m->finalized) return laser_fail(LASER_ERR_STATE, "model not finalized");
+  if (!d_k || !d_v) return laser_fail(LASER_ERR_INVALID_ARG, "NULL argument");
+  if (!kv->pool.live(seq_id)) return laser_fail(LASER_ERR_INVALID_ARG, "seq_id %d not present", seq_id);
+  hipStream_t s = (hipStream_t)stream;
+  laser_status st = flush_pending(kv, m, s);
+  if (st != LASER_OK) return st;
+  const laser_model_desc& d = m->desc;
+  HIP_TRY(launch_kv_copy(d.dtype == LASER_DTYPE_BF16, 0, kv->kpool, kv->vpool, kv->bt, kv->pool.max_pages_per_seq(),
+                         kv->pool.num_pages(), d.n_layers, d.n_kv_heads, d.head_dim, seq_id, kv->pool.len(seq_id), d_k, d_v, s));
+  return LASER_OK;
+}
+
+extern "C" laser_status laser_decode_step(laser_model* m, laser_kv* kv, int batch, const int32_t* seq_ids,
+                                          const int32_t* d_tokens, int32_t* d_next, float* d_max_prob, float* d_logits,
+                                          void* stream) {
+  laser_status st = check_ready(m, kv);
+  if (st != LASER_OK) return st;
+  if (batch < 1 || batch > m->max_rows) return laser_fail(LASER_ERR_INVALID_ARG, "batch must be in [1, %d]", m->max_rows);
+  if (!seq_ids || !d_tokens || !d_next || !d_max_prob) return laser_fail(LASER_ERR_INVALID_ARG, "NULL argument");
+  std::vector<int> seqs(seq_ids, seq_ids + batch), grow(batch, 1);
+  st = check_growth(m, kv, seqs, grow);
+  if (st != LASER_OK) return st;
+  hipStream_t s = (hipStream_t)stream;
+  st = flush_pending(kv, m, s);
+  if (st != LASER_OK) return st;
+  Plan* p = new (std::nothrow) Plan;
+  if (!p) return laser_fail(LASER_ERR_INVALID_ARG, "allocation failed");
+  p->M = batch;
+  p->n_out = batch;
+  p->n_bt = 0;
+  std::vector<PageUpdate> upd;
+  for (int b = 0; b < batch; ++b) {
+    const int pos = kv->pool.len(seqs[b]);
+    kv->pool.append(seqs[b], 1, &upd);
+    p->rows[b] = RowDesc{seqs[b], pos, 0, b};
+    p->outs[b] = OutDesc{b, 0, b, 0};
+  }
+  push_updates(*p, upd);
+  Outs o;
+  o.tok[0] = d_next;
+  o.p[0] = d_max_prob;
+  o.logits[0] = d_logits;
+  st = run_forward(m, kv, *p, d_tokens, d_tokens, o, s);
+  delete p;
+  return st;
+}
+
+extern "C" laser_status laser_prefill(laser_model* m, laser_kv* kv, int seq_id, const int32_t* d_tokens, int n,
+                                      float* d_logits_last, void* stream) {
+  laser_status st = check_ready(m, kv);
+  if (st != LASER_OK) return st;
+  if (!d_tokens || n < 1) return laser_fail(LASER_ERR_INVALID_ARG, "need n >= 1 tokens");
+  std::vector<int> seqs{seq_id}, grow{n};
+  st = check_growth(m, kv, seqs, grow);
+  if (st != LASER_OK) return st;
+  hipStream_t s = (hipStream_t)stream;
+  st = flush_pending(kv, m, s);
+  if (st != LASER_OK) return st;
+  Plan* p = new (std::nothrow) Plan;
+  if (!p) return laser_fail(LASER_ERR_INVALID_ARG, "allocation failed");
+  for (int c0 = 0; c0 < n && st == LASER_OK; c0 += m->max_rows) {
+    const int M = std::min(m->max_rows, n - c0);
+    p->M = M;
+    p->n_bt = 0;
+    std::vector<PageUpdate> upd;
+    const int pos0 = kv->pool.len(seq_id);
+    kv->pool.append(seq_id, M, &upd);
+    for (int i = 0; i < M; ++i) p->rows[i] = RowDesc{seq_id, pos0 + i, 0, c0 + i};
+    push_updates(*p, upd);
+    const bool last = c0 + M >= n;
+    p->n_out = (last && d_logits_last) ? 1 : 0;
+    p->outs[0] = OutDesc{M - 1, 0, 0, 0};
+    Outs o;
+    o.tok[0] = m->wsp<int>(m->lay.tok_buf);
+    o.p[0] = m->wsp<float>(m->lay.p_buf);
+    o.logits[0] = d_logits_last;
+    st = run_forward(m, kv, *p, d_tokens, d_tokens, o, s);
+  }
+  delete p;
+  return st;
+}
+
+// Trial-token forwards j = 1..T-1 of a probe: row r feeds t_j (d_argmax[r*T + j-1]).
+static laser_status run_trials(laser_model* m, laser_kv* kv, Plan* p, const std::vector<int>& seqs,
+                               const std::vector<int>& base_pos, int S, int T, int32_t* d_argmax, float* probe_p,
+                               float* d_logits, hipStream_t s) {
+  for (int j = 1; j < T; ++j) {
+    const int n = (int)seqs.size();
+    p->M = n;
+    p->n_out = n;
+    p->n_bt = 0;
+    for (int r = 0; r < n; ++r) {
+      p->rows[r] = RowDesc{seqs[r], base_pos[r] + S + j - 1, 0, r * T + j - 1};
+      p->outs[r] = OutDesc{r, 0, r * T + j, 0};
+    }
+    Outs o;
+    o.tok[0] = d_argmax;
+    o.p[0] = probe_p;
+    o.logits[0] = d_logits;
+    laser_status st = run_forward(m, kv, *p, d_argmax, d_argmax, o, s);
+    if (st != LASER_OK) return st;
+  }
+  return LASER_OK;
+}
+
+extern "C" laser_status laser_probe_confidence(laser_model* m, laser_kv* kv, int batch, const int32_t* seq_ids,
+                                               const int32_t* d_suffix, int S, int T, float* d_conf, int32_t* d_argmax,
+                                               float* d_logits, void* stream) {
+  laser_status st = check_ready(m, kv);
+  if (st != LASER_OK) return st;
+  if (!seq_ids || !d_suffix || !d_conf || !d_argmax) return laser_fail(LASER_ERR_INVALID_ARG, "NULL argument");
+  if (S < 1 || T < 1 || T > kMaxT) return laser_fail(LASER_ERR_INVALID_ARG, "need S >= 1 and 1 <= T <= %d", kMaxT);
+  if (batch < 1 || (long long)batch * S > m->max_rows)
+    return laser_fail(LASER_ERR_INVALID_ARG, "batch*S must be in [1, %d]", m->max_rows);
+  std::vector<int> seqs(seq_ids, seq_ids + batch), grow(batch, S + T - 1);
+  st = check_growth(m, kv, seqs, grow);
+  if (st != LASER_OK) return st;
+  hipStream_t s = (hipStream_t)stream;
+  st = flush_pending(kv, m, s);
+  if (st != LASER_OK) return st;
+  Plan* p = new (std::nothrow) Plan;
+  if (!p) return laser_fail(LASER_ERR_INVALID_ARG, "allocation failed");
+  std::vector<int> L0(batch);
+  std::vector<PageUpdate> upd;
+  for (int r = 0; r < batch; ++r) {
+    L0[r] = kv->pool.len(seqs[r]);
+    kv->pool.append(seqs[r], S + T - 1, &upd);  // scratch positions for the suffix and fed-back trials
+  }
+  float* probe_p = m->wsp<float>(m->lay.probe_p);
+  // chunk forward: the S suffix rows of every request; the last row of each gives t_1, p_1
+  p->M = batch * S;
+  p->n_out = batch;
+  p->n_bt = 0;
+  push_updates(*p, upd);
+  for (int r = 0; r < batch; ++r) {
+    for (int i = 0; i < S; ++i) p->rows[r * S + i] = RowDesc{seqs[r], L0[r] + i, 0, i};
+    p->outs[r] = OutDesc{r * S + S - 1, 0, r * T, 0};
+  }
+  Outs o;
+  o.tok[0] = d_argmax;
+  o.p[0] = probe_p;
+  o.logits[0] = d_logits;
+  st = run_forward(m, kv, *p, d_suffix, d_suffix, o, s);
+  if (st == LASER_OK) st = run_trials(m, kv, p, seqs, L0, S, T, d_argmax, probe_p, d_logits, s);
+  if (st == LASER_OK) {
+    hipError_t e = timed(m, LASER_K_OTHER, s, [&] { return launch_confidence(probe_p, T, batch, d_conf, s); });
+    if (e != hipSuccess) st = laser_fail(LASER_ERR_HIP, "confidence: %s", hipGetErrorString(e));
+  }
+  for (int r = 0; r < batch; ++r) kv->pool.truncate(seqs[r], L0[r]);  // the probe leaves no trace
+  delete p;
+  return st;
+}
+
+extern "C" laser_status laser_step_mixed(laser_model* m, laser_kv* kv, int batch, const int32_t* seq_ids,
+                                         const int32_t* d_tokens, int32_t* d_next, float* d_max_prob, int n_probe,
+                                         const int32_t* probe_idx, const int32_t* d_suffix, int S, int T, float* d_conf,
+                                         int32_t* d_argmax, void* stream) {
+  laser_status st = check_ready(m, kv);
+  if (st != LASER_OK) return st;
+  if (!seq_ids || !d_tokens || !d_next || !d_max_prob) return laser_fail(LASER_ERR_INVALID_ARG, "NULL argument");
+  if (batch < 1 || n_probe < 0 || n_probe > batch) return laser_fail(LASER_ERR_INVALID_ARG, "bad batch / n_probe");
+  if (n_probe > 0) {
+    if (!probe_idx || !d_suffix || !d_conf || !d_argmax) return laser_fail(LASER_ERR_INVALID_ARG, "NULL probe argument");
+    if (S < 1 || T < 1 || T > kMaxT) return laser_fail(LASER_ERR_INVALID_ARG, "need S >= 1 and 1 <= T <= %d", kMaxT);
+  }
+  if ((long long)batch + (long long)S * n_probe > m->max_rows)
+    return laser_fail(LASER_ERR_INVALID_ARG, "batch + S*n_probe exceeds max_rows %d", m->max_rows);
+  std::vector<int> probing(batch, -1);
+  for (int i = 0; i < n_probe; ++i) {
+    const int b = probe_idx[i];
+    if (b < 0 || b >= batch || probing[b] >= 0) return laser_fail(LASER_ERR_INVALID_ARG, "bad or repeated probe_idx");
+    if (i > 0 && b <= probe_idx[i - 1]) return laser_fail(LASER_ERR_INVALID_ARG, "probe_idx must be increasing");
+    probing[b] = i;
+  }
+  std::vector<int> seqs(seq_ids, seq_ids + batch), grow(batch, 1);
+  for (int b = 0; b < batch; ++b)
+    if (probing[b] >= 0) grow[b] += S + T - 1;
+  st = check_growth(m, kv, seqs, grow);
+  if (st != LASER_OK) return st;
+  hipStream_t s = (hipStream_t)stream;
+  st = flush_pending(kv, m, s);
+  if (st != LASER_OK) return st;
+  Plan* p = new (std::nothrow) Plan;
+  if (!p) return laser_fail(LASER_ERR_INVALID_ARG, "allocation failed");
+  std::vector<PageUpdate> upd;
+  std::vector<int> pseqs, pbase;
+  int M = 0, nout = 0;
+  p->n_bt = 0;
+  // committed decode positions first (batch order), then the probes' scratch positions
+  std::vector<int> pos0(batch);
+  for (int b = 0; b < batch; ++b) {
+    pos0[b] = kv->pool.len(seqs[b]);
+    kv->pool.append(seqs[b], 1, &upd);
+  }
+  for (int b = 0; b < batch; ++b)
+    if (probing[b] >= 0) kv->pool.append(seqs[b], S + T - 1, &upd);
+  for (int b = 0; b < batch; ++b) {
+    const int pos = pos0[b];
+    p->rows[M] = RowDesc{seqs[b], pos, 0, b};
+    p->outs[nout++] = OutDesc{M, 0, b, 0};
+    ++M;
+    if (probing[b] >= 0) {
+      const int i = probing[b];
+      for (int q = 0; q < S; ++q) p->rows[M + q] = RowDesc{seqs[b], pos + 1 + q, 1, q};
+      p->outs[nout++] = OutDesc{M + S - 1, 1, i * T, 0};
+      M += S;
+      pseqs.push_back(seqs[b]);
+      pbase.push_back(pos + 1);
+    }
+  }
+  p->M = M;
+  p->n_out = nout;
+  push_updates(*p, upd);
+  float* probe_p = m->wsp<float>(m->lay.probe_p);
+  Outs o;
+  o.tok[0] = d_next;
+  o.p[0] = d_max_prob;
+  o.tok[1] = d_argmax;
+  o.p[1] = probe_p;
+  st = run_forward(m, kv, *p, d_tokens, d_suffix, o, s);
+  if (st == LASER_OK && n_probe > 0) st = run_trials(m, kv, p, pseqs, pbase, S, T, d_argmax, probe_p, nullptr, s);
+  if (st == LASER_OK && n_probe > 0) {
+    hipError_t e = timed(m, LASER_K_OTHER, s, [&] { return launch_confidence(probe_p, T, n_probe, d_conf, s); });
+    if (e != hipSuccess) st = laser_fail(LASER_ERR_HIP, "confidence: %s", hipGetErrorString(e));
+  }
+  for (size_t i = 0; i < pseqs.size(); ++i) kv->pool.truncate(pseqs[i], pbase[i]);
+  delete p;
+  return st;
+}
+
+// ----------------------------------------------------------------------------- timing
+
+extern "C" laser_status laser_timing_enable(laser_model* m, int kernel_class, int enable) {
+  if (!model_of(m)) return laser_fail(LASER_ERR_STATE, "invalid or destroyed model");
+  if (kernel_class < 0 || kernel_class >= LASER_K_NCLASS) return laser_fail(LASER_ERR_INVALID_ARG, "bad kernel class");
+  m->timers[kernel_class].enabled = enable != 0;
+  m->timers[kernel_class].used = 0;
+  return LASER_OK;
+}
+
+extern "C" laser_status laser_timing_read(laser_model* m, int kernel_class, double* total_ms, int* launches) {
+  if (!model_of(m)) return laser_fail(LASER_ERR_STATE, "invalid or destroyed model");
+  if (kernel_class < 0 || kernel_class >= LASER_K_NCLASS) return laser_fail(LASER_ERR_INVALID_ARG, "bad kernel class");
+  if (!total_ms || !launches) return laser_fail(LASER_ERR_INVALID_ARG, "NULL argument");
+  Timer& t = m->timers[kernel_class];
+  double tot = 0.0;
+  if (t.used > 0) HIP_TRY(hipEventSynchronize(t.ev[2 * t.used - 1]));
+  for (int i = 0; i < t.used; ++i) {
+    float ms = 0.f;
+    HIP_TRY(hipEventElapsedTime(&ms, t.ev[2 * i], t.ev[2 * i + 1]));
+    tot += ms;
+  }
+  *total_ms = tot;
+  *launches = t.used;
+  t.used = 0;
+  return LASER_OK;
+}

@@ -1,0 +1,325 @@
+"""ctypes binding of liblaser.so (C ABI in include/laser.h).
+
+Functions keep the C names and signatures (argument marshalling only); every step of
+the hot path runs in the library's HIP kernels.  `Model` and `KVCache` are thin owners
+of the device memory (allocated with PyTorch) that the library borrows.  Loading fails
+loudly when the library has not been built.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+from typing import Dict, Optional, Sequence
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "lib", "liblaser.so")
+
+OK, ERR_INVALID_ARG, ERR_OUT_OF_PAGES, ERR_HIP, ERR_UNSUPPORTED, ERR_STATE = 0, -1, -2, -3, -4, -5
+DTYPE_F32, DTYPE_BF16 = 0, 1
+CONTINUE, EARLY_EXIT, BUDGET_EXHAUSTED = 0, 1, 2
+K_EMBED, K_QKV, K_ATTN, K_OPROJ, K_GATEUP, K_DOWN, K_LMHEAD, K_OTHER = range(8)
+KERNEL_CLASSES = {"embed": 0, "qkv": 1, "attn": 2, "oproj": 3, "gateup": 4, "down": 5, "lmhead": 6, "other": 7}
+
+
+class LaserError(RuntimeError):
+    def __init__(self, code: int, fn: str, msg: str):
+        super().__init__(f"{fn} failed ({code}): {msg}")
+        self.code = code
+
+
+class laser_params(C.Structure):
+    _fields_ = [(n, C.c_double) for n in ("lambda_base", "beta", "gamma", "alpha", "L_target", "lambda_min", "lambda_max")] + [
+        ("B_base", C.c_int), ("B_min", C.c_int), ("f_min", C.c_double), ("f_max", C.c_double), ("p_min", C.c_int), ("p_max", C.c_int)]
+
+
+class laser_load_state(C.Structure):
+    _fields_ = [("L_bar", C.c_double)]
+
+
+class laser_model_desc(C.Structure):
+    _fields_ = [(n, C.c_int) for n in ("n_layers", "d_model", "n_q_heads", "n_kv_heads", "head_dim", "d_ffn", "vocab",
+                                       "tied_embeddings", "qkv_bias", "dtype")] + [
+        ("rope_theta", C.c_float), ("rms_eps", C.c_float), ("max_positions", C.c_int)]
+
+
+_P = C.c_void_p
+_I = C.c_int
+_I32P = C.POINTER(C.c_int32)
+_SIGS = {
+    "laser_last_error": (C.c_char_p, []),
+    "laser_abi_version": (_I, []),
+    "laser_params_default": (None, [C.POINTER(laser_params)]),
+    "laser_ema_update": (_I, [C.POINTER(laser_params), C.POINTER(laser_load_state), _I]),
+    "laser_threshold": (_I, [C.POINTER(laser_params), C.c_double, C.POINTER(C.c_double)]),
+    "laser_budget": (_I, [C.POINTER(laser_params), _I, _I, C.POINTER(_I)]),
+    "laser_exit_decision": (_I, [C.POINTER(laser_params), C.POINTER(laser_load_state), C.c_float, _I, _I, _I,
+                                 C.POINTER(_I), C.POINTER(C.c_double)]),
+    "laser_pages_create": (_I, [_I, _I, _I, _I, C.POINTER(_P)]),
+    "laser_pages_add_seq": (_I, [_P, _I, _I]),
+    "laser_pages_append": (_I, [_P, _I, _I]),
+    "laser_pages_truncate": (_I, [_P, _I, _I]),
+    "laser_pages_free_seq": (_I, [_P, _I]),
+    "laser_pages_table": (_I, [_P, _I, _I32P, _I, C.POINTER(_I)]),
+    "laser_pages_seq_len": (_I, [_P, _I, C.POINTER(_I)]),
+    "laser_pages_num_free": (_I, [_P, C.POINTER(_I)]),
+    "laser_pages_destroy": (_I, [_P]),
+    "laser_model_create": (_I, [C.POINTER(laser_model_desc), C.POINTER(_P)]),
+    "laser_model_set_tensor": (_I, [_P, C.c_char_p, _P, C.c_size_t]),
+    "laser_workspace_size": (_I, [_P, _I, C.POINTER(C.c_size_t)]),
+    "laser_model_finalize": (_I, [_P, _I, _P, C.c_size_t, _P]),
+    "laser_model_destroy": (_I, [_P]),
+    "laser_kv_pool_bytes": (_I, [_P, _I, C.POINTER(C.c_size_t)]),
+    "laser_kv_create": (_I, [_P, _I, _I, _I, _P, _P, _P, C.POINTER(_P)]),
+    "laser_kv_add_seq": (_I, [_P, _I, _I]),
+    "laser_kv_import": (_I, [_P, _I, _P, _P, _I, _P]),
+    "laser_kv_export": (_I, [_P, _I, _P, _P, _P]),
+    "laser_kv_free_seq": (_I, [_P, _I]),
+    "laser_kv_seq_len": (_I, [_P, _I, C.POINTER(_I)]),
+    "laser_kv_page_table": (_I, [_P, _I, _I32P, _I, C.POINTER(_I)]),
+    "laser_kv_destroy": (_I, [_P]),
+    "laser_prefill": (_I, [_P, _P, _I, _P, _I, _P, _P]),
+    "laser_decode_step": (_I, [_P, _P, _I, _I32P, _P, _P, _P, _P, _P]),
+    "laser_probe_confidence": (_I, [_P, _P, _I, _I32P, _P, _I, _I, _P, _P, _P, _P]),
+    "laser_step_mixed": (_I, [_P, _P, _I, _I32P, _P, _P, _P, _I, _I32P, _P, _I, _I, _P, _P, _P]),
+    "laser_timing_enable": (_I, [_P, _I, _I]),
+    "laser_timing_read": (_I, [_P, _I, C.POINTER(C.c_double), C.POINTER(_I)]),
+}
+
+_lib = None
+
+
+def lib() -> C.CDLL:
+    """The loaded liblaser.so (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with `python -m paper_2606_31580_amd.build`")
+        L = C.CDLL(LIB_PATH)
+        for name, (res, args) in _SIGS.items():
+            f = getattr(L, name)
+            f.restype = res
+            f.argtypes = args
+        _lib = L
+    return _lib
+
+
+def exported_symbols():
+    return list(_SIGS)
+
+
+def check(code: int, fn: str) -> int:
+    if code != OK:
+        raise LaserError(code, fn, lib().laser_last_error().decode())
+    return code
+
+
+def _call(name, *args):
+    return check(getattr(lib(), name)(*args), name)
+
+
+def _i32arr(vals: Sequence[int]):
+    return (C.c_int32 * len(vals))(*[int(v) for v in vals])
+
+
+def _ptr(t) -> Optional[int]:
+    return None if t is None else t.data_ptr()
+
+
+# --------------------------------------------------------------------------- controller
+
+def laser_params_default() -> laser_params:
+    p = laser_params()
+    lib().laser_params_default(C.byref(p))
+    return p
+
+
+def laser_ema_update(p: laser_params, state: laser_load_state, active_requests: int) -> None:
+    _call("laser_ema_update", C.byref(p), C.byref(state), active_requests)
+
+
+def laser_threshold(p: laser_params, L_bar: float) -> float:
+    out = C.c_double()
+    _call("laser_threshold", C.byref(p), L_bar, C.byref(out))
+    return out.value
+
+
+def laser_budget(p: laser_params, prompt_len: int, active_requests: int) -> int:
+    out = C.c_int()
+    _call("laser_budget", C.byref(p), prompt_len, active_requests, C.byref(out))
+    return out.value
+
+
+def laser_exit_decision(p: laser_params, state: laser_load_state, confidence: float, active_requests: int, k_done: int,
+                        B_i: int):
+    d, lam = C.c_int(), C.c_double()
+    _call("laser_exit_decision", C.byref(p), C.byref(state), confidence, active_requests, k_done, B_i, C.byref(d),
+          C.byref(lam))
+    return d.value, lam.value
+
+
+# --------------------------------------------------------------------------- page pool
+
+class PagePool:
+    """Host page pool (laser_pages_*)."""
+
+    def __init__(self, num_pages: int, page_size: int = 16, max_seqs: int = 64, max_pages_per_seq: int = 4096):
+        h = C.c_void_p()
+        _call("laser_pages_create", num_pages, page_size, max_seqs, max_pages_per_seq, C.byref(h))
+        self.h = h
+        self.max_pages_per_seq = max_pages_per_seq
+
+    def add_seq(self, seq, length):
+        _call("laser_pages_add_seq", self.h, seq, length)
+
+    def append(self, seq, n=1):
+        _call("laser_pages_append", self.h, seq, n)
+
+    def truncate(self, seq, length):
+        _call("laser_pages_truncate", self.h, seq, length)
+
+    def free_seq(self, seq):
+        _call("laser_pages_free_seq", self.h, seq)
+
+    def table(self, seq):
+        buf = (C.c_int32 * self.max_pages_per_seq)()
+        n = C.c_int()
+        _call("laser_pages_table", self.h, seq, buf, self.max_pages_per_seq, C.byref(n))
+        return list(buf[: n.value])
+
+    def seq_len(self, seq):
+        n = C.c_int()
+        _call("laser_pages_seq_len", self.h, seq, C.byref(n))
+        return n.value
+
+    def num_free(self):
+        n = C.c_int()
+        _call("laser_pages_num_free", self.h, C.byref(n))
+        return n.value
+
+    def destroy(self):
+        if self.h:
+            _call("laser_pages_destroy", self.h)
+            self.h = None
+
+
+# --------------------------------------------------------------------------- model / KV (device)
+
+def desc_from_shape(shape, max_positions: int = 16640) -> laser_model_desc:
+    return laser_model_desc(
+        shape.n_layers, shape.d_model, shape.n_q_heads, shape.n_kv_heads, shape.head_dim, shape.d_ffn, shape.vocab,
+        int(shape.tied_embeddings), int(shape.qkv_bias), DTYPE_BF16 if shape.dtype == "bf16" else DTYPE_F32,
+        float(shape.rope_theta), float(shape.rms_eps), int(max_positions))
+
+
+def _stream_ptr(stream) -> Optional[int]:
+    import torch
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return stream.cuda_stream
+
+
+class Model:
+    """A finalized model over device weights (dict name -> torch tensor on the GPU)."""
+
+    def __init__(self, shape, weights: Dict[str, "object"], max_rows: int = 16, max_positions: int = 16640, stream=None):
+        import torch
+        self.shape = shape
+        self.weights = weights  # kept alive: the library borrows them
+        self.desc = desc_from_shape(shape, max_positions)
+        h = C.c_void_p()
+        _call("laser_model_create", C.byref(self.desc), C.byref(h))
+        self.h = h
+        for name, t in weights.items():
+            assert t.is_cuda and t.is_contiguous()
+            _call("laser_model_set_tensor", self.h, name.encode(), t.data_ptr(), t.numel() * t.element_size())
+        nbytes = C.c_size_t()
+        _call("laser_workspace_size", self.h, max_rows, C.byref(nbytes))
+        self.workspace = torch.empty(nbytes.value, dtype=torch.uint8, device=next(iter(weights.values())).device)
+        self.max_rows = max_rows
+        _call("laser_model_finalize", self.h, max_rows, self.workspace.data_ptr(), nbytes.value, _stream_ptr(stream))
+
+    def timing_enable(self, cls: int, on: bool = True):
+        _call("laser_timing_enable", self.h, cls, int(on))
+
+    def timing_read(self, cls: int):
+        ms, n = C.c_double(), C.c_int()
+        _call("laser_timing_read", self.h, cls, C.byref(ms), C.byref(n))
+        return ms.value, n.value
+
+    def destroy(self):
+        if self.h:
+            _call("laser_model_destroy", self.h)
+            self.h = None
+
+
+class KVCache:
+    """Paged KV cache: device pools and block table allocated here, bookkeeping in the library."""
+
+    def __init__(self, model: Model, num_pages: int, max_seqs: int, max_pages_per_seq: int):
+        import torch
+        dev = model.workspace.device
+        nb = C.c_size_t()
+        _call("laser_kv_pool_bytes", model.h, num_pages, C.byref(nb))
+        self.k_pool = torch.empty(nb.value, dtype=torch.uint8, device=dev)
+        self.v_pool = torch.empty(nb.value, dtype=torch.uint8, device=dev)
+        self.block_table = torch.zeros(max_seqs * max_pages_per_seq, dtype=torch.int32, device=dev)
+        self.model = model
+        self.max_pages_per_seq = max_pages_per_seq
+        h = C.c_void_p()
+        _call("laser_kv_create", model.h, num_pages, max_seqs, max_pages_per_seq, self.k_pool.data_ptr(),
+              self.v_pool.data_ptr(), self.block_table.data_ptr(), C.byref(h))
+        self.h = h
+
+    def add_seq(self, seq: int, length: int):
+        _call("laser_kv_add_seq", self.h, seq, length)
+
+    def import_kv(self, seq: int, k, v, stream=None):
+        _call("laser_kv_import", self.h, seq, k.data_ptr(), v.data_ptr(), k.shape[1], _stream_ptr(stream))
+
+    def export_kv(self, seq: int, k, v, stream=None):
+        _call("laser_kv_export", self.h, seq, k.data_ptr(), v.data_ptr(), _stream_ptr(stream))
+
+    def free_seq(self, seq: int):
+        _call("laser_kv_free_seq", self.h, seq)
+
+    def seq_len(self, seq: int) -> int:
+        n = C.c_int()
+        _call("laser_kv_seq_len", self.h, seq, C.byref(n))
+        return n.value
+
+    def page_table(self, seq: int):
+        buf = (C.c_int32 * self.max_pages_per_seq)()
+        n = C.c_int()
+        _call("laser_kv_page_table", self.h, seq, buf, self.max_pages_per_seq, C.byref(n))
+        return list(buf[: n.value])
+
+    def destroy(self):
+        if self.h:
+            _call("laser_kv_destroy", self.h)
+            self.h = None
+
+
+# --------------------------------------------------------------------------- hot path
+
+def laser_prefill(model: Model, kv: KVCache, seq_id: int, d_tokens, d_logits_last=None, stream=None):
+    _call("laser_prefill", model.h, kv.h, seq_id, d_tokens.data_ptr(), d_tokens.numel(), _ptr(d_logits_last),
+          _stream_ptr(stream))
+
+
+def laser_decode_step(model: Model, kv: KVCache, seq_ids: Sequence[int], d_tokens, d_next, d_max_prob, d_logits=None,
+                      stream=None):
+    _call("laser_decode_step", model.h, kv.h, len(seq_ids), _i32arr(seq_ids), d_tokens.data_ptr(), d_next.data_ptr(),
+          d_max_prob.data_ptr(), _ptr(d_logits), _stream_ptr(stream))
+
+
+def laser_probe_confidence(model: Model, kv: KVCache, seq_ids: Sequence[int], d_suffix, T: int, d_conf, d_argmax,
+                           d_logits=None, stream=None):
+    _call("laser_probe_confidence", model.h, kv.h, len(seq_ids), _i32arr(seq_ids), d_suffix.data_ptr(), d_suffix.numel(), T,
+          d_conf.data_ptr(), d_argmax.data_ptr(), _ptr(d_logits), _stream_ptr(stream))
+
+
+def laser_step_mixed(model: Model, kv: KVCache, seq_ids: Sequence[int], d_tokens, d_next, d_max_prob,
+                     probe_idx: Sequence[int], d_suffix, T: int, d_conf, d_argmax, stream=None):
+    n = len(probe_idx)
+    _call("laser_step_mixed", model.h, kv.h, len(seq_ids), _i32arr(seq_ids), d_tokens.data_ptr(), d_next.data_ptr(),
+          d_max_prob.data_ptr(), n, _i32arr(probe_idx) if n else None, _ptr(d_suffix) if n else None,
+          d_suffix.numel() if n else 0, T, _ptr(d_conf) if n else None, _ptr(d_argmax) if n else None, _stream_ptr(stream))
