@@ -32,7 +32,7 @@ def parse():
     ap.add_argument("--warmup", type=int, default=16)
     ap.add_argument("--workload", default="7B-b1-kv14336")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--profile-only", action="store_true", help="decode loop only (for rocprofv3 runs)")
+    ap.add_argument("--profile-only", action="store_true", help="steps only, no reporting (for rocprofv3 runs)")
     return ap.parse_args()
 
 
@@ -91,6 +91,8 @@ def main():
         L.laser_decode_step(model, kv, seqs, tokens, nxt, pmax)
         tokens.copy_(nxt)
         if wl.probe_every and (i + 1) % wl.probe_every == 0:
+            if timed_probe:  # latency of the probe itself, not of decode steps still queued
+                torch.cuda.synchronize()
             t0 = time.perf_counter()
             L.laser_probe_confidence(model, kv, seqs, suffix, T, conf, argm)
             c = conf.cpu().numpy()  # the controller needs the confidence on the host
@@ -104,10 +106,9 @@ def main():
         step(i, False)
     torch.cuda.synchronize()
 
-    if args.profile_only:
+    if args.profile_only:  # the timed loop's work (decode steps with their probes), nothing else
         for i in range(args.steps):
-            L.laser_decode_step(model, kv, seqs, tokens, nxt, pmax)
-            tokens.copy_(nxt)
+            step(args.warmup + i, False)
         torch.cuda.synchronize()
         log("profile loop done")
         return

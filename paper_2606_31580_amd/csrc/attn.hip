@@ -10,8 +10,10 @@
 //   O^T[d][c] += V^T[d][t] P^T[t][c] v_mfma_f32_16x16x16_bf16, B = P^T taken straight from
 //                                    the S^T accumulator layout (bf16 hi+lo)
 // The KV page layout makes every operand load a contiguous 1 KB (K) / 512 B (V) per wave
-// instruction.  Waves merge (m, l, O) in LDS; workgroups of the same (group, kv head)
-// merge through fp32 partials, combined in workgroup order by the last to arrive.
+// instruction.  Waves merge (m, l, O) in LDS; when a (group, kv head) spans several
+// workgroups their fp32 partials are combined by k_attn_merge, launched next.
+#include <type_traits>
+
 #include "device_common.hpp"
 #include "kernels.hpp"
 
@@ -34,7 +36,6 @@ __global__ __launch_bounds__(64 * kAttnWaves) void k_attn(AttnArgs a) {
   __shared__ int s_pos[NC];
   __shared__ float s_m[2][NC];
   __shared__ float s_l[2][NC];
-  __shared__ int s_last;
 
   const GroupDesc gd = a.plan->groups[blockIdx.z];
   const int wg = blockIdx.x;
@@ -44,23 +45,6 @@ __global__ __launch_bounds__(64 * kAttnWaves) void k_attn(AttnArgs a) {
   const int w = tid >> 6, l = tid & 63;
   const int lc = l & 15, lg = l >> 4;
   const int NQ = gd.nrows * a.G;
-
-  // stage queries (bf16 hi/lo) and each column's visible length
-  for (int idx = tid; idx < NC * HD; idx += blockDim.x) {
-    const int c = idx / HD, d = idx - c * HD;
-    float v = 0.f;
-    if (c < NQ) {
-      const int row = gd.row0 + c / a.G;
-      const int head = kvh * a.G + c % a.G;
-      v = a.q[((size_t)row * a.hq + head) * HD + d];
-    }
-    uint16_t hi, lo;
-    split_bf16(v, hi, lo);
-    s_qh[idx] = hi;
-    s_ql[idx] = lo;
-  }
-  for (int c = tid; c < NC; c += blockDim.x) s_pos[c] = c < NQ ? a.plan->rows[gd.row0 + c / a.G].pos : -1;
-  __syncthreads();
 
   float m_run[NT], l_run[NT];
   f32x4 o[NT][ND];
@@ -79,25 +63,51 @@ __global__ __launch_bounds__(64 * kAttnWaves) void k_attn(AttnArgs a) {
   const size_t layer_base = (size_t)a.layer * a.num_pages;
   const size_t blk_elems = (size_t)16 * HD;
 
-  for (int pg = p0; pg < p1; ++pg) {
+  // Page operands are loaded one page ahead of their use (raw bits; fp32 pools are split
+  // into bf16 hi/lo when used).
+  constexpr int KW = sizeof(KT) == 2 ? 1 : 2;  // 16-byte K loads per k-step
+  u32x4 kraw[2][NS][KW];
+  u32x4 vraw[2][ND];  // bf16: only the low 8 bytes are used
+  auto load_page = [&](int pg, auto bufc) {
+    constexpr int buf = decltype(bufc)::value;
     const int pid = btrow[pg];
     const size_t blk = ((layer_base + pid) * a.hkv + kvh) * blk_elems;
-    // K operand: lane l reads elements [s*512 + 8l, +8) -> K[t = l%16][d = 32s + 8(l/16) + j]
-    bf16x8 khi[NS], klo[NS];
-    s16x4 vhi[ND], vlo[ND];
     if (sizeof(KT) == 2) {
       const uint16_t* kb = (const uint16_t*)a.kpool + blk;
       const uint16_t* vb = (const uint16_t*)a.vpool + blk;
 #pragma unroll
-      for (int s = 0; s < NS; ++s) khi[s] = __builtin_bit_cast(bf16x8, ld_nt16(kb + s * 512 + 8 * l));
+      for (int s = 0; s < NS; ++s) kraw[buf][s][0] = ld_nt16(kb + s * 512 + 8 * l);
 #pragma unroll
-      for (int dt = 0; dt < ND; ++dt) vhi[dt] = __builtin_bit_cast(s16x4, ld_nt8(vb + dt * 256 + 4 * l));
+      for (int dt = 0; dt < ND; ++dt) {
+        const u32x2 t = ld_nt8(vb + dt * 256 + 4 * l);
+        vraw[buf][dt] = u32x4{t[0], t[1], 0u, 0u};
+      }
     } else {
       const float* kb = (const float*)a.kpool + blk;
       const float* vb = (const float*)a.vpool + blk;
 #pragma unroll
       for (int s = 0; s < NS; ++s) {
-        u32x4 x0 = ld_nt16(kb + s * 512 + 8 * l), x1 = ld_nt16(kb + s * 512 + 8 * l + 4);
+        kraw[buf][s][0] = ld_nt16(kb + s * 512 + 8 * l);
+        kraw[buf][s][KW - 1] = ld_nt16(kb + s * 512 + 8 * l + 4);
+      }
+#pragma unroll
+      for (int dt = 0; dt < ND; ++dt) vraw[buf][dt] = ld_nt16(vb + dt * 256 + 4 * l);
+    }
+  };
+  auto process_page = [&](int pg, auto cbc) {
+    constexpr int cb = decltype(cbc)::value;
+    // K operand: lane l holds K[t = l%16][d = 32s + 8(l/16) + j]; V^T: V[t = 4(l/16) + j][16dt + l%16]
+    bf16x8 khi[NS], klo[NS];
+    s16x4 vhi[ND], vlo[ND];
+    if (sizeof(KT) == 2) {
+#pragma unroll
+      for (int s = 0; s < NS; ++s) khi[s] = __builtin_bit_cast(bf16x8, kraw[cb][s][0]);
+#pragma unroll
+      for (int dt = 0; dt < ND; ++dt) vhi[dt] = __builtin_bit_cast(s16x4, u32x2{vraw[cb][dt][0], vraw[cb][dt][1]});
+    } else {
+#pragma unroll
+      for (int s = 0; s < NS; ++s) {
+        const u32x4 x0 = kraw[cb][s][0], x1 = kraw[cb][s][KW - 1];
         u32x4 ph, pl;
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
@@ -113,7 +123,7 @@ __global__ __launch_bounds__(64 * kAttnWaves) void k_attn(AttnArgs a) {
       }
 #pragma unroll
       for (int dt = 0; dt < ND; ++dt) {
-        u32x4 x = ld_nt16(vb + dt * 256 + 4 * l);
+        const u32x4 x = vraw[cb][dt];
         s16x4 h4, l4;
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
@@ -125,6 +135,18 @@ __global__ __launch_bounds__(64 * kAttnWaves) void k_attn(AttnArgs a) {
         vhi[dt] = h4;
         vlo[dt] = l4;
       }
+    }
+    // Slots past the group's last position hold no written value (possibly not even a
+    // finite one); P is zero there but 0 * NaN is not, so those V entries are zeroed.
+    if (pg * 16 + 15 > gd.maxpos) {
+#pragma unroll
+      for (int dt = 0; dt < ND; ++dt)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          if (pg * 16 + 4 * lg + j > gd.maxpos) {
+            vhi[dt][j] = 0;
+            if (sizeof(KT) == 4) vlo[dt][j] = 0;
+          }
     }
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
@@ -178,6 +200,34 @@ __global__ __launch_bounds__(64 * kAttnWaves) void k_attn(AttnArgs a) {
         o[nt][dt] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vhi[dt], plo, o[nt][dt], 0, 0, 0);
         if (sizeof(KT) == 4) o[nt][dt] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vlo[dt], phi, o[nt][dt], 0, 0, 0);
       }
+    }
+  };
+  using B0 = std::integral_constant<int, 0>;
+  using B1 = std::integral_constant<int, 1>;
+  if (p0 < p1) load_page(p0, B0{});
+  // queries are staged while the first page is in flight
+  for (int idx = tid; idx < NC * HD; idx += blockDim.x) {
+    const int c = idx / HD, d = idx - c * HD;
+    float v = 0.f;
+    if (c < NQ) {
+      const int row = gd.row0 + c / a.G;
+      const int head = kvh * a.G + c % a.G;
+      v = a.q[((size_t)row * a.hq + head) * HD + d];
+    }
+    uint16_t hi, lo;
+    split_bf16(v, hi, lo);
+    s_qh[idx] = hi;
+    s_ql[idx] = lo;
+  }
+  for (int c = tid; c < NC; c += blockDim.x) s_pos[c] = c < NQ ? a.plan->rows[gd.row0 + c / a.G].pos : -1;
+  __syncthreads();
+
+  for (int pg = p0; pg < p1; pg += 2) {
+    if (pg + 1 < p1) load_page(pg + 1, B1{});
+    process_page(pg, B0{});
+    if (pg + 1 < p1) {
+      if (pg + 2 < p1) load_page(pg + 2, B0{});
+      process_page(pg + 1, B1{});
     }
   }
 
@@ -240,31 +290,82 @@ __global__ __launch_bounds__(64 * kAttnWaves) void k_attn(AttnArgs a) {
     a.ml[(slot_base + c) * 2 + 0] = s_m[1][c];
     a.ml[(slot_base + c) * 2 + 1] = s_l[1][c];
   }
-  __threadfence();
-  __syncthreads();
-  int* cnt = a.cnt + blockIdx.z * a.hkv + kvh;
-  if (tid == 0) s_last = (atomicAdd(cnt, 1) == gd.nwg - 1);
-  __syncthreads();
-  if (!s_last) return;
-  __threadfence();
-  for (int idx = tid; idx < NQ * HD; idx += blockDim.x) {
-    const int c = idx / HD, d = idx - c * HD;
-    float M = -INFINITY;
-    for (int q = 0; q < gd.nwg; ++q) {
-      const size_t sb = ((size_t)kvh * kAttnMaxWG + q) * ncols + (size_t)gd.row0 * a.G + c;
-      M = fmaxf(M, __builtin_nontemporal_load(a.ml + sb * 2));
-    }
-    float L = 0.f, O = 0.f;
-    for (int q = 0; q < gd.nwg; ++q) {
-      const size_t sb = ((size_t)kvh * kAttnMaxWG + q) * ncols + (size_t)gd.row0 * a.G + c;
-      const float f = (M == -INFINITY) ? 0.f : safe_exp2(__builtin_nontemporal_load(a.ml + sb * 2) - M);
-      L += __builtin_nontemporal_load(a.ml + sb * 2 + 1) * f;
-      O += __builtin_nontemporal_load(a.part + sb * HD + d) * f;
-    }
-    const int row = gd.row0 + c / a.G, head = kvh * a.G + c % a.G;
-    a.o[((size_t)row * a.hq + head) * HD + d] = O / L;
+}
+
+// Combines the workgroup partials (m, l, O) of every (row, query head) whose group used
+// more than one attention workgroup: o = sum_w O_w 2^(m_w - M) / sum_w l_w 2^(m_w - M),
+// M = max_w m_w.  grid (rows, query heads), 256 threads: wave v takes partials w = v mod 4
+// (all loads of a wave issued together), lanes take dims; the four waves are combined in
+// LDS in fixed order.
+__global__ __launch_bounds__(256) void k_attn_merge(AttnArgs a, int hd) {
+  constexpr int PER = kAttnMaxWG / 4;
+  __shared__ float s_m[4], s_l[4];
+  __shared__ float s_o[4][128];
+  const int row = blockIdx.x, head = blockIdx.y;
+  const int v = threadIdx.x >> 6, l = threadIdx.x & 63;
+  const int kvh = head / a.G, gi = head - kvh * a.G;
+  const size_t ncols = (size_t)a.max_rows * a.G;
+  const size_t col = (size_t)row * a.G + gi;
+  // every slot is loaded before the group's workgroup count is known (slots past it are
+  // masked below), so the loads overlap the plan lookup
+  float mv[PER], lv[PER], o0[PER], o1[PER];
+#pragma unroll
+  for (int i = 0; i < PER; ++i) {
+    const size_t sb = ((size_t)kvh * kAttnMaxWG + v + 4 * i) * ncols + col;
+    mv[i] = a.ml[sb * 2];
+    lv[i] = a.ml[sb * 2 + 1];
+    o0[i] = a.part[sb * hd + l];
+    o1[i] = (l + 64 < hd) ? a.part[sb * hd + l + 64] : 0.f;
   }
-  if (tid == 0) *cnt = 0;
+  const Plan* plan = a.plan;
+  int z = 0;
+  while (z + 1 < plan->n_groups && plan->groups[z + 1].row0 <= row) ++z;
+  const int nwg = plan->groups[z].nwg;
+  if (nwg <= 1) return;  // written directly by the attention kernel
+#pragma unroll
+  for (int i = 0; i < PER; ++i)
+    if (v + 4 * i >= nwg) {
+      mv[i] = -INFINITY;
+      lv[i] = 0.f;
+      o0[i] = o1[i] = 0.f;
+    }
+  float M = -INFINITY;
+#pragma unroll
+  for (int i = 0; i < PER; ++i) M = fmaxf(M, mv[i]);
+  float L = 0.f, O0 = 0.f, O1 = 0.f;
+#pragma unroll
+  for (int i = 0; i < PER; ++i) {
+    const float f = (M == -INFINITY) ? 0.f : safe_exp2(mv[i] - M);
+    L += lv[i] * f;
+    O0 += o0[i] * f;
+    O1 += o1[i] * f;
+  }
+  if (l == 0) {
+    s_m[v] = M;
+    s_l[v] = L;
+  }
+  s_o[v][l] = O0;
+  s_o[v][l + 64] = O1;
+  __syncthreads();
+  if (v == 0) {
+    float Mt = fmaxf(fmaxf(s_m[0], s_m[1]), fmaxf(s_m[2], s_m[3]));
+    float Lt = 0.f, Ot0 = 0.f, Ot1 = 0.f;
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const float f = (s_m[u] == -INFINITY) ? 0.f : safe_exp2(s_m[u] - Mt);
+      Lt += s_l[u] * f;
+      Ot0 += s_o[u][l] * f;
+      Ot1 += s_o[u][l + 64] * f;
+    }
+    float* out = a.o + ((size_t)row * a.hq + head) * hd;
+    out[l] = Ot0 / Lt;
+    if (l + 64 < hd) out[l + 64] = Ot1 / Lt;
+  }
+}
+
+hipError_t launch_attn_merge(const AttnArgs& a, int M, int hd, hipStream_t s) {
+  hipLaunchKernelGGL(k_attn_merge, dim3(M, a.hq), dim3(256), 0, s, a, hd);
+  return hipGetLastError();
 }
 
 template <class KT, int HD>

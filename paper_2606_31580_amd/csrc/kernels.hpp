@@ -7,13 +7,13 @@
 
 namespace laser {
 
-constexpr int kMaxRows = 64;       // rows (tokens) of one forward
-constexpr int kPage = 16;          // positions per KV page
-constexpr int kMaxBt = 1024;       // block-table updates carried by one plan
-constexpr int kAttnWaves = 4;      // waves per attention workgroup (one split each)
-constexpr int kAttnMaxWG = 64;     // attention workgroups per (group, kv head)
-constexpr int kGemmThreads = 256;  // 4 waves; a GEMM unit covers 64 weight rows
-constexpr int kGroupRows = 64;
+constexpr int kMaxRows = 64;      // rows (tokens) of one forward
+constexpr int kPage = 16;         // positions per KV page
+constexpr int kMaxBt = 1024;      // block-table updates carried by one plan
+constexpr int kAttnWaves = 4;     // waves per attention workgroup (one split each)
+constexpr int kAttnMaxWG = 64;    // attention workgroups per (group, kv head)
+constexpr int kGemmThreads = 256; // 4 waves
+constexpr int kGemvMaxThreads = 512;
 
 // One row of a forward: request slot, position, and where its input token id lives.
 struct RowDesc {
@@ -22,6 +22,7 @@ struct RowDesc {
 // Rows of one request that share its KV pages in attention (contiguous rows).
 struct GroupDesc {
   int seq, row0, nrows, npages, pps, nwg;  // pps: pages per wave split; nwg: workgroups
+  int maxpos;                              // last position any row of the group sees
 };
 // LM-head output row: activation row, destination (sel, off) for token / prob / logits.
 struct OutDesc {
@@ -40,6 +41,7 @@ struct Plan {
   BtUpdate bt[kMaxBt];
 };
 
+// Softmax statistics of one group of vocabulary rows for one output row.
 struct LmPart {
   float mx, sum;
   int idx, pad;
@@ -47,24 +49,23 @@ struct LmPart {
 
 enum Epi { EPI_QKV = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_LMHEAD = 3 };
 
+// Output rows per workgroup of a projection: 8 on the VALU path, 16 (one matrix-core tile)
+// on the MFMA path.  Rotary and gate/up rows come in pairs, half of a group each.
+constexpr int rows_per_group(int, bool mfma) { return mfma ? 16 : 8; }
+
 struct GemmArgs {
   // weights (row-major [rows][K] in the model dtype)
   const void* w0;
   const void* w1;
   const void* w2;
-  int K, N, n_groups, n_splits, kslice, M;
-  // A operand: fp32 activations [row][ldx]; optional RMSNorm (gain, ss partials)
+  int K, N, M, n_groups;
+  // A operand: fp32 activation rows [row][ldx]; optional RMSNorm over the full row (gain)
   const float* x;
   int ldx;
   const void* gain;
-  const float* ss;  // [n_ss][kMaxRows] sums of squares of x rows
-  int n_ss;
   float eps;
   int row_map;  // A row m = plan->outs[m].row (LM head)
   const Plan* plan;
-  // split-K
-  float* part;
-  int* cnt;
   // EPI_QKV
   const void* b0;
   const void* b1;
@@ -77,17 +78,13 @@ struct GemmArgs {
   const int* bt;
   int max_pps, num_pages, layer;
   // EPI_RESID
-  float* h;       // [M][N]
-  float* ss_out;  // [N/64][kMaxRows]
+  float* h;  // [M][N]
   // EPI_SWIGLU
-  float* act;  // [M][F] (F = N/2 logical pairs)
+  float* act;  // [M][F]
   int F;
   // EPI_LMHEAD
   float* logits[2];  // [..][vocab] or null
-  int* tok_out[2];
-  float* p_out[2];
-  LmPart* lm_part;  // [n_groups][kMaxRows]
-  int* lm_cnt;
+  LmPart* lm_part;   // [n_groups][kMaxRows]
 };
 
 struct AttnArgs {
@@ -102,15 +99,16 @@ struct AttnArgs {
   float scale_log2;
   float* part;  // [hkv][kAttnMaxWG][max_rows*G][hd]
   float* ml;    // [hkv][kAttnMaxWG][max_rows*G][2]
-  int* cnt;     // [n_groups][hkv]
 };
 
 // dtype: 0 fp32, 1 bf16.  mode: 1..4 VALU rows per forward, 5..8 MFMA with 1..4 m-tiles.
-size_t gemm_lds_bytes(int dtype, int mode, int kslice, int M);
-hipError_t launch_gemm(int dtype, int mode, int epi, const GemmArgs& a, int grid, hipStream_t s);
+hipError_t launch_gemm(int dtype, int mode, int epi, const GemmArgs& a, hipStream_t s);
 hipError_t launch_attn(int dtype, int hd, int nt, const AttnArgs& a, dim3 grid, hipStream_t s);
+hipError_t launch_attn_merge(const AttnArgs& a, int M, int hd, hipStream_t s);
+hipError_t launch_lm_reduce(const Plan* plan, const LmPart* part, int n_groups, int n_out, int* tok0, int* tok1,
+                            float* p0, float* p1, hipStream_t s);
 hipError_t launch_embed(int dtype, const Plan* plan, int M, const void* embed, int d, int vocab, const int* tok0,
-                        const int* tok1, float* h, float* ss, int* bt, int max_pps, hipStream_t s);
+                        const int* tok1, float* h, int* bt, int max_pps, hipStream_t s);
 hipError_t launch_apply_bt(const Plan* plan, int* bt, int max_pps, hipStream_t s);
 hipError_t launch_kv_copy(int dtype, int to_pool, void* kpool, void* vpool, const int* bt, int max_pps,
                           int num_pages, int n_layers, int hkv, int hd, int seq, int len, void* k_lin,

@@ -67,15 +67,10 @@ struct LayerW {
 
 constexpr int kRing = 16;   // plan slots (pinned host + device)
 constexpr int kMaxT = 16;   // trial tokens per probe
-constexpr int kTargetUnits = 1024;  // GEMM workgroups aimed for per launch
 constexpr int kTargetAttnWaves = 2048;
-constexpr int kGemmLdsBudget = 48 * 1024;
 
 struct Layout {
-  size_t rope, h, ss, q, o, act, part, cnt, lm_part, lm_cnt, attn_part, attn_ml, attn_cnt, plans, probe_p, tok_buf,
-      p_buf, total;
-  size_t part_floats;
-  int cnt_ints;
+  size_t rope, h, q, o, act, lm_part, attn_part, attn_ml, plans, probe_p, tok_buf, p_buf, total;
 };
 
 struct Timer {
@@ -126,24 +121,11 @@ static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 static int gemm_mode(int M) { return M <= 4 ? M : 4 + ceil_div(M, 16); }
 
-// Split-K choice for a projection with n_groups 64-row groups, K inputs and M rows.
-static void gemm_plan(int K, int n_groups, int M, int* n_splits, int* kslice) {
-  int kmax = (kGemmLdsBudget / 4 - 64 * M) / M - 8;
-  kmax = std::max(32, kmax & ~31);
-  int splits = ceil_div(K, kmax);
-  const int want = ceil_div(kTargetUnits, n_groups);
-  const int by_width = std::max(1, K / 512);
-  splits = std::max(splits, std::min(want, by_width));
-  int ks = ceil_div(ceil_div(K, splits), 32) * 32;
-  if (ks > kmax) ks = kmax;
-  *kslice = ks;
-  *n_splits = ceil_div(K, ks);
-}
-
-static int groups_qkv(const laser_model_desc& d) { return (d.n_q_heads + 2 * d.n_kv_heads) * d.head_dim / 64; }
-static int groups_gateup(const laser_model_desc& d) { return ceil_div(d.d_ffn, 32); }
-static int groups_resid(const laser_model_desc& d) { return d.d_model / 64; }
-static int groups_lm(const laser_model_desc& d) { return ceil_div(d.vocab, 64); }
+static int rw_of(int M) { return rows_per_group(0, M > 4); }
+static int groups_qkv(const laser_model_desc& d, int M) { return (d.n_q_heads + 2 * d.n_kv_heads) * d.head_dim / rw_of(M); }
+static int groups_gateup(const laser_model_desc& d, int M) { return ceil_div(d.d_ffn, rw_of(M) / 2); }
+static int groups_resid(const laser_model_desc& d, int M) { return d.d_model / rw_of(M); }
+static int groups_lm(const laser_model_desc& d, int M) { return ceil_div(d.vocab, rw_of(M)); }
 
 static Layout make_layout(const laser_model_desc& d, int max_rows) {
   Layout L{};
@@ -154,38 +136,14 @@ static Layout make_layout(const laser_model_desc& d, int max_rows) {
     off = align256(off + bytes);
     return o;
   };
-  // largest split-K partial buffer over the projections and row counts
-  size_t part = 0;
-  int cnt = groups_lm(d) + 1;
-  struct K_ {
-    int K, groups;
-  } ks[5] = {{d.d_model, groups_qkv(d)},
-             {d.n_q_heads * hd, groups_resid(d)},
-             {d.d_model, groups_gateup(d)},
-             {d.d_ffn, groups_resid(d)},
-             {d.d_model, groups_lm(d)}};
-  for (int M = 1; M <= max_rows; ++M)
-    for (auto& k : ks) {
-      int ns, kl;
-      gemm_plan(k.K, k.groups, M, &ns, &kl);
-      if (ns > 1) part = std::max(part, (size_t)k.groups * ns * M * 64);
-      cnt = std::max(cnt, k.groups);
-    }
-  L.part_floats = part;
-  L.cnt_ints = cnt;
   L.rope = take((size_t)d.max_positions * (hd / 2) * sizeof(float2));
   L.h = take((size_t)max_rows * d.d_model * 4);
-  L.ss = take((size_t)(d.d_model / 64) * kMaxRows * 4);
   L.q = take((size_t)max_rows * d.n_q_heads * hd * 4);
   L.o = take((size_t)max_rows * d.n_q_heads * hd * 4);
   L.act = take((size_t)max_rows * d.d_ffn * 4);
-  L.part = take(std::max<size_t>(part, 1) * 4);
-  L.cnt = take((size_t)cnt * 4);
-  L.lm_part = take((size_t)groups_lm(d) * kMaxRows * sizeof(LmPart));
-  L.lm_cnt = take(4);
+  L.lm_part = take((size_t)groups_lm(d, 1) * kMaxRows * sizeof(LmPart));  // the VALU path has the most groups
   L.attn_part = take((size_t)d.n_kv_heads * kAttnMaxWG * max_rows * G * hd * 4);
   L.attn_ml = take((size_t)d.n_kv_heads * kAttnMaxWG * max_rows * G * 2 * 4);
-  L.attn_cnt = take((size_t)kMaxRows * d.n_kv_heads * 4);
   L.plans = take((size_t)kRing * sizeof(Plan));
   L.probe_p = take((size_t)kMaxRows * kMaxT * 4);
   L.tok_buf = take((size_t)kMaxRows * 4);
@@ -327,9 +285,6 @@ extern "C" laser_status laser_model_finalize(laser_model* m, int max_rows, void*
   }
   char* ws = (char*)d_workspace;
   HIP_TRY(hipMemcpyAsync(ws + L.rope, rope.data(), rope.size() * sizeof(float2), hipMemcpyHostToDevice, s));
-  HIP_TRY(hipMemsetAsync(ws + L.cnt, 0, (size_t)L.cnt_ints * 4, s));
-  HIP_TRY(hipMemsetAsync(ws + L.lm_cnt, 0, 4, s));
-  HIP_TRY(hipMemsetAsync(ws + L.attn_cnt, 0, (size_t)kMaxRows * d.n_kv_heads * 4, s));
   HIP_TRY(hipStreamSynchronize(s));  // the host rope table goes out of scope
   m->ws = ws;
   m->lay = L;
@@ -511,6 +466,7 @@ static void plan_groups(const laser_model* m, Plan& p) {
     g.row0 = r;
     g.nrows = e - r;
     g.npages = maxpos / kPage + 1;
+    g.maxpos = maxpos;
     units += (long long)g.npages * d.n_kv_heads;
     r = e;
   }
@@ -534,15 +490,12 @@ static laser_status run_forward(laser_model* m, laser_kv* kv, Plan& p, const int
   laser_status st = upload_plan(m, p, s, &dp);
   if (st != LASER_OK) return st;
   float* h = m->wsp<float>(L.h);
-  float* ss = m->wsp<float>(L.ss);
   HIP_TRY(timed(m, LASER_K_EMBED, s, [&] {
-    return launch_embed(dt, dp, p.M, m->embed, d.d_model, d.vocab, tok0, tok1, h, ss, kv->bt, max_pps, s);
+    return launch_embed(dt, dp, p.M, m->embed, d.d_model, d.vocab, tok0, tok1, h, kv->bt, max_pps, s);
   }));
 
   GemmArgs base{};
   base.plan = dp;
-  base.part = m->wsp<float>(L.part);
-  base.cnt = m->wsp<int>(L.cnt);
   base.eps = d.rms_eps;
   base.hq = d.n_q_heads;
   base.hkv = d.n_kv_heads;
@@ -555,20 +508,16 @@ static laser_status run_forward(laser_model* m, laser_kv* kv, Plan& p, const int
   base.max_pps = max_pps;
   base.num_pages = kv->pool.num_pages();
   base.h = h;
-  base.ss_out = ss;
   base.act = m->wsp<float>(L.act);
   base.F = d.d_ffn;
-  base.ss = ss;
-  base.n_ss = d.d_model / 64;
 
   auto gemm = [&](int cls, int epi, GemmArgs a, int K, int N, int n_groups, int M) -> laser_status {
     a.K = K;
     a.N = N;
     a.n_groups = n_groups;
     a.M = M;
-    gemm_plan(K, n_groups, M, &a.n_splits, &a.kslice);
     const int mode = gemm_mode(M);
-    HIP_TRY(timed(m, cls, s, [&] { return launch_gemm(dt, mode, epi, a, n_groups * a.n_splits, s); }));
+    HIP_TRY(timed(m, cls, s, [&] { return launch_gemm(dt, mode, epi, a, s); }));
     return LASER_OK;
   };
 
@@ -588,7 +537,6 @@ static laser_status run_forward(laser_model* m, laser_kv* kv, Plan& p, const int
   aa.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)hd));
   aa.part = m->wsp<float>(L.attn_part);
   aa.ml = m->wsp<float>(L.attn_ml);
-  aa.cnt = m->wsp<int>(L.attn_cnt);
   int max_nwg = 1, nt = 1;
   for (int i = 0; i < p.n_groups; ++i) {
     max_nwg = std::max(max_nwg, p.groups[i].nwg);
@@ -610,18 +558,22 @@ static laser_status run_forward(laser_model* m, laser_kv* kv, Plan& p, const int
     a.ldx = d.d_model;
     a.gain = W.attn_norm;
     a.layer = li;
-    st = gemm(LASER_K_QKV, EPI_QKV, a, d.d_model, (d.n_q_heads + 2 * d.n_kv_heads) * hd, groups_qkv(d), p.M);
+    st = gemm(LASER_K_QKV, EPI_QKV, a, d.d_model, (d.n_q_heads + 2 * d.n_kv_heads) * hd, groups_qkv(d, p.M), p.M);
     if (st != LASER_OK) return st;
 
     aa.layer = li;
-    HIP_TRY(timed(m, LASER_K_ATTN, s, [&] { return launch_attn(dt, hd, nt, aa, agrid, s); }));
+    HIP_TRY(timed(m, LASER_K_ATTN, s, [&] {
+      hipError_t e = launch_attn(dt, hd, nt, aa, agrid, s);
+      if (e == hipSuccess && max_nwg > 1) e = launch_attn_merge(aa, p.M, hd, s);
+      return e;
+    }));
 
     a = base;
     a.w0 = W.wo;
     a.x = m->wsp<float>(L.o);
     a.ldx = d.n_q_heads * hd;
     a.gain = nullptr;
-    st = gemm(LASER_K_OPROJ, EPI_RESID, a, d.n_q_heads * hd, d.d_model, groups_resid(d), p.M);
+    st = gemm(LASER_K_OPROJ, EPI_RESID, a, d.n_q_heads * hd, d.d_model, groups_resid(d, p.M), p.M);
     if (st != LASER_OK) return st;
 
     a = base;
@@ -630,7 +582,7 @@ static laser_status run_forward(laser_model* m, laser_kv* kv, Plan& p, const int
     a.x = h;
     a.ldx = d.d_model;
     a.gain = W.mlp_norm;
-    st = gemm(LASER_K_GATEUP, EPI_SWIGLU, a, d.d_model, 2 * d.d_ffn, groups_gateup(d), p.M);
+    st = gemm(LASER_K_GATEUP, EPI_SWIGLU, a, d.d_model, 2 * d.d_ffn, groups_gateup(d, p.M), p.M);
     if (st != LASER_OK) return st;
 
     a = base;
@@ -638,7 +590,7 @@ static laser_status run_forward(laser_model* m, laser_kv* kv, Plan& p, const int
     a.x = m->wsp<float>(L.act);
     a.ldx = d.d_ffn;
     a.gain = nullptr;
-    st = gemm(LASER_K_DOWN, EPI_RESID, a, d.d_ffn, d.d_model, groups_resid(d), p.M);
+    st = gemm(LASER_K_DOWN, EPI_RESID, a, d.d_ffn, d.d_model, groups_resid(d, p.M), p.M);
     if (st != LASER_OK) return st;
   }
   if (p.n_out > 0) {
@@ -648,15 +600,15 @@ static laser_status run_forward(laser_model* m, laser_kv* kv, Plan& p, const int
     a.ldx = d.d_model;
     a.gain = m->final_norm;
     a.row_map = 1;
-    for (int i = 0; i < 2; ++i) {
-      a.logits[i] = outs.logits[i];
-      a.tok_out[i] = outs.tok[i];
-      a.p_out[i] = outs.p[i];
-    }
+    a.logits[0] = outs.logits[0];
+    a.logits[1] = outs.logits[1];
     a.lm_part = m->wsp<LmPart>(L.lm_part);
-    a.lm_cnt = m->wsp<int>(L.lm_cnt);
-    st = gemm(LASER_K_LMHEAD, EPI_LMHEAD, a, d.d_model, d.vocab, groups_lm(d), p.n_out);
+    const int ng = groups_lm(d, p.n_out);
+    st = gemm(LASER_K_LMHEAD, EPI_LMHEAD, a, d.d_model, d.vocab, ng, p.n_out);
     if (st != LASER_OK) return st;
+    HIP_TRY(timed(m, LASER_K_LMHEAD, s, [&] {
+      return launch_lm_reduce(dp, a.lm_part, ng, p.n_out, outs.tok[0], outs.tok[1], outs.p[0], outs.p[1], s);
+    }));
   }
   return LASER_OK;
 }

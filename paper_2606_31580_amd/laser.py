@@ -220,7 +220,8 @@ def _stream_ptr(stream) -> Optional[int]:
 class Model:
     """A finalized model over device weights (dict name -> torch tensor on the GPU)."""
 
-    def __init__(self, shape, weights: Dict[str, "object"], max_rows: int = 16, max_positions: int = 16640, stream=None):
+    def __init__(self, shape, weights: Dict[str, "object"], max_rows: int = 16, max_positions: int = 16640, stream=None,
+                 poison: bool = False):
         import torch
         self.shape = shape
         self.weights = weights  # kept alive: the library borrows them
@@ -235,6 +236,8 @@ class Model:
         _call("laser_workspace_size", self.h, max_rows, C.byref(nbytes))
         self.workspace = torch.empty(nbytes.value, dtype=torch.uint8, device=next(iter(weights.values())).device)
         self.max_rows = max_rows
+        if poison:  # tests: NaN bytes everywhere, so any read of unwritten workspace shows
+            self.workspace.fill_(0xFF)
         _call("laser_model_finalize", self.h, max_rows, self.workspace.data_ptr(), nbytes.value, _stream_ptr(stream))
 
     def timing_enable(self, cls: int, on: bool = True):
@@ -254,7 +257,7 @@ class Model:
 class KVCache:
     """Paged KV cache: device pools and block table allocated here, bookkeeping in the library."""
 
-    def __init__(self, model: Model, num_pages: int, max_seqs: int, max_pages_per_seq: int):
+    def __init__(self, model: Model, num_pages: int, max_seqs: int, max_pages_per_seq: int, poison: bool = False):
         import torch
         dev = model.workspace.device
         nb = C.c_size_t()
@@ -262,6 +265,9 @@ class KVCache:
         self.k_pool = torch.empty(nb.value, dtype=torch.uint8, device=dev)
         self.v_pool = torch.empty(nb.value, dtype=torch.uint8, device=dev)
         self.block_table = torch.zeros(max_seqs * max_pages_per_seq, dtype=torch.int32, device=dev)
+        if poison:  # tests: unwritten KV slots read as NaN
+            self.k_pool.fill_(0xFF)
+            self.v_pool.fill_(0xFF)
         self.model = model
         self.max_pages_per_seq = max_pages_per_seq
         h = C.c_void_p()

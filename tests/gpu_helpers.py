@@ -33,12 +33,12 @@ def make_pair(shape, max_rows, max_positions, weights_on_device=False, cache_ora
         w_dev = {k: v.to(dev) for k, v in synth.make_weights(shape).items()}
     host = {k: synth.to_numpy(v) for k, v in w_dev.items()}
     orc = DecoderOracle(shape, host, cache_weights=cache_oracle)
-    model = L.Model(shape, w_dev, max_rows=max_rows, max_positions=max_positions)
+    model = L.Model(shape, w_dev, max_rows=max_rows, max_positions=max_positions, poison=True)
     return model, orc, w_dev
 
 
 def kv_pair(model, shape, num_pages, max_seqs, max_pages_per_seq):
-    return L.KVCache(model, num_pages, max_seqs, max_pages_per_seq), OraclePool(num_pages)
+    return L.KVCache(model, num_pages, max_seqs, max_pages_per_seq, poison=True), OraclePool(num_pages)
 
 
 def export_seq(kv, shape, seq):

@@ -37,7 +37,7 @@ def probe_and_compare(model, kv, orc, states, seqs, suffix, d_suffix, what):
     lens = [kv.seq_len(s) for s in seqs]
     L.laser_probe_confidence(model, kv, seqs, d_suffix, T, d_conf, d_arg, d_log)
     torch.cuda.synchronize()
-    conf, arg, lg = d_conf.cpu().numpy(), d_arg.cpu().numpy(), d_log.cpu().numpy().reshape(B, T, V)
+    conf, arg, lg = d_conf.cpu().numpy(), d_arg.cpu().numpy().reshape(B, T), d_log.cpu().numpy().reshape(B, T, V)
     for b, s in enumerate(seqs):
         res = orc.probe(states[b], suffix, T, keep_logits=True)
         agree = True

@@ -5,6 +5,7 @@ times); the oracle starts from the same pre-filled KV and weights (host copies) 
 computes the sampled outputs one token at a time: decode logits, greedy tokens,
 max-probabilities, the probe's confidence and trial tokens, page tables.
 """
+import gc
 import sys
 import time
 
@@ -12,82 +13,159 @@ import numpy as np
 import pytest
 import torch
 
-from gpu_helpers import PROB_TOL, check_token, compare_logits, export_seq, make_pair, require_gpu
+from gpu_helpers import PROB_TOL, check_token, compare_logits, make_pair, require_gpu
+from oracle.pages import PagePool as OraclePool
 from oracle.transformer import SeqState, lm_stats
 from paper_2606_31580_amd import laser as L
 from paper_2606_31580_amd import synth
-from paper_2606_31580_amd.configs import QWEN_1P5B
+from paper_2606_31580_amd.configs import LLAMA_8B, QWEN_1P5B, QWEN_7B
 
 pytestmark = pytest.mark.gpu
 
 S, T = 8, 4
+T0 = [time.time()]
 
 
 def log(*a):
-    print(*a, flush=True)
+    print(f"[{time.time() - T0[0]:6.1f}s]", *a, flush=True)
     sys.stdout.flush()
 
 
-def run_state_injection(shape, lens, n_steps, probe_seq=0, max_rows=16):
-    dev = require_gpu()
-    t0 = time.time()
-    max_pos = max(lens) + n_steps + S + T + 64
-    model, orc, _ = make_pair(shape, max_rows=max_rows, max_positions=max_pos, weights_on_device=True,
-                              cache_oracle=True)
-    pps = max_pos // 16 + 1
-    kv = L.KVCache(model, sum(n // 16 + 4 for n in lens) + 8, len(lens), pps)
-    states = []
-    for i, n in enumerate(lens):
-        k0, v0 = synth.make_prefill_kv(shape, n, i, device=dev)
-        kv.add_seq(i, n)
-        kv.import_kv(i, k0, v0)
-        states.append(SeqState.from_prefill(shape, synth.to_numpy(k0), synth.to_numpy(v0), max_pos))
-        del k0, v0
-    log(f"{shape.name}: setup {time.time() - t0:.1f}s")
-    B = len(lens)
-    V = shape.vocab
-    seqs = list(range(B))
-    toks = [int(t) for t in synth.make_tokens(B, V, 3003)]
-    d_tok = torch.zeros(B, dtype=torch.int32, device=dev)
-    d_next = torch.zeros(B, dtype=torch.int32, device=dev)
-    d_p = torch.zeros(B, device=dev)
-    d_logits = torch.zeros(B, V, device=dev)
-    for step in range(n_steps):
-        d_tok.copy_(torch.tensor(toks, dtype=torch.int32))
-        L.laser_decode_step(model, kv, seqs, d_tok, d_next, d_p, d_logits)
+class Setup:
+    def __init__(self, shape, lens, extra=64):
+        T0[0] = time.time()
+        dev = require_gpu()
+        self.shape, self.lens, self.dev = shape, lens, dev
+        max_pos = max(lens) + extra + S + T + 64
+        self.model, self.orc, _ = make_pair(shape, max_rows=64, max_positions=max_pos, weights_on_device=True,
+                                            cache_oracle=True)
+        pps = max_pos // 16 + 1
+        num_pages = sum(n // 16 + 4 for n in lens) + 8 * len(lens) + 8
+        self.kv = L.KVCache(self.model, num_pages, len(lens), pps, poison=True)
+        self.opool = OraclePool(num_pages)
+        self.states = []
+        for i, n in enumerate(lens):
+            k0, v0 = synth.make_prefill_kv(shape, n, i, device=dev)
+            self.kv.add_seq(i, n)
+            self.opool.add_seq(i, n)
+            self.kv.import_kv(i, k0, v0)
+            self.states.append(SeqState.from_prefill(shape, synth.to_numpy(k0), synth.to_numpy(v0), max_pos))
+            del k0, v0
+        self.seqs = list(range(len(lens)))
+        self.toks = [int(t) for t in synth.make_tokens(len(lens), shape.vocab, 3003)]
+        self.suffix = [int(t) for t in synth.make_suffix(S, shape.vocab)]
+        self.d_suffix = torch.tensor(self.suffix, dtype=torch.int32, device=dev)
+        log(f"{shape.name} lens {lens}: setup done")
+
+    def check_tables(self):
+        for s in self.seqs:
+            assert self.kv.page_table(s) == self.opool.tables[s], f"page table of seq {s}"
+            assert self.kv.seq_len(s) == self.states[s].length
+
+    def decode(self, n_steps):
+        B, V = len(self.seqs), self.shape.vocab
+        d_tok = torch.zeros(B, dtype=torch.int32, device=self.dev)
+        d_next = torch.zeros(B, dtype=torch.int32, device=self.dev)
+        d_p = torch.zeros(B, device=self.dev)
+        d_logits = torch.zeros(B, V, device=self.dev)
+        for step in range(n_steps):
+            d_tok.copy_(torch.tensor(self.toks, dtype=torch.int32))
+            L.laser_decode_step(self.model, self.kv, self.seqs, d_tok, d_next, d_p, d_logits)
+            torch.cuda.synchronize()
+            for b in self.seqs:
+                self.opool.append(b, 1)
+                ref = self.orc.decode_token(self.states[b], self.toks[b])
+                err = compare_logits(d_logits[b].cpu().numpy(), ref, f"step {step} seq {b}")
+                check_token(d_next[b].item(), ref, f"step {step} seq {b}")
+                assert abs(d_p[b].item() - lm_stats(ref)[1]) <= PROB_TOL
+                self.toks[b] = lm_stats(ref)[0]
+                log(f"decode step {step} seq {b} (ctx {self.states[b].length}): logits err {err:.3g}")
+            self.check_tables()
+
+    def compare_probe(self, b, gpu_tokens, gpu_conf, gpu_logits=None):
+        res = self.orc.probe(self.states[b], self.suffix, T, keep_logits=gpu_logits is not None)
+        agree = True
+        for j in range(T):
+            if not agree:
+                break
+            tok, _, margin = lm_stats(res.logits[j]) if res.logits else (res.tokens[j], 0, res.margins[j])
+            if gpu_logits is not None:
+                compare_logits(gpu_logits[j], res.logits[j], f"probe seq {b} trial {j}")
+            agree = int(gpu_tokens[j]) == tok
+            if margin > 1e-2:
+                assert agree, f"probe seq {b} trial {j}: {gpu_tokens[j]} vs {tok}"
+        if agree:
+            assert abs(gpu_conf - res.confidence) <= PROB_TOL
+        log(f"probe seq {b}: conf gpu {gpu_conf:.6g} oracle {res.confidence:.6g}")
+
+    def probe(self, seqs):
+        B, V = len(seqs), self.shape.vocab
+        d_conf = torch.zeros(B, device=self.dev)
+        d_arg = torch.zeros(B * T, dtype=torch.int32, device=self.dev)
+        d_plog = torch.zeros(B * T, V, device=self.dev)
+        L.laser_probe_confidence(self.model, self.kv, seqs, self.d_suffix, T, d_conf, d_arg, d_plog)
         torch.cuda.synchronize()
-        for b in seqs:
-            ref = orc.decode_token(states[b], toks[b])
-            err = compare_logits(d_logits[b].cpu().numpy(), ref, f"step {step} seq {b}")
-            check_token(d_next[b].item(), ref, f"step {step} seq {b}")
-            assert abs(d_p[b].item() - lm_stats(ref)[1]) <= PROB_TOL
-            toks[b] = lm_stats(ref)[0]
-            log(f"{shape.name} step {step} seq {b}: logits err {err:.3g} ({time.time() - t0:.0f}s)")
-    # the probe of one request at full size
-    suffix = [int(t) for t in synth.make_suffix(S, V)]
-    d_suffix = torch.tensor(suffix, dtype=torch.int32, device=dev)
-    table = kv.page_table(probe_seq)
-    d_conf = torch.zeros(1, device=dev)
-    d_arg = torch.zeros(T, dtype=torch.int32, device=dev)
-    d_plog = torch.zeros(T, V, device=dev)
-    L.laser_probe_confidence(model, kv, [probe_seq], d_suffix, T, d_conf, d_arg, d_plog)
-    torch.cuda.synchronize()
-    res = orc.probe(states[probe_seq], suffix, T, keep_logits=True)
-    agree = True
-    for j in range(T):
-        if not agree:
-            break
-        compare_logits(d_plog[j].cpu().numpy(), res.logits[j], f"probe trial {j}")
-        tok, _, margin = lm_stats(res.logits[j])
-        agree = int(d_arg[j].item()) == tok
-        if margin > 1e-2:
-            assert agree
-    if agree:
-        assert abs(d_conf.item() - res.confidence) <= PROB_TOL
-    assert kv.page_table(probe_seq) == table
-    log(f"{shape.name}: probe conf gpu {d_conf.item():.6g} oracle {res.confidence:.6g} ({time.time() - t0:.0f}s)")
-    return model, kv
+        arg = d_arg.cpu().numpy().reshape(B, T)
+        lg = d_plog.cpu().numpy().reshape(B, T, V)
+        for i, b in enumerate(seqs):
+            self.compare_probe(b, arg[i], d_conf[i].item(), lg[i])
+        self.check_tables()
+
+    def release(self):
+        self.kv.destroy()
+        self.model.destroy()
+        del self.orc, self.states
+        gc.collect()
+        torch.cuda.empty_cache()
 
 
 def test_qwen1p5b_kv4096_state_injection():
-    run_state_injection(QWEN_1P5B, [4096], n_steps=2)
+    st = Setup(QWEN_1P5B, [4096])
+    st.decode(2)
+    st.probe([0])
+    st.release()
+
+
+def test_qwen7b_b1_kv14336_state_injection():
+    st = Setup(QWEN_7B, [14336])
+    st.decode(1)
+    st.probe([0])
+    st.release()
+
+
+def test_qwen7b_b4_ragged_state_injection():
+    st = Setup(QWEN_7B, [3000, 6000, 10000, 14000])
+    st.decode(1)
+    st.probe([0, 1, 2, 3])  # 32 chunk rows through the MFMA path
+    st.release()
+
+
+def test_llama8b_b8_mixed_step_state_injection():
+    lens = synth.make_ragged_lengths(8, 3000, 14000)
+    st = Setup(LLAMA_8B, lens)
+    probe_idx = synth.make_mixed_schedule(8, 1)[0]
+    B, V = 8, LLAMA_8B.vocab
+    d_tok = torch.tensor(st.toks, dtype=torch.int32, device=st.dev)
+    d_next = torch.zeros(B, dtype=torch.int32, device=st.dev)
+    d_p = torch.zeros(B, device=st.dev)
+    d_conf = torch.zeros(len(probe_idx), device=st.dev)
+    d_arg = torch.zeros(len(probe_idx) * T, dtype=torch.int32, device=st.dev)
+    # 8 decode rows + 4 x 8 probe rows = 40 rows in one forward
+    L.laser_step_mixed(st.model, st.kv, st.seqs, d_tok, d_next, d_p, probe_idx, st.d_suffix, T, d_conf, d_arg)
+    torch.cuda.synchronize()
+    for b in st.seqs:
+        st.opool.append(b, 1)
+    for b in probe_idx:
+        st.opool.append(b, S + T - 1)
+    for b in st.seqs:
+        ref = st.orc.decode_token(st.states[b], st.toks[b])
+        check_token(d_next[b].item(), ref, f"mixed decode seq {b}")
+        assert abs(d_p[b].item() - lm_stats(ref)[1]) <= PROB_TOL
+        log(f"mixed decode seq {b} ok")
+    for b in probe_idx:
+        st.opool.truncate(b, st.states[b].length)
+    arg = d_arg.cpu().numpy().reshape(len(probe_idx), T)
+    for i, b in enumerate(probe_idx):
+        st.compare_probe(b, arg[i], d_conf[i].item())
+    st.check_tables()
+    st.release()
