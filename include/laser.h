@@ -247,17 +247,37 @@ laser_status laser_step_mixed(laser_model* m, laser_kv* kv, int batch, const int
                               int32_t* d_argmax, void* stream);
 
 /* ========================================================================== */
-/* Kernel timing (HIP events recorded around every launch of the enabled classes). */
+/* Kernel timing.  While any class is enabled (a timing session), forwards launch their
+ * kernels one by one (no graph replay) and every launch records a HIP event, created
+ * without a system-scope fence, at its end.  A launch of a class is timed from the end of
+ * the kernel launched just before it to the end of the class's last kernel (attention
+ * includes its merge kernel, the LM head its reduce kernel), which with back-to-back
+ * kernels equals the sum of their kernel-trace durations; each event adds about a
+ * microsecond to the kernel it ends.  At most 65536 launches are timed per session. */
 /* ========================================================================== */
 enum {
   LASER_K_EMBED = 0, LASER_K_QKV = 1, LASER_K_ATTN = 2, LASER_K_OPROJ = 3,
   LASER_K_GATEUP = 4, LASER_K_DOWN = 5, LASER_K_LMHEAD = 6, LASER_K_OTHER = 7, LASER_K_NCLASS = 8
 };
-/* Enables (1) or disables (0) event timing of one kernel class; clears its totals. */
+/* Enables (1) or disables (0) timing of one kernel class; clears its spans. */
 laser_status laser_timing_enable(laser_model* m, int kernel_class, int enable);
-/* Synchronises the recorded events and returns the summed duration (ms) and launch
- * count of the class since it was enabled or last read, then clears them. */
+/* Waits for the class's last recorded event and returns the summed duration (ms) and the
+ * number of timed launches since it was enabled or last read, then clears them. */
 laser_status laser_timing_read(laser_model* m, int kernel_class, double* total_ms, int* launches);
+
+/* ========================================================================== */
+/* Graph replay                                                               */
+/* ========================================================================== */
+/* With graphs on (the default), the kernels of a decode, probe or mixed forward are
+ * captured once per launch signature (rows, outputs, request groups, attention grid, KV
+ * cache) into a HIP graph and replayed; per-call data (positions, pages, the caller's
+ * token and output buffers) travels in the plan each forward uploads.  Results are
+ * bitwise identical to launching the kernels one by one, which is what happens with
+ * graphs off, while any kernel class is being timed, and for laser_prefill.  Up to 16
+ * graphs are kept per model; the least recently used is released first.
+ * Forwards of one model must be ordered (one stream, or synchronised between streams):
+ * they share the model's workspace and its one device plan slot. */
+laser_status laser_model_set_graphs(laser_model* m, int enable);
 
 #ifdef __cplusplus
 }

@@ -19,6 +19,16 @@
 
 namespace laser {
 
+// Calls f(integral_constant<int, i>) for i = 0 .. N-1 (compile-time ring-buffer indices, so
+// register arrays are never indexed dynamically).
+template <int N, int I = 0, class F>
+__device__ __forceinline__ void static_for(F&& f) {
+  if constexpr (I < N) {
+    f(std::integral_constant<int, I>{});
+    static_for<N, I + 1>(f);
+  }
+}
+
 __device__ __forceinline__ float safe_exp2(float x) { return x == -INFINITY ? 0.f : exp2f(x); }
 
 template <class KT, int HD, int NT>
@@ -63,11 +73,13 @@ __global__ __launch_bounds__(64 * kAttnWaves) void k_attn(AttnArgs a) {
   const size_t layer_base = (size_t)a.layer * a.num_pages;
   const size_t blk_elems = (size_t)16 * HD;
 
-  // Page operands are loaded one page ahead of their use (raw bits; fp32 pools are split
-  // into bf16 hi/lo when used).
+  // Page operands are loaded D pages ahead of their use into a ring of raw buffers (bf16
+  // bits; fp32 pools are split into bf16 hi/lo when used).  With one query tile a wave's
+  // whole run of pages is usually in flight at once.
+  constexpr int D = (sizeof(KT) == 2 && NT == 1) ? 4 : 2;
   constexpr int KW = sizeof(KT) == 2 ? 1 : 2;  // 16-byte K loads per k-step
-  u32x4 kraw[2][NS][KW];
-  u32x4 vraw[2][ND];  // bf16: only the low 8 bytes are used
+  u32x4 kraw[D][NS][KW];
+  u32x4 vraw[D][ND];  // bf16: only the low 8 bytes are used
   auto load_page = [&](int pg, auto bufc) {
     constexpr int buf = decltype(bufc)::value;
     const int pid = btrow[pg];
@@ -202,10 +214,10 @@ __global__ __launch_bounds__(64 * kAttnWaves) void k_attn(AttnArgs a) {
       }
     }
   };
-  using B0 = std::integral_constant<int, 0>;
-  using B1 = std::integral_constant<int, 1>;
-  if (p0 < p1) load_page(p0, B0{});
-  // queries are staged while the first page is in flight
+  static_for<D>([&](auto b) {
+    if (p0 + (int)b < p1) load_page(p0 + (int)b, b);
+  });
+  // queries are staged while the first pages are in flight
   for (int idx = tid; idx < NC * HD; idx += blockDim.x) {
     const int c = idx / HD, d = idx - c * HD;
     float v = 0.f;
@@ -222,13 +234,14 @@ __global__ __launch_bounds__(64 * kAttnWaves) void k_attn(AttnArgs a) {
   for (int c = tid; c < NC; c += blockDim.x) s_pos[c] = c < NQ ? a.plan->rows[gd.row0 + c / a.G].pos : -1;
   __syncthreads();
 
-  for (int pg = p0; pg < p1; pg += 2) {
-    if (pg + 1 < p1) load_page(pg + 1, B1{});
-    process_page(pg, B0{});
-    if (pg + 1 < p1) {
-      if (pg + 2 < p1) load_page(pg + 2, B0{});
-      process_page(pg + 1, B1{});
-    }
+  for (int base = p0; base < p1; base += D) {
+    static_for<D>([&](auto b) {
+      const int pg = base + (int)b;
+      if (pg < p1) {
+        process_page(pg, b);
+        if (pg + D < p1) load_page(pg + D, b);
+      }
+    });
   }
 
   // ---- merge the 4 waves in two rounds through 2 LDS slots
@@ -294,24 +307,25 @@ __global__ __launch_bounds__(64 * kAttnWaves) void k_attn(AttnArgs a) {
 
 // Combines the workgroup partials (m, l, O) of every (row, query head) whose group used
 // more than one attention workgroup: o = sum_w O_w 2^(m_w - M) / sum_w l_w 2^(m_w - M),
-// M = max_w m_w.  grid (rows, query heads), 256 threads: wave v takes partials w = v mod 4
-// (all loads of a wave issued together), lanes take dims; the four waves are combined in
-// LDS in fixed order.
-__global__ __launch_bounds__(256) void k_attn_merge(AttnArgs a, int hd) {
-  constexpr int PER = kAttnMaxWG / 4;
-  __shared__ float s_m[4], s_l[4];
-  __shared__ float s_o[4][128];
+// M = max_w m_w.  grid (rows, query heads), 16 waves: wave v takes partials w = v mod 16
+// (all loads of a wave issued together, before the plan lookup), lanes take dims; the
+// waves are then combined in LDS in fixed order.
+constexpr int kMergeWaves = 16;
+__global__ __launch_bounds__(64 * kMergeWaves) void k_attn_merge(AttnArgs a, int hd) {
+  constexpr int PER = kAttnMaxWG / kMergeWaves;
+  __shared__ float s_m[kMergeWaves], s_l[kMergeWaves];
+  __shared__ float s_o[kMergeWaves][128];
   const int row = blockIdx.x, head = blockIdx.y;
   const int v = threadIdx.x >> 6, l = threadIdx.x & 63;
   const int kvh = head / a.G, gi = head - kvh * a.G;
   const size_t ncols = (size_t)a.max_rows * a.G;
   const size_t col = (size_t)row * a.G + gi;
   // every slot is loaded before the group's workgroup count is known (slots past it are
-  // masked below), so the loads overlap the plan lookup
+  // replaced below, never combined), so the loads overlap the plan lookup
   float mv[PER], lv[PER], o0[PER], o1[PER];
 #pragma unroll
   for (int i = 0; i < PER; ++i) {
-    const size_t sb = ((size_t)kvh * kAttnMaxWG + v + 4 * i) * ncols + col;
+    const size_t sb = ((size_t)kvh * kAttnMaxWG + v + kMergeWaves * i) * ncols + col;
     mv[i] = a.ml[sb * 2];
     lv[i] = a.ml[sb * 2 + 1];
     o0[i] = a.part[sb * hd + l];
@@ -324,7 +338,7 @@ __global__ __launch_bounds__(256) void k_attn_merge(AttnArgs a, int hd) {
   if (nwg <= 1) return;  // written directly by the attention kernel
 #pragma unroll
   for (int i = 0; i < PER; ++i)
-    if (v + 4 * i >= nwg) {
+    if (v + kMergeWaves * i >= nwg) {
       mv[i] = -INFINITY;
       lv[i] = 0.f;
       o0[i] = o1[i] = 0.f;
@@ -348,10 +362,12 @@ __global__ __launch_bounds__(256) void k_attn_merge(AttnArgs a, int hd) {
   s_o[v][l + 64] = O1;
   __syncthreads();
   if (v == 0) {
-    float Mt = fmaxf(fmaxf(s_m[0], s_m[1]), fmaxf(s_m[2], s_m[3]));
+    float Mt = -INFINITY;
+#pragma unroll
+    for (int u = 0; u < kMergeWaves; ++u) Mt = fmaxf(Mt, s_m[u]);
     float Lt = 0.f, Ot0 = 0.f, Ot1 = 0.f;
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
+    for (int u = 0; u < kMergeWaves; ++u) {
       const float f = (s_m[u] == -INFINITY) ? 0.f : safe_exp2(s_m[u] - Mt);
       Lt += s_l[u] * f;
       Ot0 += s_o[u][l] * f;
@@ -364,20 +380,18 @@ __global__ __launch_bounds__(256) void k_attn_merge(AttnArgs a, int hd) {
 }
 
 hipError_t launch_attn_merge(const AttnArgs& a, int M, int hd, hipStream_t s) {
-  hipLaunchKernelGGL(k_attn_merge, dim3(M, a.hq), dim3(256), 0, s, a, hd);
-  return hipGetLastError();
+  return launch_k(k_attn_merge, dim3(M, a.hq), dim3(64 * kMergeWaves), s, a, hd);
 }
 
 template <class KT, int HD>
 static hipError_t launch_nt(int nt, const AttnArgs& a, dim3 grid, hipStream_t s) {
   const dim3 block(64 * kAttnWaves);
   switch (nt) {
-    case 1: hipLaunchKernelGGL((k_attn<KT, HD, 1>), grid, block, 0, s, a); break;
-    case 2: hipLaunchKernelGGL((k_attn<KT, HD, 2>), grid, block, 0, s, a); break;
-    case 4: hipLaunchKernelGGL((k_attn<KT, HD, 4>), grid, block, 0, s, a); break;
+    case 1: return launch_k(k_attn<KT, HD, 1>, grid, block, s, a);
+    case 2: return launch_k(k_attn<KT, HD, 2>, grid, block, s, a);
+    case 4: return launch_k(k_attn<KT, HD, 4>, grid, block, s, a);
     default: return hipErrorInvalidValue;
   }
-  return hipGetLastError();
 }
 
 hipError_t launch_attn(int dtype, int hd, int nt, const AttnArgs& a, dim3 grid, hipStream_t s) {

@@ -7,7 +7,8 @@
 //   epilogue  EPI_QKV    bias, rotary embedding of q/k, K/V appended to the paged cache;
 //             EPI_RESID  residual add into h;
 //             EPI_SWIGLU silu(gate) * up;
-//             EPI_LMHEAD logits and per-group (max, sum exp, argmax) for k_lm_reduce.
+//             EPI_LMHEAD logits and per-group (max, sum exp, argmax) for k_lm_reduce,
+//                        stored [row][group].
 // A workgroup owns complete output rows (8 on the VALU path, 16 on the MFMA path), so every
 // epilogue stays inside the workgroup: the four waves split K and are reduced through LDS,
 // with no synchronisation between workgroups and results that do not depend on scheduling.
@@ -101,41 +102,99 @@ __device__ __forceinline__ int transpose_index(int lane) {
 
 // ----------------------------------------------------------------------------- epilogues
 
-template <class WT, int RW>
-__device__ __forceinline__ void epi_qkv(const GemmArgs& a, int g, int M, const float* Y) {
-  constexpr int P = RW / 2;
+// One output item of the QKV (a rotary pair of one row) or residual (one element) epilogue,
+// with the global values it needs.  The VALU path fetches them while its weight loads are
+// in flight, so nothing but stores is left after the reduction.
+struct EpiItem {
+  bool live = false;
+  int m = 0, j = 0;          // activation row; pair (QKV) or row (residual) within the group
+  float v0 = 0.f, v1 = 0.f;  // QKV: bias of the pair's two dims; residual: current h
+  int pos = 0, seq = 0;      // QKV: the row's position and request
+  float2 cs = {1.f, 0.f};    // QKV: cos/sin of the pair's rotation at pos
+  int page = 0;              // QKV: KV page that holds pos
+};
+
+struct QkvGroup {
+  int hh, p;  // head within q/k/v, group within the head
+  bool isq, isk;
+  const void* bias;
+};
+
+template <int RW>
+__device__ __forceinline__ QkvGroup qkv_group(const GemmArgs& a, int g) {
+  QkvGroup q;
   const int per_head = a.hd / RW;
-  const int h = g / per_head, p = g - h * per_head;
-  const int half = a.hd >> 1;
-  const bool isq = h < a.hq, isk = !isq && h < a.hq + a.hkv;
-  const int hh = isq ? h : (isk ? h - a.hq : h - a.hq - a.hkv);
-  const void* bias = pick3(isq, isk, a.b0, a.b1, a.b2);
-  for (int idx = threadIdx.x; idx < M * P; idx += blockDim.x) {
-    const int m = idx / P, jj = idx - m * P;
-    const int i = P * p + jj;  // rotary pair index
-    const int dlo = i, dhi = half + i;
-    float ylo = Y[m * RW + jj], yhi = Y[m * RW + P + jj];
-    if (bias != nullptr) {
-      ylo += ldw<WT>(bias, (size_t)hh * a.hd + dlo);
-      yhi += ldw<WT>(bias, (size_t)hh * a.hd + dhi);
+  const int h = g / per_head;
+  q.p = g - h * per_head;
+  q.isq = h < a.hq;
+  q.isk = !q.isq && h < a.hq + a.hkv;
+  q.hh = q.isq ? h : (q.isk ? h - a.hq : h - a.hq - a.hkv);
+  q.bias = pick3(q.isq, q.isk, a.b0, a.b1, a.b2);
+  return q;
+}
+
+// First fetch: what depends only on the item (row descriptor, bias, current h).
+template <class WT, int EPI, int RW>
+__device__ __forceinline__ void epi_fetch_a(const GemmArgs& a, int g, int M, int idx, EpiItem& it) {
+  constexpr int P = RW / 2;
+  if (EPI == EPI_QKV) {
+    if (idx >= M * P) return;
+    const QkvGroup q = qkv_group<RW>(a, g);
+    it.live = true;
+    it.m = idx / P;
+    it.j = idx - it.m * P;
+    const int i = P * q.p + it.j;
+    if (q.bias != nullptr) {
+      it.v0 = ldw<WT>(q.bias, (size_t)q.hh * a.hd + i);
+      it.v1 = ldw<WT>(q.bias, (size_t)q.hh * a.hd + (a.hd >> 1) + i);
     }
-    const RowDesc rd = a.plan->rows[m];
-    if (isq || isk) {
-      const float2 cs = a.rope[(size_t)rd.pos * half + i];
-      const float rlo = ylo * cs.x - yhi * cs.y;
-      const float rhi = yhi * cs.x + ylo * cs.y;
+    const RowDesc rd = a.plan->rows[it.m];
+    it.pos = rd.pos;
+    it.seq = rd.seq;
+  } else if (EPI == EPI_RESID) {
+    if (idx >= M * RW) return;
+    it.m = idx / RW;
+    it.j = idx - it.m * RW;
+    const int r = RW * g + it.j;
+    it.live = r < a.N;
+    if (it.live) it.v0 = a.h[(size_t)it.m * a.N + r];
+  }
+}
+
+// Second fetch (QKV): what is addressed by the row's position (rotation, KV page).
+template <class WT, int EPI, int RW>
+__device__ __forceinline__ void epi_fetch_b(const GemmArgs& a, int g, EpiItem& it) {
+  if (EPI != EPI_QKV || !it.live) return;
+  constexpr int P = RW / 2;
+  const QkvGroup q = qkv_group<RW>(a, g);
+  if (q.isq || q.isk) it.cs = a.rope[(size_t)it.pos * (a.hd >> 1) + P * q.p + it.j];
+  if (!q.isq) it.page = a.bt[(size_t)it.seq * a.max_pps + (it.pos >> 4)];
+}
+
+// Bias, rotation and stores of one item; Y holds the group's outputs [m][RW].
+template <class WT, int EPI, int RW>
+__device__ __forceinline__ void epi_apply(const GemmArgs& a, int g, const EpiItem& it, const float* Y) {
+  if (!it.live) return;
+  constexpr int P = RW / 2;
+  if (EPI == EPI_QKV) {
+    const QkvGroup q = qkv_group<RW>(a, g);
+    const int i = P * q.p + it.j;
+    const int dlo = i, dhi = (a.hd >> 1) + i;
+    float ylo = Y[it.m * RW + it.j] + it.v0, yhi = Y[it.m * RW + P + it.j] + it.v1;
+    if (q.isq || q.isk) {
+      const float rlo = ylo * it.cs.x - yhi * it.cs.y;
+      const float rhi = yhi * it.cs.x + ylo * it.cs.y;
       ylo = rlo;
       yhi = rhi;
     }
-    if (isq) {
-      float* q = a.q_out + ((size_t)m * a.hq + hh) * a.hd;
-      q[dlo] = ylo;
-      q[dhi] = yhi;
+    if (q.isq) {
+      float* qo = a.q_out + ((size_t)it.m * a.hq + q.hh) * a.hd;
+      qo[dlo] = ylo;
+      qo[dhi] = yhi;
     } else {
-      const int page = a.bt[(size_t)rd.seq * a.max_pps + (rd.pos >> 4)];
-      const int t = rd.pos & 15;
-      const size_t blk = (((size_t)a.layer * a.num_pages + page) * a.hkv + hh) * (size_t)(16 * a.hd);
-      if (isk) {
+      const int t = it.pos & 15;
+      const size_t blk = (((size_t)a.layer * a.num_pages + it.page) * a.hkv + q.hh) * (size_t)(16 * a.hd);
+      if (q.isk) {
         stw<WT>(a.kpool, blk + k_block_off(t, dlo), ylo);
         stw<WT>(a.kpool, blk + k_block_off(t, dhi), yhi);
       } else {
@@ -143,15 +202,27 @@ __device__ __forceinline__ void epi_qkv(const GemmArgs& a, int g, int M, const f
         stw<WT>(a.vpool, blk + v_block_off(t, dhi), yhi);
       }
     }
+  } else if (EPI == EPI_RESID) {
+    a.h[(size_t)it.m * a.N + RW * g + it.j] = it.v0 + Y[it.m * RW + it.j];
+  }
+}
+
+template <class WT, int RW>
+__device__ __forceinline__ void epi_qkv(const GemmArgs& a, int g, int M, const float* Y) {
+  for (int idx = threadIdx.x; idx < M * (RW / 2); idx += blockDim.x) {
+    EpiItem it;
+    epi_fetch_a<WT, EPI_QKV, RW>(a, g, M, idx, it);
+    epi_fetch_b<WT, EPI_QKV, RW>(a, g, it);
+    epi_apply<WT, EPI_QKV, RW>(a, g, it, Y);
   }
 }
 
 template <int RW>
 __device__ __forceinline__ void epi_resid(const GemmArgs& a, int g, int M, const float* Y) {
   for (int idx = threadIdx.x; idx < M * RW; idx += blockDim.x) {
-    const int m = idx / RW, j = idx - m * RW;
-    const int r = RW * g + j;
-    if (r < a.N) a.h[(size_t)m * a.N + r] += Y[idx];
+    EpiItem it;
+    epi_fetch_a<float, EPI_RESID, RW>(a, g, M, idx, it);
+    epi_apply<float, EPI_RESID, RW>(a, g, it, Y);
   }
 }
 
@@ -175,7 +246,7 @@ __device__ __forceinline__ void epi_lmhead(const GemmArgs& a, int g, int M, cons
     const int m = idx / RW, j = idx - m * RW;
     const int r = RW * g + j;
     const OutDesc od = a.plan->outs[m];
-    float* lg = pick2(od.sel == 0, a.logits[0], a.logits[1]);
+    float* lg = a.plan->io.logits[od.sel];
     if (r < a.N && lg != nullptr) lg[(size_t)od.off * a.N + r] = Y[idx];
   }
   if (tid < M) {
@@ -193,7 +264,7 @@ __device__ __forceinline__ void epi_lmhead(const GemmArgs& a, int g, int M, cons
       const int r = RW * g + j;
       if (r < a.N) s += expf(Y[tid * RW + j] - mx);
     }
-    a.lm_part[(size_t)g * kMaxRows + tid] = LmPart{mx, s, arg, 0};
+    a.lm_part[(size_t)tid * a.n_groups + g] = LmPart{mx, s, arg, 0};
   }
 }
 
@@ -250,6 +321,10 @@ __global__ __launch_bounds__(kGemvMaxThreads) void k_gemv(GemmArgs a) {
 #pragma unroll
     for (int r = 0; r < RW; ++r) acc[r][m] = 0.f;
   }
+  constexpr bool kPre = EPI == EPI_QKV || EPI == EPI_RESID;  // at most one item per thread here
+  EpiItem item;
+  if (kPre) epi_fetch_a<WT, EPI, RW>(a, g, M, tid, item);
+  bool need_b = kPre && item.live;
   for (int c0 = tid; c0 < nch; c0 += U * T) {
     u32x4 wv[U][RW];
     float4 xv[U][M][CH / 4];
@@ -266,6 +341,10 @@ __global__ __launch_bounds__(kGemvMaxThreads) void k_gemv(GemmArgs a) {
           for (int e4 = 0; e4 < CH / 4; ++e4) xv[u][m][e4] = *(const float4*)(xr[m] + c * CH + 4 * e4);
         if (norm) gv[u] = *(const u32x4*)((const char*)a.gain + (size_t)c * 16);
       }
+    }
+    if (need_b) {  // issued behind the first weight loads
+      epi_fetch_b<WT, EPI, RW>(a, g, item);
+      need_b = false;
     }
 #pragma unroll
     for (int u = 0; u < U; ++u) {
@@ -308,7 +387,8 @@ __global__ __launch_bounds__(kGemvMaxThreads) void k_gemv(GemmArgs a) {
       }
     }
   }
-  // wave totals, then the four waves in fixed order
+  if (need_b) epi_fetch_b<WT, EPI, RW>(a, g, item);
+  // wave totals, then the waves in fixed order
 #pragma unroll
   for (int m = 0; m < M; ++m) {
     float vv[RW];
@@ -335,7 +415,10 @@ __global__ __launch_bounds__(kGemvMaxThreads) void k_gemv(GemmArgs a) {
     Y[m * RW + r] = norm ? v * s_scale[m] : v;
   }
   __syncthreads();
-  run_epilogue<WT, EPI, RW>(a, g, M, Y);
+  if (kPre)
+    epi_apply<WT, EPI, RW>(a, g, item, Y);
+  else
+    run_epilogue<WT, EPI, RW>(a, g, M, Y);
 }
 
 // ----------------------------------------------------------------------------- MFMA GEMM
@@ -495,22 +578,21 @@ static hipError_t launch_epi(int epi, const GemmArgs& a, hipStream_t s) {
     // long rows (the down projection) use 8 waves so each thread streams fewer chunks
     if (a.K / (16 / (int)sizeof(WT)) > 2048) block = dim3(kGemvMaxThreads);
     switch (epi) {
-      case EPI_QKV: hipLaunchKernelGGL((k_gemv<WT, MODE, EPI_QKV>), grid, block, 0, s, a); break;
-      case EPI_RESID: hipLaunchKernelGGL((k_gemv<WT, MODE, EPI_RESID>), grid, block, 0, s, a); break;
-      case EPI_SWIGLU: hipLaunchKernelGGL((k_gemv<WT, MODE, EPI_SWIGLU>), grid, block, 0, s, a); break;
-      case EPI_LMHEAD: hipLaunchKernelGGL((k_gemv<WT, MODE, EPI_LMHEAD>), grid, block, 0, s, a); break;
+      case EPI_QKV: return launch_k(k_gemv<WT, MODE, EPI_QKV>, grid, block, s, a);
+      case EPI_RESID: return launch_k(k_gemv<WT, MODE, EPI_RESID>, grid, block, s, a);
+      case EPI_SWIGLU: return launch_k(k_gemv<WT, MODE, EPI_SWIGLU>, grid, block, s, a);
+      case EPI_LMHEAD: return launch_k(k_gemv<WT, MODE, EPI_LMHEAD>, grid, block, s, a);
       default: return hipErrorInvalidValue;
     }
   } else {
     switch (epi) {
-      case EPI_QKV: hipLaunchKernelGGL((k_gemm_mfma<WT, MODE - 4, EPI_QKV>), grid, block, 0, s, a); break;
-      case EPI_RESID: hipLaunchKernelGGL((k_gemm_mfma<WT, MODE - 4, EPI_RESID>), grid, block, 0, s, a); break;
-      case EPI_SWIGLU: hipLaunchKernelGGL((k_gemm_mfma<WT, MODE - 4, EPI_SWIGLU>), grid, block, 0, s, a); break;
-      case EPI_LMHEAD: hipLaunchKernelGGL((k_gemm_mfma<WT, MODE - 4, EPI_LMHEAD>), grid, block, 0, s, a); break;
+      case EPI_QKV: return launch_k(k_gemm_mfma<WT, MODE - 4, EPI_QKV>, grid, block, s, a);
+      case EPI_RESID: return launch_k(k_gemm_mfma<WT, MODE - 4, EPI_RESID>, grid, block, s, a);
+      case EPI_SWIGLU: return launch_k(k_gemm_mfma<WT, MODE - 4, EPI_SWIGLU>, grid, block, s, a);
+      case EPI_LMHEAD: return launch_k(k_gemm_mfma<WT, MODE - 4, EPI_LMHEAD>, grid, block, s, a);
       default: return hipErrorInvalidValue;
     }
   }
-  return hipGetLastError();
 }
 
 template <class WT>

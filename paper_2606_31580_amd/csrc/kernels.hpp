@@ -1,6 +1,7 @@
 // Internal interface between the host runtime and the gfx950 kernels of liblaser.
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
@@ -11,7 +12,7 @@ constexpr int kMaxRows = 64;      // rows (tokens) of one forward
 constexpr int kPage = 16;         // positions per KV page
 constexpr int kMaxBt = 1024;      // block-table updates carried by one plan
 constexpr int kAttnWaves = 4;     // waves per attention workgroup (one split each)
-constexpr int kAttnMaxWG = 64;    // attention workgroups per (group, kv head)
+constexpr int kAttnMaxWG = 128;   // attention workgroups per (group, kv head)
 constexpr int kGemmThreads = 256; // 4 waves
 constexpr int kGemvMaxThreads = 512;
 
@@ -32,9 +33,19 @@ struct BtUpdate {
   int seq, idx, page;
 };
 
+// Caller buffers of one forward (they may change from call to call, so they travel in the
+// plan rather than in kernel arguments, which a replayed graph keeps fixed).
+struct PlanIO {
+  const int* tok_src[2];  // input token of row r: tok_src[rows[r].tok_sel][rows[r].tok_off]
+  int* tok_dst[2];        // greedy token of output o: tok_dst[outs[o].sel][outs[o].off]
+  float* p_dst[2];        // its max-softmax probability, same index
+  float* logits[2];       // optional logits rows [..][vocab], same index; may be null
+};
+
 // Everything the kernels of one forward need that changes per call; uploaded once.
 struct Plan {
   int M, n_groups, n_out, n_bt;
+  PlanIO io;
   RowDesc rows[kMaxRows];
   GroupDesc groups[kMaxRows];
   OutDesc outs[kMaxRows];
@@ -82,9 +93,8 @@ struct GemmArgs {
   // EPI_SWIGLU
   float* act;  // [M][F]
   int F;
-  // EPI_LMHEAD
-  float* logits[2];  // [..][vocab] or null
-  LmPart* lm_part;   // [n_groups][kMaxRows]
+  // EPI_LMHEAD (logits destinations come from plan->io)
+  LmPart* lm_part;  // [M][n_groups]
 };
 
 struct AttnArgs {
@@ -101,14 +111,36 @@ struct AttnArgs {
   float* ml;    // [hkv][kAttnMaxWG][max_rows*G][2]
 };
 
+// Kernel timing hooks.  `start`/`stop` are bound to the next launch only; when `next_stop`
+// is set (a timing session), every launch without an explicit stop event gets one from it,
+// so the end of each kernel is known.
+struct LaunchEvents {
+  hipEvent_t start = nullptr, stop = nullptr;
+  hipEvent_t (*next_stop)(void*) = nullptr;
+  void* ctx = nullptr;
+};
+LaunchEvents& launch_events();
+
+template <class K, class... Args>
+inline hipError_t launch_k(K kernel, dim3 grid, dim3 block, hipStream_t s, Args... args) {
+  LaunchEvents& e = launch_events();
+  hipEvent_t stop = e.stop;
+  if (!stop && e.next_stop) stop = e.next_stop(e.ctx);
+  if (e.start || stop)
+    hipExtLaunchKernelGGL(kernel, grid, block, 0, s, e.start, stop, 0, args...);
+  else
+    hipLaunchKernelGGL(kernel, grid, block, 0, s, args...);
+  e.start = e.stop = nullptr;
+  return hipGetLastError();
+}
+
 // dtype: 0 fp32, 1 bf16.  mode: 1..4 VALU rows per forward, 5..8 MFMA with 1..4 m-tiles.
 hipError_t launch_gemm(int dtype, int mode, int epi, const GemmArgs& a, hipStream_t s);
 hipError_t launch_attn(int dtype, int hd, int nt, const AttnArgs& a, dim3 grid, hipStream_t s);
 hipError_t launch_attn_merge(const AttnArgs& a, int M, int hd, hipStream_t s);
-hipError_t launch_lm_reduce(const Plan* plan, const LmPart* part, int n_groups, int n_out, int* tok0, int* tok1,
-                            float* p0, float* p1, hipStream_t s);
-hipError_t launch_embed(int dtype, const Plan* plan, int M, const void* embed, int d, int vocab, const int* tok0,
-                        const int* tok1, float* h, int* bt, int max_pps, hipStream_t s);
+hipError_t launch_lm_reduce(const Plan* plan, const LmPart* part, int n_groups, int n_out, hipStream_t s);
+hipError_t launch_embed(int dtype, const Plan* plan, int M, const void* embed, int d, int vocab, float* h, int* bt,
+                        int max_pps, hipStream_t s);
 hipError_t launch_apply_bt(const Plan* plan, int* bt, int max_pps, hipStream_t s);
 hipError_t launch_kv_copy(int dtype, int to_pool, void* kpool, void* vpool, const int* bt, int max_pps,
                           int num_pages, int n_layers, int hkv, int hd, int seq, int len, void* k_lin,

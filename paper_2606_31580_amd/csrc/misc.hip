@@ -15,17 +15,18 @@ __device__ void apply_bt_updates(const Plan* plan, int* bt, int max_pps) {
 
 // grid (M, d/64), block 64: h[m][64g..64g+63] = embed[token(m)].
 template <class WT>
-__global__ __launch_bounds__(64) void k_embed(const Plan* plan, const void* embed, int d, int vocab, const int* tok0,
-                                              const int* tok1, float* h, int* bt, int max_pps) {
+__global__ __launch_bounds__(64) void k_embed(const Plan* plan, const void* embed, int d, int vocab, float* h, int* bt,
+                                              int max_pps) {
   if (blockIdx.x == 0 && blockIdx.y == 0) apply_bt_updates(plan, bt, max_pps);
   const int m = blockIdx.x, g = blockIdx.y, j = threadIdx.x;
   const RowDesc rd = plan->rows[m];
-  int tok = (rd.tok_sel == 0 ? tok0 : tok1)[rd.tok_off];
+  int tok = plan->io.tok_src[rd.tok_sel][rd.tok_off];
   if (tok < 0 || tok >= vocab) tok = 0;  // ids outside the vocabulary never index past the table
   h[(size_t)m * d + 64 * g + j] = ldw<WT>(embed, (size_t)tok * d + 64 * g + j);
 }
 
-// (mx, sum, idx) of a range merged with the statistics of a range of higher indices.
+// (mx, sum, idx) merged with the statistics of another range; among equal maxima the lower
+// index wins, so the result does not depend on the merge order.
 __device__ __forceinline__ void lm_merge(float& mx, float& sum, int& idx, float mx2, float sum2, int idx2) {
   if (mx2 > mx) {
     sum = sum * expf(mx - mx2) + sum2;
@@ -33,53 +34,62 @@ __device__ __forceinline__ void lm_merge(float& mx, float& sum, int& idx, float 
     idx = idx2;
   } else if (mx2 == mx) {
     sum += sum2;
+    idx = min(idx, idx2);
   } else {
     sum += sum2 * expf(mx2 - mx);
   }
 }
 
-// One workgroup per LM-head output row: merges the per-group softmax statistics in index
-// order (contiguous chunks per thread, loaded 8 at a time, then a pairwise tree; ties keep
-// the lower index) into the greedy token and p_max = 1 / sum_j exp(l_j - l_max).
+// One workgroup per LM-head output row: merges the per-group softmax statistics (row m's
+// groups are contiguous; each load instruction of a wave reads 64 consecutive groups) and
+// then across lanes and waves, into the greedy token (lowest index among equal
+// maxima) and p_max = 1 / sum_j exp(l_j - l_max).
 constexpr int kLmThreads = 1024;
-__global__ __launch_bounds__(kLmThreads) void k_lm_reduce(const Plan* plan, const LmPart* part, int n_groups, int* tok0,
-                                                          int* tok1, float* p0, float* p1) {
-  __shared__ float s_mx[kLmThreads];
-  __shared__ float s_sum[kLmThreads];
-  __shared__ int s_idx[kLmThreads];
+__global__ __launch_bounds__(kLmThreads) void k_lm_reduce(const Plan* plan, const LmPart* part, int n_groups) {
+  __shared__ float s_mx[kLmThreads / 64];
+  __shared__ float s_sum[kLmThreads / 64];
+  __shared__ int s_idx[kLmThreads / 64];
   const int m = blockIdx.x, tid = threadIdx.x;
-  const int C = (n_groups + kLmThreads - 1) / kLmThreads;
+  const LmPart* row = part + (size_t)m * n_groups;
   float mx = -INFINITY, sum = 0.f;
-  int idx = 0;
-  const int g0 = tid * C, g1 = min(g0 + C, n_groups);
-  for (int g = g0; g < g1; g += 8) {
-    LmPart pp[8];
+  int idx = 0x7fffffff;
+  constexpr int U = 8;
+  for (int g0 = tid; g0 < n_groups; g0 += U * kLmThreads) {
+    LmPart pp[U];
 #pragma unroll
-    for (int u = 0; u < 8; ++u)
-      if (g + u < g1) pp[u] = part[(size_t)(g + u) * kMaxRows + m];
-#pragma unroll
-    for (int u = 0; u < 8; ++u)
-      if (g + u < g1) lm_merge(mx, sum, idx, pp[u].mx, pp[u].sum, pp[u].idx);
-  }
-  s_mx[tid] = mx;
-  s_sum[tid] = sum;
-  s_idx[tid] = idx;
-  __syncthreads();
-  for (int stride = 1; stride < kLmThreads; stride <<= 1) {
-    if ((tid & (2 * stride - 1)) == 0) {
-      float m0 = s_mx[tid], su = s_sum[tid];
-      int i0 = s_idx[tid];
-      lm_merge(m0, su, i0, s_mx[tid + stride], s_sum[tid + stride], s_idx[tid + stride]);
-      s_mx[tid] = m0;
-      s_sum[tid] = su;
-      s_idx[tid] = i0;
+    for (int u = 0; u < U; ++u) {
+      const int g = g0 + u * kLmThreads;
+      pp[u] = g < n_groups ? row[g] : LmPart{-INFINITY, 0.f, 0x7fffffff, 0};
     }
-    __syncthreads();
+#pragma unroll
+    for (int u = 0; u < U; ++u) lm_merge(mx, sum, idx, pp[u].mx, pp[u].sum, pp[u].idx);
   }
-  if (tid == 0) {
+  // within each wave, then across the 16 waves
+  for (int off = 32; off > 0; off >>= 1)
+    lm_merge(mx, sum, idx, __shfl_xor(mx, off), __shfl_xor(sum, off), __shfl_xor(idx, off));
+  const int lane = tid & 63, w = tid >> 6;
+  if (lane == 0) {
+    s_mx[w] = mx;
+    s_sum[w] = sum;
+    s_idx[w] = idx;
+  }
+  __syncthreads();
+  if (w == 0) {
+    mx = lane < kLmThreads / 64 ? s_mx[lane] : -INFINITY;
+    sum = lane < kLmThreads / 64 ? s_sum[lane] : 0.f;
+    idx = lane < kLmThreads / 64 ? s_idx[lane] : 0x7fffffff;
+    for (int off = 8; off > 0; off >>= 1)
+      lm_merge(mx, sum, idx, __shfl_xor(mx, off), __shfl_xor(sum, off), __shfl_xor(idx, off));
+    if (lane == 0) {
+      s_mx[0] = mx;
+      s_sum[0] = sum;
+      s_idx[0] = idx;
+    }
+  }
+  if (tid == 0) {  // lane 0 of wave 0 holds the total
     const OutDesc od = plan->outs[m];
-    (od.sel == 0 ? tok0 : tok1)[od.off] = s_idx[0];
-    (od.sel == 0 ? p0 : p1)[od.off] = 1.f / s_sum[0];
+    plan->io.tok_dst[od.sel][od.off] = s_idx[0] == 0x7fffffff ? 0 : s_idx[0];
+    plan->io.p_dst[od.sel][od.off] = 1.f / s_sum[0];
   }
 }
 
@@ -120,20 +130,17 @@ __global__ void k_confidence(const float* p, int T, int n, float* conf) {
   conf[r] = s / (float)T;
 }
 
-hipError_t launch_embed(int dtype, const Plan* plan, int M, const void* embed, int d, int vocab, const int* tok0,
-                        const int* tok1, float* h, int* bt, int max_pps, hipStream_t s) {
+hipError_t launch_embed(int dtype, const Plan* plan, int M, const void* embed, int d, int vocab, float* h, int* bt,
+                        int max_pps, hipStream_t s) {
   const dim3 grid(M, d / 64);
   if (dtype == 1)
-    hipLaunchKernelGGL(k_embed<bf16_t>, grid, dim3(64), 0, s, plan, embed, d, vocab, tok0, tok1, h, bt, max_pps);
+    return launch_k(k_embed<bf16_t>, grid, dim3(64), s, plan, embed, d, vocab, h, bt, max_pps);
   else
-    hipLaunchKernelGGL(k_embed<float>, grid, dim3(64), 0, s, plan, embed, d, vocab, tok0, tok1, h, bt, max_pps);
-  return hipGetLastError();
+    return launch_k(k_embed<float>, grid, dim3(64), s, plan, embed, d, vocab, h, bt, max_pps);
 }
 
-hipError_t launch_lm_reduce(const Plan* plan, const LmPart* part, int n_groups, int n_out, int* tok0, int* tok1,
-                            float* p0, float* p1, hipStream_t s) {
-  hipLaunchKernelGGL(k_lm_reduce, dim3(n_out), dim3(kLmThreads), 0, s, plan, part, n_groups, tok0, tok1, p0, p1);
-  return hipGetLastError();
+hipError_t launch_lm_reduce(const Plan* plan, const LmPart* part, int n_groups, int n_out, hipStream_t s) {
+  return launch_k(k_lm_reduce, dim3(n_out), dim3(kLmThreads), s, plan, part, n_groups);
 }
 
 hipError_t launch_apply_bt(const Plan* plan, int* bt, int max_pps, hipStream_t s) {
@@ -158,8 +165,7 @@ hipError_t launch_kv_copy(int dtype, int to_pool, void* kpool, void* vpool, cons
 }
 
 hipError_t launch_confidence(const float* p, int T, int n, float* conf, hipStream_t s) {
-  hipLaunchKernelGGL(k_confidence, dim3((n + 63) / 64), dim3(64), 0, s, p, T, n, conf);
-  return hipGetLastError();
+  return launch_k(k_confidence, dim3((n + 63) / 64), dim3(64), s, p, T, n, conf);
 }
 
 }  // namespace laser

@@ -3,6 +3,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <atomic>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -65,19 +66,44 @@ struct LayerW {
   const void *attn_norm, *wq, *wk, *wv, *bq, *bk, *bv, *wo, *mlp_norm, *w_gate, *w_up, *w_down;
 };
 
-constexpr int kRing = 16;   // plan slots (pinned host + device)
+constexpr int kRing = 16;   // pinned host staging slots for plan uploads
+constexpr int kMaxGraphs = 16;  // captured forwards kept per model (least recently used evicted)
 constexpr int kMaxT = 16;   // trial tokens per probe
-constexpr int kTargetAttnWaves = 2048;
+#ifndef LASER_ATTN_TARGET_WAVES
+#define LASER_ATTN_TARGET_WAVES 2048
+#endif
+constexpr int kTargetAttnWaves = LASER_ATTN_TARGET_WAVES;  // attention waves a forward aims for
 
 struct Layout {
   size_t rope, h, q, o, act, lm_part, attn_part, attn_ml, plans, probe_p, tok_buf, p_buf, total;
 };
 
+// Launch signature of a forward.  With the plan in its fixed device slot and the caller's
+// buffers inside the plan, these values fix every kernel launch of the forward and all of
+// its arguments, so one captured graph serves every forward with the same key.
+struct FwdKey {
+  int M, n_out, n_groups, nt, agx, merge;
+  uint64_t kv_id;
+  bool operator==(const FwdKey& o) const {
+    return M == o.M && n_out == o.n_out && n_groups == o.n_groups && nt == o.nt && agx == o.agx && merge == o.merge &&
+           kv_id == o.kv_id;
+  }
+};
+
+struct GraphEntry {
+  FwdKey key;
+  hipGraphExec_t exec;
+  uint64_t last_use;
+};
+
+// Spans of one kernel class in a timing session: (end of the kernel launched before the
+// class's launch, end of the class's last kernel), as indices into the model's event pool.
 struct Timer {
   bool enabled = false;
-  std::vector<hipEvent_t> ev;  // pairs
-  int used = 0;
+  std::vector<std::pair<int, int>> spans;
 };
+
+constexpr int kMaxTimingEvents = 1 << 16;  // per session; later launches go untimed
 
 }  // namespace
 
@@ -98,6 +124,13 @@ struct laser_model {
   bool ring_used[kRing] = {};
   int ring_pos = 0;
   Timer timers[LASER_K_NCLASS];
+  std::vector<hipEvent_t> ev_pool;  // fence-free timing events, reused across sessions
+  int ev_used = 0;
+  int last_stop = -1;  // pool index bound to the most recent launch's end
+  bool use_graphs = true;
+  hipStream_t cap_stream = nullptr;  // private stream that forwards are captured on
+  std::vector<GraphEntry> graphs;
+  uint64_t graph_clock = 0;
 
   template <class T>
   T* wsp(size_t off) const { return (T*)(ws + off); }
@@ -105,14 +138,26 @@ struct laser_model {
 
 struct laser_kv {
   const laser_model* m;
+  uint64_t id;  // unique over the process (graph keys must not match a later cache at the same address)
   PagePool pool;
   void* kpool;
   void* vpool;
   int32_t* bt;
   std::vector<PageUpdate> pending;  // block-table writes not yet on the device
   laser_kv(const laser_model* mm, int np, int ms, int mpps, void* k, void* v, int32_t* b)
-      : m(mm), pool(np, kPage, ms, mpps), kpool(k), vpool(v), bt(b) {}
+      : m(mm), id(next_id()), pool(np, kPage, ms, mpps), kpool(k), vpool(v), bt(b) {}
+  static uint64_t next_id() {
+    static std::atomic<uint64_t> n{1};
+    return n.fetch_add(1);
+  }
 };
+
+namespace laser {
+LaunchEvents& launch_events() {
+  static thread_local LaunchEvents ev;
+  return ev;
+}
+}  // namespace laser
 
 namespace {
 
@@ -144,7 +189,7 @@ static Layout make_layout(const laser_model_desc& d, int max_rows) {
   L.lm_part = take((size_t)groups_lm(d, 1) * kMaxRows * sizeof(LmPart));  // the VALU path has the most groups
   L.attn_part = take((size_t)d.n_kv_heads * kAttnMaxWG * max_rows * G * hd * 4);
   L.attn_ml = take((size_t)d.n_kv_heads * kAttnMaxWG * max_rows * G * 2 * 4);
-  L.plans = take((size_t)kRing * sizeof(Plan));
+  L.plans = take(sizeof(Plan));  // the one device plan slot every forward reads
   L.probe_p = take((size_t)kMaxRows * kMaxT * 4);
   L.tok_buf = take((size_t)kMaxRows * 4);
   L.p_buf = take((size_t)kMaxRows * 4);
@@ -283,6 +328,16 @@ extern "C" laser_status laser_model_finalize(laser_model* m, int max_rows, void*
       return laser_fail(LASER_ERR_HIP, "hipEventCreate: %s", hipGetErrorString(e));
     }
   }
+  hipStream_t cs = nullptr;
+  {
+    hipError_t e = hipStreamCreateWithFlags(&cs, hipStreamNonBlocking);
+    if (e != hipSuccess) {
+      for (int j = 0; j < kRing; ++j) (void)hipEventDestroy(m->ring_ev[j]);
+      (void)hipHostFree(hp);
+      return laser_fail(LASER_ERR_HIP, "hipStreamCreate: %s", hipGetErrorString(e));
+    }
+  }
+  m->cap_stream = cs;
   char* ws = (char*)d_workspace;
   HIP_TRY(hipMemcpyAsync(ws + L.rope, rope.data(), rope.size() * sizeof(float2), hipMemcpyHostToDevice, s));
   HIP_TRY(hipStreamSynchronize(s));  // the host rope table goes out of scope
@@ -303,9 +358,10 @@ extern "C" laser_status laser_model_destroy(laser_model* m) {
       (void)hipEventDestroy(m->ring_ev[i]);
     }
     (void)hipHostFree(m->h_plans);
+    for (auto& g : m->graphs) (void)hipGraphExecDestroy(g.exec);
+    if (m->cap_stream) (void)hipStreamDestroy(m->cap_stream);
   }
-  for (auto& t : m->timers)
-    for (auto e : t.ev) (void)hipEventDestroy(e);
+  for (auto e : m->ev_pool) (void)hipEventDestroy(e);
   delete m;
   return LASER_OK;
 }
@@ -383,28 +439,53 @@ struct Launch {
   hipStream_t s;
 };
 
-// Records timing events around a launch of class `cls` when enabled.
+// Timing session: while any class is enabled, forwards launch kernel by kernel and every
+// launch records a fence-free event at its end (`next_stop`).  A class's launch then spans
+// from the end of the kernel launched just before it to the end of its own last kernel;
+// with kernels running back to back this equals the sum of their kernel-trace durations.
+static hipEvent_t next_timing_event(void* ctx) {
+  laser_model* m = (laser_model*)ctx;
+  if (m->ev_used >= kMaxTimingEvents) return nullptr;
+  if (m->ev_used == (int)m->ev_pool.size()) {
+    hipEvent_t e = nullptr;
+    if (hipEventCreateWithFlags(&e, hipEventDisableSystemFence) != hipSuccess) return nullptr;
+    m->ev_pool.push_back(e);
+  }
+  m->last_stop = m->ev_used;
+  return m->ev_pool[m->ev_used++];
+}
+
+static bool timing_session(const laser_model* m) {
+  for (const auto& t : m->timers)
+    if (t.enabled) return true;
+  return false;
+}
+
+// Arms the end-of-launch events for the current thread while a forward is being launched.
+struct TimingScope {
+  LaunchEvents saved;
+  explicit TimingScope(laser_model* m) : saved(launch_events()) {
+    if (timing_session(m)) {
+      launch_events().next_stop = next_timing_event;
+      launch_events().ctx = m;
+    }
+  }
+  ~TimingScope() { launch_events() = saved; }
+};
+
 template <class F>
 static hipError_t timed(laser_model* m, int cls, hipStream_t s, F&& f) {
+  (void)s;
   Timer& t = m->timers[cls];
   if (!t.enabled) return f();
-  if ((int)t.ev.size() < 2 * (t.used + 1)) {
-    hipEvent_t a, b;
-    hipError_t e = hipEventCreate(&a);
-    if (e != hipSuccess) return e;
-    e = hipEventCreate(&b);
-    if (e != hipSuccess) return e;
-    t.ev.push_back(a);
-    t.ev.push_back(b);
-  }
-  (void)hipEventRecord(t.ev[2 * t.used], s);
+  const int before = m->last_stop;
   hipError_t e = f();
-  (void)hipEventRecord(t.ev[2 * t.used + 1], s);
-  t.used++;
+  if (e == hipSuccess && before >= 0 && m->last_stop != before) t.spans.emplace_back(before, m->last_stop);
   return e;
 }
 
-// Copies a plan into the next ring slot (pinned) and on to the device; returns the device copy.
+// Copies a plan into the next pinned staging slot and on to the device plan slot (forwards of
+// one model are ordered on its stream, so one device slot suffices); returns the device copy.
 static laser_status upload_plan(laser_model* m, const Plan& p, hipStream_t s, Plan** d_out) {
   const int slot = m->ring_pos;
   m->ring_pos = (m->ring_pos + 1) % kRing;
@@ -412,7 +493,7 @@ static laser_status upload_plan(laser_model* m, const Plan& p, hipStream_t s, Pl
   Plan* hp = m->h_plans + slot;
   const size_t bytes = offsetof(Plan, bt) + sizeof(BtUpdate) * (size_t)p.n_bt;
   std::memcpy(hp, &p, bytes);
-  Plan* dp = m->wsp<Plan>(m->lay.plans) + slot;
+  Plan* dp = m->wsp<Plan>(m->lay.plans);  // stream order keeps forwards off each other's plan
   HIP_TRY(hipMemcpyAsync(dp, hp, bytes, hipMemcpyHostToDevice, s));
   HIP_TRY(hipEventRecord(m->ring_ev[slot], s));
   m->ring_used[slot] = true;
@@ -436,18 +517,12 @@ static laser_status flush_pending(laser_kv* kv, laser_model* m, hipStream_t s) {
     laser_status st = upload_plan(m, *p, s, &dp);
     delete p;
     if (st != LASER_OK) return st;
+    TimingScope scope(m);
     HIP_TRY(launch_apply_bt(dp, kv->bt, kv->pool.max_pages_per_seq(), s));
   }
   kv->pending.clear();
   return LASER_OK;
 }
-
-// Output destinations of a forward's LM head.
-struct Outs {
-  int* tok[2] = {nullptr, nullptr};
-  float* p[2] = {nullptr, nullptr};
-  float* logits[2] = {nullptr, nullptr};
-};
 
 // Fill row groups (contiguous rows of one request) and their attention splits.
 static void plan_groups(const laser_model* m, Plan& p) {
@@ -467,7 +542,8 @@ static void plan_groups(const laser_model* m, Plan& p) {
     g.nrows = e - r;
     g.npages = maxpos / kPage + 1;
     g.maxpos = maxpos;
-    units += (long long)g.npages * d.n_kv_heads;
+    // a page costs one 16-column query tile per 16 columns of the group
+    units += (long long)g.npages * d.n_kv_heads * ceil_div(g.nrows * G, 16);
     r = e;
   }
   const int base = std::max(1, (int)((units + kTargetAttnWaves - 1) / kTargetAttnWaves));
@@ -478,20 +554,84 @@ static void plan_groups(const laser_model* m, Plan& p) {
   }
 }
 
-static laser_status run_forward(laser_model* m, laser_kv* kv, Plan& p, const int* tok0, const int* tok1, const Outs& outs,
-                                hipStream_t s) {
+static laser_status launch_forward(laser_model* m, laser_kv* kv, const FwdKey& key, hipStream_t s);
+
+// Runs one forward: plans the attention splits, uploads the plan, then launches the
+// forward's kernels (replaying a captured graph of them when graphs are on and no kernel
+// class is being timed).
+static laser_status run_forward(laser_model* m, laser_kv* kv, Plan& p, const PlanIO& io, hipStream_t s,
+                                bool allow_graph = true) {
+  const laser_model_desc& d = m->desc;
+  const int G = d.n_q_heads / d.n_kv_heads;
+  plan_groups(m, p);
+  p.io = io;
+  FwdKey key{};
+  key.M = p.M;
+  key.n_out = p.n_out;
+  key.n_groups = p.n_groups;
+  int max_nwg = 1, nt = 1;
+  for (int i = 0; i < p.n_groups; ++i) {
+    max_nwg = std::max(max_nwg, p.groups[i].nwg);
+    nt = std::max(nt, ceil_div(p.groups[i].nrows * G, 16));
+  }
+  key.nt = nt == 3 ? 4 : nt;
+  // the grid is rounded up (extra workgroups exit at once) so that a growing context keeps
+  // the same key for a while
+  key.agx = max_nwg == 1 ? 1 : std::min(kAttnMaxWG, ceil_div(max_nwg, 8) * 8);
+  key.merge = max_nwg > 1;
+  key.kv_id = kv->id;
+  Plan* dp = nullptr;
+  laser_status st = upload_plan(m, p, s, &dp);
+  if (st != LASER_OK) return st;
+  const bool timing = timing_session(m);
+  if (!allow_graph || !m->use_graphs || timing) {
+    TimingScope scope(m);
+    return launch_forward(m, kv, key, s);
+  }
+
+  GraphEntry* ge = nullptr;
+  for (auto& g : m->graphs)
+    if (g.key == key) ge = &g;
+  if (!ge) {
+    hipGraph_t graph = nullptr;
+    HIP_TRY(hipStreamBeginCapture(m->cap_stream, hipStreamCaptureModeThreadLocal));
+    st = launch_forward(m, kv, key, m->cap_stream);
+    const hipError_t ec = hipStreamEndCapture(m->cap_stream, &graph);
+    if (st != LASER_OK) {
+      if (graph) (void)hipGraphDestroy(graph);
+      return st;
+    }
+    if (ec != hipSuccess) return laser_fail(LASER_ERR_HIP, "graph capture: %s", hipGetErrorString(ec));
+    hipGraphExec_t exec = nullptr;
+    const hipError_t ei = hipGraphInstantiate(&exec, graph, nullptr, nullptr, 0);
+    (void)hipGraphDestroy(graph);
+    if (ei != hipSuccess) return laser_fail(LASER_ERR_HIP, "graph instantiate: %s", hipGetErrorString(ei));
+    if ((int)m->graphs.size() >= kMaxGraphs) {
+      auto lru = std::min_element(m->graphs.begin(), m->graphs.end(),
+                                  [](const GraphEntry& x, const GraphEntry& y) { return x.last_use < y.last_use; });
+      (void)hipGraphExecDestroy(lru->exec);  // safe while a launch of it is in flight
+      m->graphs.erase(lru);
+    }
+    m->graphs.push_back(GraphEntry{key, exec, 0});
+    ge = &m->graphs.back();
+  }
+  ge->last_use = ++m->graph_clock;
+  HIP_TRY(hipGraphLaunch(ge->exec, s));
+  return LASER_OK;
+}
+
+// Launches the kernels of one forward whose plan is in the device plan slot.
+static laser_status launch_forward(laser_model* m, laser_kv* kv, const FwdKey& key, hipStream_t s) {
   const laser_model_desc& d = m->desc;
   const Layout& L = m->lay;
   const int hd = d.head_dim, G = d.n_q_heads / d.n_kv_heads;
   const int dt = d.dtype == LASER_DTYPE_BF16 ? 1 : 0;
   const int max_pps = kv->pool.max_pages_per_seq();
-  plan_groups(m, p);
-  Plan* dp = nullptr;
-  laser_status st = upload_plan(m, p, s, &dp);
-  if (st != LASER_OK) return st;
+  const Plan* dp = m->wsp<Plan>(L.plans);
+  laser_status st = LASER_OK;
   float* h = m->wsp<float>(L.h);
   HIP_TRY(timed(m, LASER_K_EMBED, s, [&] {
-    return launch_embed(dt, dp, p.M, m->embed, d.d_model, d.vocab, tok0, tok1, h, kv->bt, max_pps, s);
+    return launch_embed(dt, dp, key.M, m->embed, d.d_model, d.vocab, h, kv->bt, max_pps, s);
   }));
 
   GemmArgs base{};
@@ -537,13 +677,7 @@ static laser_status run_forward(laser_model* m, laser_kv* kv, Plan& p, const int
   aa.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)hd));
   aa.part = m->wsp<float>(L.attn_part);
   aa.ml = m->wsp<float>(L.attn_ml);
-  int max_nwg = 1, nt = 1;
-  for (int i = 0; i < p.n_groups; ++i) {
-    max_nwg = std::max(max_nwg, p.groups[i].nwg);
-    nt = std::max(nt, ceil_div(p.groups[i].nrows * G, 16));
-  }
-  if (nt == 3) nt = 4;
-  const dim3 agrid(max_nwg, d.n_kv_heads, p.n_groups);
+  const dim3 agrid(key.agx, d.n_kv_heads, key.n_groups);
 
   for (int li = 0; li < d.n_layers; ++li) {
     const LayerW& W = m->layers[li];
@@ -558,13 +692,13 @@ static laser_status run_forward(laser_model* m, laser_kv* kv, Plan& p, const int
     a.ldx = d.d_model;
     a.gain = W.attn_norm;
     a.layer = li;
-    st = gemm(LASER_K_QKV, EPI_QKV, a, d.d_model, (d.n_q_heads + 2 * d.n_kv_heads) * hd, groups_qkv(d, p.M), p.M);
+    st = gemm(LASER_K_QKV, EPI_QKV, a, d.d_model, (d.n_q_heads + 2 * d.n_kv_heads) * hd, groups_qkv(d, key.M), key.M);
     if (st != LASER_OK) return st;
 
     aa.layer = li;
     HIP_TRY(timed(m, LASER_K_ATTN, s, [&] {
-      hipError_t e = launch_attn(dt, hd, nt, aa, agrid, s);
-      if (e == hipSuccess && max_nwg > 1) e = launch_attn_merge(aa, p.M, hd, s);
+      hipError_t e = launch_attn(dt, hd, key.nt, aa, agrid, s);
+      if (e == hipSuccess && key.merge) e = launch_attn_merge(aa, key.M, hd, s);
       return e;
     }));
 
@@ -573,7 +707,7 @@ static laser_status run_forward(laser_model* m, laser_kv* kv, Plan& p, const int
     a.x = m->wsp<float>(L.o);
     a.ldx = d.n_q_heads * hd;
     a.gain = nullptr;
-    st = gemm(LASER_K_OPROJ, EPI_RESID, a, d.n_q_heads * hd, d.d_model, groups_resid(d, p.M), p.M);
+    st = gemm(LASER_K_OPROJ, EPI_RESID, a, d.n_q_heads * hd, d.d_model, groups_resid(d, key.M), key.M);
     if (st != LASER_OK) return st;
 
     a = base;
@@ -582,7 +716,7 @@ static laser_status run_forward(laser_model* m, laser_kv* kv, Plan& p, const int
     a.x = h;
     a.ldx = d.d_model;
     a.gain = W.mlp_norm;
-    st = gemm(LASER_K_GATEUP, EPI_SWIGLU, a, d.d_model, 2 * d.d_ffn, groups_gateup(d, p.M), p.M);
+    st = gemm(LASER_K_GATEUP, EPI_SWIGLU, a, d.d_model, 2 * d.d_ffn, groups_gateup(d, key.M), key.M);
     if (st != LASER_OK) return st;
 
     a = base;
@@ -590,25 +724,21 @@ static laser_status run_forward(laser_model* m, laser_kv* kv, Plan& p, const int
     a.x = m->wsp<float>(L.act);
     a.ldx = d.d_ffn;
     a.gain = nullptr;
-    st = gemm(LASER_K_DOWN, EPI_RESID, a, d.d_ffn, d.d_model, groups_resid(d, p.M), p.M);
+    st = gemm(LASER_K_DOWN, EPI_RESID, a, d.d_ffn, d.d_model, groups_resid(d, key.M), key.M);
     if (st != LASER_OK) return st;
   }
-  if (p.n_out > 0) {
+  if (key.n_out > 0) {
     GemmArgs a = base;
     a.w0 = d.tied_embeddings ? m->embed : m->lm_head;
     a.x = h;
     a.ldx = d.d_model;
     a.gain = m->final_norm;
     a.row_map = 1;
-    a.logits[0] = outs.logits[0];
-    a.logits[1] = outs.logits[1];
     a.lm_part = m->wsp<LmPart>(L.lm_part);
-    const int ng = groups_lm(d, p.n_out);
-    st = gemm(LASER_K_LMHEAD, EPI_LMHEAD, a, d.d_model, d.vocab, ng, p.n_out);
+    const int ng = groups_lm(d, key.n_out);
+    st = gemm(LASER_K_LMHEAD, EPI_LMHEAD, a, d.d_model, d.vocab, ng, key.n_out);
     if (st != LASER_OK) return st;
-    HIP_TRY(timed(m, LASER_K_LMHEAD, s, [&] {
-      return launch_lm_reduce(dp, a.lm_part, ng, p.n_out, outs.tok[0], outs.tok[1], outs.p[0], outs.p[1], s);
-    }));
+    HIP_TRY(timed(m, LASER_K_LMHEAD, s, [&] { return launch_lm_reduce(dp, a.lm_part, ng, key.n_out, s); }));
   }
   return LASER_OK;
 }
@@ -705,11 +835,12 @@ extern "C" laser_status laser_decode_step(laser_model* m, laser_kv* kv, int batc
     p->outs[b] = OutDesc{b, 0, b, 0};
   }
   push_updates(*p, upd);
-  Outs o;
-  o.tok[0] = d_next;
-  o.p[0] = d_max_prob;
-  o.logits[0] = d_logits;
-  st = run_forward(m, kv, *p, d_tokens, d_tokens, o, s);
+  PlanIO io{};
+  io.tok_src[0] = io.tok_src[1] = d_tokens;
+  io.tok_dst[0] = d_next;
+  io.p_dst[0] = d_max_prob;
+  io.logits[0] = d_logits;
+  st = run_forward(m, kv, *p, io, s);
   delete p;
   return st;
 }
@@ -739,11 +870,12 @@ extern "C" laser_status laser_prefill(laser_model* m, laser_kv* kv, int seq_id, 
     const bool last = c0 + M >= n;
     p->n_out = (last && d_logits_last) ? 1 : 0;
     p->outs[0] = OutDesc{M - 1, 0, 0, 0};
-    Outs o;
-    o.tok[0] = m->wsp<int>(m->lay.tok_buf);
-    o.p[0] = m->wsp<float>(m->lay.p_buf);
-    o.logits[0] = d_logits_last;
-    st = run_forward(m, kv, *p, d_tokens, d_tokens, o, s);
+    PlanIO io{};
+    io.tok_src[0] = io.tok_src[1] = d_tokens;
+    io.tok_dst[0] = m->wsp<int>(m->lay.tok_buf);
+    io.p_dst[0] = m->wsp<float>(m->lay.p_buf);
+    io.logits[0] = d_logits_last;
+    st = run_forward(m, kv, *p, io, s, /*allow_graph=*/false);  // one-off chunk shapes
   }
   delete p;
   return st;
@@ -762,11 +894,12 @@ static laser_status run_trials(laser_model* m, laser_kv* kv, Plan* p, const std:
       p->rows[r] = RowDesc{seqs[r], base_pos[r] + S + j - 1, 0, r * T + j - 1};
       p->outs[r] = OutDesc{r, 0, r * T + j, 0};
     }
-    Outs o;
-    o.tok[0] = d_argmax;
-    o.p[0] = probe_p;
-    o.logits[0] = d_logits;
-    laser_status st = run_forward(m, kv, *p, d_argmax, d_argmax, o, s);
+    PlanIO io{};
+    io.tok_src[0] = io.tok_src[1] = d_argmax;
+    io.tok_dst[0] = d_argmax;
+    io.p_dst[0] = probe_p;
+    io.logits[0] = d_logits;
+    laser_status st = run_forward(m, kv, *p, io, s);
     if (st != LASER_OK) return st;
   }
   return LASER_OK;
@@ -805,13 +938,15 @@ extern "C" laser_status laser_probe_confidence(laser_model* m, laser_kv* kv, int
     for (int i = 0; i < S; ++i) p->rows[r * S + i] = RowDesc{seqs[r], L0[r] + i, 0, i};
     p->outs[r] = OutDesc{r * S + S - 1, 0, r * T, 0};
   }
-  Outs o;
-  o.tok[0] = d_argmax;
-  o.p[0] = probe_p;
-  o.logits[0] = d_logits;
-  st = run_forward(m, kv, *p, d_suffix, d_suffix, o, s);
+  PlanIO io{};
+  io.tok_src[0] = io.tok_src[1] = d_suffix;
+  io.tok_dst[0] = d_argmax;
+  io.p_dst[0] = probe_p;
+  io.logits[0] = d_logits;
+  st = run_forward(m, kv, *p, io, s);
   if (st == LASER_OK) st = run_trials(m, kv, p, seqs, L0, S, T, d_argmax, probe_p, d_logits, s);
   if (st == LASER_OK) {
+    TimingScope scope(m);
     hipError_t e = timed(m, LASER_K_OTHER, s, [&] { return launch_confidence(probe_p, T, batch, d_conf, s); });
     if (e != hipSuccess) st = laser_fail(LASER_ERR_HIP, "confidence: %s", hipGetErrorString(e));
   }
@@ -881,14 +1016,17 @@ extern "C" laser_status laser_step_mixed(laser_model* m, laser_kv* kv, int batch
   p->n_out = nout;
   push_updates(*p, upd);
   float* probe_p = m->wsp<float>(m->lay.probe_p);
-  Outs o;
-  o.tok[0] = d_next;
-  o.p[0] = d_max_prob;
-  o.tok[1] = d_argmax;
-  o.p[1] = probe_p;
-  st = run_forward(m, kv, *p, d_tokens, d_suffix, o, s);
+  PlanIO io{};
+  io.tok_src[0] = d_tokens;
+  io.tok_src[1] = d_suffix;
+  io.tok_dst[0] = d_next;
+  io.p_dst[0] = d_max_prob;
+  io.tok_dst[1] = d_argmax;
+  io.p_dst[1] = probe_p;
+  st = run_forward(m, kv, *p, io, s);
   if (st == LASER_OK && n_probe > 0) st = run_trials(m, kv, p, pseqs, pbase, S, T, d_argmax, probe_p, nullptr, s);
   if (st == LASER_OK && n_probe > 0) {
+    TimingScope scope(m);
     hipError_t e = timed(m, LASER_K_OTHER, s, [&] { return launch_confidence(probe_p, T, n_probe, d_conf, s); });
     if (e != hipSuccess) st = laser_fail(LASER_ERR_HIP, "confidence: %s", hipGetErrorString(e));
   }
@@ -897,14 +1035,32 @@ extern "C" laser_status laser_step_mixed(laser_model* m, laser_kv* kv, int batch
   return st;
 }
 
+// ----------------------------------------------------------------------------- graphs
+
+extern "C" laser_status laser_model_set_graphs(laser_model* m, int enable) {
+  if (!model_of(m)) return laser_fail(LASER_ERR_STATE, "invalid or destroyed model");
+  m->use_graphs = enable != 0;
+  return LASER_OK;
+}
+
 // ----------------------------------------------------------------------------- timing
+
+// Restarts the event pool once no class holds unread spans (after its last event is done).
+static laser_status maybe_reset_pool(laser_model* m) {
+  for (const auto& t : m->timers)
+    if (!t.spans.empty()) return LASER_OK;
+  if (m->ev_used > 0) HIP_TRY(hipEventSynchronize(m->ev_pool[m->ev_used - 1]));
+  m->ev_used = 0;
+  m->last_stop = -1;
+  return LASER_OK;
+}
 
 extern "C" laser_status laser_timing_enable(laser_model* m, int kernel_class, int enable) {
   if (!model_of(m)) return laser_fail(LASER_ERR_STATE, "invalid or destroyed model");
   if (kernel_class < 0 || kernel_class >= LASER_K_NCLASS) return laser_fail(LASER_ERR_INVALID_ARG, "bad kernel class");
   m->timers[kernel_class].enabled = enable != 0;
-  m->timers[kernel_class].used = 0;
-  return LASER_OK;
+  m->timers[kernel_class].spans.clear();
+  return maybe_reset_pool(m);
 }
 
 extern "C" laser_status laser_timing_read(laser_model* m, int kernel_class, double* total_ms, int* launches) {
@@ -913,14 +1069,14 @@ extern "C" laser_status laser_timing_read(laser_model* m, int kernel_class, doub
   if (!total_ms || !launches) return laser_fail(LASER_ERR_INVALID_ARG, "NULL argument");
   Timer& t = m->timers[kernel_class];
   double tot = 0.0;
-  if (t.used > 0) HIP_TRY(hipEventSynchronize(t.ev[2 * t.used - 1]));
-  for (int i = 0; i < t.used; ++i) {
+  if (!t.spans.empty()) HIP_TRY(hipEventSynchronize(m->ev_pool[t.spans.back().second]));
+  for (const auto& sp : t.spans) {
     float ms = 0.f;
-    HIP_TRY(hipEventElapsedTime(&ms, t.ev[2 * i], t.ev[2 * i + 1]));
+    HIP_TRY(hipEventElapsedTime(&ms, m->ev_pool[sp.first], m->ev_pool[sp.second]));
     tot += ms;
   }
   *total_ms = tot;
-  *launches = t.used;
-  t.used = 0;
-  return LASER_OK;
+  *launches = (int)t.spans.size();
+  t.spans.clear();
+  return maybe_reset_pool(m);
 }

@@ -82,6 +82,7 @@ _SIGS = {
     "laser_step_mixed": (_I, [_P, _P, _I, _I32P, _P, _P, _P, _I, _I32P, _P, _I, _I, _P, _P, _P]),
     "laser_timing_enable": (_I, [_P, _I, _I]),
     "laser_timing_read": (_I, [_P, _I, C.POINTER(C.c_double), C.POINTER(_I)]),
+    "laser_model_set_graphs": (_I, [_P, _I]),
 }
 
 _lib = None
@@ -239,6 +240,10 @@ class Model:
         if poison:  # tests: NaN bytes everywhere, so any read of unwritten workspace shows
             self.workspace.fill_(0xFF)
         _call("laser_model_finalize", self.h, max_rows, self.workspace.data_ptr(), nbytes.value, _stream_ptr(stream))
+
+    def set_graphs(self, on: bool):
+        """Replay forwards from captured HIP graphs (default) or launch kernels one by one."""
+        _call("laser_model_set_graphs", self.h, int(on))
 
     def timing_enable(self, cls: int, on: bool = True):
         _call("laser_timing_enable", self.h, cls, int(on))
