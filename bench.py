@@ -33,6 +33,8 @@ def parse():
     ap.add_argument("--workload", default="7B-b1-kv14336")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--profile-only", action="store_true", help="steps only, no reporting (for rocprofv3 runs)")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run a plain 256 MiB device-to-device copy three times (scale for HBM byte counters)")
     return ap.parse_args()
 
 
@@ -44,6 +46,16 @@ def main():
         sys.exit(2)
     import numpy as np
     import torch
+
+    if args.copy_calibration:
+        n = 256 << 20
+        src = torch.full((n,), 7, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(f"[bench] copy calibration: 3 copies of {n} bytes", file=sys.stderr, flush=True)
+        return
 
     from paper_2606_31580_amd import laser as L
     from paper_2606_31580_amd import synth

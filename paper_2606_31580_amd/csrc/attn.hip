@@ -10,7 +10,10 @@
 //   O^T[d][c] += V^T[d][t] P^T[t][c] v_mfma_f32_16x16x16_bf16, B = P^T taken straight from
 //                                    the S^T accumulator layout (bf16 hi+lo)
 // The KV page layout makes every operand load a contiguous 1 KB (K) / 512 B (V) per wave
-// instruction.  Waves merge (m, l, O) in LDS; when a (group, kv head) spans several
+// instruction.  With one query tile (decode rows) the queries stay in registers and pages
+// are taken in pairs, so the cross-lane max and sum reductions run once per 32 positions,
+// and the four waves merge (m, l, O) in one LDS round; wider tiles (probe chunks) take one
+// page at a time and merge in two rounds.  When a (group, kv head) spans several
 // workgroups their fp32 partials are combined by k_attn_merge, launched next.
 #include <type_traits>
 
@@ -36,16 +39,21 @@ __global__ __launch_bounds__(64 * kAttnWaves) void k_attn(AttnArgs a) {
   constexpr int NS = HD / 32;  // QK k-steps
   constexpr int ND = HD / 16;  // PV d-tiles
   constexpr int NC = 16 * NT;  // padded query columns
-  // Q (bf16 hi/lo) is only read in the page loop; the merge slots reuse the same LDS.
+  // LDS: queries (bf16 hi/lo) and the merge slots of the waves.  One query tile merges in
+  // one round (waves 1-3 publish, wave 0 absorbs) with separate slots; wider tiles merge
+  // in two rounds through two slots that reuse the query space.
+  constexpr int NSLOT = NT == 1 ? 3 : 2;
+  constexpr bool ALIAS = NT != 1;
   constexpr int QBYTES = NC * HD * 2 * 2;
-  constexpr int OBYTES = 2 * NC * HD * 4;
-  __shared__ __align__(16) char s_raw[QBYTES > OBYTES ? QBYTES : OBYTES];
+  constexpr int SBYTES = NSLOT * NC * HD * 4;
+  constexpr int LBYTES = ALIAS ? (QBYTES > SBYTES ? QBYTES : SBYTES) : QBYTES + SBYTES;
+  __shared__ __align__(16) char s_raw[LBYTES];
   uint16_t* s_qh = (uint16_t*)s_raw;
   uint16_t* s_ql = s_qh + NC * HD;
-  float* const s_of = (float*)s_raw;  // merge slot k at s_of + k * NC * HD
+  float* const s_of = (float*)(s_raw + (ALIAS ? 0 : QBYTES));  // slot k at s_of + k * NC * HD
   __shared__ int s_pos[NC];
-  __shared__ float s_m[2][NC];
-  __shared__ float s_l[2][NC];
+  __shared__ float s_m[NSLOT][NC];
+  __shared__ float s_l[NSLOT][NC];
 
   const GroupDesc gd = a.plan->groups[blockIdx.z];
   const int wg = blockIdx.x;
@@ -74,9 +82,9 @@ __global__ __launch_bounds__(64 * kAttnWaves) void k_attn(AttnArgs a) {
   const size_t blk_elems = (size_t)16 * HD;
 
   // Page operands are loaded D pages ahead of their use into a ring of raw buffers (bf16
-  // bits; fp32 pools are split into bf16 hi/lo when used).  With one query tile a wave's
-  // whole run of pages is usually in flight at once.
-  constexpr int D = (sizeof(KT) == 2 && NT == 1) ? 4 : 2;
+  // bits; fp32 pools are split into bf16 hi/lo when used).  A decode split is usually two
+  // pages, so its whole run is in flight at once.
+  constexpr int D = 2;
   constexpr int KW = sizeof(KT) == 2 ? 1 : 2;  // 16-byte K loads per k-step
   u32x4 kraw[D][NS][KW];
   u32x4 vraw[D][ND];  // bf16: only the low 8 bytes are used
@@ -106,16 +114,21 @@ __global__ __launch_bounds__(64 * kAttnWaves) void k_attn(AttnArgs a) {
       for (int dt = 0; dt < ND; ++dt) vraw[buf][dt] = ld_nt16(vb + dt * 256 + 4 * l);
     }
   };
-  auto process_page = [&](int pg, auto cbc) {
-    constexpr int cb = decltype(cbc)::value;
-    // K operand: lane l holds K[t = l%16][d = 32s + 8(l/16) + j]; V^T: V[t = 4(l/16) + j][16dt + l%16]
+  // MFMA operands of one page.  K: lane l holds K[t = l%16][d = 32s + 8(l/16) + j];
+  // V^T: V[t = 4(l/16) + j][d = 16dt + l%16].  Slots past the group's last position hold no
+  // written value (possibly not even a finite one); P is zero there but 0 * NaN is not, so
+  // those V entries are zeroed.
+  struct PageOps {
     bf16x8 khi[NS], klo[NS];
     s16x4 vhi[ND], vlo[ND];
+  };
+  auto unpack = [&](int pg, auto cbc, PageOps& P) {
+    constexpr int cb = decltype(cbc)::value;
     if (sizeof(KT) == 2) {
 #pragma unroll
-      for (int s = 0; s < NS; ++s) khi[s] = __builtin_bit_cast(bf16x8, kraw[cb][s][0]);
+      for (int s = 0; s < NS; ++s) P.khi[s] = __builtin_bit_cast(bf16x8, kraw[cb][s][0]);
 #pragma unroll
-      for (int dt = 0; dt < ND; ++dt) vhi[dt] = __builtin_bit_cast(s16x4, u32x2{vraw[cb][dt][0], vraw[cb][dt][1]});
+      for (int dt = 0; dt < ND; ++dt) P.vhi[dt] = __builtin_bit_cast(s16x4, u32x2{vraw[cb][dt][0], vraw[cb][dt][1]});
     } else {
 #pragma unroll
       for (int s = 0; s < NS; ++s) {
@@ -130,8 +143,8 @@ __global__ __launch_bounds__(64 * kAttnWaves) void k_attn(AttnArgs a) {
           ph[q] = (uint32_t)h0 | ((uint32_t)h1 << 16);
           pl[q] = (uint32_t)l0 | ((uint32_t)l1 << 16);
         }
-        khi[s] = __builtin_bit_cast(bf16x8, ph);
-        klo[s] = __builtin_bit_cast(bf16x8, pl);
+        P.khi[s] = __builtin_bit_cast(bf16x8, ph);
+        P.klo[s] = __builtin_bit_cast(bf16x8, pl);
       }
 #pragma unroll
       for (int dt = 0; dt < ND; ++dt) {
@@ -144,76 +157,50 @@ __global__ __launch_bounds__(64 * kAttnWaves) void k_attn(AttnArgs a) {
           h4[q] = (short)hh;
           l4[q] = (short)ll;
         }
-        vhi[dt] = h4;
-        vlo[dt] = l4;
+        P.vhi[dt] = h4;
+        P.vlo[dt] = l4;
       }
     }
-    // Slots past the group's last position hold no written value (possibly not even a
-    // finite one); P is zero there but 0 * NaN is not, so those V entries are zeroed.
     if (pg * 16 + 15 > gd.maxpos) {
 #pragma unroll
       for (int dt = 0; dt < ND; ++dt)
 #pragma unroll
         for (int j = 0; j < 4; ++j)
           if (pg * 16 + 4 * lg + j > gd.maxpos) {
-            vhi[dt][j] = 0;
-            if (sizeof(KT) == 4) vlo[dt][j] = 0;
+            P.vhi[dt][j] = 0;
+            if (sizeof(KT) == 4) P.vlo[dt][j] = 0;
           }
     }
+  };
+  // S^T tile of one page: lane (c = lc, lg) gets the scores of positions 16pg + 4lg + i.
+  auto scores = [&](const PageOps& P, const bf16x8* qh, const bf16x8* ql) {
+    f32x4 sacc = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int nt = 0; nt < NT; ++nt) {
-      if (nt * 16 >= NQ) break;
-      f32x4 sacc = f32x4{0.f, 0.f, 0.f, 0.f};
-      const int qrow = (nt * 16 + lc) * HD;
+    for (int s = 0; s < NS; ++s) {
+      sacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(P.khi[s], qh[s], sacc, 0, 0, 0);
+      sacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(P.khi[s], ql[s], sacc, 0, 0, 0);
+      if (sizeof(KT) == 4) sacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(P.klo[s], qh[s], sacc, 0, 0, 0);
+    }
+    return sacc;
+  };
+  // O^T += V^T P^T for one page; P^T comes straight from the score accumulator layout.
+  auto accumulate = [&](const PageOps& P, const float* pv, f32x4* acc) {
+    s16x4 phi, plo;
 #pragma unroll
-      for (int s = 0; s < NS; ++s) {
-        const bf16x8 qh = *(const bf16x8*)(s_qh + qrow + 32 * s + 8 * lg);
-        const bf16x8 ql = *(const bf16x8*)(s_ql + qrow + 32 * s + 8 * lg);
-        sacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(khi[s], qh, sacc, 0, 0, 0);
-        sacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(khi[s], ql, sacc, 0, 0, 0);
-        if (sizeof(KT) == 4) sacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(klo[s], qh, sacc, 0, 0, 0);
-      }
-      // lane (c = lc, lg): sacc[i] = score of position pg*16 + 4*lg + i for column c
-      const int cpos = s_pos[nt * 16 + lc];
-      float sv[4];
-      float mloc = -INFINITY;
+    for (int i = 0; i < 4; ++i) {
+      uint16_t hh, ll;
+      split_bf16(pv[i], hh, ll);
+      phi[i] = (short)hh;
+      plo[i] = (short)ll;
+    }
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int tg = pg * 16 + 4 * lg + i;
-        sv[i] = (tg <= cpos) ? sacc[i] * a.scale_log2 : -INFINITY;
-        mloc = fmaxf(mloc, sv[i]);
-      }
-      mloc = fmaxf(mloc, __shfl_xor(mloc, 16));
-      mloc = fmaxf(mloc, __shfl_xor(mloc, 32));
-      const float m_new = fmaxf(m_run[nt], mloc);
-      const float alpha = (m_new == -INFINITY) ? 1.f : safe_exp2(m_run[nt] - m_new);
-      float pv[4], ls = 0.f;
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        pv[i] = (sv[i] == -INFINITY) ? 0.f : exp2f(sv[i] - m_new);
-        ls += pv[i];
-      }
-      ls += __shfl_xor(ls, 16);
-      ls += __shfl_xor(ls, 32);
-      l_run[nt] = l_run[nt] * alpha + ls;
-      m_run[nt] = m_new;
-      s16x4 phi, plo;
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        uint16_t hh, ll;
-        split_bf16(pv[i], hh, ll);
-        phi[i] = (short)hh;
-        plo[i] = (short)ll;
-      }
-#pragma unroll
-      for (int dt = 0; dt < ND; ++dt) {
-        o[nt][dt] *= alpha;
-        o[nt][dt] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vhi[dt], phi, o[nt][dt], 0, 0, 0);
-        o[nt][dt] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vhi[dt], plo, o[nt][dt], 0, 0, 0);
-        if (sizeof(KT) == 4) o[nt][dt] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vlo[dt], phi, o[nt][dt], 0, 0, 0);
-      }
+    for (int dt = 0; dt < ND; ++dt) {
+      acc[dt] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(P.vhi[dt], phi, acc[dt], 0, 0, 0);
+      acc[dt] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(P.vhi[dt], plo, acc[dt], 0, 0, 0);
+      if (sizeof(KT) == 4) acc[dt] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(P.vlo[dt], phi, acc[dt], 0, 0, 0);
     }
   };
+
   static_for<D>([&](auto b) {
     if (p0 + (int)b < p1) load_page(p0 + (int)b, b);
   });
@@ -234,74 +221,223 @@ __global__ __launch_bounds__(64 * kAttnWaves) void k_attn(AttnArgs a) {
   for (int c = tid; c < NC; c += blockDim.x) s_pos[c] = c < NQ ? a.plan->rows[gd.row0 + c / a.G].pos : -1;
   __syncthreads();
 
-  for (int base = p0; base < p1; base += D) {
-    static_for<D>([&](auto b) {
-      const int pg = base + (int)b;
-      if (pg < p1) {
-        process_page(pg, b);
-        if (pg + D < p1) load_page(pg + D, b);
+  if constexpr (NT == 1) {
+    // ---- one query tile: queries in registers, pages in pairs (one max and one sum
+    // reduction across the lane groups per 32 positions)
+    bf16x8 qh[NS], ql[NS];
+#pragma unroll
+    for (int s = 0; s < NS; ++s) {
+      qh[s] = *(const bf16x8*)(s_qh + lc * HD + 32 * s + 8 * lg);
+      ql[s] = *(const bf16x8*)(s_ql + lc * HD + 32 * s + 8 * lg);
+    }
+    const int cpos = s_pos[lc];
+    auto pair = [&](int pgA, auto ca, auto cbB) {
+      const int pgB = pgA + 1;
+      const bool hasB = pgB < p1;  // wave-uniform
+      PageOps A, B;
+      unpack(pgA, ca, A);
+      const f32x4 sa = scores(A, qh, ql);
+      f32x4 sb = f32x4{0.f, 0.f, 0.f, 0.f};
+      if (hasB) {
+        unpack(pgB, cbB, B);
+        sb = scores(B, qh, ql);
       }
-    });
-  }
+      float sv[8];
+      float mloc = -INFINITY;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int ta = pgA * 16 + 4 * lg + i, tb = pgB * 16 + 4 * lg + i;
+        sv[i] = (ta <= cpos) ? sa[i] * a.scale_log2 : -INFINITY;
+        sv[4 + i] = (hasB && tb <= cpos) ? sb[i] * a.scale_log2 : -INFINITY;
+        mloc = fmaxf(mloc, fmaxf(sv[i], sv[4 + i]));
+      }
+      mloc = fmaxf(mloc, __shfl_xor(mloc, 16));
+      mloc = fmaxf(mloc, __shfl_xor(mloc, 32));
+      const float m_new = fmaxf(m_run[0], mloc);
+      // o and l are still zero while m_run is -inf, so they need no rescale then
+      const bool grow = m_run[0] != -INFINITY && m_new != m_run[0];
+      const float alpha = grow ? __builtin_amdgcn_exp2f(m_run[0] - m_new) : 1.f;
+      float pv[8], ls = 0.f;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        pv[i] = (sv[i] == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(sv[i] - m_new);
+        ls += pv[i];
+      }
+      ls += __shfl_xor(ls, 16);
+      ls += __shfl_xor(ls, 32);
+      l_run[0] = l_run[0] * alpha + ls;
+      m_run[0] = m_new;
+      if (__builtin_amdgcn_read_exec() & __ballot(grow)) {  // any lane whose max moved
+#pragma unroll
+        for (int dt = 0; dt < ND; ++dt) o[0][dt] *= alpha;
+      }
+      accumulate(A, pv, o[0]);
+      if (hasB) accumulate(B, pv + 4, o[0]);
+    };
+    for (int base = p0; base < p1; base += D) {
+      static_for<D / 2>([&](auto h) {
+        constexpr int bA = 2 * decltype(h)::value;
+        const int pg = base + bA;
+        if (pg < p1) {
+          pair(pg, std::integral_constant<int, bA>{}, std::integral_constant<int, bA + 1>{});
+          if (pg + D < p1) load_page(pg + D, std::integral_constant<int, bA>{});
+          if (pg + 1 + D < p1) load_page(pg + 1 + D, std::integral_constant<int, bA + 1>{});
+        }
+      });
+    }
 
-  // ---- merge the 4 waves in two rounds through 2 LDS slots
-  auto publish = [&](int slot) {
+    // ---- one-round merge: waves 1-3 publish, wave 0 absorbs in order and stores
+    if (w > 0) {
 #pragma unroll
-    for (int nt = 0; nt < NT; ++nt) {
-      const int c = nt * 16 + lc;
-#pragma unroll
-      for (int dt = 0; dt < ND; ++dt)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) s_of[slot * NC * HD + c * HD + 16 * dt + 4 * lg + i] = o[nt][dt][i];
+      for (int dt = 0; dt < ND; ++dt) *(f32x4*)(s_of + (w - 1) * NC * HD + lc * HD + 16 * dt + 4 * lg) = o[0][dt];
       if (lg == 0) {
-        s_m[slot][c] = m_run[nt];
-        s_l[slot][c] = l_run[nt];
+        s_m[w - 1][lc] = m_run[0];
+        s_l[w - 1][lc] = l_run[0];
       }
     }
-  };
-  auto absorb = [&](int slot) {
+    __syncthreads();
+    if (w != 0) return;
 #pragma unroll
-    for (int nt = 0; nt < NT; ++nt) {
-      const int c = nt * 16 + lc;
-      const float m2 = s_m[slot][c], l2 = s_l[slot][c];
-      const float mm = fmaxf(m_run[nt], m2);
-      const float ca = (mm == -INFINITY) ? 0.f : safe_exp2(m_run[nt] - mm);
-      const float cb = (mm == -INFINITY) ? 0.f : safe_exp2(m2 - mm);
-      l_run[nt] = l_run[nt] * ca + l2 * cb;
-      m_run[nt] = mm;
+    for (int u = 0; u < 3; ++u) {
+      const float m2 = s_m[u][lc], l2 = s_l[u][lc];
+      const float mm = fmaxf(m_run[0], m2);
+      const float ca = (mm == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(m_run[0] - mm);
+      const float cb2 = (mm == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(m2 - mm);
+      l_run[0] = l_run[0] * ca + l2 * cb2;
+      m_run[0] = mm;
 #pragma unroll
-      for (int dt = 0; dt < ND; ++dt)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) o[nt][dt][i] = o[nt][dt][i] * ca + s_of[slot * NC * HD + c * HD + 16 * dt + 4 * lg + i] * cb;
+      for (int dt = 0; dt < ND; ++dt) {
+        const f32x4 x = *(const f32x4*)(s_of + u * NC * HD + lc * HD + 16 * dt + 4 * lg);
+        o[0][dt] = o[0][dt] * ca + x * cb2;
+      }
     }
-  };
-  __syncthreads();  // every wave is done with Q before the slots overwrite it
-  if (w >= 2) publish(w - 2);
-  __syncthreads();
-  if (w < 2) absorb(w);
-  __syncthreads();
-  if (w == 1) publish(0);
-  __syncthreads();
-  if (w == 0) {
-    absorb(0);
-    publish(1);  // workgroup result (unnormalised) in slot 1
-  }
-  __syncthreads();
+    if (lc >= NQ) return;
+    const int row = gd.row0 + lc / a.G, head = kvh * a.G + lc % a.G;
+    if (gd.nwg == 1) {
+      float* out = a.o + ((size_t)row * a.hq + head) * HD;
+      const float inv = 1.f / l_run[0];
+#pragma unroll
+      for (int dt = 0; dt < ND; ++dt) *(f32x4*)(out + 16 * dt + 4 * lg) = o[0][dt] * inv;
+      return;
+    }
+    const size_t ncols = (size_t)a.max_rows * a.G;
+    const size_t col = ((size_t)kvh * kAttnMaxWG + wg) * ncols + (size_t)gd.row0 * a.G + lc;
+#pragma unroll
+    for (int dt = 0; dt < ND; ++dt) *(f32x4*)(a.part + col * HD + 16 * dt + 4 * lg) = o[0][dt];
+    if (lg == 0) {
+      a.ml[col * 2 + 0] = m_run[0];
+      a.ml[col * 2 + 1] = l_run[0];
+    }
+  } else {
+    // ---- several query tiles: one page at a time, queries read from LDS
+    auto process_page = [&](int pg, auto cbc) {
+      PageOps P;
+      unpack(pg, cbc, P);
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) {
+        if (nt * 16 >= NQ) break;
+        const int qrow = (nt * 16 + lc) * HD;
+        bf16x8 qh[NS], ql[NS];
+#pragma unroll
+        for (int s = 0; s < NS; ++s) {
+          qh[s] = *(const bf16x8*)(s_qh + qrow + 32 * s + 8 * lg);
+          ql[s] = *(const bf16x8*)(s_ql + qrow + 32 * s + 8 * lg);
+        }
+        const f32x4 sacc = scores(P, qh, ql);
+        const int cpos = s_pos[nt * 16 + lc];
+        float sv[4];
+        float mloc = -INFINITY;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int tg = pg * 16 + 4 * lg + i;
+          sv[i] = (tg <= cpos) ? sacc[i] * a.scale_log2 : -INFINITY;
+          mloc = fmaxf(mloc, sv[i]);
+        }
+        mloc = fmaxf(mloc, __shfl_xor(mloc, 16));
+        mloc = fmaxf(mloc, __shfl_xor(mloc, 32));
+        const float m_new = fmaxf(m_run[nt], mloc);
+        const float alpha = (m_new == -INFINITY) ? 1.f : safe_exp2(m_run[nt] - m_new);
+        float pv[4], ls = 0.f;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          pv[i] = (sv[i] == -INFINITY) ? 0.f : exp2f(sv[i] - m_new);
+          ls += pv[i];
+        }
+        ls += __shfl_xor(ls, 16);
+        ls += __shfl_xor(ls, 32);
+        l_run[nt] = l_run[nt] * alpha + ls;
+        m_run[nt] = m_new;
+#pragma unroll
+        for (int dt = 0; dt < ND; ++dt) o[nt][dt] *= alpha;
+        accumulate(P, pv, o[nt]);
+      }
+    };
+    for (int base = p0; base < p1; base += D) {
+      static_for<D>([&](auto b) {
+        const int pg = base + (int)b;
+        if (pg < p1) {
+          process_page(pg, b);
+          if (pg + D < p1) load_page(pg + D, b);
+        }
+      });
+    }
 
-  const int ncols = a.max_rows * a.G;
-  if (gd.nwg == 1) {
-    for (int idx = tid; idx < NQ * HD; idx += blockDim.x) {
-      const int c = idx / HD, d = idx - c * HD;
-      const int row = gd.row0 + c / a.G, head = kvh * a.G + c % a.G;
-      a.o[((size_t)row * a.hq + head) * HD + d] = s_of[1 * NC * HD + c * HD + d] / s_l[1][c];
+    // ---- merge the 4 waves in two rounds through 2 LDS slots
+    auto publish = [&](int slot) {
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) {
+        const int c = nt * 16 + lc;
+#pragma unroll
+        for (int dt = 0; dt < ND; ++dt) *(f32x4*)(s_of + slot * NC * HD + c * HD + 16 * dt + 4 * lg) = o[nt][dt];
+        if (lg == 0) {
+          s_m[slot][c] = m_run[nt];
+          s_l[slot][c] = l_run[nt];
+        }
+      }
+    };
+    auto absorb = [&](int slot) {
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) {
+        const int c = nt * 16 + lc;
+        const float m2 = s_m[slot][c], l2 = s_l[slot][c];
+        const float mm = fmaxf(m_run[nt], m2);
+        const float ca = (mm == -INFINITY) ? 0.f : safe_exp2(m_run[nt] - mm);
+        const float cb2 = (mm == -INFINITY) ? 0.f : safe_exp2(m2 - mm);
+        l_run[nt] = l_run[nt] * ca + l2 * cb2;
+        m_run[nt] = mm;
+#pragma unroll
+        for (int dt = 0; dt < ND; ++dt)
+          o[nt][dt] = o[nt][dt] * ca + *(const f32x4*)(s_of + slot * NC * HD + c * HD + 16 * dt + 4 * lg) * cb2;
+      }
+    };
+    __syncthreads();  // every wave is done with Q before the slots overwrite it
+    if (w >= 2) publish(w - 2);
+    __syncthreads();
+    if (w < 2) absorb(w);
+    __syncthreads();
+    if (w == 1) publish(0);
+    __syncthreads();
+    if (w == 0) {
+      absorb(0);
+      publish(1);  // workgroup result (unnormalised) in slot 1
     }
-    return;
-  }
-  const size_t slot_base = ((size_t)kvh * kAttnMaxWG + wg) * ncols + (size_t)gd.row0 * a.G;
-  for (int idx = tid; idx < NQ * HD; idx += blockDim.x) a.part[slot_base * HD + idx] = s_of[1 * NC * HD + idx];
-  for (int c = tid; c < NQ; c += blockDim.x) {
-    a.ml[(slot_base + c) * 2 + 0] = s_m[1][c];
-    a.ml[(slot_base + c) * 2 + 1] = s_l[1][c];
+    __syncthreads();
+
+    const int ncols = a.max_rows * a.G;
+    if (gd.nwg == 1) {
+      for (int idx = tid; idx < NQ * HD; idx += blockDim.x) {
+        const int c = idx / HD, d = idx - c * HD;
+        const int row = gd.row0 + c / a.G, head = kvh * a.G + c % a.G;
+        a.o[((size_t)row * a.hq + head) * HD + d] = s_of[1 * NC * HD + c * HD + d] / s_l[1][c];
+      }
+      return;
+    }
+    const size_t slot_base = ((size_t)kvh * kAttnMaxWG + wg) * ncols + (size_t)gd.row0 * a.G;
+    for (int idx = tid; idx < NQ * HD; idx += blockDim.x) a.part[slot_base * HD + idx] = s_of[1 * NC * HD + idx];
+    for (int c = tid; c < NQ; c += blockDim.x) {
+      a.ml[(slot_base + c) * 2 + 0] = s_m[1][c];
+      a.ml[(slot_base + c) * 2 + 1] = s_l[1][c];
+    }
   }
 }
 

@@ -735,10 +735,15 @@ static laser_status launch_forward(laser_model* m, laser_kv* kv, const FwdKey& k
     a.gain = m->final_norm;
     a.row_map = 1;
     a.lm_part = m->wsp<LmPart>(L.lm_part);
-    const int ng = groups_lm(d, key.n_out);
-    st = gemm(LASER_K_LMHEAD, EPI_LMHEAD, a, d.d_model, d.vocab, ng, key.n_out);
-    if (st != LASER_OK) return st;
-    HIP_TRY(timed(m, LASER_K_LMHEAD, s, [&] { return launch_lm_reduce(dp, a.lm_part, ng, key.n_out, s); }));
+    a.K = d.d_model;
+    a.N = d.vocab;
+    a.n_groups = groups_lm(d, key.n_out);
+    a.M = key.n_out;
+    HIP_TRY(timed(m, LASER_K_LMHEAD, s, [&] {
+      hipError_t e = launch_gemm(dt, gemm_mode(key.n_out), EPI_LMHEAD, a, s);
+      if (e == hipSuccess) e = launch_lm_reduce(dp, a.lm_part, a.n_groups, key.n_out, s);
+      return e;
+    }));
   }
   return LASER_OK;
 }
