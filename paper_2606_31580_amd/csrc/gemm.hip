@@ -41,21 +41,42 @@ __device__ __forceinline__ T* pick2(bool c0, T* p0, T* p1) {
   return (T*)(u0 * (uint64_t)c0 + u1 * (uint64_t)(!c0));
 }
 
-// Row j (< RW) of workgroup g: its weights.  QKV groups hold RW/2 rotary pairs
-// (i, i + hd/2) of one head, SwiGLU groups RW/2 gate rows and the matching up rows; rows
-// past the matrix read row 0 (their results are discarded).
+// Rotary pair gp of the QKV rows: pair (i, i + hd/2) of head h, heads numbered q, then k,
+// then v.  A workgroup holds RW/2 consecutive pairs (they may span two heads).
+struct QkvPair {
+  int hh, i;  // head within q, k or v; pair index within the head
+  bool isq, isk;
+  const void* bias;
+  const void* w;
+};
+
+__device__ __forceinline__ QkvPair qkv_pair(const GemmArgs& a, int gp) {
+  QkvPair q;
+  const int half = a.hd >> 1;
+  const int h = gp / half;
+  q.i = gp - h * half;
+  q.isq = h < a.hq;
+  q.isk = !q.isq && h < a.hq + a.hkv;
+  q.hh = q.isq ? h : (q.isk ? h - a.hq : h - a.hq - a.hkv);
+  q.bias = pick3(q.isq, q.isk, a.b0, a.b1, a.b2);
+  q.w = pick3(q.isq, q.isk, a.w0, a.w1, a.w2);
+  return q;
+}
+
+// Row j (< RW) of workgroup g: its weights.  QKV groups hold RW/2 rotary pairs, SwiGLU
+// groups RW/2 gate rows and the matching up rows; rows past the matrix read row 0 (their
+// results are discarded).
 template <class WT, int EPI, int RW>
 __device__ __forceinline__ const char* weight_row(const GemmArgs& a, int g, int j) {
   constexpr int P = RW / 2;
   const size_t rowbytes = (size_t)a.K * sizeof(WT);
   if (EPI == EPI_QKV) {
-    const int per_head = a.hd / RW;
-    const int h = g / per_head, p = g - h * per_head;
-    const int dim = (j < P) ? (P * p + j) : (a.hd / 2 + P * p + (j - P));
-    const bool isq = h < a.hq, isk = !isq && h < a.hq + a.hkv;
-    const char* base = (const char*)pick3(isq, isk, a.w0, a.w1, a.w2);
-    const int hr = isq ? h : (isk ? h - a.hq : h - a.hq - a.hkv);
-    return base + (size_t)(hr * a.hd + dim) * rowbytes;
+    const int jj = j < P ? j : j - P;
+    int gp = P * g + jj;
+    if (gp >= (a.hq + 2 * a.hkv) * (a.hd >> 1)) gp = 0;
+    const QkvPair q = qkv_pair(a, gp);
+    const int dim = j < P ? q.i : (a.hd >> 1) + q.i;
+    return (const char*)q.w + (size_t)(q.hh * a.hd + dim) * rowbytes;
   } else if (EPI == EPI_SWIGLU) {
     int r = P * g + (j % P);
     if (r >= a.F) r = 0;
@@ -114,39 +135,21 @@ struct EpiItem {
   int page = 0;              // QKV: KV page that holds pos
 };
 
-struct QkvGroup {
-  int hh, p;  // head within q/k/v, group within the head
-  bool isq, isk;
-  const void* bias;
-};
-
-template <int RW>
-__device__ __forceinline__ QkvGroup qkv_group(const GemmArgs& a, int g) {
-  QkvGroup q;
-  const int per_head = a.hd / RW;
-  const int h = g / per_head;
-  q.p = g - h * per_head;
-  q.isq = h < a.hq;
-  q.isk = !q.isq && h < a.hq + a.hkv;
-  q.hh = q.isq ? h : (q.isk ? h - a.hq : h - a.hq - a.hkv);
-  q.bias = pick3(q.isq, q.isk, a.b0, a.b1, a.b2);
-  return q;
-}
-
 // First fetch: what depends only on the item (row descriptor, bias, current h).
 template <class WT, int EPI, int RW>
 __device__ __forceinline__ void epi_fetch_a(const GemmArgs& a, int g, int M, int idx, EpiItem& it) {
   constexpr int P = RW / 2;
   if (EPI == EPI_QKV) {
     if (idx >= M * P) return;
-    const QkvGroup q = qkv_group<RW>(a, g);
-    it.live = true;
     it.m = idx / P;
     it.j = idx - it.m * P;
-    const int i = P * q.p + it.j;
+    const int gp = P * g + it.j;
+    it.live = gp < (a.hq + 2 * a.hkv) * (a.hd >> 1);
+    if (!it.live) return;
+    const QkvPair q = qkv_pair(a, gp);
     if (q.bias != nullptr) {
-      it.v0 = ldw<WT>(q.bias, (size_t)q.hh * a.hd + i);
-      it.v1 = ldw<WT>(q.bias, (size_t)q.hh * a.hd + (a.hd >> 1) + i);
+      it.v0 = ldw<WT>(q.bias, (size_t)q.hh * a.hd + q.i);
+      it.v1 = ldw<WT>(q.bias, (size_t)q.hh * a.hd + (a.hd >> 1) + q.i);
     }
     const RowDesc rd = a.plan->rows[it.m];
     it.pos = rd.pos;
@@ -166,8 +169,8 @@ template <class WT, int EPI, int RW>
 __device__ __forceinline__ void epi_fetch_b(const GemmArgs& a, int g, EpiItem& it) {
   if (EPI != EPI_QKV || !it.live) return;
   constexpr int P = RW / 2;
-  const QkvGroup q = qkv_group<RW>(a, g);
-  if (q.isq || q.isk) it.cs = a.rope[(size_t)it.pos * (a.hd >> 1) + P * q.p + it.j];
+  const QkvPair q = qkv_pair(a, P * g + it.j);
+  if (q.isq || q.isk) it.cs = a.rope[(size_t)it.pos * (a.hd >> 1) + q.i];
   if (!q.isq) it.page = a.bt[(size_t)it.seq * a.max_pps + (it.pos >> 4)];
 }
 
@@ -177,9 +180,8 @@ __device__ __forceinline__ void epi_apply(const GemmArgs& a, int g, const EpiIte
   if (!it.live) return;
   constexpr int P = RW / 2;
   if (EPI == EPI_QKV) {
-    const QkvGroup q = qkv_group<RW>(a, g);
-    const int i = P * q.p + it.j;
-    const int dlo = i, dhi = (a.hd >> 1) + i;
+    const QkvPair q = qkv_pair(a, P * g + it.j);
+    const int dlo = q.i, dhi = (a.hd >> 1) + q.i;
     float ylo = Y[it.m * RW + it.j] + it.v0, yhi = Y[it.m * RW + P + it.j] + it.v1;
     if (q.isq || q.isk) {
       const float rlo = ylo * it.cs.x - yhi * it.cs.y;
@@ -293,9 +295,9 @@ __device__ __forceinline__ void unpack16(const u32x4& raw, float* out) {
 
 // ----------------------------------------------------------------------------- VALU GEMV
 
-template <class WT, int M, int EPI>
+template <class WT, int M, int EPI, int RW>
 __global__ __launch_bounds__(kGemvMaxThreads) void k_gemv(GemmArgs a) {
-  constexpr int RW = rows_per_group(EPI, false);
+  constexpr int RWP = RW <= 4 ? 4 : (RW <= 8 ? 8 : 16);  // RW padded to a power of two
   constexpr int CH = 16 / (int)sizeof(WT);  // elements per 16-byte load
   constexpr int U = 2;                      // chunks in flight per thread
   constexpr int NV = RW * M + M;            // per-wave totals: outputs, then sums of squares
@@ -391,11 +393,12 @@ __global__ __launch_bounds__(kGemvMaxThreads) void k_gemv(GemmArgs a) {
   // wave totals, then the waves in fixed order
 #pragma unroll
   for (int m = 0; m < M; ++m) {
-    float vv[RW];
+    float vv[RWP];
 #pragma unroll
-    for (int r = 0; r < RW; ++r) vv[r] = acc[r][m];
-    const float t = transpose_reduce<RW>(vv, l);
-    if ((l & (64 / RW - 1)) == 0) s_red[w][transpose_index<RW>(l) * M + m] = t;
+    for (int r = 0; r < RWP; ++r) vv[r] = r < RW ? acc[r][m] : 0.f;
+    const float t = transpose_reduce<RWP>(vv, l);
+    const int ti = transpose_index<RWP>(l);
+    if ((l & (64 / RWP - 1)) == 0 && ti < RW) s_red[w][ti * M + m] = t;
     if (norm) {
       const float s = wave_sum(sq[m]);
       if (l == 0) s_red[w][RW * M + m] = s;
@@ -424,12 +427,13 @@ __global__ __launch_bounds__(kGemvMaxThreads) void k_gemv(GemmArgs a) {
 // ----------------------------------------------------------------------------- MFMA GEMM
 
 template <class WT, int MT, int EPI>
-__global__ __launch_bounds__(kGemmThreads) void k_gemm_mfma(GemmArgs a) {
+__global__ __launch_bounds__(64 * kMfmaMaxWaves) void k_gemm_mfma(GemmArgs a) {
   constexpr int RW = rows_per_group(EPI, true);
   constexpr int NLD = (int)sizeof(WT) / 2;  // 16-byte loads per step (bf16: 1, fp32: 2)
-  constexpr int U = 4;                      // steps kept in flight per wave
-  __shared__ float s_red[4][16 * MT * RW];
-  __shared__ float s_sq[4][16 * MT];
+  constexpr int U = MT == 1 ? 6 : (MT == 2 ? 4 : 2);  // steps kept in flight per wave
+  const int W = blockDim.x >> 6;            // waves splitting K: 4, or 8 for few row groups
+  __shared__ float s_red[kMfmaMaxWaves][16 * MT * RW];
+  __shared__ float s_sq[kMfmaMaxWaves][16 * MT];
   __shared__ float Y[16 * MT * RW];
   __shared__ float s_scale[16 * MT];
   const int tid = threadIdx.x, w = tid >> 6, l = tid & 63;
@@ -446,7 +450,7 @@ __global__ __launch_bounds__(kGemmThreads) void k_gemm_mfma(GemmArgs a) {
     xr[mt] = a.x + (size_t)a_src_row(a, min(16 * mt + n, M - 1)) * a.ldx;
   }
   const int nsteps = (a.K + 31) >> 5;
-  const int niter = nsteps > w ? (nsteps - w + 3) >> 2 : 0;  // this wave's steps: s = w + 4*it
+  const int niter = nsteps > w ? (nsteps - w + W - 1) / W : 0;  // this wave's steps: s = w + W*it
   f32x4 acc[MT];
   float sq[MT];
 #pragma unroll
@@ -456,41 +460,50 @@ __global__ __launch_bounds__(kGemmThreads) void k_gemm_mfma(GemmArgs a) {
   }
   // K offset of this lane's 8 elements at iteration it, or -1 past the end of K
   auto kof = [&](int it) {
-    const int k = 32 * (w + 4 * it) + kg;
+    const int k = 32 * (w + W * it) + kg;
     return k < a.K ? k : -1;
   };
-  auto ldw16 = [&](int it, int q) -> u32x4 {
-    const int k = kof(it);
-    return ld_nt16(wp + (size_t)(k < 0 ? 0 : k) * sizeof(WT) + 16 * q);
+  // Every operand of a step (weights, activations, gain) is loaded U steps ahead of its use.
+  struct Step {
+    u32x4 wv[NLD];
+    u32x4 gv[NLD];
+    float4 xv[MT][2];
   };
-  u32x4 buf[U][NLD];
+  auto issue = [&](int it, Step& st) {
+    const int k = kof(it), kk = k < 0 ? 0 : k;
+#pragma unroll
+    for (int q = 0; q < NLD; ++q) st.wv[q] = ld_nt16(wp + (size_t)kk * sizeof(WT) + 16 * q);
+    if (norm)
+#pragma unroll
+      for (int q = 0; q < NLD; ++q) st.gv[q] = *(const u32x4*)((const char*)a.gain + (size_t)kk * sizeof(WT) + 16 * q);
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) {
+      st.xv[mt][0] = *(const float4*)(xr[mt] + kk);
+      st.xv[mt][1] = *(const float4*)(xr[mt] + kk + 4);
+    }
+  };
+  Step buf[U];
 #pragma unroll
   for (int u = 0; u < U; ++u)
-    if (u < niter)
-#pragma unroll
-      for (int q = 0; q < NLD; ++q) buf[u][q] = ldw16(u, q);
+    if (u < niter) issue(u, buf[u]);
   for (int it0 = 0; it0 < niter; it0 += U) {
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int it = it0 + u;
       if (it < niter) {
-        u32x4 cur[NLD];
-#pragma unroll
-        for (int q = 0; q < NLD; ++q) cur[q] = buf[u][q];
-        if (it + U < niter)
-#pragma unroll
-          for (int q = 0; q < NLD; ++q) buf[u][q] = ldw16(it + U, q);
+        const Step cur = buf[u];
+        if (it + U < niter) issue(it + U, buf[u]);
         const int k = kof(it);
         bf16x8 bhi, blo;
         if (NLD == 1) {
-          bhi = __builtin_bit_cast(bf16x8, cur[0]);
+          bhi = __builtin_bit_cast(bf16x8, cur.wv[0]);
         } else {
           u32x4 ph, pl;
 #pragma unroll
           for (int q = 0; q < 4; ++q) {
             uint16_t h0, l0, h1, l1;
-            split_bf16(__uint_as_float(cur[q >> 1][(q & 1) * 2 + 0]), h0, l0);
-            split_bf16(__uint_as_float(cur[q >> 1][(q & 1) * 2 + 1]), h1, l1);
+            split_bf16(__uint_as_float(cur.wv[q >> 1][(q & 1) * 2 + 0]), h0, l0);
+            split_bf16(__uint_as_float(cur.wv[q >> 1][(q & 1) * 2 + 1]), h1, l1);
             ph[q] = (uint32_t)h0 | ((uint32_t)h1 << 16);
             pl[q] = (uint32_t)l0 | ((uint32_t)l1 << 16);
           }
@@ -500,20 +513,15 @@ __global__ __launch_bounds__(kGemmThreads) void k_gemm_mfma(GemmArgs a) {
         float gf[8];
 #pragma unroll
         for (int e = 0; e < 8; ++e) gf[e] = 1.f;
-        if (norm && k >= 0) {
-          u32x4 g0 = *(const u32x4*)((const char*)a.gain + (size_t)k * sizeof(WT));
-          unpack16<WT>(g0, gf);
-          if (sizeof(WT) == 4) {
-            u32x4 g1 = *(const u32x4*)((const char*)a.gain + (size_t)k * sizeof(WT) + 16);
-            unpack16<WT>(g1, gf + 4);
-          }
+        if (norm) {
+          unpack16<WT>(cur.gv[0], gf);
+          if (sizeof(WT) == 4) unpack16<WT>(cur.gv[NLD - 1], gf + 4);
         }
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt) {
           u32x4 ph, pl;
           if (k >= 0) {
-            const float4 x0 = *(const float4*)(xr[mt] + k);
-            const float4 x1 = *(const float4*)(xr[mt] + k + 4);
+            const float4 x0 = cur.xv[mt][0], x1 = cur.xv[mt][1];
             float xe[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
             if (norm) {
 #pragma unroll
@@ -524,11 +532,10 @@ __global__ __launch_bounds__(kGemmThreads) void k_gemm_mfma(GemmArgs a) {
             }
 #pragma unroll
             for (int q = 0; q < 4; ++q) {
-              uint16_t h0, l0, h1, l1;
-              split_bf16(xe[2 * q], h0, l0);
-              split_bf16(xe[2 * q + 1], h1, l1);
-              ph[q] = (uint32_t)h0 | ((uint32_t)h1 << 16);
-              pl[q] = (uint32_t)l0 | ((uint32_t)l1 << 16);
+              uint32_t h, lo;
+              split_trunc2(xe[2 * q], xe[2 * q + 1], h, lo);
+              ph[q] = h;
+              pl[q] = lo;
             }
           } else {
             ph = u32x4{0u, 0u, 0u, 0u};
@@ -556,12 +563,14 @@ __global__ __launch_bounds__(kGemmThreads) void k_gemm_mfma(GemmArgs a) {
   }
   __syncthreads();
   if (norm && tid < M) {
-    const float s = (s_sq[0][tid] + s_sq[1][tid]) + (s_sq[2][tid] + s_sq[3][tid]);
+    float s = 0.f;
+    for (int v = 0; v < W; ++v) s += s_sq[v][tid];
     s_scale[tid] = rsqrtf(s / (float)a.K + a.eps);
   }
   __syncthreads();
   for (int idx = tid; idx < M * RW; idx += blockDim.x) {
-    const float v = (s_red[0][idx] + s_red[1][idx]) + (s_red[2][idx] + s_red[3][idx]);
+    float v = 0.f;
+    for (int q = 0; q < W; ++q) v += s_red[q][idx];
     Y[idx] = norm ? v * s_scale[idx / RW] : v;
   }
   __syncthreads();
@@ -571,20 +580,24 @@ __global__ __launch_bounds__(kGemmThreads) void k_gemm_mfma(GemmArgs a) {
 // ----------------------------------------------------------------------------- launch
 
 template <class WT, int MODE>
-static hipError_t launch_epi(int epi, const GemmArgs& a, hipStream_t s) {
+static hipError_t launch_epi(int epi, int rw, const GemmArgs& a, hipStream_t s) {
   const dim3 grid(a.n_groups);
   dim3 block(kGemmThreads);
   if constexpr (MODE <= 4) {
     // long rows (the down projection) use 8 waves so each thread streams fewer chunks
     if (a.K / (16 / (int)sizeof(WT)) > 2048) block = dim3(kGemvMaxThreads);
-    switch (epi) {
-      case EPI_QKV: return launch_k(k_gemv<WT, MODE, EPI_QKV>, grid, block, s, a);
-      case EPI_RESID: return launch_k(k_gemv<WT, MODE, EPI_RESID>, grid, block, s, a);
-      case EPI_SWIGLU: return launch_k(k_gemv<WT, MODE, EPI_SWIGLU>, grid, block, s, a);
-      case EPI_LMHEAD: return launch_k(k_gemv<WT, MODE, EPI_LMHEAD>, grid, block, s, a);
-      default: return hipErrorInvalidValue;
-    }
+    if (epi == EPI_QKV && rw == 6) return launch_k(k_gemv<WT, MODE, EPI_QKV, 6>, grid, block, s, a);
+    if (epi == EPI_QKV && rw == 8) return launch_k(k_gemv<WT, MODE, EPI_QKV, 8>, grid, block, s, a);
+    if (epi == EPI_RESID && rw == 6) return launch_k(k_gemv<WT, MODE, EPI_RESID, 6>, grid, block, s, a);
+    if (epi == EPI_RESID && rw == 7) return launch_k(k_gemv<WT, MODE, EPI_RESID, 7>, grid, block, s, a);
+    if (epi == EPI_RESID && rw == 8) return launch_k(k_gemv<WT, MODE, EPI_RESID, 8>, grid, block, s, a);
+    if (epi == EPI_SWIGLU && rw == 8) return launch_k(k_gemv<WT, MODE, EPI_SWIGLU, 8>, grid, block, s, a);
+    if (epi == EPI_LMHEAD && rw == 8) return launch_k(k_gemv<WT, MODE, EPI_LMHEAD, 8>, grid, block, s, a);
+    return hipErrorInvalidValue;
   } else {
+    if (rw != rows_per_group(epi, true)) return hipErrorInvalidValue;
+    // few row groups (the O, down and QKV projections): 8 waves split K more finely
+    if (a.n_groups < 512) block = dim3(64 * kMfmaMaxWaves);
     switch (epi) {
       case EPI_QKV: return launch_k(k_gemm_mfma<WT, MODE - 4, EPI_QKV>, grid, block, s, a);
       case EPI_RESID: return launch_k(k_gemm_mfma<WT, MODE - 4, EPI_RESID>, grid, block, s, a);
@@ -596,23 +609,23 @@ static hipError_t launch_epi(int epi, const GemmArgs& a, hipStream_t s) {
 }
 
 template <class WT>
-static hipError_t launch_mode(int mode, int epi, const GemmArgs& a, hipStream_t s) {
+static hipError_t launch_mode(int mode, int epi, int rw, const GemmArgs& a, hipStream_t s) {
   switch (mode) {
-    case 1: return launch_epi<WT, 1>(epi, a, s);
-    case 2: return launch_epi<WT, 2>(epi, a, s);
-    case 3: return launch_epi<WT, 3>(epi, a, s);
-    case 4: return launch_epi<WT, 4>(epi, a, s);
-    case 5: return launch_epi<WT, 5>(epi, a, s);
-    case 6: return launch_epi<WT, 6>(epi, a, s);
-    case 7: return launch_epi<WT, 7>(epi, a, s);
-    case 8: return launch_epi<WT, 8>(epi, a, s);
+    case 1: return launch_epi<WT, 1>(epi, rw, a, s);
+    case 2: return launch_epi<WT, 2>(epi, rw, a, s);
+    case 3: return launch_epi<WT, 3>(epi, rw, a, s);
+    case 4: return launch_epi<WT, 4>(epi, rw, a, s);
+    case 5: return launch_epi<WT, 5>(epi, rw, a, s);
+    case 6: return launch_epi<WT, 6>(epi, rw, a, s);
+    case 7: return launch_epi<WT, 7>(epi, rw, a, s);
+    case 8: return launch_epi<WT, 8>(epi, rw, a, s);
     default: return hipErrorInvalidValue;
   }
 }
 
-hipError_t launch_gemm(int dtype, int mode, int epi, const GemmArgs& a, hipStream_t s) {
-  if (dtype == 1) return launch_mode<bf16_t>(mode, epi, a, s);
-  return launch_mode<float>(mode, epi, a, s);
+hipError_t launch_gemm(int dtype, int mode, int epi, int rw, const GemmArgs& a, hipStream_t s) {
+  if (dtype == 1) return launch_mode<bf16_t>(mode, epi, rw, a, s);
+  return launch_mode<float>(mode, epi, rw, a, s);
 }
 
 }  // namespace laser

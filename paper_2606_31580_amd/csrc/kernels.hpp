@@ -15,6 +15,7 @@ constexpr int kAttnWaves = 4;     // waves per attention workgroup (one split ea
 constexpr int kAttnMaxWG = 128;   // attention workgroups per (group, kv head)
 constexpr int kGemmThreads = 256; // 4 waves
 constexpr int kGemvMaxThreads = 512;
+constexpr int kMfmaMaxWaves = 8;    // waves of an MFMA projection workgroup with few row groups
 
 // One row of a forward: request slot, position, and where its input token id lives.
 struct RowDesc {
@@ -60,9 +61,10 @@ struct LmPart {
 
 enum Epi { EPI_QKV = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_LMHEAD = 3 };
 
-// Output rows per workgroup of a projection: 8 on the VALU path, 16 (one matrix-core tile)
-// on the MFMA path.  Rotary and gate/up rows come in pairs, half of a group each.
-constexpr int rows_per_group(int, bool mfma) { return mfma ? 16 : 8; }
+// Output rows per workgroup of a projection on the MFMA path (one matrix-core tile).  The
+// VALU path takes 8, or 6 / 7 where that spreads the groups evenly over the compute units
+// (launch_gemm's rw).  Rotary and gate/up rows come in pairs, half of a group each.
+constexpr int rows_per_group(int, bool) { return 16; }
 
 struct GemmArgs {
   // weights (row-major [rows][K] in the model dtype)
@@ -135,7 +137,8 @@ inline hipError_t launch_k(K kernel, dim3 grid, dim3 block, hipStream_t s, Args.
 }
 
 // dtype: 0 fp32, 1 bf16.  mode: 1..4 VALU rows per forward, 5..8 MFMA with 1..4 m-tiles.
-hipError_t launch_gemm(int dtype, int mode, int epi, const GemmArgs& a, hipStream_t s);
+// rw: rows per workgroup (VALU: QKV 6 or 8, residual 6, 7 or 8, others 8; MFMA: 16).
+hipError_t launch_gemm(int dtype, int mode, int epi, int rw, const GemmArgs& a, hipStream_t s);
 hipError_t launch_attn(int dtype, int hd, int nt, const AttnArgs& a, dim3 grid, hipStream_t s);
 hipError_t launch_attn_merge(const AttnArgs& a, int M, int hd, hipStream_t s);
 hipError_t launch_lm_reduce(const Plan* plan, const LmPart* part, int n_groups, int n_out, hipStream_t s);

@@ -110,7 +110,8 @@ constexpr int kMaxTimingEvents = 1 << 16;  // per session; later launches go unt
 struct laser_model {
   laser_model_desc desc;
   int device = 0;
-  int es = 4;  // bytes per stored element
+  int cus = 256;  // compute units of the device (set at creation)
+  int es = 4;     // bytes per stored element
   const void* embed = nullptr;
   const void* lm_head = nullptr;
   const void* final_norm = nullptr;
@@ -166,11 +167,34 @@ static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 static int gemm_mode(int M) { return M <= 4 ? M : 4 + ceil_div(M, 16); }
 
-static int rw_of(int M) { return rows_per_group(0, M > 4); }
-static int groups_qkv(const laser_model_desc& d, int M) { return (d.n_q_heads + 2 * d.n_kv_heads) * d.head_dim / rw_of(M); }
-static int groups_gateup(const laser_model_desc& d, int M) { return ceil_div(d.d_ffn, rw_of(M) / 2); }
-static int groups_resid(const laser_model_desc& d, int M) { return d.d_model / rw_of(M); }
-static int groups_lm(const laser_model_desc& d, int M) { return ceil_div(d.vocab, rw_of(M)); }
+// Workgroups of a projection with `rows` output rows (SwiGLU: gate + up rows) at rw rows each.
+static int proj_groups(int epi, int rows, int rw) {
+  return epi == EPI_SWIGLU ? ceil_div(rows / 2, rw / 2) : ceil_div(rows, rw);
+}
+
+// Rows per workgroup: 16 on the MFMA path (M > 4).  On the VALU path the candidate that
+// puts the fewest rows on the busiest compute unit (workgroups dealt round-robin over
+// `cus`), larger groups first on ties; QKV groups must tile the rotary pairs exactly.
+static int proj_rw(int epi, int rows, int M, int cus) {
+  if (M > 4) return rows_per_group(epi, true);
+  static const int kQkv[] = {8, 6}, kResid[] = {8, 7, 6}, kOther[] = {8};
+  const int* cand = epi == EPI_QKV ? kQkv : (epi == EPI_RESID ? kResid : kOther);
+  const int nc = epi == EPI_QKV ? 2 : (epi == EPI_RESID ? 3 : 1);
+  int best = 8;
+  long long best_cost = -1;
+  for (int c = 0; c < nc; ++c) {
+    const int rw = cand[c];
+    if (epi == EPI_QKV && rows % rw) continue;
+    const long long cost = (long long)ceil_div(proj_groups(epi, rows, rw), cus) * rw;
+    if (best_cost < 0 || cost < best_cost) {
+      best = rw;
+      best_cost = cost;
+    }
+  }
+  return best;
+}
+
+static int groups_lm(const laser_model_desc& d, int M) { return ceil_div(d.vocab, M > 4 ? 16 : 8); }
 
 static Layout make_layout(const laser_model_desc& d, int max_rows) {
   Layout L{};
@@ -227,6 +251,10 @@ extern "C" laser_status laser_model_create(const laser_model_desc* desc, laser_m
   m->es = desc->dtype == LASER_DTYPE_BF16 ? 2 : 4;
   m->layers.assign(desc->n_layers, LayerW{});
   (void)hipGetDevice(&m->device);
+  {
+    int cus = 0;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, m->device) == hipSuccess && cus > 0) m->cus = cus;
+  }
   handle_add(m);
   *out = m;
   return LASER_OK;
@@ -542,8 +570,8 @@ static void plan_groups(const laser_model* m, Plan& p) {
     g.nrows = e - r;
     g.npages = maxpos / kPage + 1;
     g.maxpos = maxpos;
-    // a page costs one 16-column query tile per 16 columns of the group
-    units += (long long)g.npages * d.n_kv_heads * ceil_div(g.nrows * G, 16);
+    // wider query tiles make a page costlier: weight by half the group's 16-column tiles
+    units += (long long)g.npages * d.n_kv_heads * ceil_div(ceil_div(g.nrows * G, 16), 2);
     r = e;
   }
   const int base = std::max(1, (int)((units + kTargetAttnWaves - 1) / kTargetAttnWaves));
@@ -651,13 +679,15 @@ static laser_status launch_forward(laser_model* m, laser_kv* kv, const FwdKey& k
   base.act = m->wsp<float>(L.act);
   base.F = d.d_ffn;
 
-  auto gemm = [&](int cls, int epi, GemmArgs a, int K, int N, int n_groups, int M) -> laser_status {
+  // rows: output rows of the projection (SwiGLU: gate and up rows together)
+  auto gemm = [&](int cls, int epi, GemmArgs a, int K, int N, int rows, int M) -> laser_status {
+    const int rw = proj_rw(epi, rows, M, m->cus);
     a.K = K;
     a.N = N;
-    a.n_groups = n_groups;
+    a.n_groups = proj_groups(epi, rows, rw);
     a.M = M;
     const int mode = gemm_mode(M);
-    HIP_TRY(timed(m, cls, s, [&] { return launch_gemm(dt, mode, epi, a, s); }));
+    HIP_TRY(timed(m, cls, s, [&] { return launch_gemm(dt, mode, epi, rw, a, s); }));
     return LASER_OK;
   };
 
@@ -692,7 +722,8 @@ static laser_status launch_forward(laser_model* m, laser_kv* kv, const FwdKey& k
     a.ldx = d.d_model;
     a.gain = W.attn_norm;
     a.layer = li;
-    st = gemm(LASER_K_QKV, EPI_QKV, a, d.d_model, (d.n_q_heads + 2 * d.n_kv_heads) * hd, groups_qkv(d, key.M), key.M);
+    st = gemm(LASER_K_QKV, EPI_QKV, a, d.d_model, (d.n_q_heads + 2 * d.n_kv_heads) * hd,
+              (d.n_q_heads + 2 * d.n_kv_heads) * hd, key.M);
     if (st != LASER_OK) return st;
 
     aa.layer = li;
@@ -707,7 +738,7 @@ static laser_status launch_forward(laser_model* m, laser_kv* kv, const FwdKey& k
     a.x = m->wsp<float>(L.o);
     a.ldx = d.n_q_heads * hd;
     a.gain = nullptr;
-    st = gemm(LASER_K_OPROJ, EPI_RESID, a, d.n_q_heads * hd, d.d_model, groups_resid(d, key.M), key.M);
+    st = gemm(LASER_K_OPROJ, EPI_RESID, a, d.n_q_heads * hd, d.d_model, d.d_model, key.M);
     if (st != LASER_OK) return st;
 
     a = base;
@@ -716,7 +747,7 @@ static laser_status launch_forward(laser_model* m, laser_kv* kv, const FwdKey& k
     a.x = h;
     a.ldx = d.d_model;
     a.gain = W.mlp_norm;
-    st = gemm(LASER_K_GATEUP, EPI_SWIGLU, a, d.d_model, 2 * d.d_ffn, groups_gateup(d, key.M), key.M);
+    st = gemm(LASER_K_GATEUP, EPI_SWIGLU, a, d.d_model, 2 * d.d_ffn, 2 * d.d_ffn, key.M);
     if (st != LASER_OK) return st;
 
     a = base;
@@ -724,7 +755,7 @@ static laser_status launch_forward(laser_model* m, laser_kv* kv, const FwdKey& k
     a.x = m->wsp<float>(L.act);
     a.ldx = d.d_ffn;
     a.gain = nullptr;
-    st = gemm(LASER_K_DOWN, EPI_RESID, a, d.d_ffn, d.d_model, groups_resid(d, key.M), key.M);
+    st = gemm(LASER_K_DOWN, EPI_RESID, a, d.d_ffn, d.d_model, d.d_model, key.M);
     if (st != LASER_OK) return st;
   }
   if (key.n_out > 0) {
@@ -740,7 +771,7 @@ static laser_status launch_forward(laser_model* m, laser_kv* kv, const FwdKey& k
     a.n_groups = groups_lm(d, key.n_out);
     a.M = key.n_out;
     HIP_TRY(timed(m, LASER_K_LMHEAD, s, [&] {
-      hipError_t e = launch_gemm(dt, gemm_mode(key.n_out), EPI_LMHEAD, a, s);
+      hipError_t e = launch_gemm(dt, gemm_mode(key.n_out), EPI_LMHEAD, key.n_out > 4 ? 16 : 8, a, s);
       if (e == hipSuccess) e = launch_lm_reduce(dp, a.lm_part, a.n_groups, key.n_out, s);
       return e;
     }));
