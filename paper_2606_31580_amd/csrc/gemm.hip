@@ -482,72 +482,86 @@ __global__ __launch_bounds__(64 * kMfmaMaxWaves) void k_gemm_mfma(GemmArgs a) {
       st.xv[mt][1] = *(const float4*)(xr[mt] + kk + 4);
     }
   };
+  // The MFMAs of one step from its operands (k < 0: past the end of K, contributes zero;
+  // checked only when `checkc` is true, i.e. in the tail steps).
+  auto compute = [&](const Step& cur, int k, auto checkc) {
+    constexpr bool check = decltype(checkc)::value;
+    bf16x8 bhi, blo;
+    if (NLD == 1) {
+      bhi = __builtin_bit_cast(bf16x8, cur.wv[0]);
+    } else {
+      u32x4 ph, pl;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        uint16_t h0, l0, h1, l1;
+        split_bf16(__uint_as_float(cur.wv[q >> 1][(q & 1) * 2 + 0]), h0, l0);
+        split_bf16(__uint_as_float(cur.wv[q >> 1][(q & 1) * 2 + 1]), h1, l1);
+        ph[q] = (uint32_t)h0 | ((uint32_t)h1 << 16);
+        pl[q] = (uint32_t)l0 | ((uint32_t)l1 << 16);
+      }
+      bhi = __builtin_bit_cast(bf16x8, ph);
+      blo = __builtin_bit_cast(bf16x8, pl);
+    }
+    float gf[8];
+    if (norm) {
+      unpack16<WT>(cur.gv[0], gf);
+      if (sizeof(WT) == 4) unpack16<WT>(cur.gv[NLD - 1], gf + 4);
+    }
+    const bool live = !check || k >= 0;
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) {
+      const float4 x0 = cur.xv[mt][0], x1 = cur.xv[mt][1];
+      float xe[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
+      if (check)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) xe[e] = live ? xe[e] : 0.f;
+      if (norm) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          sq[mt] = fmaf(xe[e], xe[e], sq[mt]);
+          xe[e] *= gf[e];
+        }
+      }
+      u32x4 ph, pl;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        uint32_t h, lo;
+        split_trunc2(xe[2 * q], xe[2 * q + 1], h, lo);
+        ph[q] = h;
+        pl[q] = lo;
+      }
+      const bf16x8 ahi = __builtin_bit_cast(bf16x8, ph), alo = __builtin_bit_cast(bf16x8, pl);
+      acc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ahi, bhi, acc[mt], 0, 0, 0);
+      acc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(alo, bhi, acc[mt], 0, 0, 0);
+      if (NLD == 2) acc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ahi, blo, acc[mt], 0, 0, 0);
+    }
+  };
   Step buf[U];
 #pragma unroll
   for (int u = 0; u < U; ++u)
     if (u < niter) issue(u, buf[u]);
-  for (int it0 = 0; it0 < niter; it0 += U) {
+  // Steps whose 32 columns all lie inside K need no end check; with K a multiple of 32 (all
+  // model shapes) that is every step.
+  const int nfull = (a.K >> 5) > w ? ((a.K >> 5) - w + W - 1) / W : 0;
+  using Check = std::integral_constant<bool, true>;
+  using NoCheck = std::integral_constant<bool, false>;
+  int it0 = 0;
+  // steady state: U whole steps per trip, each buffer refilled right after its use
+  for (; it0 + U <= nfull; it0 += U) {
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      const int it = it0 + u;
-      if (it < niter) {
-        const Step cur = buf[u];
-        if (it + U < niter) issue(it + U, buf[u]);
-        const int k = kof(it);
-        bf16x8 bhi, blo;
-        if (NLD == 1) {
-          bhi = __builtin_bit_cast(bf16x8, cur.wv[0]);
-        } else {
-          u32x4 ph, pl;
-#pragma unroll
-          for (int q = 0; q < 4; ++q) {
-            uint16_t h0, l0, h1, l1;
-            split_bf16(__uint_as_float(cur.wv[q >> 1][(q & 1) * 2 + 0]), h0, l0);
-            split_bf16(__uint_as_float(cur.wv[q >> 1][(q & 1) * 2 + 1]), h1, l1);
-            ph[q] = (uint32_t)h0 | ((uint32_t)h1 << 16);
-            pl[q] = (uint32_t)l0 | ((uint32_t)l1 << 16);
-          }
-          bhi = __builtin_bit_cast(bf16x8, ph);
-          blo = __builtin_bit_cast(bf16x8, pl);
-        }
-        float gf[8];
-#pragma unroll
-        for (int e = 0; e < 8; ++e) gf[e] = 1.f;
-        if (norm) {
-          unpack16<WT>(cur.gv[0], gf);
-          if (sizeof(WT) == 4) unpack16<WT>(cur.gv[NLD - 1], gf + 4);
-        }
-#pragma unroll
-        for (int mt = 0; mt < MT; ++mt) {
-          u32x4 ph, pl;
-          if (k >= 0) {
-            const float4 x0 = cur.xv[mt][0], x1 = cur.xv[mt][1];
-            float xe[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
-            if (norm) {
-#pragma unroll
-              for (int e = 0; e < 8; ++e) {
-                sq[mt] = fmaf(xe[e], xe[e], sq[mt]);
-                xe[e] *= gf[e];
-              }
-            }
-#pragma unroll
-            for (int q = 0; q < 4; ++q) {
-              uint32_t h, lo;
-              split_trunc2(xe[2 * q], xe[2 * q + 1], h, lo);
-              ph[q] = h;
-              pl[q] = lo;
-            }
-          } else {
-            ph = u32x4{0u, 0u, 0u, 0u};
-            pl = ph;
-          }
-          const bf16x8 ahi = __builtin_bit_cast(bf16x8, ph), alo = __builtin_bit_cast(bf16x8, pl);
-          acc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ahi, bhi, acc[mt], 0, 0, 0);
-          acc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(alo, bhi, acc[mt], 0, 0, 0);
-          if (NLD == 2) acc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ahi, blo, acc[mt], 0, 0, 0);
-        }
-      }
+      compute(buf[u], kof(it0 + u), NoCheck{});
+      if (it0 + u + U < niter) issue(it0 + u + U, buf[u]);
     }
+  }
+  // remaining steps (fewer than U whole steps, then a partial one): operands already issued
+  for (; it0 < niter; it0 += U) {
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+      if (it0 + u < niter) {
+        compute(buf[u], kof(it0 + u), Check{});
+        if (it0 + u + U < niter) issue(it0 + u + U, buf[u]);
+      }
   }
   // lane (n, l/16): acc[mt][i] = Y[m = 16mt + 4(l/16) + i][n]; sq over the lanes of row n
 #pragma unroll
