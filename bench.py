@@ -4,7 +4,11 @@
 One step = one chain-of-thought decode token for every request of the batch; every
 `probe_every` steps each request also runs the trial-answer probe (S=8 suffix tokens,
 T=4 trial tokens) and the host takes the load-aware exit decision on its confidence,
-as at an action transition point.  Inputs are synthetic and seeded: random-initialised
+as at an action transition point.  By default the probe rides along: the request is
+forked at the ATP and the fork's suffix rows (one per forward by default) and fed-back
+trial tokens join the next decode forwards, so the probe costs an extra row in those
+forwards instead of its own weight passes; the decision follows S + T - 1 forwards later.  With
+--probe-mode separate the probe runs as its own forwards between decode steps.  Inputs are synthetic and seeded: random-initialised
 weights of the named shape and pre-filled random KV (stand-ins for the paper's trained
 reasoners and their chains of thought, which are not available here).
 
@@ -33,6 +37,10 @@ def parse():
     ap.add_argument("--workload", default="7B-b1-kv14336")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--profile-only", action="store_true", help="steps only, no reporting (for rocprofv3 runs)")
+    ap.add_argument("--probe-mode", choices=["riding", "separate"], default="riding",
+                    help="riding: each probe's rows ride along with the next decode forwards on a fork of the "
+                         "request; separate: the probe runs as its own forwards between decode steps")
+    ap.add_argument("--probe-rows", type=int, default=1, help="probe rows per forward in riding mode")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 256 MiB device-to-device copy three times (scale for HBM byte counters)")
     return ap.parse_args()
@@ -76,10 +84,11 @@ def main():
 
     log(f"workload {wl.name}: generating weights")
     weights = synth.make_weights(shape, device=dev)
-    model = L.Model(shape, weights, max_rows=max(B, B * S), max_positions=max_pos)
+    R = args.probe_rows
+    model = L.Model(shape, weights, max_rows=max(B + B * R, B * S), max_positions=max_pos)
     pps = max_pos // PAGE + 1
-    num_pages = sum((n + 2 * total_steps + S + T) // PAGE + 2 for n in lens) + 8
-    kv = L.KVCache(model, num_pages, B, pps)
+    num_pages = sum((n + 2 * total_steps + S + T) // PAGE + 2 for n in lens) + B * ((S + T) // PAGE + 3) + 8
+    kv = L.KVCache(model, num_pages, 2 * B, pps)  # slots B..2B-1 hold the probes' forks
     for i, n in enumerate(lens):
         k0, v0 = synth.make_prefill_kv(shape, n, i, device=dev)
         kv.add_seq(i, n)
@@ -87,36 +96,81 @@ def main():
         del k0, v0
     torch.cuda.synchronize()
     seqs = list(range(B))
+    forks = [B + b for b in seqs]
     tokens = synth.make_tokens(B, shape.vocab, 3003).to(dev)
     nxt = torch.empty(B, dtype=torch.int32, device=dev)
     pmax = torch.empty(B, device=dev)
     suffix = synth.make_suffix(S, shape.vocab).to(dev)
     conf = torch.empty(B, device=dev)
     argm = torch.empty(B * T, dtype=torch.int32, device=dev)
+    ptrial = torch.empty(B * T, device=dev)
     params = L.laser_params_default()
     load_state = L.laser_load_state(0.0)
     stream = torch.cuda.current_stream()
 
-    probe_ms = []
+    probe_ms = []  # riding: ATP to exit decision (wall, the decode forwards included); separate: the probe
+    n_probes = [0]
+    ride = {}  # progress of the riding probes in flight: suffix rows and trial tokens done
+
+    def decide(c):
+        for b in range(B):  # the controller needs the confidence on the host
+            L.laser_exit_decision(params, load_state, float(c[b]), B, 0, 10)
+        n_probes[0] += 1
 
     def step(i, timed_probe):
-        L.laser_decode_step(model, kv, seqs, tokens, nxt, pmax)
+        at_atp = wl.probe_every and i % wl.probe_every == 0
+        if args.probe_mode == "separate":
+            L.laser_decode_step(model, kv, seqs, tokens, nxt, pmax)
+            tokens.copy_(nxt)
+            if at_atp:
+                if timed_probe:  # latency of the probe itself, not of decode steps still queued
+                    torch.cuda.synchronize()
+                t0 = time.perf_counter()
+                L.laser_probe_confidence(model, kv, seqs, suffix, T, conf, argm)
+                decide(conf.cpu().numpy())
+                if timed_probe:
+                    probe_ms.append((time.perf_counter() - t0) * 1e3)
+            return
+        if at_atp and not ride:  # fork every request at its current length
+            ev0 = torch.cuda.Event(enable_timing=True)
+            ev0.record(stream)
+            for b in seqs:
+                kv.fork(b, forks[b])
+            ride.update(s=0, t=0, ev0=ev0)
+        spans = [L.span(b, 1, 0, b, out=(0, b)) for b in seqs]
+        tok1 = None
+        if ride:
+            if ride["s"] < S:
+                k = min(R, S - ride["s"])
+                last = ride["s"] + k == S
+                spans += [L.span(forks[b], k, 1, ride["s"], out=(1, b * T) if last else None) for b in seqs]
+                tok1 = suffix
+                ride["s"] += k
+            else:
+                ride["t"] += 1
+                j = ride["t"]
+                spans += [L.span(forks[b], 1, 1, b * T + j - 1, out=(1, b * T + j)) for b in seqs]
+                tok1 = argm
+        L.laser_forward(model, kv, spans, tokens, tok1, nxt, pmax, argm, ptrial)
         tokens.copy_(nxt)
-        if wl.probe_every and (i + 1) % wl.probe_every == 0:
-            if timed_probe:  # latency of the probe itself, not of decode steps still queued
-                torch.cuda.synchronize()
-            t0 = time.perf_counter()
-            L.laser_probe_confidence(model, kv, seqs, suffix, T, conf, argm)
-            c = conf.cpu().numpy()  # the controller needs the confidence on the host
-            for b in range(B):
-                L.laser_exit_decision(params, load_state, float(c[b]), B, 0, 10)
-            if timed_probe:
-                probe_ms.append((time.perf_counter() - t0) * 1e3)
+        if ride and ride["s"] == S and ride["t"] == T - 1:
+            L.laser_confidence(model, ptrial, T, B, conf)
+            ev1 = torch.cuda.Event(enable_timing=True)
+            ev1.record(stream)
+            decide(conf.cpu().numpy())
+            for b in seqs:
+                kv.free_seq(forks[b])
+            if timed_probe:  # device time from the fork to the confidence (decode forwards included)
+                probe_ms.append(ride["ev0"].elapsed_time(ev1))
+            ride.clear()
 
     log("warmup")
     for i in range(args.warmup):
         step(i, False)
+    while ride:  # no probe crosses into the timed region
+        step(-1, False)
     torch.cuda.synchronize()
+    n_probes[0] = 0
 
     if args.profile_only:  # the timed loop's work (decode steps with their probes), nothing else
         for i in range(args.steps):
@@ -138,6 +192,17 @@ def main():
     ms_total = e0.elapsed_time(e1)
     ms_per_step = ms_total / args.steps
     value = args.steps * B / (ms_total / 1e3)
+    probes_timed = n_probes[0]
+    while ride:  # a probe still riding: finish it outside the timed region
+        step(-1, False)
+    # reference: the probe run as separate forwards (the cost it has when nothing rides along)
+    sep_ms = []
+    for _ in range(2):
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        L.laser_probe_confidence(model, kv, seqs, suffix, T, conf, argm)
+        conf.cpu()
+        sep_ms.append((time.perf_counter() - t0) * 1e3)
     log(f"timed {args.steps} steps: {ms_per_step:.3f} ms/step, {value:.1f} tok/s (wall {wall:.2f}s)")
 
     # ---- decode only (same cache, no probes)
@@ -207,6 +272,12 @@ def main():
         "decode_only_tok_s": round(B / (dec_ms / 1e3), 2),
         "probe_latency_ms": {"mean": round(float(np.mean(probe_ms)), 3) if probe_ms else None,
                              "max": round(float(np.max(probe_ms)), 3) if probe_ms else None, "n": len(probe_ms)},
+        "probe": {"mode": args.probe_mode, "rows_per_forward": R if args.probe_mode == "riding" else S,
+                  "forwards_per_probe": (-(-S // R) + T - 1) if args.probe_mode == "riding" else 1 + T - 1,
+                  "probes_in_timed_region": probes_timed,
+                  "latency_meaning": "device time from the ATP fork to the confidence, decode forwards included"
+                  if args.probe_mode == "riding" else "host time of the probe call with its confidence copy",
+                  "separate_probe_latency_ms": round(float(np.mean(sep_ms)), 3)},
         "step_hbm": {"bytes": step_bytes, "achieved_GBs": round(step_gbs, 1), "frac_of_peak": round(step_gbs / HBM_PEAK_GBS, 4)},
         "roofline": {"kernel": "gate/up projection + SwiGLU (k_gemv, EPI_SWIGLU)", "bound": "hbm",
                      "achieved": round(gu_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",

@@ -12,6 +12,8 @@
  *   laser_decode_step        one greedy decode token per request over a paged KV cache
  *   laser_probe_confidence   the trial-answer probe, returning confidence and argmax ids
  *   laser_step_mixed         decode for a batch plus probe chunks for a subset, one forward
+ *   laser_kv_fork, laser_forward, laser_confidence
+ *                            the pieces of a probe that rides along with later decode steps
  *   laser_exit_decision      the host-side ATP decision (Eq. 5 threshold, Algorithm 1)
  *   laser_budget             the budget pre-allocation of Eq. 6-8
  *
@@ -118,7 +120,10 @@ laser_status laser_exit_decision(const laser_params* p, laser_load_state* state,
  * a token lands at a length that is a multiple of page_size; a sequence added with a
  * length takes its pages in ascending id order; truncation returns the pages beyond the
  * kept length.  Every allocation is all-or-nothing (OUT_OF_PAGES leaves the pool as it
- * was).  Sequence ids are 0 <= seq_id < max_seqs. */
+ * was).  Sequence ids are 0 <= seq_id < max_seqs.  A fork shares its source's full pages
+ * (reference counted: a page returns to the pool when no sequence holds it) and takes a
+ * fresh lowest-id page for a copy of the source's partial last page; a truncation that
+ * would end inside a shared page is refused (INVALID_ARG). */
 typedef struct laser_page_pool laser_page_pool;
 
 laser_status laser_pages_create(int num_pages, int page_size, int max_seqs, int max_pages_per_seq,
@@ -127,6 +132,8 @@ laser_status laser_pages_add_seq(laser_page_pool* pool, int seq_id, int length);
 laser_status laser_pages_append(laser_page_pool* pool, int seq_id, int n_tokens);
 laser_status laser_pages_truncate(laser_page_pool* pool, int seq_id, int length);
 laser_status laser_pages_free_seq(laser_page_pool* pool, int seq_id);
+/* dst_seq (a free slot) gets src_seq's length and contents as described above. */
+laser_status laser_pages_fork(laser_page_pool* pool, int src_seq, int dst_seq);
 /* Copies the page ids of seq_id (in sequence order) to out[0..n-1]; *n_out = n.
  * INVALID_ARG if cap < n. */
 laser_status laser_pages_table(const laser_page_pool* pool, int seq_id, int32_t* out, int cap, int* n_out);
@@ -201,6 +208,11 @@ laser_status laser_kv_import(laser_kv* kv, int seq_id, const void* d_k, const vo
 /* Inverse of import: gathers all positions of seq_id into [n_layers][len][hkv][hd]. */
 laser_status laser_kv_export(const laser_kv* kv, int seq_id, void* d_k, void* d_v, void* stream);
 laser_status laser_kv_free_seq(laser_kv* kv, int seq_id);
+/* Forks src_seq into the free slot dst_seq (page pool rules above): dst_seq starts with
+ * src_seq's length and sees the same K/V; the partial last page, if any, is copied on
+ * `stream` (all layers and kv heads).  Appending to either sequence afterwards never
+ * touches the other's positions.  Used to run a probe beside the request's decode. */
+laser_status laser_kv_fork(laser_kv* kv, int src_seq, int dst_seq, void* stream);
 laser_status laser_kv_seq_len(const laser_kv* kv, int seq_id, int* len_out);
 laser_status laser_kv_page_table(const laser_kv* kv, int seq_id, int32_t* out, int cap, int* n_out);
 laser_status laser_kv_destroy(laser_kv* kv);
@@ -245,6 +257,27 @@ laser_status laser_step_mixed(laser_model* m, laser_kv* kv, int batch, const int
                               const int32_t* d_tokens, int32_t* d_next, float* d_max_prob, int n_probe,
                               const int32_t* probe_idx, const int32_t* d_suffix, int S, int T, float* d_conf,
                               int32_t* d_argmax, void* stream);
+
+/* One forward over spans of rows: span i appends spans[i].n_tokens tokens to sequence
+ * spans[i].seq at its current length, with input ids (tok_sel ? d_tok1 : d_tok0)
+ * [tok_off .. tok_off + n_tokens - 1]; if spans[i].out is nonzero the greedy token and
+ * max-softmax probability of the span's last row go to (out_sel ? d_out_tok1 : d_out_tok0)
+ * [out_off] and (out_sel ? d_out_p1 : d_out_p0)[out_off].  A decode step is a span of one
+ * token per request; a prompt or probe chunk is a longer span; spans of different
+ * sequences mix freely (this is how a probe rides along with decode steps on a fork of
+ * the request: Section 3.1's probe, with the request's own tokens unaffected).  Sequences
+ * are distinct across spans; the total rows are at most max_rows.  Input and output
+ * arrays may alias when no output index is also read as an input of the same call. */
+typedef struct {
+  int32_t seq, n_tokens, tok_sel, tok_off, out, out_sel, out_off;
+} laser_span;
+laser_status laser_forward(laser_model* m, laser_kv* kv, int n_spans, const laser_span* spans,
+                           const int32_t* d_tok0, const int32_t* d_tok1, int32_t* d_out_tok0, float* d_out_p0,
+                           int32_t* d_out_tok1, float* d_out_p1, void* stream);
+
+/* d_conf[i] = (d_p[i*T] + ... + d_p[i*T + T-1]) / T for i < n: the confidence of
+ * Section 3.1 from the trial tokens' max-softmax probabilities. */
+laser_status laser_confidence(laser_model* m, const float* d_p, int T, int n, float* d_conf, void* stream);
 
 /* ========================================================================== */
 /* Kernel timing.  While any class is enabled (a timing session), forwards launch their

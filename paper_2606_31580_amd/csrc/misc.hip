@@ -130,6 +130,25 @@ __global__ void k_confidence(const float* p, int T, int n, float* conf) {
   conf[r] = s / (float)T;
 }
 
+// Copy of one page (every layer and kv head, K and V) from page src to page dst: grid
+// (n_layers * hkv), 16-byte chunks of the 16 x hd block.
+__global__ __launch_bounds__(256) void k_page_copy(void* kpool, void* vpool, int num_pages, int hkv, size_t blk_bytes,
+                                                   int src, int dst) {
+  const int layer = blockIdx.x / hkv, h = blockIdx.x - layer * hkv;
+  const size_t s_off = (((size_t)layer * num_pages + src) * hkv + h) * blk_bytes;
+  const size_t d_off = (((size_t)layer * num_pages + dst) * hkv + h) * blk_bytes;
+  for (size_t c = threadIdx.x; c < blk_bytes / 16; c += blockDim.x) {
+    *(u32x4*)((char*)kpool + d_off + 16 * c) = *(const u32x4*)((const char*)kpool + s_off + 16 * c);
+    *(u32x4*)((char*)vpool + d_off + 16 * c) = *(const u32x4*)((const char*)vpool + s_off + 16 * c);
+  }
+}
+
+hipError_t launch_page_copy(int dtype, void* kpool, void* vpool, int num_pages, int n_layers, int hkv, int hd, int src,
+                            int dst, hipStream_t s) {
+  const size_t blk_bytes = (size_t)16 * hd * (dtype == 1 ? 2 : 4);
+  return launch_k(k_page_copy, dim3(n_layers * hkv), dim3(256), s, kpool, vpool, num_pages, hkv, blk_bytes, src, dst);
+}
+
 hipError_t launch_embed(int dtype, const Plan* plan, int M, const void* embed, int d, int vocab, float* h, int* bt,
                         int max_pps, hipStream_t s) {
   const dim3 grid(M, d / 64);

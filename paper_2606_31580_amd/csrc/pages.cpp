@@ -10,14 +10,19 @@ namespace laser {
 
 PagePool::PagePool(int num_pages, int page_size, int max_seqs, int max_pages_per_seq)
     : num_pages_(num_pages), page_size_(page_size), max_seqs_(max_seqs), max_pages_per_seq_(max_pages_per_seq),
-      tables_(max_seqs), lens_(max_seqs, 0), live_(max_seqs, 0) {
+      tables_(max_seqs), lens_(max_seqs, 0), live_(max_seqs, 0), refs_(num_pages, 0) {
   for (int i = 0; i < num_pages; ++i) free_.insert(free_.end(), i);
 }
 
 int PagePool::take_lowest() {
   int p = *free_.begin();
   free_.erase(free_.begin());
+  refs_[p] = 1;
   return p;
+}
+
+void PagePool::release(int page) {
+  if (--refs_[page] == 0) free_.insert(page);
 }
 
 int PagePool::add_seq(int seq, int length, std::vector<PageUpdate>* upd) {
@@ -63,9 +68,38 @@ int PagePool::truncate(int seq, int length) {
   if (!live(seq)) return laser_fail(LASER_ERR_INVALID_ARG, "seq_id %d not present", seq);
   if (length < 0 || length > lens_[seq]) return laser_fail(LASER_ERR_INVALID_ARG, "truncate length out of range");
   int keep = pages_for(length);
-  for (size_t i = keep; i < tables_[seq].size(); ++i) free_.insert(tables_[seq][i]);
+  if (length % page_size_ != 0 && refs_[tables_[seq][keep - 1]] > 1)
+    return laser_fail(LASER_ERR_INVALID_ARG, "seq %d: length %d ends inside a shared page", seq, length);
+  for (size_t i = keep; i < tables_[seq].size(); ++i) release(tables_[seq][i]);
   tables_[seq].resize(keep);
   lens_[seq] = length;
+  return LASER_OK;
+}
+
+int PagePool::fork(int src, int dst, std::vector<PageUpdate>* upd, PageCopy* copy, bool* has_copy) {
+  if (!live(src)) return laser_fail(LASER_ERR_INVALID_ARG, "seq_id %d not present", src);
+  if (dst < 0 || dst >= max_seqs_) return laser_fail(LASER_ERR_INVALID_ARG, "seq_id %d out of range", dst);
+  if (live_[dst]) return laser_fail(LASER_ERR_INVALID_ARG, "seq_id %d already present", dst);
+  const int full = lens_[src] / page_size_;
+  const bool partial = lens_[src] % page_size_ != 0;
+  if (partial && free_.empty()) return laser_fail(LASER_ERR_OUT_OF_PAGES, "need 1 page, 0 free");
+  tables_[dst].clear();
+  for (int i = 0; i < full; ++i) {
+    const int p = tables_[src][i];
+    ++refs_[p];
+    tables_[dst].push_back(p);
+    if (upd) upd->push_back({dst, i, p});
+  }
+  *has_copy = partial;
+  if (partial) {
+    const int p = take_lowest();
+    copy->src = tables_[src][full];
+    copy->dst = p;
+    tables_[dst].push_back(p);
+    if (upd) upd->push_back({dst, full, p});
+  }
+  lens_[dst] = lens_[src];
+  live_[dst] = 1;
   return LASER_OK;
 }
 
@@ -120,6 +154,13 @@ laser_status laser_pages_append(laser_page_pool* h, int seq_id, int n_tokens) {
 laser_status laser_pages_truncate(laser_page_pool* h, int seq_id, int length) {
   POOL_OR_FAIL(h);
   return (laser_status)P->truncate(seq_id, length);
+}
+
+laser_status laser_pages_fork(laser_page_pool* h, int src_seq, int dst_seq) {
+  POOL_OR_FAIL(h);
+  laser::PageCopy c{};
+  bool has = false;
+  return (laser_status)P->fork(src_seq, dst_seq, nullptr, &c, &has);
 }
 
 laser_status laser_pages_free_seq(laser_page_pool* h, int seq_id) {

@@ -11,6 +11,11 @@ struct PageUpdate {
   int seq, idx, page;  // block_table[seq][idx] = page
 };
 
+// A page whose contents must be copied to another page (the partial last page of a fork).
+struct PageCopy {
+  int src, dst;
+};
+
 class PagePool {
  public:
   PagePool(int num_pages, int page_size, int max_seqs, int max_pages_per_seq);
@@ -32,14 +37,20 @@ class PagePool {
   int append(int seq, int n, std::vector<PageUpdate>* upd);
   int truncate(int seq, int length);
   int free_seq(int seq);
+  // dst (a free slot) sees src's current positions: src's full pages are shared (reference
+  // counted), the page holding the partial tail (if any) is copied into a fresh page.
+  int fork(int src, int dst, std::vector<PageUpdate>* upd, PageCopy* copy, bool* has_copy);
+  int refs(int page) const { return refs_[page]; }
 
  private:
   int take_lowest();
+  void release(int page);
   int num_pages_, page_size_, max_seqs_, max_pages_per_seq_;
   std::set<int> free_;
   std::vector<std::vector<int>> tables_;
   std::vector<int> lens_;
   std::vector<char> live_;
+  std::vector<int> refs_;  // tables referencing each page
 };
 
 }  // namespace laser

@@ -1071,6 +1071,97 @@ extern "C" laser_status laser_step_mixed(laser_model* m, laser_kv* kv, int batch
   return st;
 }
 
+// ----------------------------------------------------------------------------- forks, spans
+
+extern "C" laser_status laser_kv_fork(laser_kv* kv, int src_seq, int dst_seq, void* stream) {
+  if (!kv_of(kv)) return laser_fail(LASER_ERR_STATE, "invalid or destroyed kv");
+  laser_model* m = const_cast<laser_model*>(kv->m);
+  if (!model_of(m) || !m->finalized) return laser_fail(LASER_ERR_STATE, "model not finalized");
+  PageCopy c{};
+  bool has = false;
+  std::vector<PageUpdate> upd;
+  const int st = kv->pool.fork(src_seq, dst_seq, &upd, &c, &has);
+  if (st != LASER_OK) return (laser_status)st;
+  kv->pending.insert(kv->pending.end(), upd.begin(), upd.end());  // block-table rows travel with the next plan
+  if (has) {
+    hipStream_t s = (hipStream_t)stream;
+    const laser_model_desc& d = m->desc;
+    TimingScope scope(m);
+    const hipError_t e = timed(m, LASER_K_OTHER, s, [&] {
+      return launch_page_copy(d.dtype == LASER_DTYPE_BF16, kv->kpool, kv->vpool, kv->pool.num_pages(), d.n_layers,
+                              d.n_kv_heads, d.head_dim, c.src, c.dst, s);
+    });
+    if (e != hipSuccess) return laser_fail(LASER_ERR_HIP, "page copy: %s", hipGetErrorString(e));
+  }
+  return LASER_OK;
+}
+
+extern "C" laser_status laser_forward(laser_model* m, laser_kv* kv, int n_spans, const laser_span* spans,
+                                      const int32_t* d_tok0, const int32_t* d_tok1, int32_t* d_out_tok0, float* d_out_p0,
+                                      int32_t* d_out_tok1, float* d_out_p1, void* stream) {
+  laser_status st = check_ready(m, kv);
+  if (st != LASER_OK) return st;
+  if (n_spans < 1 || !spans) return laser_fail(LASER_ERR_INVALID_ARG, "need at least one span");
+  long long rows = 0;
+  std::vector<int> seqs, grow;
+  for (int i = 0; i < n_spans; ++i) {
+    const laser_span& sp = spans[i];
+    if (sp.n_tokens < 1 || sp.tok_off < 0 || (sp.tok_sel != 0 && sp.tok_sel != 1))
+      return laser_fail(LASER_ERR_INVALID_ARG, "span %d: bad n_tokens, tok_sel or tok_off", i);
+    if (!(sp.tok_sel ? d_tok1 : d_tok0)) return laser_fail(LASER_ERR_INVALID_ARG, "span %d: its token array is NULL", i);
+    if (sp.out) {
+      if ((sp.out_sel != 0 && sp.out_sel != 1) || sp.out_off < 0)
+        return laser_fail(LASER_ERR_INVALID_ARG, "span %d: bad out_sel or out_off", i);
+      if (!(sp.out_sel ? d_out_tok1 : d_out_tok0) || !(sp.out_sel ? d_out_p1 : d_out_p0))
+        return laser_fail(LASER_ERR_INVALID_ARG, "span %d: its output arrays are NULL", i);
+    }
+    rows += sp.n_tokens;
+    seqs.push_back(sp.seq);
+    grow.push_back(sp.n_tokens);
+  }
+  if (rows > m->max_rows) return laser_fail(LASER_ERR_INVALID_ARG, "%lld rows exceed max_rows %d", rows, m->max_rows);
+  st = check_growth(m, kv, seqs, grow);
+  if (st != LASER_OK) return st;
+  hipStream_t s = (hipStream_t)stream;
+  st = flush_pending(kv, m, s);
+  if (st != LASER_OK) return st;
+  Plan* p = new (std::nothrow) Plan;
+  if (!p) return laser_fail(LASER_ERR_INVALID_ARG, "allocation failed");
+  p->M = 0;
+  p->n_out = 0;
+  p->n_bt = 0;
+  std::vector<PageUpdate> upd;
+  for (int i = 0; i < n_spans; ++i) {
+    const laser_span& sp = spans[i];
+    const int pos0 = kv->pool.len(sp.seq);
+    kv->pool.append(sp.seq, sp.n_tokens, &upd);
+    for (int t = 0; t < sp.n_tokens; ++t) p->rows[p->M + t] = RowDesc{sp.seq, pos0 + t, sp.tok_sel, sp.tok_off + t};
+    p->M += sp.n_tokens;
+    if (sp.out) p->outs[p->n_out++] = OutDesc{p->M - 1, sp.out_sel, sp.out_off, 0};
+  }
+  push_updates(*p, upd);
+  PlanIO io{};
+  io.tok_src[0] = d_tok0;
+  io.tok_src[1] = d_tok1;
+  io.tok_dst[0] = d_out_tok0;
+  io.tok_dst[1] = d_out_tok1;
+  io.p_dst[0] = d_out_p0;
+  io.p_dst[1] = d_out_p1;
+  st = run_forward(m, kv, *p, io, s);
+  delete p;
+  return st;
+}
+
+extern "C" laser_status laser_confidence(laser_model* m, const float* d_p, int T, int n, float* d_conf, void* stream) {
+  if (!model_of(m)) return laser_fail(LASER_ERR_STATE, "invalid or destroyed model");
+  if (!d_p || !d_conf || T < 1 || n < 1) return laser_fail(LASER_ERR_INVALID_ARG, "bad argument");
+  hipStream_t s = (hipStream_t)stream;
+  TimingScope scope(m);
+  const hipError_t e = timed(m, LASER_K_OTHER, s, [&] { return launch_confidence(d_p, T, n, d_conf, s); });
+  if (e != hipSuccess) return laser_fail(LASER_ERR_HIP, "confidence: %s", hipGetErrorString(e));
+  return LASER_OK;
+}
+
 // ----------------------------------------------------------------------------- graphs
 
 extern "C" laser_status laser_model_set_graphs(laser_model* m, int enable) {

@@ -58,6 +58,7 @@ _SIGS = {
     "laser_pages_append": (_I, [_P, _I, _I]),
     "laser_pages_truncate": (_I, [_P, _I, _I]),
     "laser_pages_free_seq": (_I, [_P, _I]),
+    "laser_pages_fork": (_I, [_P, _I, _I]),
     "laser_pages_table": (_I, [_P, _I, _I32P, _I, C.POINTER(_I)]),
     "laser_pages_seq_len": (_I, [_P, _I, C.POINTER(_I)]),
     "laser_pages_num_free": (_I, [_P, C.POINTER(_I)]),
@@ -73,6 +74,7 @@ _SIGS = {
     "laser_kv_import": (_I, [_P, _I, _P, _P, _I, _P]),
     "laser_kv_export": (_I, [_P, _I, _P, _P, _P]),
     "laser_kv_free_seq": (_I, [_P, _I]),
+    "laser_kv_fork": (_I, [_P, _I, _I, _P]),
     "laser_kv_seq_len": (_I, [_P, _I, C.POINTER(_I)]),
     "laser_kv_page_table": (_I, [_P, _I, _I32P, _I, C.POINTER(_I)]),
     "laser_kv_destroy": (_I, [_P]),
@@ -80,6 +82,8 @@ _SIGS = {
     "laser_decode_step": (_I, [_P, _P, _I, _I32P, _P, _P, _P, _P, _P]),
     "laser_probe_confidence": (_I, [_P, _P, _I, _I32P, _P, _I, _I, _P, _P, _P, _P]),
     "laser_step_mixed": (_I, [_P, _P, _I, _I32P, _P, _P, _P, _I, _I32P, _P, _I, _I, _P, _P, _P]),
+    "laser_forward": (_I, [_P, _P, _I, _P, _P, _P, _P, _P, _P, _P, _P]),
+    "laser_confidence": (_I, [_P, _P, _I, _I, _P, _P]),
     "laser_timing_enable": (_I, [_P, _I, _I]),
     "laser_timing_read": (_I, [_P, _I, C.POINTER(C.c_double), C.POINTER(_I)]),
     "laser_model_set_graphs": (_I, [_P, _I]),
@@ -179,6 +183,9 @@ class PagePool:
 
     def free_seq(self, seq):
         _call("laser_pages_free_seq", self.h, seq)
+
+    def fork(self, src, dst):
+        _call("laser_pages_fork", self.h, src, dst)
 
     def table(self, seq):
         buf = (C.c_int32 * self.max_pages_per_seq)()
@@ -292,6 +299,10 @@ class KVCache:
     def free_seq(self, seq: int):
         _call("laser_kv_free_seq", self.h, seq)
 
+    def fork(self, src: int, dst: int, stream=None):
+        """dst (a free slot) starts as a copy of src that shares src's full pages."""
+        _call("laser_kv_fork", self.h, src, dst, _stream_ptr(stream))
+
     def seq_len(self, seq: int) -> int:
         n = C.c_int()
         _call("laser_kv_seq_len", self.h, seq, C.byref(n))
@@ -326,6 +337,28 @@ def laser_probe_confidence(model: Model, kv: KVCache, seq_ids: Sequence[int], d_
                            d_logits=None, stream=None):
     _call("laser_probe_confidence", model.h, kv.h, len(seq_ids), _i32arr(seq_ids), d_suffix.data_ptr(), d_suffix.numel(), T,
           d_conf.data_ptr(), d_argmax.data_ptr(), _ptr(d_logits), _stream_ptr(stream))
+
+
+class laser_span(C.Structure):
+    _fields_ = [("seq", C.c_int32), ("n_tokens", C.c_int32), ("tok_sel", C.c_int32), ("tok_off", C.c_int32),
+                ("out", C.c_int32), ("out_sel", C.c_int32), ("out_off", C.c_int32)]
+
+
+def span(seq, n_tokens, tok_sel=0, tok_off=0, out=None):
+    """A laser_span; out = (out_sel, out_off) to emit the last row's token and max-prob."""
+    o = out is not None
+    return laser_span(seq, n_tokens, tok_sel, tok_off, int(o), out[0] if o else 0, out[1] if o else 0)
+
+
+def laser_forward(model: Model, kv: KVCache, spans: Sequence[laser_span], d_tok0, d_tok1=None, d_out_tok0=None,
+                  d_out_p0=None, d_out_tok1=None, d_out_p1=None, stream=None):
+    arr = (laser_span * len(spans))(*spans)
+    _call("laser_forward", model.h, kv.h, len(spans), arr, _ptr(d_tok0), _ptr(d_tok1), _ptr(d_out_tok0),
+          _ptr(d_out_p0), _ptr(d_out_tok1), _ptr(d_out_p1), _stream_ptr(stream))
+
+
+def laser_confidence(model: Model, d_p, T: int, n: int, d_conf, stream=None):
+    _call("laser_confidence", model.h, _ptr(d_p), T, n, _ptr(d_conf), _stream_ptr(stream))
 
 
 def laser_step_mixed(model: Model, kv: KVCache, seq_ids: Sequence[int], d_tokens, d_next, d_max_prob,

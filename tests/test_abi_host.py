@@ -146,11 +146,35 @@ def test_page_pool_matches_oracle_policy(lib):
                     with pytest.raises(L.LaserError) as e:
                         pool.append(seq, k)
                     assert e.value.code == L.ERR_OUT_OF_PAGES
-            elif op < 0.92 and live:
+            elif op < 0.86 and live:
                 seq = rng.choice(live)
                 cut = rng.randint(0, ref.lens[seq])
-                ref.truncate(seq, cut)
-                pool.truncate(seq, cut)
+                try:
+                    ref.truncate(seq, cut)
+                    ok = True
+                except ValueError:  # would end inside a shared page
+                    ok = False
+                if ok:
+                    pool.truncate(seq, cut)
+                else:
+                    with pytest.raises(L.LaserError) as e:
+                        pool.truncate(seq, cut)
+                    assert e.value.code == L.ERR_INVALID_ARG
+            elif op < 0.92 and live and len(live) < 12:
+                src = rng.choice(live)
+                dst = next(s for s in range(16) if s not in live)
+                try:
+                    ref.fork(src, dst)
+                    ok = True
+                except OutOfPages:
+                    ok = False
+                if ok:
+                    pool.fork(src, dst)
+                    live.append(dst)
+                else:
+                    with pytest.raises(L.LaserError) as e:
+                        pool.fork(src, dst)
+                    assert e.value.code == L.ERR_OUT_OF_PAGES
             elif live:
                 seq = live.pop(rng.randrange(len(live)))
                 ref.free_seq(seq)

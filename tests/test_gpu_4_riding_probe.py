@@ -1,0 +1,124 @@
+"""A probe that rides along with decode steps on a fork of the request.
+
+At an ATP each probing request is forked (full pages shared, the partial last page copied);
+the following forwards carry, beside every request's decode row, a few of the fork's suffix
+rows and then its fed-back trial rows (laser_forward spans).  Checked against the oracle:
+
+* every decode row equals plain decoding of the request (the fork's rows never touch it);
+* the confidence and trial tokens equal the oracle's probe of the request's state at the
+  ATP (Section 3.1);
+* page tables (request, fork, and the pool after the fork is freed) equal the oracle page
+  model's, bit for bit.
+"""
+import pytest
+import torch
+
+from gpu_helpers import PROB_TOL, check_token, kv_pair, make_pair, require_gpu
+from oracle.transformer import SeqState, lm_stats
+from paper_2606_31580_amd import laser as L
+from paper_2606_31580_amd import synth
+from paper_2606_31580_amd.configs import QWEN_1P5B, TINY
+
+pytestmark = pytest.mark.gpu
+
+S, T = 8, 4
+
+
+def riding_probe_run(shape, model, orc, kv, opool, states, seqs, probing, forks, per_step, toks, suffix, tag):
+    """Runs decode steps for `seqs` while requests `probing` (forked into `forks`) carry their
+    probe rows, per_step rows per forward; returns (forwards, the next input tokens)."""
+    V = shape.vocab
+    B, P = len(seqs), len(probing)
+    d_tok = torch.tensor(toks, dtype=torch.int32, device="cuda")
+    d_next = torch.zeros(B, dtype=torch.int32, device="cuda")
+    d_p = torch.zeros(B, device="cuda")
+    d_suffix = torch.tensor(suffix, dtype=torch.int32, device="cuda")
+    d_arg = torch.zeros(P * T, dtype=torch.int32, device="cuda")
+    d_pp = torch.zeros(P * T, device="cuda")
+    d_conf = torch.zeros(P, device="cuda")
+    atp = {b: states[b].copy() for b in probing}
+    for b, f in zip(probing, forks):
+        kv.fork(b, f)
+        opool.fork(b, f)
+        assert kv.page_table(f) == opool.tables[f], f"{tag}: fork table"
+    done_s, done_t, n_fwd = 0, 0, 0
+    while done_t < T - 1 or done_s < S:
+        spans = [L.span(b, 1, 0, i, out=(0, i)) for i, b in enumerate(seqs)]
+        if done_s < S:
+            k = min(per_step, S - done_s)
+            last = done_s + k == S
+            for i, f in enumerate(forks):
+                spans.append(L.span(f, k, 1, done_s, out=(1, i * T) if last else None))
+            tok1, done_s = d_suffix, done_s + k
+            adv = k
+        else:
+            done_t += 1
+            for i, f in enumerate(forks):  # trial j = done_t reads t_j, writes t_{j+1}
+                spans.append(L.span(f, 1, 1, i * T + done_t - 1, out=(1, i * T + done_t)))
+            tok1, adv = d_arg, 1
+        L.laser_forward(model, kv, spans, d_tok, tok1, d_next, d_p, d_arg, d_pp)
+        torch.cuda.synchronize()
+        n_fwd += 1
+        for i, b in enumerate(seqs):
+            opool.append(b, 1)
+            ref = orc.decode_token(states[b], int(d_tok[i].item()))
+            check_token(d_next[i].item(), ref, f"{tag}: decode seq {b} forward {n_fwd}")
+            assert abs(d_p[i].item() - lm_stats(ref)[1]) <= PROB_TOL
+            assert kv.page_table(b) == opool.tables[b]
+        for f in forks:
+            opool.append(f, adv)
+            assert kv.page_table(f) == opool.tables[f], f"{tag}: fork table after forward {n_fwd}"
+        d_tok.copy_(d_next)
+    L.laser_confidence(model, d_pp, T, P, d_conf)
+    torch.cuda.synchronize()
+    for i, b in enumerate(probing):
+        res = orc.probe(atp[b], suffix, T)
+        got = [int(x) for x in d_arg[i * T:(i + 1) * T].cpu().numpy()]
+        print(f"{tag}: probe seq {b}: conf gpu {d_conf[i].item():.6g} oracle {res.confidence:.6g}", flush=True)
+        if got == res.tokens:
+            assert abs(d_conf[i].item() - res.confidence) <= PROB_TOL
+        else:  # a trial token may differ only where the oracle's top-2 margin is tiny
+            assert any(m <= 1e-2 for m in res.margins), f"{tag}: trial tokens {got} vs {res.tokens}"
+    for f in forks:
+        kv.free_seq(f)
+        opool.free_seq(f)
+    for b in seqs:
+        assert kv.page_table(b) == opool.tables[b] and kv.seq_len(b) == states[b].length
+    return n_fwd, [int(x) for x in d_tok.cpu().numpy()]
+
+
+def test_riding_probe_tiny():
+    require_gpu()
+    model, orc, _ = make_pair(TINY, max_rows=32, max_positions=1024)
+    kv, opool = kv_pair(model, TINY, num_pages=160, max_seqs=8, max_pages_per_seq=64)
+    lens = [37, 48, 250]  # a partial last page, a page boundary, a longer context
+    states = []
+    for s, n in enumerate(lens):
+        K0, V0 = synth.make_prefill_kv(TINY, n, 30 + s)
+        kv.add_seq(s, n)
+        opool.add_seq(s, n)
+        kv.import_kv(s, K0.cuda(), V0.cuda())
+        states.append(SeqState.from_prefill(TINY, K0.numpy(), V0.numpy(), 1024))
+    toks = [int(t) for t in synth.make_tokens(len(lens), TINY.vocab, 3010)]
+    suffix = [int(t) for t in synth.make_suffix(S, TINY.vocab)]
+    for per_step in (3, 8):
+        n, toks = riding_probe_run(TINY, model, orc, kv, opool, states, [0, 1, 2], [0, 1], [5, 6], per_step,
+                                   toks, suffix, f"tiny per_step={per_step}")
+        assert n == -(-S // per_step) + T - 1
+
+
+def test_riding_probe_1p5b_bf16():
+    require_gpu()
+    shape = QWEN_1P5B
+    model, orc, _ = make_pair(shape, max_rows=16, max_positions=4352, weights_on_device=True, cache_oracle=True)
+    kv, opool = kv_pair(model, shape, num_pages=600, max_seqs=4, max_pages_per_seq=272)
+    n0 = 4093  # partial last page: the fork copies it
+    K0, V0 = synth.make_prefill_kv(shape, n0, 0, device="cuda")
+    kv.add_seq(0, n0)
+    opool.add_seq(0, n0)
+    kv.import_kv(0, K0, V0)
+    states = [SeqState.from_prefill(shape, synth.to_numpy(K0), synth.to_numpy(V0), 4352)]
+    del K0, V0
+    toks = [int(synth.make_tokens(1, shape.vocab, 3011)[0])]
+    suffix = [int(t) for t in synth.make_suffix(S, shape.vocab)]
+    riding_probe_run(shape, model, orc, kv, opool, states, [0], [0], [2], 3, toks, suffix, "1.5B")
