@@ -251,8 +251,8 @@ __global__ __launch_bounds__(64 * kAttnWaves) void k_attn(AttnArgs a) {
         sv[4 + i] = (hasB && tb <= cpos) ? sb[i] * a.scale_log2 : -INFINITY;
         mloc = fmaxf(mloc, fmaxf(sv[i], sv[4 + i]));
       }
-      mloc = fmaxf(mloc, __shfl_xor(mloc, 16));
-      mloc = fmaxf(mloc, __shfl_xor(mloc, 32));
+      mloc = max_x16(mloc);
+      mloc = max_x32(mloc);
       const float m_new = fmaxf(m_run[0], mloc);
       // o and l are still zero while m_run is -inf, so they need no rescale then
       const bool grow = m_run[0] != -INFINITY && m_new != m_run[0];
@@ -263,8 +263,8 @@ __global__ __launch_bounds__(64 * kAttnWaves) void k_attn(AttnArgs a) {
         pv[i] = (sv[i] == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(sv[i] - m_new);
         ls += pv[i];
       }
-      ls += __shfl_xor(ls, 16);
-      ls += __shfl_xor(ls, 32);
+      ls = sum_x16(ls);
+      ls = sum_x32(ls);
       l_run[0] = l_run[0] * alpha + ls;
       m_run[0] = m_new;
       if (__builtin_amdgcn_read_exec() & __ballot(grow)) {  // any lane whose max moved
@@ -353,8 +353,8 @@ __global__ __launch_bounds__(64 * kAttnWaves) void k_attn(AttnArgs a) {
           sv[i] = (tg <= cpos) ? sacc[i] * a.scale_log2 : -INFINITY;
           mloc = fmaxf(mloc, sv[i]);
         }
-        mloc = fmaxf(mloc, __shfl_xor(mloc, 16));
-        mloc = fmaxf(mloc, __shfl_xor(mloc, 32));
+        mloc = max_x16(mloc);
+        mloc = max_x32(mloc);
         const float m_new = fmaxf(m_run[nt], mloc);
         const float alpha = (m_new == -INFINITY) ? 1.f : safe_exp2(m_run[nt] - m_new);
         float pv[4], ls = 0.f;
@@ -363,8 +363,8 @@ __global__ __launch_bounds__(64 * kAttnWaves) void k_attn(AttnArgs a) {
           pv[i] = (sv[i] == -INFINITY) ? 0.f : exp2f(sv[i] - m_new);
           ls += pv[i];
         }
-        ls += __shfl_xor(ls, 16);
-        ls += __shfl_xor(ls, 32);
+        ls = sum_x16(ls);
+        ls = sum_x32(ls);
         l_run[nt] = l_run[nt] * alpha + ls;
         m_run[nt] = m_new;
 #pragma unroll

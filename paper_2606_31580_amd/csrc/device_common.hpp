@@ -45,11 +45,61 @@ __device__ __forceinline__ void split_trunc2(float x0, float x1, uint32_t& hi, u
 __device__ __forceinline__ u32x4 ld_nt16(const void* p) { return __builtin_nontemporal_load((const u32x4*)p); }
 __device__ __forceinline__ u32x2 ld_nt8(const void* p) { return __builtin_nontemporal_load((const u32x2*)p); }
 
-__device__ __forceinline__ float wave_sum(float x) {
-#pragma unroll
-  for (int off = 32; off > 0; off >>= 1) x += __shfl_xor(x, off);
+// Cross-lane primitives of gfx950 (no LDS traffic): DPP inside 16-lane rows, and the
+// permlane swaps across rows.  permlane16_swap(a, b) leaves (a.r0, b.r0, a.r2, b.r2) and
+// (a.r1, b.r1, a.r3, b.r3) (rows of 16 lanes); permlane32_swap(a, b) leaves (a.lo, b.lo) and
+// (a.hi, b.hi).  Summing the two results pairs every lane with its partner 16 or 32 lanes
+// away, in an order that does not depend on the lane.
+template <int CTRL>
+__device__ __forceinline__ float dpp_f(float x) {
+  return __uint_as_float(__builtin_amdgcn_update_dpp(0u, __float_as_uint(x), CTRL, 0xf, 0xf, false));
+}
+constexpr int kDppQuad1032 = 0xB1;    // lane ^ 1
+constexpr int kDppQuad2301 = 0x4E;    // lane ^ 2
+constexpr int kDppHalfMirror = 0x141; // lane i <-> 7 - i within 8 lanes
+constexpr int kDppRowRor8 = 0x128;    // lane ^ 8 within 16 lanes
+
+__device__ __forceinline__ void swap16(float& a, float& b) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(a), __float_as_uint(b), false, false);
+  a = __uint_as_float(r[0]);
+  b = __uint_as_float(r[1]);
+}
+__device__ __forceinline__ void swap32(float& a, float& b) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(a), __float_as_uint(b), false, false);
+  a = __uint_as_float(r[0]);
+  b = __uint_as_float(r[1]);
+}
+// x combined with the value of the lane 16 (32) away: sum or max.
+__device__ __forceinline__ float sum_x16(float x) {
+  float a = x, b = x;
+  swap16(a, b);
+  return a + b;
+}
+__device__ __forceinline__ float sum_x32(float x) {
+  float a = x, b = x;
+  swap32(a, b);
+  return a + b;
+}
+__device__ __forceinline__ float max_x16(float x) {
+  float a = x, b = x;
+  swap16(a, b);
+  return fmaxf(a, b);
+}
+__device__ __forceinline__ float max_x32(float x) {
+  float a = x, b = x;
+  swap32(a, b);
+  return fmaxf(a, b);
+}
+// Sum over the 16 lanes of a row, in every lane of it.
+__device__ __forceinline__ float row_sum16(float x) {
+  x += dpp_f<kDppQuad1032>(x);
+  x += dpp_f<kDppQuad2301>(x);
+  x += dpp_f<kDppHalfMirror>(x);
+  x += dpp_f<kDppRowRor8>(x);
   return x;
 }
+
+__device__ __forceinline__ float wave_sum(float x) { return sum_x32(sum_x16(row_sum16(x))); }
 
 // Value of element e of a stored tensor (fp32 or bf16 bits).
 template <class WT>

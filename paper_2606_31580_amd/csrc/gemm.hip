@@ -90,26 +90,47 @@ __device__ __forceinline__ const char* weight_row(const GemmArgs& a, int g, int 
 
 __device__ __forceinline__ int a_src_row(const GemmArgs& a, int m) { return a.row_map ? a.plan->outs[m].row : m; }
 
-// Sum over the 64 lanes of NV values at once (NV in {8, 16}): each halving stage trades
-// half of the values with the partner lane.  Returns the total of value idx(lane), where
-// idx = sum over stages st of bit (5 - st) of lane times NV >> (st + 1).
+// Sum over the 64 lanes of NV values at once (NV in {4, 8, 16}): each halving stage trades
+// half of the values with the partner lane (32, 16, 8, then 4 lanes away; the last two
+// inside a row, the 4-lane stage pairing lane i with 7 - i of its 8-lane group), then the
+// lanes still holding the same value index are summed.  Returns the total of value
+// idx(lane), where idx = sum over stages st of bit (5 - st) of lane times NV >> (st + 1).
 template <int NV>
 __device__ __forceinline__ float transpose_reduce(float* v, int lane) {
-  int off = 32;
+  static_assert(NV == 4 || NV == 8 || NV == 16, "NV");
 #pragma unroll
-  for (int st = 0; (NV >> st) > 1; ++st) {
-    const int half = (NV >> st) >> 1;
-    const bool up = (lane & off) != 0;
+  for (int i = 0; i < NV / 2; ++i) {  // 32 lanes away: lower lanes keep v[i], upper v[i + NV/2]
+    float x = v[i], y = v[i + NV / 2];
+    swap32(x, y);
+    v[i] = x + y;
+  }
 #pragma unroll
-    for (int i = 0; i < half; ++i) {
-      const float send = up ? v[i] : v[i + half];
-      const float keep = up ? v[i + half] : v[i];
-      v[i] = keep + __shfl_xor(send, off);
+  for (int i = 0; i < NV / 4; ++i) {  // 16 lanes away
+    float x = v[i], y = v[i + NV / 4];
+    swap16(x, y);
+    v[i] = x + y;
+  }
+  if (NV >= 8) {  // 8 lanes away (within the row)
+    const bool up = (lane & 8) != 0;
+#pragma unroll
+    for (int i = 0; i < NV / 8; ++i) {
+      const float send = up ? v[i] : v[i + NV / 8];
+      const float keep = up ? v[i + NV / 8] : v[i];
+      v[i] = keep + dpp_f<kDppRowRor8>(send);
     }
-    off >>= 1;
+  }
+  if (NV >= 16) {  // the other half of the 8-lane group (lane i with 7 - i)
+    const bool up = (lane & 4) != 0;
+    const float send = up ? v[0] : v[1];
+    const float keep = up ? v[1] : v[0];
+    v[0] = keep + dpp_f<kDppHalfMirror>(send);
   }
   float t = v[0];
-  for (; off > 0; off >>= 1) t += __shfl_xor(t, off);
+  // lanes that differ only below the last stage's bit hold the same index: sum them
+  t += dpp_f<kDppQuad1032>(t);
+  t += dpp_f<kDppQuad2301>(t);
+  if (NV <= 8) t += dpp_f<kDppHalfMirror>(t);
+  if (NV <= 4) t += dpp_f<kDppRowRor8>(t);
   return t;
 }
 
@@ -570,8 +591,8 @@ __global__ __launch_bounds__(64 * kMfmaMaxWaves) void k_gemm_mfma(GemmArgs a) {
     for (int i = 0; i < 4; ++i) s_red[w][(16 * mt + 4 * (l >> 4) + i) * RW + n] = acc[mt][i];
     if (norm) {
       float s = own[mt] ? sq[mt] : 0.f;
-      s += __shfl_xor(s, 16);
-      s += __shfl_xor(s, 32);
+      s = sum_x16(s);
+      s = sum_x32(s);
       if (l < 16) s_sq[w][16 * mt + n] = s;
     }
   }
