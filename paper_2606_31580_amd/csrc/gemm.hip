@@ -447,22 +447,32 @@ __global__ __launch_bounds__(kGemvMaxThreads) void k_gemv(GemmArgs a) {
 
 // ----------------------------------------------------------------------------- MFMA GEMM
 
-template <class WT, int MT, int EPI>
+// A workgroup computes NR consecutive 16-row groups; its W waves split K in blocks of four
+// 32-column steps (so a wave reads 256 contiguous bytes of every row it streams).  Each
+// activation fragment is split into bf16 hi/lo once per step and used for all NR groups,
+// which is what keeps the per-step load and VALU work small when M is small.
+template <class WT, int MT, int EPI, int NR>
 __global__ __launch_bounds__(64 * kMfmaMaxWaves) void k_gemm_mfma(GemmArgs a) {
   constexpr int RW = rows_per_group(EPI, true);
   constexpr int NLD = (int)sizeof(WT) / 2;  // 16-byte loads per step (bf16: 1, fp32: 2)
-  constexpr int U = MT == 1 ? 6 : (MT == 2 ? 4 : 2);  // steps kept in flight per wave
-  const int W = blockDim.x >> 6;            // waves splitting K: 4, or 8 for few row groups
-  __shared__ float s_red[kMfmaMaxWaves][16 * MT * RW];
-  __shared__ float s_sq[kMfmaMaxWaves][16 * MT];
-  __shared__ float Y[16 * MT * RW];
+  // steps kept in flight per wave
+  constexpr int U = MT == 1 ? (NR == 1 ? 6 : (NR == 2 ? 4 : 3)) : (MT == 2 ? 4 : 2);
+  constexpr int WMAX = NR == 1 ? kMfmaMaxWaves : 4;  // several groups: always 4 waves
+  constexpr int YN = 16 * MT * RW;                   // outputs of one group
+  const int W = blockDim.x >> 6;                     // waves splitting K
+  __shared__ float s_red[WMAX][NR * YN];
+  __shared__ float s_sq[WMAX][16 * MT];
+  __shared__ float Y[NR * YN];
   __shared__ float s_scale[16 * MT];
   const int tid = threadIdx.x, w = tid >> 6, l = tid & 63;
-  const int g = blockIdx.x;
+  const int g0 = blockIdx.x * NR;
+  const int nlive = min(NR, a.n_groups - g0);  // groups past n_groups read clamped rows, unused
   const int M = a.M;
   const bool norm = a.gain != nullptr;
   const int n = l & 15, kg = 8 * (l >> 4);
-  const char* wp = weight_row<WT, EPI, RW>(a, g, n);
+  const char* wp[NR];
+#pragma unroll
+  for (int r = 0; r < NR; ++r) wp[r] = weight_row<WT, EPI, RW>(a, g0 + (r < nlive ? r : 0), n);
   const float* xr[MT];
   bool own[MT];  // this lane's A row is a real row (rows past M repeat row M-1)
 #pragma unroll
@@ -471,29 +481,34 @@ __global__ __launch_bounds__(64 * kMfmaMaxWaves) void k_gemm_mfma(GemmArgs a) {
     xr[mt] = a.x + (size_t)a_src_row(a, min(16 * mt + n, M - 1)) * a.ldx;
   }
   const int nsteps = (a.K + 31) >> 5;
-  const int niter = nsteps > w ? (nsteps - w + W - 1) / W : 0;  // this wave's steps: s = w + W*it
-  f32x4 acc[MT];
+  const int nblk = (nsteps + 3) >> 2;
+  const int niter = nblk > w ? 4 * ((nblk - w + W - 1) / W) : 0;  // this wave's steps
+  auto step_of = [&](int it) { return 4 * (w + W * (it >> 2)) + (it & 3); };
+  f32x4 acc[NR][MT];
   float sq[MT];
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt) {
-    acc[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
     sq[mt] = 0.f;
+#pragma unroll
+    for (int r = 0; r < NR; ++r) acc[r][mt] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
   // K offset of this lane's 8 elements at iteration it, or -1 past the end of K
   auto kof = [&](int it) {
-    const int k = 32 * (w + W * it) + kg;
+    const int k = 32 * step_of(it) + kg;
     return k < a.K ? k : -1;
   };
   // Every operand of a step (weights, activations, gain) is loaded U steps ahead of its use.
   struct Step {
-    u32x4 wv[NLD];
+    u32x4 wv[NR][NLD];
     u32x4 gv[NLD];
     float4 xv[MT][2];
   };
   auto issue = [&](int it, Step& st) {
     const int k = kof(it), kk = k < 0 ? 0 : k;
 #pragma unroll
-    for (int q = 0; q < NLD; ++q) st.wv[q] = ld_nt16(wp + (size_t)kk * sizeof(WT) + 16 * q);
+    for (int r = 0; r < NR; ++r)
+#pragma unroll
+      for (int q = 0; q < NLD; ++q) st.wv[r][q] = ld_nt16(wp[r] + (size_t)kk * sizeof(WT) + 16 * q);
     if (norm)
 #pragma unroll
       for (int q = 0; q < NLD; ++q) st.gv[q] = *(const u32x4*)((const char*)a.gain + (size_t)kk * sizeof(WT) + 16 * q);
@@ -507,21 +522,24 @@ __global__ __launch_bounds__(64 * kMfmaMaxWaves) void k_gemm_mfma(GemmArgs a) {
   // checked only when `checkc` is true, i.e. in the tail steps).
   auto compute = [&](const Step& cur, int k, auto checkc) {
     constexpr bool check = decltype(checkc)::value;
-    bf16x8 bhi, blo;
-    if (NLD == 1) {
-      bhi = __builtin_bit_cast(bf16x8, cur.wv[0]);
-    } else {
-      u32x4 ph, pl;
+    bf16x8 bhi[NR], blo[NR];
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        uint16_t h0, l0, h1, l1;
-        split_bf16(__uint_as_float(cur.wv[q >> 1][(q & 1) * 2 + 0]), h0, l0);
-        split_bf16(__uint_as_float(cur.wv[q >> 1][(q & 1) * 2 + 1]), h1, l1);
-        ph[q] = (uint32_t)h0 | ((uint32_t)h1 << 16);
-        pl[q] = (uint32_t)l0 | ((uint32_t)l1 << 16);
+    for (int r = 0; r < NR; ++r) {
+      if (NLD == 1) {
+        bhi[r] = __builtin_bit_cast(bf16x8, cur.wv[r][0]);
+      } else {
+        u32x4 ph, pl;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          uint16_t h0, l0, h1, l1;
+          split_bf16(__uint_as_float(cur.wv[r][q >> 1][(q & 1) * 2 + 0]), h0, l0);
+          split_bf16(__uint_as_float(cur.wv[r][q >> 1][(q & 1) * 2 + 1]), h1, l1);
+          ph[q] = (uint32_t)h0 | ((uint32_t)h1 << 16);
+          pl[q] = (uint32_t)l0 | ((uint32_t)l1 << 16);
+        }
+        bhi[r] = __builtin_bit_cast(bf16x8, ph);
+        blo[r] = __builtin_bit_cast(bf16x8, pl);
       }
-      bhi = __builtin_bit_cast(bf16x8, ph);
-      blo = __builtin_bit_cast(bf16x8, pl);
     }
     float gf[8];
     if (norm) {
@@ -552,18 +570,22 @@ __global__ __launch_bounds__(64 * kMfmaMaxWaves) void k_gemm_mfma(GemmArgs a) {
         pl[q] = lo;
       }
       const bf16x8 ahi = __builtin_bit_cast(bf16x8, ph), alo = __builtin_bit_cast(bf16x8, pl);
-      acc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ahi, bhi, acc[mt], 0, 0, 0);
-      acc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(alo, bhi, acc[mt], 0, 0, 0);
-      if (NLD == 2) acc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ahi, blo, acc[mt], 0, 0, 0);
+#pragma unroll
+      for (int r = 0; r < NR; ++r) {
+        acc[r][mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ahi, bhi[r], acc[r][mt], 0, 0, 0);
+        acc[r][mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(alo, bhi[r], acc[r][mt], 0, 0, 0);
+        if (NLD == 2) acc[r][mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ahi, blo[r], acc[r][mt], 0, 0, 0);
+      }
     }
   };
   Step buf[U];
 #pragma unroll
   for (int u = 0; u < U; ++u)
     if (u < niter) issue(u, buf[u]);
-  // Steps whose 32 columns all lie inside K need no end check; with K a multiple of 32 (all
-  // model shapes) that is every step.
-  const int nfull = (a.K >> 5) > w ? ((a.K >> 5) - w + W - 1) / W : 0;
+  // Steps whose 32 columns all lie inside K need no end check; they come first.  With K a
+  // multiple of 128 (all model shapes but the tiny one) that is every step.
+  int nfull = niter;
+  while (nfull > 0 && step_of(nfull - 1) >= (a.K >> 5)) --nfull;
   using Check = std::integral_constant<bool, true>;
   using NoCheck = std::integral_constant<bool, false>;
   int it0 = 0;
@@ -575,7 +597,7 @@ __global__ __launch_bounds__(64 * kMfmaMaxWaves) void k_gemm_mfma(GemmArgs a) {
       if (it0 + u + U < niter) issue(it0 + u + U, buf[u]);
     }
   }
-  // remaining steps (fewer than U whole steps, then a partial one): operands already issued
+  // remaining steps (fewer than U whole steps, then partial ones): operands already issued
   for (; it0 < niter; it0 += U) {
 #pragma unroll
     for (int u = 0; u < U; ++u)
@@ -584,11 +606,13 @@ __global__ __launch_bounds__(64 * kMfmaMaxWaves) void k_gemm_mfma(GemmArgs a) {
         if (it0 + u + U < niter) issue(it0 + u + U, buf[u]);
       }
   }
-  // lane (n, l/16): acc[mt][i] = Y[m = 16mt + 4(l/16) + i][n]; sq over the lanes of row n
+  // lane (n, l/16): acc[r][mt][i] = Y_r[m = 16mt + 4(l/16) + i][n]; sq over the lanes of row n
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) s_red[w][(16 * mt + 4 * (l >> 4) + i) * RW + n] = acc[mt][i];
+    for (int r = 0; r < NR; ++r)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) s_red[w][r * YN + (16 * mt + 4 * (l >> 4) + i) * RW + n] = acc[r][mt][i];
     if (norm) {
       float s = own[mt] ? sq[mt] : 0.f;
       s = sum_x16(s);
@@ -603,16 +627,29 @@ __global__ __launch_bounds__(64 * kMfmaMaxWaves) void k_gemm_mfma(GemmArgs a) {
     s_scale[tid] = rsqrtf(s / (float)a.K + a.eps);
   }
   __syncthreads();
-  for (int idx = tid; idx < M * RW; idx += blockDim.x) {
+  for (int idx = tid; idx < NR * YN; idx += blockDim.x) {
+    const int j = idx % YN;
+    if (j >= M * RW) continue;
     float v = 0.f;
     for (int q = 0; q < W; ++q) v += s_red[q][idx];
-    Y[idx] = norm ? v * s_scale[idx / RW] : v;
+    Y[idx] = norm ? v * s_scale[j / RW] : v;
   }
   __syncthreads();
-  run_epilogue<WT, EPI, RW>(a, g, M, Y);
+  for (int r = 0; r < nlive; ++r) run_epilogue<WT, EPI, RW>(a, g0 + r, M, Y + r * YN);
 }
 
 // ----------------------------------------------------------------------------- launch
+
+template <class WT, int MT, int NR>
+static hipError_t launch_mfma(int epi, dim3 grid, dim3 block, const GemmArgs& a, hipStream_t s) {
+  switch (epi) {
+    case EPI_QKV: return launch_k(k_gemm_mfma<WT, MT, EPI_QKV, NR>, grid, block, s, a);
+    case EPI_RESID: return launch_k(k_gemm_mfma<WT, MT, EPI_RESID, NR>, grid, block, s, a);
+    case EPI_SWIGLU: return launch_k(k_gemm_mfma<WT, MT, EPI_SWIGLU, NR>, grid, block, s, a);
+    case EPI_LMHEAD: return launch_k(k_gemm_mfma<WT, MT, EPI_LMHEAD, NR>, grid, block, s, a);
+    default: return hipErrorInvalidValue;
+  }
+}
 
 template <class WT, int MODE>
 static hipError_t launch_epi(int epi, int rw, const GemmArgs& a, hipStream_t s) {
@@ -630,16 +667,18 @@ static hipError_t launch_epi(int epi, int rw, const GemmArgs& a, hipStream_t s) 
     if (epi == EPI_LMHEAD && rw == 8) return launch_k(k_gemv<WT, MODE, EPI_LMHEAD, 8>, grid, block, s, a);
     return hipErrorInvalidValue;
   } else {
+    constexpr int MT = MODE - 4;
     if (rw != rows_per_group(epi, true)) return hipErrorInvalidValue;
+    const int nr = a.nr < 1 ? 1 : a.nr;
+    if (nr != 1 && (MT > 1 || (nr != 2 && nr != 4))) return hipErrorInvalidValue;
+    const dim3 mgrid((a.n_groups + nr - 1) / nr);
     // few row groups (the O, down and QKV projections): 8 waves split K more finely
-    if (a.n_groups < 512) block = dim3(64 * kMfmaMaxWaves);
-    switch (epi) {
-      case EPI_QKV: return launch_k(k_gemm_mfma<WT, MODE - 4, EPI_QKV>, grid, block, s, a);
-      case EPI_RESID: return launch_k(k_gemm_mfma<WT, MODE - 4, EPI_RESID>, grid, block, s, a);
-      case EPI_SWIGLU: return launch_k(k_gemm_mfma<WT, MODE - 4, EPI_SWIGLU>, grid, block, s, a);
-      case EPI_LMHEAD: return launch_k(k_gemm_mfma<WT, MODE - 4, EPI_LMHEAD>, grid, block, s, a);
-      default: return hipErrorInvalidValue;
+    if (nr == 1 && a.n_groups < 512) block = dim3(64 * kMfmaMaxWaves);
+    if constexpr (MT == 1) {
+      if (nr == 2) return launch_mfma<WT, MT, 2>(epi, mgrid, block, a, s);
+      if (nr == 4) return launch_mfma<WT, MT, 4>(epi, mgrid, block, a, s);
     }
+    return launch_mfma<WT, MT, 1>(epi, mgrid, block, a, s);
   }
 }
 

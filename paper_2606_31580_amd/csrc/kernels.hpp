@@ -72,6 +72,7 @@ struct GemmArgs {
   const void* w1;
   const void* w2;
   int K, N, M, n_groups;
+  int nr;  // MFMA path: row groups per workgroup (1; 2 or 4 with one 16-row activation tile)
   // A operand: fp32 activation rows [row][ldx]; optional RMSNorm over the full row (gain)
   const float* x;
   int ldx;

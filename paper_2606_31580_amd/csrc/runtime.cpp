@@ -196,6 +196,16 @@ static int proj_rw(int epi, int rows, int M, int cus) {
 
 static int groups_lm(const laser_model_desc& d, int M) { return ceil_div(d.vocab, M > 4 ? 16 : 8); }
 
+// Row groups per MFMA workgroup: several (so each activation fragment serves several row
+// groups) when there are still at least two workgroups per compute unit; one for the
+// narrow projections and for more than one 16-row activation tile.
+static int mfma_nr(int n_groups, int M, int cus) {
+  if (M <= 4 || M > 16) return 1;
+  if (n_groups / 4 >= 2 * cus) return 4;
+  if (n_groups / 2 >= 2 * cus) return 2;
+  return 1;
+}
+
 static Layout make_layout(const laser_model_desc& d, int max_rows) {
   Layout L{};
   const int hd = d.head_dim, G = d.n_q_heads / d.n_kv_heads;
@@ -685,6 +695,7 @@ static laser_status launch_forward(laser_model* m, laser_kv* kv, const FwdKey& k
     a.K = K;
     a.N = N;
     a.n_groups = proj_groups(epi, rows, rw);
+    a.nr = mfma_nr(a.n_groups, M, m->cus);
     a.M = M;
     const int mode = gemm_mode(M);
     HIP_TRY(timed(m, cls, s, [&] { return launch_gemm(dt, mode, epi, rw, a, s); }));
@@ -769,6 +780,7 @@ static laser_status launch_forward(laser_model* m, laser_kv* kv, const FwdKey& k
     a.K = d.d_model;
     a.N = d.vocab;
     a.n_groups = groups_lm(d, key.n_out);
+    a.nr = mfma_nr(a.n_groups, key.n_out, m->cus);
     a.M = key.n_out;
     HIP_TRY(timed(m, LASER_K_LMHEAD, s, [&] {
       hipError_t e = launch_gemm(dt, gemm_mode(key.n_out), EPI_LMHEAD, key.n_out > 4 ? 16 : 8, a, s);
