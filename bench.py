@@ -27,6 +27,7 @@ import time
 
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, published
 PAGE = 16
+COST_CTX = 2048  # the shorter context of the cost-model pass
 
 
 def parse():
@@ -88,6 +89,7 @@ def main():
     model = L.Model(shape, weights, max_rows=max(B + B * R, B * S), max_positions=max_pos)
     pps = max_pos // PAGE + 1
     num_pages = sum((n + 2 * total_steps + S + T) // PAGE + 2 for n in lens) + B * ((S + T) // PAGE + 3) + 8
+    num_pages += (COST_CTX + 512) // PAGE + 4  # the cost-model pass (a shorter request in a fork slot)
     kv = L.KVCache(model, num_pages, 2 * B, pps)  # slots B..2B-1 hold the probes' forks
     for i, n in enumerate(lens):
         k0, v0 = synth.make_prefill_kv(shape, n, i, device=dev)
@@ -207,6 +209,7 @@ def main():
 
     # ---- decode only (same cache, no probes)
     n_dec = min(args.steps, 128)
+    ctx_dec = kv.seq_len(0) + n_dec / 2.0
     torch.cuda.synchronize()
     e0.record(stream)
     for i in range(n_dec):
@@ -234,6 +237,11 @@ def main():
         model.timing_enable(c, False)
     gu_avg_ms = kernel_us["gate_up"]["avg_us"] / 1e3
     gu_n = kernel_us["gate_up"]["launches"]
+
+    # ---- cost model of the serving simulation (one-request workloads)
+    sim_costs = None
+    if B == 1:
+        sim_costs = cost_model(L, synth, model, kv, shape, dev, forks[0], dec_ms, ctx_dec, suffix, T, log)
 
     # ---- algorithmic bytes
     es = 2 if shape.dtype == "bf16" else 4
@@ -284,10 +292,86 @@ def main():
                      "frac": round(gu_gbs / HBM_PEAK_GBS, 4), "traffic": traffic,
                      "avg_launch_us": round(gu_avg_ms * 1e3, 2), "launches": gu_n, "bytes_per_launch": gu_bytes},
         "kernel_us_per_launch": kernel_us,
+        "sim_costs": sim_costs,
     }
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(shape, weights, kv, lens, model, dev, log)
     print(json.dumps(out), flush=True)
+
+
+def cost_model(L, synth, model, kv, shape, dev, slot, dec_long_ms, ctx_long, suffix, T, log):
+    """Per-token decode, probe and prefill times of this engine, each fitted as a + b * x from
+    two measured points: decode steps and probes at the workload's context and at COST_CTX,
+    prompt prefills of 64 and 256 tokens.  These drive the serving simulation (Eq. 2)."""
+    import torch
+
+    stream = torch.cuda.current_stream()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+
+    def timed(fn, reps):
+        torch.cuda.synchronize()
+        ev[0].record(stream)
+        for _ in range(reps):
+            fn()
+        ev[1].record(stream)
+        torch.cuda.synchronize()
+        return ev[0].elapsed_time(ev[1]) / reps
+
+    log(f"cost model: decode and probe at context {COST_CTX}")
+    k0, v0 = synth.make_prefill_kv(shape, COST_CTX, 9, device=dev)
+    kv.add_seq(slot, COST_CTX)
+    kv.import_kv(slot, k0, v0)
+    del k0, v0
+    tok = synth.make_tokens(1, shape.vocab, 3005).to(dev)
+    nxt = torch.empty(1, dtype=torch.int32, device=dev)
+    pm = torch.empty(1, device=dev)
+    conf = torch.empty(1, device=dev)
+    argm = torch.empty(T, dtype=torch.int32, device=dev)
+
+    def dec():
+        L.laser_decode_step(model, kv, [slot], tok, nxt, pm)
+        tok.copy_(nxt)
+
+    timed(dec, 4)
+    n = 32
+    ctx_short = kv.seq_len(slot) + n / 2.0
+    dec_short_ms = timed(dec, n)
+    probe_short_ms = timed(lambda: L.laser_probe_confidence(model, kv, [slot], suffix, T, conf, argm), 3)
+    ctx_probe_long = kv.seq_len(0)
+    probe_long_ms = timed(lambda: L.laser_probe_confidence(model, kv, [0], suffix, T, conf, argm), 3)
+    kv.free_seq(slot)
+    log("cost model: prompt prefill of 64 and 256 tokens")
+    pre = {}
+    for n_p in (64, 256):
+        ptok = synth.make_tokens(n_p, shape.vocab, 3006).to(dev)
+
+        def run():
+            kv.add_seq(slot, 0)
+            L.laser_prefill(model, kv, slot, ptok)
+            torch.cuda.synchronize()
+            kv.free_seq(slot)
+
+        run()
+        t0 = time.perf_counter()
+        for _ in range(2):
+            run()
+        pre[n_p] = (time.perf_counter() - t0) * 1e3 / 2
+
+    def fit(x0, y0, x1, y1):
+        b = (y1 - y0) / (x1 - x0)
+        return y0 - b * x0, b
+
+    dec_a, dec_b = fit(ctx_short, dec_short_ms, ctx_long, dec_long_ms)
+    pr_a, pr_b = fit(COST_CTX, probe_short_ms, ctx_probe_long, probe_long_ms)
+    pf_a, pf_b = fit(64, pre[64], 256, pre[256])
+    return {"decode_ms": round(dec_a, 5), "decode_ms_per_ctx": round(dec_b, 9),
+            "probe_ms": round(pr_a, 4), "probe_ms_per_ctx": round(pr_b, 8),
+            "prefill_ms": round(max(pf_a, 0.0), 3), "prefill_ms_per_token": round(pf_b, 5),
+            "points": {"decode_ms": [[round(ctx_short, 1), round(dec_short_ms, 4)], [round(ctx_long, 1), round(dec_long_ms, 4)]],
+                       "probe_ms": [[COST_CTX, round(probe_short_ms, 3)], [ctx_probe_long, round(probe_long_ms, 3)]],
+                       "prefill_ms": [[64, round(pre[64], 3)], [256, round(pre[256], 3)]]},
+            "meaning": "ms per decoded token = decode_ms + decode_ms_per_ctx * context; per probe (separate forwards) = "
+                       "probe_ms + probe_ms_per_ctx * context; per prompt = prefill_ms + prefill_ms_per_token * tokens"}
 
 
 def cpu_baseline(shape, weights, kv, lens, model, dev, log):

@@ -16,6 +16,8 @@
  *                            the pieces of a probe that rides along with later decode steps
  *   laser_exit_decision      the host-side ATP decision (Eq. 5 threshold, Algorithm 1)
  *   laser_budget             the budget pre-allocation of Eq. 6-8
+ *   laser_simulate           the paper's serving evaluation: one FIFO server, Poisson or
+ *                            phased arrivals, per-request inference time from Eq. 2
  *
  * Conventions for every function:
  *   - The return value is a laser_status; LASER_OK (0) on success, a negative code on
@@ -111,6 +113,91 @@ laser_status laser_budget(const laser_params* p, int prompt_len, int active_requ
 laser_status laser_exit_decision(const laser_params* p, laser_load_state* state, float confidence,
                                  int active_requests, int k_done, int B_i, int* decision_out,
                                  double* lambda_out);
+
+/* ========================================================================== */
+/* Serving simulation (Section 5.1 evaluation setup)                          */
+/* ========================================================================== */
+/* Discrete-event simulation of one server that takes requests first come, first served,
+ * as the paper evaluates serving.  Request i's latency is its queueing delay plus its
+ * inference time (Eq. 1), and the inference time follows Eq. 2 from the request's
+ * reasoning trace and a cost model:
+ *   prefill(p) = prefill_ms + prefill_ms_per_token * p
+ *   decoding n tokens from context c = n * decode_ms + decode_ms_per_ctx * (n*c + n(n-1)/2)
+ *   a probe (trial answer + confidence) at context c = probe_ms + probe_ms_per_ctx * c.
+ * A trace has K_i >= 1 reasoning chunks; an ATP follows every chunk but the last, whose end
+ * closes the thinking phase.  At each ATP the methods that probe pay one probe and decide
+ * as Algorithm 1 does (laser_exit_decision; the fixed-threshold methods compare with
+ * fixed_lambda instead of Eq. 5).  The load L(t) is the number of requests in the system,
+ * waiting or in service, at time t (arrivals at exactly t included): it feeds the EMA at
+ * every probe (one global L_bar, starting at 0) and Eq. 8 at the start of service.  Probe
+ * tokens do not stay in the context.  After the thinking phase the conclusion's tokens are
+ * decoded from the context reached.
+ * Methods (Section 5.1 baselines and the Section 5.4 ablation):
+ *   VANILLA         no probes: every chunk, then the conclusion
+ *   FIXED           probe at every ATP, exit when confidence > fixed_lambda
+ *   LASER           Eq. 5 threshold and Eq. 6-8 budget
+ *   THRESHOLD_ONLY  Eq. 5 threshold, no budget
+ *   BUDGET_ONLY     fixed_lambda and the Eq. 6-8 budget
+ *   NOTHINKING      no reasoning chunks: prefill, then the conclusion
+ * max_probes (> 0) caps the probes of the methods without a budget (a step limit);
+ * max_think_tokens (> 0) ends thinking once that many reasoning tokens are generated (the
+ * chunk in progress is cut there, no probe follows, the conclusion is forced). */
+enum {
+  LASER_SIM_VANILLA = 0, LASER_SIM_FIXED = 1, LASER_SIM_LASER = 2,
+  LASER_SIM_THRESHOLD_ONLY = 3, LASER_SIM_BUDGET_ONLY = 4, LASER_SIM_NOTHINKING = 5
+};
+/* outcome of a request */
+enum {
+  LASER_SIM_FINISHED = 0,   /* the last chunk ended the thinking phase */
+  LASER_SIM_EXITED = 1,     /* confidence above the threshold at an ATP */
+  LASER_SIM_EXHAUSTED = 2,  /* budget or probe cap reached: conclusion forced */
+  LASER_SIM_CAPPED = 3,     /* max_think_tokens reached: conclusion forced */
+  LASER_SIM_SKIPPED = 4     /* NOTHINKING */
+};
+typedef struct {
+  int method;
+  double fixed_lambda;
+  int max_probes, max_think_tokens;
+  double prefill_ms, prefill_ms_per_token;
+  double decode_ms, decode_ms_per_ctx;
+  double probe_ms, probe_ms_per_ctx;
+  double slo_s; /* latency deadline of the SLO rate */
+} laser_sim_config;
+typedef struct {
+  double arrival_s; /* non-decreasing over the requests */
+  int32_t prompt_len, n_chunks, conclusion_tokens;
+  int32_t nothink_correct; /* correctness of the answer without reasoning (NOTHINKING) */
+} laser_sim_request;
+typedef struct {
+  double start_s, finish_s, latency_s;
+  double lambda_last; /* threshold at the last probe; NaN without probes */
+  int32_t budget;     /* B_i of the budgeted methods, else 0 */
+  int32_t chunks;     /* reasoning chunks generated (a cut chunk counts) */
+  int32_t probes, think_tokens, outcome, correct;
+} laser_sim_result;
+typedef struct {
+  int32_t n;
+  double mean_latency_s;
+  double p95_latency_s;   /* nearest rank: the ceil(0.95 n)-th smallest latency */
+  double throughput_qps;  /* n / (last finish - first arrival) */
+  double slo_rate;        /* fraction with latency <= slo_s */
+  double accuracy;        /* fraction answered correctly */
+  double mean_tokens;     /* reasoning + conclusion tokens per request */
+  double early_exit_rate; /* fraction with outcome EXITED */
+} laser_sim_summary;
+/* Simulates n requests.  The per-chunk arrays hold sum(n_chunks) entries, request after
+ * request: chunk_tokens[c] >= 1; confidence[c] of the trial answer at the ATP after chunk
+ * c (not read for a request's last chunk); correct[c] nonzero if the answer given after
+ * chunk c is right (for the last chunk: the answer after full reasoning).  A request that
+ * stops after chunk c is scored with correct[c].  out (n entries) and summary may be NULL.
+ * Host only, O(total chunks + n log n).  Errors: INVALID_ARG for NULL required arrays,
+ * n < 0, an unknown method, negative costs, decreasing arrivals, n_chunks < 1 (except
+ * for NOTHINKING, which reads no chunks), chunk_tokens < 1, prompt_len or
+ * conclusion_tokens < 0, NaN confidence, or invalid params (as laser_budget /
+ * laser_threshold). */
+laser_status laser_simulate(const laser_params* p, const laser_sim_config* cfg, int n, const laser_sim_request* req,
+                            const int32_t* chunk_tokens, const float* confidence, const uint8_t* correct,
+                            laser_sim_result* out, laser_sim_summary* summary);
 
 /* ========================================================================== */
 /* Page pool: host bookkeeping of the paged KV cache.                          */

@@ -22,13 +22,13 @@ LIB = os.path.join(LIBDIR, "liblaser.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 HIP_SOURCES = ["gemm.hip", "attn.hip", "misc.hip", "runtime.cpp", "pages.cpp"]
-C_SOURCES = ["controller.c"]
+C_SOURCES = ["controller.c", "sim.c"]
 HIP_FLAGS = [
     f"--offload-arch={ARCH}", "-O3", "-fPIC", "-std=c++17", "-Wall", "-Wno-unused-result",
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     f"-I{INCLUDE}", f"-I{CSRC}",
 ]
-C_FLAGS = ["-O2", "-fPIC", "-std=c99", "-Wall", f"-I{INCLUDE}", f"-I{CSRC}"]
+C_FLAGS = ["-O2", "-fPIC", "-std=c99", "-Wall", "-ffp-contract=off", f"-I{INCLUDE}", f"-I{CSRC}"]
 
 
 def _run(cmd):

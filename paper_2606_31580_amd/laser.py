@@ -41,6 +41,32 @@ class laser_model_desc(C.Structure):
         ("rope_theta", C.c_float), ("rms_eps", C.c_float), ("max_positions", C.c_int)]
 
 
+class laser_sim_config(C.Structure):
+    _fields_ = [("method", C.c_int), ("fixed_lambda", C.c_double), ("max_probes", C.c_int),
+                ("max_think_tokens", C.c_int)] + [(n, C.c_double) for n in (
+                    "prefill_ms", "prefill_ms_per_token", "decode_ms", "decode_ms_per_ctx", "probe_ms",
+                    "probe_ms_per_ctx", "slo_s")]
+
+
+class laser_sim_request(C.Structure):
+    _fields_ = [("arrival_s", C.c_double), ("prompt_len", C.c_int32), ("n_chunks", C.c_int32),
+                ("conclusion_tokens", C.c_int32), ("nothink_correct", C.c_int32)]
+
+
+class laser_sim_result(C.Structure):
+    _fields_ = [(n, C.c_double) for n in ("start_s", "finish_s", "latency_s", "lambda_last")] + [
+        (n, C.c_int32) for n in ("budget", "chunks", "probes", "think_tokens", "outcome", "correct")]
+
+
+class laser_sim_summary(C.Structure):
+    _fields_ = [("n", C.c_int32)] + [(n, C.c_double) for n in (
+        "mean_latency_s", "p95_latency_s", "throughput_qps", "slo_rate", "accuracy", "mean_tokens",
+        "early_exit_rate")]
+
+
+SIM_VANILLA, SIM_FIXED, SIM_LASER, SIM_THRESHOLD_ONLY, SIM_BUDGET_ONLY, SIM_NOTHINKING = range(6)
+SIM_FINISHED, SIM_EXITED, SIM_EXHAUSTED, SIM_CAPPED, SIM_SKIPPED = range(5)
+
 _P = C.c_void_p
 _I = C.c_int
 _I32P = C.POINTER(C.c_int32)
@@ -87,6 +113,8 @@ _SIGS = {
     "laser_timing_enable": (_I, [_P, _I, _I]),
     "laser_timing_read": (_I, [_P, _I, C.POINTER(C.c_double), C.POINTER(_I)]),
     "laser_model_set_graphs": (_I, [_P, _I]),
+    "laser_simulate": (_I, [C.POINTER(laser_params), C.POINTER(laser_sim_config), _I, C.POINTER(laser_sim_request),
+                            _P, _P, _P, C.POINTER(laser_sim_result), C.POINTER(laser_sim_summary)]),
 }
 
 _lib = None
@@ -367,3 +395,37 @@ def laser_step_mixed(model: Model, kv: KVCache, seq_ids: Sequence[int], d_tokens
     _call("laser_step_mixed", model.h, kv.h, len(seq_ids), _i32arr(seq_ids), d_tokens.data_ptr(), d_next.data_ptr(),
           d_max_prob.data_ptr(), n, _i32arr(probe_idx) if n else None, _ptr(d_suffix) if n else None,
           d_suffix.numel() if n else 0, T, _ptr(d_conf) if n else None, _ptr(d_argmax) if n else None, _stream_ptr(stream))
+
+
+# --------------------------------------------------------------------------- serving simulation
+
+def sim_config(method: int, costs: dict, fixed_lambda: float = 0.95, max_probes: int = 0, max_think_tokens: int = 0,
+               slo_s: float = 30.0) -> laser_sim_config:
+    """A laser_sim_config; costs holds the six cost-model fields (milliseconds)."""
+    cfg = laser_sim_config(method=method, fixed_lambda=fixed_lambda, max_probes=max_probes,
+                           max_think_tokens=max_think_tokens, slo_s=slo_s)
+    for k in ("prefill_ms", "prefill_ms_per_token", "decode_ms", "decode_ms_per_ctx", "probe_ms", "probe_ms_per_ctx"):
+        setattr(cfg, k, float(costs.get(k, 0.0)))
+    return cfg
+
+
+def laser_simulate(params: laser_params, cfg: laser_sim_config, arrivals, traces: dict):
+    """Runs laser_simulate on arrival times (s) and traces (the arrays of synth.make_sim_traces).
+
+    Returns (results: list of laser_sim_result, summary: laser_sim_summary).
+    """
+    import numpy as np
+
+    n = len(arrivals)
+    reqs = (laser_sim_request * max(n, 1))()
+    for i in range(n):
+        reqs[i] = laser_sim_request(float(arrivals[i]), int(traces["prompt_len"][i]), int(traces["n_chunks"][i]),
+                                    int(traces["conclusion_tokens"][i]), int(traces["nothink_correct"][i]))
+    tok = np.ascontiguousarray(traces["chunk_tokens"], dtype=np.int32)
+    conf = np.ascontiguousarray(traces["confidence"], dtype=np.float32)
+    corr = np.ascontiguousarray(traces["correct"], dtype=np.uint8)
+    out = (laser_sim_result * max(n, 1))()
+    summ = laser_sim_summary()
+    _call("laser_simulate", C.byref(params), C.byref(cfg), n, reqs, tok.ctypes.data if tok.size else None,
+          conf.ctypes.data if conf.size else None, corr.ctypes.data if corr.size else None, out, C.byref(summ))
+    return [out[i] for i in range(n)], summ

@@ -9,12 +9,29 @@ Pre-filled KV entries ~N(0, 1) stand for an already-generated chain of thought
 
 Seeds: weights 1000 + tensor index (fixed name order), pre-filled KV 2000 +
 request index, prompt/first tokens/suffix 3000.., ragged lengths and the
-mixed-step schedule 4000.
+mixed-step schedule 4000, serving-simulation traces 6000 and arrivals 7000.
+
+Serving-simulation traces (the paper's per-sample profiles of trained models are not
+available, so these stand in for them; shapes from the paper):
+  * prompt length uniform in [50, 275] tokens (the p_min..p_max range of Section 4.3);
+  * reasoning length uniform in [3000, 14000] tokens (the CoT lengths of Section 1), cut
+    into chunks of lognormal length (median 900 tokens) at ATPs;
+  * the trial answer settles early, as reasoning models overthink (Section 3.1): at chunk
+    g - 1 with g geometric (p = 0.45), at most the last chunk; from there on it is the final
+    answer (right with probability 0.85), before it right with probability 0.35;
+  * confidences are polarised (Section 4.2's rationale for tanh): after settling, 85%
+    are drawn from [0.95, 1) and the rest from [0.5, 0.95); before settling, 10% from
+    [0.9, 1) and the rest from [0.2, 0.9);
+  * conclusion length uniform in [100, 400] tokens; the answer without reasoning is
+    right with probability 0.35.
+Arrivals: exponential gaps at the given rate (Poisson), or phases of given rates and
+durations (the 1 -> 5 -> 1 QPS burst of Section 5.1).
 """
 from __future__ import annotations
 
 from typing import Dict, List, Sequence
 
+import numpy as np
 import torch
 
 from .configs import ModelShape
@@ -123,3 +140,65 @@ def to_numpy(t: torch.Tensor):
     if t.dtype == torch.bfloat16:
         return bf16_bits(t)
     return t.detach().cpu().numpy()
+
+
+def make_sim_traces(n: int, seed: int = 6000) -> Dict[str, np.ndarray]:
+    """n synthetic reasoning traces: per-request and concatenated per-chunk arrays."""
+    rng = np.random.default_rng(seed)
+    prompt = rng.integers(50, 276, size=n)
+    concl = rng.integers(100, 401, size=n)
+    nothink = rng.random(n) < 0.35
+    n_chunks, tokens, conf, correct = [], [], [], []
+    for _ in range(n):
+        total = int(rng.integers(3000, 14001))
+        lens = []
+        while sum(lens) < total:
+            lens.append(max(1, int(round(rng.lognormal(np.log(900.0), 0.6)))))
+        lens[-1] -= sum(lens) - total
+        if lens[-1] < 1:
+            lens.pop()
+            lens[-1] += total - sum(lens)
+        K = len(lens)
+        settle = min(K - 1, int(rng.geometric(0.45)) - 1)
+        final = rng.random() < 0.85
+        for c in range(K):
+            if c >= settle:
+                ok = final
+                cf = rng.uniform(0.95, 1.0) if rng.random() < 0.85 else rng.uniform(0.5, 0.95)
+            else:
+                ok = rng.random() < 0.35
+                cf = rng.uniform(0.9, 1.0) if rng.random() < 0.10 else rng.uniform(0.2, 0.9)
+            conf.append(cf)
+            correct.append(ok)
+        n_chunks.append(K)
+        tokens += lens
+    return {
+        "prompt_len": prompt.astype(np.int32),
+        "n_chunks": np.asarray(n_chunks, dtype=np.int32),
+        "conclusion_tokens": concl.astype(np.int32),
+        "nothink_correct": nothink.astype(np.int32),
+        "chunk_tokens": np.asarray(tokens, dtype=np.int32),
+        "confidence": np.asarray(conf, dtype=np.float32),
+        "correct": np.asarray(correct, dtype=np.uint8),
+    }
+
+
+def make_poisson_arrivals(n: int, qps: float, seed: int = 7000) -> np.ndarray:
+    """Arrival times (s) of n requests with exponential gaps of mean 1/qps, from t = 0."""
+    rng = np.random.default_rng(seed)
+    return np.cumsum(rng.exponential(1.0 / qps, size=n))
+
+
+def make_phased_arrivals(rates: Sequence[float], durations_s: Sequence[float], seed: int = 7001) -> np.ndarray:
+    """Poisson arrivals whose rate is rates[k] during the k-th phase of durations_s[k] seconds."""
+    rng = np.random.default_rng(seed)
+    out, t0 = [], 0.0
+    for rate, dur in zip(rates, durations_s):
+        t = t0
+        while True:
+            t += rng.exponential(1.0 / rate)
+            if t >= t0 + dur:
+                break
+            out.append(t)
+        t0 += dur
+    return np.asarray(out, dtype=np.float64)
