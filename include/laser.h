@@ -16,6 +16,7 @@
  *                            the pieces of a probe that rides along with later decode steps
  *   laser_exit_decision      the host-side ATP decision (Eq. 5 threshold, Algorithm 1)
  *   laser_budget             the budget pre-allocation of Eq. 6-8
+ *   laser_atp_match          device-side ATP detection (token-set membership)
  *   laser_simulate           the paper's serving evaluation: one FIFO server, Poisson or
  *                            phased arrivals, per-request inference time from Eq. 2
  *
@@ -365,6 +366,26 @@ laser_status laser_forward(laser_model* m, laser_kv* kv, int n_spans, const lase
 /* d_conf[i] = (d_p[i*T] + ... + d_p[i*T + T-1]) / T for i < n: the confidence of
  * Section 3.1 from the trial tokens' max-softmax probabilities. */
 laser_status laser_confidence(laser_model* m, const float* d_p, int T, int n, float* d_conf, void* stream);
+
+/* ========================================================================== */
+/* ATP detection and the forced conclusion                                     */
+/* ========================================================================== */
+/* Section 3.1 marks ATPs by linguistic cues between reasoning chunks (such as "Wait" or
+ * "Alternatively").  Given the cue tokens as a set of token ids, detection is a
+ * membership test of each freshly generated token, done on the device so that the decode
+ * loop needs no copy to the host: d_flags[i] = 1 if d_tokens[i] is in the set, else 0
+ * (ids outside [0, vocab) are never members).  The set is a bitmap of (vocab + 31) / 32
+ * words, bit t % 32 of word t / 32 for token t, built on the host by laser_atp_bitmap and
+ * copied to the device by the caller.  d_flags may alias d_tokens.
+ * The conclusion after an exit (Algorithm 1's "generate conclusion", forced when the budget
+ * is exhausted) is the closing delimiter and any answer prompt appended with laser_prefill
+ * (or a laser_forward span), followed by ordinary decode steps. */
+/* words_out receives (vocab + 31) / 32 words.  INVALID_ARG for NULL, n_ids < 0, vocab < 1
+ * or an id outside [0, vocab). */
+laser_status laser_atp_bitmap(const int32_t* ids, int n_ids, int vocab, uint32_t* words_out);
+/* n >= 1 tokens; asynchronous on `stream` (the current device). */
+laser_status laser_atp_match(const int32_t* d_tokens, int n, const uint32_t* d_bitmap, int vocab, int32_t* d_flags,
+                             void* stream);
 
 /* ========================================================================== */
 /* Kernel timing.  While any class is enabled (a timing session), forwards launch their

@@ -130,6 +130,14 @@ __global__ void k_confidence(const float* p, int T, int n, float* conf) {
   conf[r] = s / (float)T;
 }
 
+// ATP cue detection: flags[i] = membership of tokens[i] in the bitmap set.
+__global__ void k_atp_match(const int* tokens, int n, const unsigned* bitmap, int vocab, int* flags) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  const int t = tokens[i];
+  flags[i] = (t >= 0 && t < vocab) ? (int)((bitmap[t >> 5] >> (t & 31)) & 1u) : 0;
+}
+
 // Copy of one page (every layer and kv head, K and V) from page src to page dst: grid
 // (n_layers * hkv), 16-byte chunks of the 16 x hd block.
 __global__ __launch_bounds__(256) void k_page_copy(void* kpool, void* vpool, int num_pages, int hkv, size_t blk_bytes,
@@ -185,6 +193,10 @@ hipError_t launch_kv_copy(int dtype, int to_pool, void* kpool, void* vpool, cons
 
 hipError_t launch_confidence(const float* p, int T, int n, float* conf, hipStream_t s) {
   return launch_k(k_confidence, dim3((n + 63) / 64), dim3(64), s, p, T, n, conf);
+}
+
+hipError_t launch_atp_match(const int* tokens, int n, const unsigned* bitmap, int vocab, int* flags, hipStream_t s) {
+  return launch_k(k_atp_match, dim3((n + 255) / 256), dim3(256), s, tokens, n, bitmap, vocab, flags);
 }
 
 }  // namespace laser

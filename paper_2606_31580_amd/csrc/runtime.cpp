@@ -1174,6 +1174,26 @@ extern "C" laser_status laser_confidence(laser_model* m, const float* d_p, int T
   return LASER_OK;
 }
 
+// ----------------------------------------------------------------------------- ATP cues
+
+extern "C" laser_status laser_atp_bitmap(const int32_t* ids, int n_ids, int vocab, uint32_t* words_out) {
+  if (!words_out || n_ids < 0 || vocab < 1 || (n_ids > 0 && !ids)) return laser_fail(LASER_ERR_INVALID_ARG, "bad argument");
+  for (int i = 0; i < n_ids; ++i)
+    if (ids[i] < 0 || ids[i] >= vocab) return laser_fail(LASER_ERR_INVALID_ARG, "id %d outside the vocabulary", ids[i]);
+  const int nw = (vocab + 31) / 32;
+  for (int w = 0; w < nw; ++w) words_out[w] = 0u;
+  for (int i = 0; i < n_ids; ++i) words_out[ids[i] >> 5] |= 1u << (ids[i] & 31);
+  return LASER_OK;
+}
+
+extern "C" laser_status laser_atp_match(const int32_t* d_tokens, int n, const uint32_t* d_bitmap, int vocab,
+                                        int32_t* d_flags, void* stream) {
+  if (!d_tokens || !d_bitmap || !d_flags || n < 1 || vocab < 1) return laser_fail(LASER_ERR_INVALID_ARG, "bad argument");
+  const hipError_t e = launch_atp_match(d_tokens, n, d_bitmap, vocab, d_flags, (hipStream_t)stream);
+  if (e != hipSuccess) return laser_fail(LASER_ERR_HIP, "atp match: %s", hipGetErrorString(e));
+  return LASER_OK;
+}
+
 // ----------------------------------------------------------------------------- graphs
 
 extern "C" laser_status laser_model_set_graphs(laser_model* m, int enable) {

@@ -113,6 +113,8 @@ _SIGS = {
     "laser_timing_enable": (_I, [_P, _I, _I]),
     "laser_timing_read": (_I, [_P, _I, C.POINTER(C.c_double), C.POINTER(_I)]),
     "laser_model_set_graphs": (_I, [_P, _I]),
+    "laser_atp_bitmap": (_I, [_P, _I, _I, _P]),
+    "laser_atp_match": (_I, [_P, _I, _P, _I, _P, _P]),
     "laser_simulate": (_I, [C.POINTER(laser_params), C.POINTER(laser_sim_config), _I, C.POINTER(laser_sim_request),
                             _P, _P, _P, C.POINTER(laser_sim_result), C.POINTER(laser_sim_summary)]),
 }
@@ -429,3 +431,21 @@ def laser_simulate(params: laser_params, cfg: laser_sim_config, arrivals, traces
     _call("laser_simulate", C.byref(params), C.byref(cfg), n, reqs, tok.ctypes.data if tok.size else None,
           conf.ctypes.data if conf.size else None, corr.ctypes.data if corr.size else None, out, C.byref(summ))
     return [out[i] for i in range(n)], summ
+
+
+# --------------------------------------------------------------------------- ATP cues
+
+def laser_atp_bitmap(ids: Sequence[int], vocab: int):
+    """Bitmap words (numpy uint32, (vocab + 31) // 32) of the ATP cue token set."""
+    import numpy as np
+
+    words = np.zeros((vocab + 31) // 32, dtype=np.uint32)
+    arr = np.ascontiguousarray(np.asarray(list(ids), dtype=np.int32))
+    _call("laser_atp_bitmap", arr.ctypes.data if arr.size else None, int(arr.size), vocab, words.ctypes.data)
+    return words
+
+
+def laser_atp_match(d_tokens, d_bitmap, vocab: int, d_flags, n: Optional[int] = None, stream=None) -> None:
+    """d_flags[i] = 1 if d_tokens[i] is an ATP cue token (device tensors, int32 / uint32 words)."""
+    n = d_tokens.numel() if n is None else n
+    _call("laser_atp_match", d_tokens.data_ptr(), n, d_bitmap.data_ptr(), vocab, d_flags.data_ptr(), _stream_ptr(stream))
