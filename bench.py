@@ -41,7 +41,7 @@ def parse():
     ap.add_argument("--probe-mode", choices=["riding", "separate"], default="riding",
                     help="riding: each probe's rows ride along with the next decode forwards on a fork of the "
                          "request; separate: the probe runs as its own forwards between decode steps")
-    ap.add_argument("--probe-rows", type=int, default=1, help="probe rows per forward in riding mode")
+    ap.add_argument("--probe-rows", type=int, default=8, help="probe rows per forward in riding mode")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 256 MiB device-to-device copy three times (scale for HBM byte counters)")
     return ap.parse_args()

@@ -126,6 +126,14 @@ def test_qwen1p5b_kv4096_state_injection():
     st.release()
 
 
+def test_qwen1p5b_kv14336_state_injection():
+    # the long-CoT tail of the 1.5B shape: split-K attention over 896 pages of 2 KV heads
+    st = Setup(QWEN_1P5B, [14336])
+    st.decode(2)
+    st.probe([0])
+    st.release()
+
+
 def test_qwen7b_b1_kv14336_state_injection():
     st = Setup(QWEN_7B, [14336])
     st.decode(1)

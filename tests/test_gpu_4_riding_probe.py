@@ -4,6 +4,9 @@ At an ATP each probing request is forked (full pages shared, the partial last pa
 the following forwards carry, beside every request's decode row, a few of the fork's suffix
 rows and then its fed-back trial rows (laser_forward spans).  Checked against the oracle:
 
+Cases: tiny at 1, 3 and 8 probe rows per forward; 1.5B bf16 at 8 (the benchmark's setting:
+all suffix rows in one forward beside the decode row, then the trial rows one per forward).
+
 * every decode row equals plain decoding of the request (the fork's rows never touch it);
 * the confidence and trial tokens equal the oracle's probe of the request's state at the
   ATP (Section 3.1);
@@ -101,7 +104,7 @@ def test_riding_probe_tiny():
         states.append(SeqState.from_prefill(TINY, K0.numpy(), V0.numpy(), 1024))
     toks = [int(t) for t in synth.make_tokens(len(lens), TINY.vocab, 3010)]
     suffix = [int(t) for t in synth.make_suffix(S, TINY.vocab)]
-    for per_step in (3, 8):
+    for per_step in (1, 3, 8):
         n, toks = riding_probe_run(TINY, model, orc, kv, opool, states, [0, 1, 2], [0, 1], [5, 6], per_step,
                                    toks, suffix, f"tiny per_step={per_step}")
         assert n == -(-S // per_step) + T - 1
@@ -121,4 +124,5 @@ def test_riding_probe_1p5b_bf16():
     del K0, V0
     toks = [int(synth.make_tokens(1, shape.vocab, 3011)[0])]
     suffix = [int(t) for t in synth.make_suffix(S, shape.vocab)]
-    riding_probe_run(shape, model, orc, kv, opool, states, [0], [0], [2], 3, toks, suffix, "1.5B")
+    # the benchmark's setting: the 8 suffix rows ride in one forward (9 rows: the MFMA path)
+    riding_probe_run(shape, model, orc, kv, opool, states, [0], [0], [2], 8, toks, suffix, "1.5B")
