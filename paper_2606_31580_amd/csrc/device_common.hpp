@@ -101,6 +101,17 @@ __device__ __forceinline__ float row_sum16(float x) {
 
 __device__ __forceinline__ float wave_sum(float x) { return sum_x32(sum_x16(row_sum16(x))); }
 
+// Maximum / minimum over the 16 lanes of a row, then over the wave, in every lane.
+__device__ __forceinline__ float row_max16(float x) {
+  x = fmaxf(x, dpp_f<kDppQuad1032>(x));
+  x = fmaxf(x, dpp_f<kDppQuad2301>(x));
+  x = fmaxf(x, dpp_f<kDppHalfMirror>(x));
+  x = fmaxf(x, dpp_f<kDppRowRor8>(x));
+  return x;
+}
+__device__ __forceinline__ float wave_max(float x) { return max_x32(max_x16(row_max16(x))); }
+__device__ __forceinline__ float wave_min(float x) { return -wave_max(-x); }
+
 // Value of element e of a stored tensor (fp32 or bf16 bits).
 template <class WT>
 __device__ __forceinline__ float ldw(const void* base, size_t e);

@@ -25,71 +25,71 @@ __global__ __launch_bounds__(64) void k_embed(const Plan* plan, const void* embe
   h[(size_t)m * d + 64 * g + j] = ldw<WT>(embed, (size_t)tok * d + 64 * g + j);
 }
 
-// (mx, sum, idx) merged with the statistics of another range; among equal maxima the lower
-// index wins, so the result does not depend on the merge order.
-__device__ __forceinline__ void lm_merge(float& mx, float& sum, int& idx, float mx2, float sum2, int idx2) {
-  if (mx2 > mx) {
-    sum = sum * expf(mx - mx2) + sum2;
-    mx = mx2;
-    idx = idx2;
-  } else if (mx2 == mx) {
-    sum += sum2;
-    idx = min(idx, idx2);
-  } else {
-    sum += sum2 * expf(mx2 - mx);
-  }
-}
-
-// One workgroup per LM-head output row: merges the per-group softmax statistics (row m's
-// groups are contiguous; each load instruction of a wave reads 64 consecutive groups) and
-// then across lanes and waves, into the greedy token (lowest index among equal
-// maxima) and p_max = 1 / sum_j exp(l_j - l_max).
+// One workgroup per LM-head output row: merges the per-group softmax statistics into the
+// greedy token (lowest index among equal maxima) and p_max = 1 / sum_j exp(l_j - l_max).
+// Every thread loads all its groups at once (a 152k vocabulary at 8 rows per group is one
+// round), then the maximum is reduced first (lanes, waves) and the sums are rescaled to it
+// once, so no merge step needs an exponential of its own.  Indices are exact as floats
+// (below 2^24), which lets the lowest index be a plain minimum reduction.
 constexpr int kLmThreads = 1024;
+constexpr int kLmPer = 20;  // groups per thread per round
 __global__ __launch_bounds__(kLmThreads) void k_lm_reduce(const Plan* plan, const LmPart* part, int n_groups) {
-  __shared__ float s_mx[kLmThreads / 64];
-  __shared__ float s_sum[kLmThreads / 64];
-  __shared__ int s_idx[kLmThreads / 64];
-  const int m = blockIdx.x, tid = threadIdx.x;
+  constexpr int NW = kLmThreads / 64;
+  constexpr float kNoIdx = 3.0e38f;
+  __shared__ float s_mx[NW], s_sum[NW], s_idx[NW];
+  const int m = blockIdx.x, tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const LmPart* row = part + (size_t)m * n_groups;
-  float mx = -INFINITY, sum = 0.f;
-  int idx = 0x7fffffff;
-  constexpr int U = 8;
-  for (int g0 = tid; g0 < n_groups; g0 += U * kLmThreads) {
-    LmPart pp[U];
+  float mx = -INFINITY, sum = 0.f, idx = kNoIdx;
+  for (int g0 = tid; g0 < n_groups; g0 += kLmPer * kLmThreads) {
+    LmPart pp[kLmPer];
 #pragma unroll
-    for (int u = 0; u < U; ++u) {
+    for (int u = 0; u < kLmPer; ++u) {
       const int g = g0 + u * kLmThreads;
       pp[u] = g < n_groups ? row[g] : LmPart{-INFINITY, 0.f, 0x7fffffff, 0};
     }
+    float rm = mx;
 #pragma unroll
-    for (int u = 0; u < U; ++u) lm_merge(mx, sum, idx, pp[u].mx, pp[u].sum, pp[u].idx);
+    for (int u = 0; u < kLmPer; ++u) rm = fmaxf(rm, pp[u].mx);
+    float rs = (mx == rm) ? sum : (mx == -INFINITY ? 0.f : sum * expf(mx - rm));
+    float ri = (mx == rm) ? idx : kNoIdx;
+#pragma unroll
+    for (int u = 0; u < kLmPer; ++u) {
+      if (pp[u].mx == rm) {
+        rs += pp[u].sum;
+        if (pp[u].idx != 0x7fffffff) ri = fminf(ri, (float)pp[u].idx);
+      } else if (pp[u].mx != -INFINITY) {
+        rs += pp[u].sum * expf(pp[u].mx - rm);
+      }
+    }
+    mx = rm;
+    sum = rs;
+    idx = ri;
   }
-  // within each wave, then across the 16 waves
-  for (int off = 32; off > 0; off >>= 1)
-    lm_merge(mx, sum, idx, __shfl_xor(mx, off), __shfl_xor(sum, off), __shfl_xor(idx, off));
-  const int lane = tid & 63, w = tid >> 6;
+  // maximum over the workgroup
+  const float wm = wave_max(mx);
+  if (lane == 0) s_mx[w] = wm;
+  __syncthreads();
+  float M = s_mx[0];
+#pragma unroll
+  for (int v = 1; v < NW; ++v) M = fmaxf(M, s_mx[v]);
+  // sums rescaled to it; lowest index among the lanes at it
+  const float mine = (mx == -INFINITY || M == -INFINITY) ? 0.f : (mx == M ? sum : sum * expf(mx - M));
+  const float ws = wave_sum(mine);
+  const float wi = wave_min(mx == M ? idx : kNoIdx);
   if (lane == 0) {
-    s_mx[w] = mx;
-    s_sum[w] = sum;
-    s_idx[w] = idx;
+    s_sum[w] = ws;
+    s_idx[w] = wi;
   }
   __syncthreads();
-  if (w == 0) {
-    mx = lane < kLmThreads / 64 ? s_mx[lane] : -INFINITY;
-    sum = lane < kLmThreads / 64 ? s_sum[lane] : 0.f;
-    idx = lane < kLmThreads / 64 ? s_idx[lane] : 0x7fffffff;
-    for (int off = 8; off > 0; off >>= 1)
-      lm_merge(mx, sum, idx, __shfl_xor(mx, off), __shfl_xor(sum, off), __shfl_xor(idx, off));
-    if (lane == 0) {
-      s_mx[0] = mx;
-      s_sum[0] = sum;
-      s_idx[0] = idx;
+  if (tid == 0) {
+    float tot = 0.f, best = kNoIdx;
+    for (int v = 0; v < NW; ++v) {  // fixed order
+      tot += s_sum[v];
+      best = fminf(best, s_idx[v]);
     }
-  }
-  if (tid == 0) {  // lane 0 of wave 0 holds the total
     const OutDesc od = plan->outs[m];
-    plan->io.tok_dst[od.sel][od.off] = s_idx[0] == 0x7fffffff ? 0 : s_idx[0];
-    plan->io.p_dst[od.sel][od.off] = 1.f / s_sum[0];
+    plan->io.tok_dst[od.sel][od.off] = best >= kNoIdx ? 0 : (int)best;
+    plan->io.p_dst[od.sel][od.off] = 1.f / tot;
   }
 }
 
