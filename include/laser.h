@@ -46,7 +46,7 @@
 extern "C" {
 #endif
 
-#define LASER_ABI_VERSION 1
+#define LASER_ABI_VERSION 2
 
 typedef enum {
   LASER_OK = 0,
@@ -57,7 +57,7 @@ typedef enum {
   LASER_ERR_STATE = -5          /* call out of order (e.g. before finalize, destroyed handle) */
 } laser_status;
 
-typedef enum { LASER_DTYPE_F32 = 0, LASER_DTYPE_BF16 = 1 } laser_dtype;
+typedef enum { LASER_DTYPE_F32 = 0, LASER_DTYPE_BF16 = 1, LASER_DTYPE_FP8_E4M3 = 2 } laser_dtype;
 
 /* Message of the last failing call on this thread ("" if none).  Owned by the library. */
 const char* laser_last_error(void);
@@ -237,13 +237,17 @@ laser_status laser_pages_destroy(laser_page_pool* pool);
  * SwiGLU MLP, final RMSNorm, LM head (the embedding when tied_embeddings).
  * Supported: head_dim in {64, 128}; n_q_heads a multiple of n_kv_heads with
  * G = n_q_heads/n_kv_heads <= 16; d_model a multiple of 64; d_ffn a multiple of 8;
- * n_q_heads*head_dim a multiple of 64; dtype F32 or BF16 for every tensor and the KV
- * cache; max_positions <= 65536. */
+ * n_q_heads*head_dim a multiple of 64; dtype F32 or BF16 for every tensor (and the KV
+ * cache unless kv_dtype says FP8_E4M3); max_positions <= 65536. */
 typedef struct {
   int n_layers, d_model, n_q_heads, n_kv_heads, head_dim, d_ffn, vocab;
   int tied_embeddings, qkv_bias, dtype;
   float rope_theta, rms_eps;
   int max_positions;
+  /* KV-cache element type: 0 (or dtype) = the weights' type, or LASER_DTYPE_FP8_E4M3 (bf16
+   * models only): the OCP FP8 E4M3 format (bias 7, largest finite 448, NaN 0x7f/0xff), each
+   * new key and value rounded to nearest even and saturated at +-448, decoded exactly. */
+  int kv_dtype;
 } laser_model_desc;
 
 typedef struct laser_model laser_model;
@@ -290,7 +294,7 @@ laser_status laser_kv_create(const laser_model* m, int num_pages, int max_seqs, 
  * undefined until imported).  OUT_OF_PAGES / INVALID_ARG leave the cache unchanged. */
 laser_status laser_kv_add_seq(laser_kv* kv, int seq_id, int length);
 /* Writes positions 0..length-1 of seq_id from d_k, d_v laid out [n_layers][length]
- * [n_kv_heads][head_dim] (model dtype; keys already rotated).  length must equal the
+ * [n_kv_heads][head_dim] (KV-cache element type; keys already rotated).  length must equal the
  * sequence's length. */
 laser_status laser_kv_import(laser_kv* kv, int seq_id, const void* d_k, const void* d_v, int length, void* stream);
 /* Inverse of import: gathers all positions of seq_id into [n_layers][len][hkv][hd]. */

@@ -1,4 +1,4 @@
-"""bf16 storage rounding, written from the format's definition.
+"""bf16 and fp8 (E4M3) storage rounding, written from the formats' definitions.
 
 Oracle (test infrastructure).  bf16 has an 8-bit significand (7 stored bits
 plus the implicit one) and fp32's exponent range.  Storing a real x in bf16
@@ -28,6 +28,39 @@ def round_bf16(x) -> np.ndarray:
     return np.rint(x / ulp) * ulp  # np.rint rounds half to even
 
 
+# OCP FP8 E4M3 ("fn": no infinities): 1 sign bit, 4 exponent bits with bias 7, 3 fraction
+# bits.  Normal values (1 + f/8) 2^(e-7) for e = 1..15 except the NaN code e = 15, f = 7, so
+# the largest finite value is 1.75 * 2^8 = 448; subnormals f/8 * 2^-6 for e = 0.
+E4M3_MAX = 448.0
+E4M3_MIN_NORMAL_EXP = -6
+E4M3_SIGNIFICAND_BITS = 4
+
+
+def round_fp8_e4m3(x) -> np.ndarray:
+    """Round each element of x to the nearest E4M3 value, ties to even; magnitudes that round
+    beyond 448 saturate to 448 (the saturating conversion); NaN stays NaN.
+
+    Returns float64 values that are exactly representable in E4M3.
+    """
+    x = np.asarray(x, dtype=np.float64)
+    _, e = np.frexp(x)
+    e_eff = np.maximum(e, E4M3_MIN_NORMAL_EXP + 1)
+    ulp = np.ldexp(1.0, e_eff - E4M3_SIGNIFICAND_BITS)
+    r = np.rint(x / ulp) * ulp
+    return np.clip(r, -E4M3_MAX, E4M3_MAX)
+
+
+def fp8_e4m3_bits_to_float(bits) -> np.ndarray:
+    """Decode E4M3 bit patterns (uint8) to their values."""
+    b = np.asarray(bits, dtype=np.uint8).astype(np.int64)
+    s = np.where(b & 0x80, -1.0, 1.0)
+    e = (b >> 3) & 15
+    f = b & 7
+    mag = np.where(e == 0, np.ldexp(f.astype(np.float64), -9), np.ldexp(1.0 + f / 8.0, e - 7))
+    mag = np.where((e == 15) & (f == 7), np.nan, mag)
+    return s * mag
+
+
 def bf16_bits_to_float(bits) -> np.ndarray:
     """Decode bf16 bit patterns (uint16) to their values: the upper half of an fp32 word."""
     b = np.asarray(bits, dtype=np.uint16)
@@ -35,8 +68,11 @@ def bf16_bits_to_float(bits) -> np.ndarray:
 
 
 def as_float64(a) -> np.ndarray:
-    """Value of a stored tensor: uint16 arrays are bf16 bit patterns, anything else is a float array."""
+    """Value of a stored tensor: uint16 arrays are bf16 bit patterns, uint8 arrays E4M3 bit
+    patterns, anything else is a float array."""
     a = np.asarray(a)
     if a.dtype == np.uint16:
         return bf16_bits_to_float(a)
+    if a.dtype == np.uint8:
+        return fp8_e4m3_bits_to_float(a)
     return a.astype(np.float64)

@@ -33,7 +33,7 @@ from typing import List, Mapping, Optional, Sequence
 
 import numpy as np
 
-from .numerics import as_float64, round_bf16
+from .numerics import as_float64, round_bf16, round_fp8_e4m3
 
 
 # --------------------------------------------------------------------------- blocks
@@ -148,7 +148,7 @@ class DecoderOracle:
     """Random-initialised decoder in float64 (or float32) with the storage rounding of its KV cache.
 
     weights: name -> array; uint16 arrays are bf16 bit patterns, other arrays are values.
-    kv_storage: "bf16", "f32" or None (no rounding, for the exact recompute invariant);
+    kv_storage: "bf16", "fp8" (E4M3), "f32" or None (no rounding, for the exact recompute invariant);
     defaults to the shape's storage dtype.
     """
 
@@ -158,7 +158,7 @@ class DecoderOracle:
         self.weights = weights
         self.dtype = dtype
         if kv_storage == "auto":
-            kv_storage = shape.dtype
+            kv_storage = getattr(shape, "kv_storage", shape.dtype)
         self.kv_storage = kv_storage
         # cache_weights keeps each tensor's decoded value after first use (memory for speed)
         self._cache = {} if cache_weights else None
@@ -174,6 +174,8 @@ class DecoderOracle:
     def store_kv(self, x: np.ndarray) -> np.ndarray:
         if self.kv_storage == "bf16":
             return round_bf16(x).astype(self.dtype)
+        if self.kv_storage == "fp8":
+            return round_fp8_e4m3(x).astype(self.dtype)
         if self.kv_storage == "f32":
             return x.astype(np.float32).astype(self.dtype)
         return x

@@ -10,7 +10,7 @@ the method's arithmetic: these are plain records.
 """
 from __future__ import annotations
 
-from dataclasses import dataclass, field
+from dataclasses import dataclass, field, replace
 from typing import List, Optional
 
 
@@ -26,9 +26,14 @@ class ModelShape:
     vocab: int
     tied_embeddings: bool
     qkv_bias: bool
-    dtype: str  # "bf16" or "f32": weight and KV-cache storage type
+    dtype: str  # "bf16" or "f32": weight storage type (and the KV cache's unless kv_dtype is set)
     rope_theta: float
     rms_eps: float
+    kv_dtype: str = ""  # "" = dtype, or "fp8" (OCP E4M3 KV cache, bf16 models)
+
+    @property
+    def kv_storage(self) -> str:
+        return self.kv_dtype or self.dtype
 
     @property
     def group(self) -> int:
@@ -45,7 +50,7 @@ class ModelShape:
         return es * (self.n_layers * per_layer + self.vocab * d + d)
 
     def kv_bytes_per_token(self) -> int:
-        es = 2 if self.dtype == "bf16" else 4
+        es = {"fp8": 1, "bf16": 2}.get(self.kv_storage, 4)
         return self.n_layers * 2 * self.n_kv_heads * self.head_dim * es
 
 
@@ -69,7 +74,12 @@ QWEN_1P5B = ModelShape("qwen2-1.5B-shape", 28, 1536, 12, 2, 128, 8960, 151936, T
 QWEN_7B = ModelShape("qwen2-7B-shape", 28, 3584, 28, 4, 128, 18944, 152064, False, True, "bf16", 1.0e4, 1.0e-6)
 LLAMA_8B = ModelShape("llama-8B-shape", 32, 4096, 32, 8, 128, 14336, 128256, False, False, "bf16", 5.0e5, 1.0e-5)
 
-SHAPES = {s.name: s for s in (TINY, QWEN_1P5B, QWEN_7B, LLAMA_8B)}
+# the same shapes with an fp8 (E4M3) KV cache
+QWEN_1P5B_FP8KV = replace(QWEN_1P5B, name="qwen2-1.5B-shape-fp8kv", kv_dtype="fp8")
+QWEN_7B_FP8KV = replace(QWEN_7B, name="qwen2-7B-shape-fp8kv", kv_dtype="fp8")
+LLAMA_8B_FP8KV = replace(LLAMA_8B, name="llama-8B-shape-fp8kv", kv_dtype="fp8")
+
+SHAPES = {s.name: s for s in (TINY, QWEN_1P5B, QWEN_7B, LLAMA_8B, QWEN_1P5B_FP8KV, QWEN_7B_FP8KV, LLAMA_8B_FP8KV)}
 
 WORKLOADS = {
     w.name: w
@@ -79,6 +89,7 @@ WORKLOADS = {
         Workload("1.5B-b1-kv14336", QWEN_1P5B, 1, (14336,), 512, 128),
         Workload("7B-b4-ragged", QWEN_7B, 4, (3000, 6000, 10000, 14000), 256, 64),
         Workload("7B-b1-kv14336", QWEN_7B, 1, (14336,), 256, 64),
+        Workload("7B-b1-kv14336-fp8kv", QWEN_7B_FP8KV, 1, (14336,), 256, 64),
         Workload("8B-b8-mixed", LLAMA_8B, 8, (), 64, 1, mixed=True),
     )
 }

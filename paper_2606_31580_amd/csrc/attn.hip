@@ -85,14 +85,25 @@ __global__ __launch_bounds__(64 * kAttnWaves) void k_attn(AttnArgs a) {
   // bits; fp32 pools are split into bf16 hi/lo when used).  A decode split is usually two
   // pages, so its whole run is in flight at once.
   constexpr int D = 2;
-  constexpr int KW = sizeof(KT) == 2 ? 1 : 2;  // 16-byte K loads per k-step
+  constexpr int KW = sizeof(KT) == 4 ? 2 : 1;  // 16-byte K loads per k-step (fp8: one 8-byte load)
   u32x4 kraw[D][NS][KW];
-  u32x4 vraw[D][ND];  // bf16: only the low 8 bytes are used
+  u32x4 vraw[D][ND];  // bf16: only the low 8 bytes are used; fp8: the low 4
   auto load_page = [&](int pg, auto bufc) {
     constexpr int buf = decltype(bufc)::value;
     const int pid = btrow[pg];
     const size_t blk = ((layer_base + pid) * a.hkv + kvh) * blk_elems;
-    if (sizeof(KT) == 2) {
+    if (sizeof(KT) == 1) {
+      const uint8_t* kb = (const uint8_t*)a.kpool + blk;
+      const uint8_t* vb = (const uint8_t*)a.vpool + blk;
+#pragma unroll
+      for (int s = 0; s < NS; ++s) {
+        const u32x2 t = ld_nt8(kb + s * 512 + 8 * l);
+        kraw[buf][s][0] = u32x4{t[0], t[1], 0u, 0u};
+      }
+#pragma unroll
+      for (int dt = 0; dt < ND; ++dt)
+        vraw[buf][dt] = u32x4{__builtin_nontemporal_load((const uint32_t*)(vb + dt * 256 + 4 * l)), 0u, 0u, 0u};
+    } else if (sizeof(KT) == 2) {
       const uint16_t* kb = (const uint16_t*)a.kpool + blk;
       const uint16_t* vb = (const uint16_t*)a.vpool + blk;
 #pragma unroll
@@ -124,7 +135,21 @@ __global__ __launch_bounds__(64 * kAttnWaves) void k_attn(AttnArgs a) {
   };
   auto unpack = [&](int pg, auto cbc, PageOps& P) {
     constexpr int cb = decltype(cbc)::value;
-    if (sizeof(KT) == 2) {
+    if (sizeof(KT) == 1) {  // E4M3 -> bf16 is exact: no lo part
+#pragma unroll
+      for (int s = 0; s < NS; ++s) {
+        uint32_t w0, w1, w2, w3;
+        fp8x4_to_bf16x4(kraw[cb][s][0][0], w0, w1);
+        fp8x4_to_bf16x4(kraw[cb][s][0][1], w2, w3);
+        P.khi[s] = __builtin_bit_cast(bf16x8, u32x4{w0, w1, w2, w3});
+      }
+#pragma unroll
+      for (int dt = 0; dt < ND; ++dt) {
+        uint32_t w0, w1;
+        fp8x4_to_bf16x4(vraw[cb][dt][0], w0, w1);
+        P.vhi[dt] = __builtin_bit_cast(s16x4, u32x2{w0, w1});
+      }
+    } else if (sizeof(KT) == 2) {
 #pragma unroll
       for (int s = 0; s < NS; ++s) P.khi[s] = __builtin_bit_cast(bf16x8, kraw[cb][s][0]);
 #pragma unroll
@@ -531,7 +556,10 @@ static hipError_t launch_nt(int nt, const AttnArgs& a, dim3 grid, hipStream_t s)
 }
 
 hipError_t launch_attn(int dtype, int hd, int nt, const AttnArgs& a, dim3 grid, hipStream_t s) {
-  if (dtype == 1) {
+  if (dtype == 2) {
+    if (hd == 128) return launch_nt<fp8_t, 128>(nt, a, grid, s);
+    if (hd == 64) return launch_nt<fp8_t, 64>(nt, a, grid, s);
+  } else if (dtype == 1) {
     if (hd == 128) return launch_nt<bf16_t, 128>(nt, a, grid, s);
     if (hd == 64) return launch_nt<bf16_t, 64>(nt, a, grid, s);
   } else {

@@ -16,6 +16,36 @@ typedef __attribute__((__vector_size__(4 * sizeof(short)))) short s16x4;
 struct bf16_t {
   uint16_t bits;
 };
+// OCP FP8 E4M3 (the "fn" variant: bias 7, no infinities, 0x7f/0xff NaN, largest finite 448).
+struct fp8_t {
+  uint8_t bits;
+};
+
+// fp32 -> E4M3 bits: round to nearest even on the E4M3 grid (spacing 2^(e-3) in binade
+// [2^e, 2^(e+1)) for e >= -6, 2^-9 below), magnitudes that round past 448 saturate to 448,
+// NaN stays NaN.
+__device__ __forceinline__ uint8_t f2fp8(float v) {
+  const uint32_t sign = (__float_as_uint(v) >> 24) & 0x80u;
+  const float a = fabsf(v);
+  if (!(a == a)) return (uint8_t)(sign | 0x7fu);
+  const int e = a >= 0x1p-6f ? (int)((__float_as_uint(a) >> 23) & 0xffu) - 127 : -6;
+  const float ulp = __builtin_amdgcn_ldexpf(1.0f, (e > 8 ? 8 : e) - 3);
+  float r = rintf(a / ulp) * ulp;  // exact scaling by a power of two; rint rounds half to even
+  if (r > 448.0f) r = 448.0f;
+  if (r < 0x1p-6f) return (uint8_t)(sign | (uint32_t)(r * 512.0f));  // zero or subnormal: r = m * 2^-9
+  const int re = (int)((__float_as_uint(r) >> 23) & 0xffu) - 127;   // r may have moved up a binade
+  const uint32_t m = (__float_as_uint(r) >> 20) & 7u;
+  return (uint8_t)(sign | ((uint32_t)(re + 7) << 3) | m);
+}
+
+// Four E4M3 bytes of w -> their values as bf16 bit pairs (exact: E4M3 has 3 fraction bits):
+// lo = bytes 0, 1, hi = bytes 2, 3 (element 0 in the low half of each word).
+__device__ __forceinline__ void fp8x4_to_bf16x4(uint32_t w, uint32_t& lo, uint32_t& hi) {
+  const auto a = __builtin_amdgcn_cvt_pk_f32_fp8((int)w, false);
+  const auto b = __builtin_amdgcn_cvt_pk_f32_fp8((int)w, true);
+  lo = __builtin_amdgcn_perm(__float_as_uint(a[1]), __float_as_uint(a[0]), 0x07060302u);
+  hi = __builtin_amdgcn_perm(__float_as_uint(b[1]), __float_as_uint(b[0]), 0x07060302u);
+}
 
 __device__ __forceinline__ float bf2f(uint16_t b) { return __uint_as_float(((uint32_t)b) << 16); }
 
@@ -124,9 +154,13 @@ __device__ __forceinline__ float ldw<bf16_t>(const void* base, size_t e) {
   return bf2f(((const uint16_t*)base)[e]);
 }
 
-// Store a value in the storage type (bf16: round to nearest even).
+// Store a value in the storage type (bf16: round to nearest even; fp8: f2fp8).
 template <class WT>
 __device__ __forceinline__ void stw(void* base, size_t e, float v);
+template <>
+__device__ __forceinline__ void stw<fp8_t>(void* base, size_t e, float v) {
+  ((uint8_t*)base)[e] = f2fp8(v);
+}
 template <>
 __device__ __forceinline__ void stw<float>(void* base, size_t e, float v) {
   ((float*)base)[e] = v;

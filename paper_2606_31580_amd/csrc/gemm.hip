@@ -217,12 +217,15 @@ __device__ __forceinline__ void epi_apply(const GemmArgs& a, int g, const EpiIte
     } else {
       const int t = it.pos & 15;
       const size_t blk = (((size_t)a.layer * a.num_pages + it.page) * a.hkv + q.hh) * (size_t)(16 * a.hd);
-      if (q.isk) {
-        stw<WT>(a.kpool, blk + k_block_off(t, dlo), ylo);
-        stw<WT>(a.kpool, blk + k_block_off(t, dhi), yhi);
+      void* pool = q.isk ? a.kpool : a.vpool;
+      const size_t olo = blk + (q.isk ? k_block_off(t, dlo) : v_block_off(t, dlo));
+      const size_t ohi = blk + (q.isk ? k_block_off(t, dhi) : v_block_off(t, dhi));
+      if (a.kv_fp8) {
+        stw<fp8_t>(pool, olo, ylo);
+        stw<fp8_t>(pool, ohi, yhi);
       } else {
-        stw<WT>(a.vpool, blk + v_block_off(t, dlo), ylo);
-        stw<WT>(a.vpool, blk + v_block_off(t, dhi), yhi);
+        stw<WT>(pool, olo, ylo);
+        stw<WT>(pool, ohi, yhi);
       }
     }
   } else if (EPI == EPI_RESID) {

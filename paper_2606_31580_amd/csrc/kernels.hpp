@@ -91,6 +91,7 @@ struct GemmArgs {
   void* vpool;
   const int* bt;
   int max_pps, num_pages, layer;
+  int kv_fp8;  // K/V stored as E4M3 (else in the weight type)
   // EPI_RESID
   float* h;  // [M][N]
   // EPI_SWIGLU
@@ -140,18 +141,20 @@ inline hipError_t launch_k(K kernel, dim3 grid, dim3 block, hipStream_t s, Args.
 // dtype: 0 fp32, 1 bf16.  mode: 1..4 VALU rows per forward, 5..8 MFMA with 1..4 m-tiles.
 // rw: rows per workgroup (VALU: QKV 6 or 8, residual 6, 7 or 8, others 8; MFMA: 16).
 hipError_t launch_gemm(int dtype, int mode, int epi, int rw, const GemmArgs& a, hipStream_t s);
+// dtype: the KV element type, 0 fp32, 1 bf16, 2 fp8 (E4M3).
 hipError_t launch_attn(int dtype, int hd, int nt, const AttnArgs& a, dim3 grid, hipStream_t s);
 hipError_t launch_attn_merge(const AttnArgs& a, int M, int hd, hipStream_t s);
 hipError_t launch_lm_reduce(const Plan* plan, const LmPart* part, int n_groups, int n_out, hipStream_t s);
 hipError_t launch_embed(int dtype, const Plan* plan, int M, const void* embed, int d, int vocab, float* h, int* bt,
                         int max_pps, hipStream_t s);
 hipError_t launch_apply_bt(const Plan* plan, int* bt, int max_pps, hipStream_t s);
-hipError_t launch_kv_copy(int dtype, int to_pool, void* kpool, void* vpool, const int* bt, int max_pps,
+// kv_es: bytes per KV element (1 fp8, 2 bf16, 4 fp32); the copy moves raw elements.
+hipError_t launch_kv_copy(int kv_es, int to_pool, void* kpool, void* vpool, const int* bt, int max_pps,
                           int num_pages, int n_layers, int hkv, int hd, int seq, int len, void* k_lin,
                           void* v_lin, hipStream_t s);
 hipError_t launch_confidence(const float* p, int T, int n, float* conf, hipStream_t s);
 hipError_t launch_atp_match(const int* tokens, int n, const unsigned* bitmap, int vocab, int* flags, hipStream_t s);
-hipError_t launch_page_copy(int dtype, void* kpool, void* vpool, int num_pages, int n_layers, int hkv, int hd, int src,
+hipError_t launch_page_copy(int kv_es, void* kpool, void* vpool, int num_pages, int n_layers, int hkv, int hd, int src,
                             int dst, hipStream_t s);
 
 }  // namespace laser

@@ -151,9 +151,9 @@ __global__ __launch_bounds__(256) void k_page_copy(void* kpool, void* vpool, int
   }
 }
 
-hipError_t launch_page_copy(int dtype, void* kpool, void* vpool, int num_pages, int n_layers, int hkv, int hd, int src,
+hipError_t launch_page_copy(int kv_es, void* kpool, void* vpool, int num_pages, int n_layers, int hkv, int hd, int src,
                             int dst, hipStream_t s) {
-  const size_t blk_bytes = (size_t)16 * hd * (dtype == 1 ? 2 : 4);
+  const size_t blk_bytes = (size_t)16 * hd * kv_es;
   return launch_k(k_page_copy, dim3(n_layers * hkv), dim3(256), s, kpool, vpool, num_pages, hkv, blk_bytes, src, dst);
 }
 
@@ -175,14 +175,17 @@ hipError_t launch_apply_bt(const Plan* plan, int* bt, int max_pps, hipStream_t s
   return hipGetLastError();
 }
 
-hipError_t launch_kv_copy(int dtype, int to_pool, void* kpool, void* vpool, const int* bt, int max_pps,
+hipError_t launch_kv_copy(int kv_es, int to_pool, void* kpool, void* vpool, const int* bt, int max_pps,
                           int num_pages, int n_layers, int hkv, int hd, int seq, int len, void* k_lin,
                           void* v_lin, hipStream_t s) {
   const size_t total = (size_t)n_layers * len * hkv * hd;
   if (total == 0) return hipSuccess;
   size_t blocks = (total + 255) / 256;
   if (blocks > 65536) blocks = 65536;
-  if (dtype == 1)
+  if (kv_es == 1)
+    hipLaunchKernelGGL(k_kv_copy<uint8_t>, dim3((unsigned)blocks), dim3(256), 0, s, to_pool, kpool, vpool, bt,
+                       max_pps, num_pages, n_layers, hkv, hd, seq, len, k_lin, v_lin);
+  else if (kv_es == 2)
     hipLaunchKernelGGL(k_kv_copy<uint16_t>, dim3((unsigned)blocks), dim3(256), 0, s, to_pool, kpool, vpool, bt,
                        max_pps, num_pages, n_layers, hkv, hd, seq, len, k_lin, v_lin);
   else

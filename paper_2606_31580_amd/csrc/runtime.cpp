@@ -111,7 +111,9 @@ struct laser_model {
   laser_model_desc desc;
   int device = 0;
   int cus = 256;  // compute units of the device (set at creation)
-  int es = 4;     // bytes per stored element
+  int es = 4;     // bytes per stored weight element
+  int kv_es = 4;  // bytes per KV-cache element
+  int kv_fp8 = 0; // KV cache in E4M3
   const void* embed = nullptr;
   const void* lm_head = nullptr;
   const void* final_norm = nullptr;
@@ -242,6 +244,10 @@ static laser_status check_desc(const laser_model_desc* d) {
   if (d->d_ffn % 8) return laser_fail(LASER_ERR_UNSUPPORTED, "d_ffn must be a multiple of 8");
   if ((d->n_q_heads * d->head_dim) % 64) return laser_fail(LASER_ERR_UNSUPPORTED, "n_q_heads*head_dim % 64 != 0");
   if (d->dtype != LASER_DTYPE_F32 && d->dtype != LASER_DTYPE_BF16) return laser_fail(LASER_ERR_INVALID_ARG, "bad dtype");
+  if (d->kv_dtype != 0 && d->kv_dtype != d->dtype && d->kv_dtype != LASER_DTYPE_FP8_E4M3)
+    return laser_fail(LASER_ERR_INVALID_ARG, "bad kv_dtype");
+  if (d->kv_dtype == LASER_DTYPE_FP8_E4M3 && d->dtype != LASER_DTYPE_BF16)
+    return laser_fail(LASER_ERR_UNSUPPORTED, "an fp8 KV cache needs bf16 weights");
   if (d->max_positions < 16 || d->max_positions > 65536) return laser_fail(LASER_ERR_UNSUPPORTED, "max_positions out of range");
   if (!(d->rope_theta > 1.0f) || !(d->rms_eps > 0.0f)) return laser_fail(LASER_ERR_INVALID_ARG, "bad rope_theta or rms_eps");
   return LASER_OK;
@@ -259,6 +265,8 @@ extern "C" laser_status laser_model_create(const laser_model_desc* desc, laser_m
   if (!m) return laser_fail(LASER_ERR_INVALID_ARG, "allocation failed");
   m->desc = *desc;
   m->es = desc->dtype == LASER_DTYPE_BF16 ? 2 : 4;
+  m->kv_fp8 = desc->kv_dtype == LASER_DTYPE_FP8_E4M3;
+  m->kv_es = m->kv_fp8 ? 1 : m->es;
   m->layers.assign(desc->n_layers, LayerW{});
   (void)hipGetDevice(&m->device);
   {
@@ -410,7 +418,7 @@ extern "C" laser_status laser_kv_pool_bytes(const laser_model* m, int num_pages,
   if (!handle_live(m)) return laser_fail(LASER_ERR_STATE, "invalid or destroyed model");
   if (!bytes_per_pool || num_pages < 1) return laser_fail(LASER_ERR_INVALID_ARG, "bad argument");
   const laser_model_desc& d = m->desc;
-  *bytes_per_pool = (size_t)d.n_layers * num_pages * d.n_kv_heads * kPage * d.head_dim * m->es;
+  *bytes_per_pool = (size_t)d.n_layers * num_pages * d.n_kv_heads * kPage * d.head_dim * m->kv_es;
   return LASER_OK;
 }
 
@@ -685,6 +693,7 @@ static laser_status launch_forward(laser_model* m, laser_kv* kv, const FwdKey& k
   base.bt = kv->bt;
   base.max_pps = max_pps;
   base.num_pages = kv->pool.num_pages();
+  base.kv_fp8 = m->kv_fp8;
   base.h = h;
   base.act = m->wsp<float>(L.act);
   base.F = d.d_ffn;
@@ -739,7 +748,7 @@ static laser_status launch_forward(laser_model* m, laser_kv* kv, const FwdKey& k
 
     aa.layer = li;
     HIP_TRY(timed(m, LASER_K_ATTN, s, [&] {
-      hipError_t e = launch_attn(dt, hd, key.nt, aa, agrid, s);
+      hipError_t e = launch_attn(m->kv_fp8 ? 2 : dt, hd, key.nt, aa, agrid, s);
       if (e == hipSuccess && key.merge) e = launch_attn_merge(aa, key.M, hd, s);
       return e;
     }));
@@ -835,7 +844,7 @@ extern "C" laser_status laser_kv_import(laser_kv* kv, int seq_id, const void* d_
   laser_status st = flush_pending(kv, m, s);
   if (st != LASER_OK) return st;
   const laser_model_desc& d = m->desc;
-  HIP_TRY(launch_kv_copy(d.dtype == LASER_DTYPE_BF16, 1, kv->kpool, kv->vpool, kv->bt, kv->pool.max_pages_per_seq(),
+  HIP_TRY(launch_kv_copy(m->kv_es, 1, kv->kpool, kv->vpool, kv->bt, kv->pool.max_pages_per_seq(),
                          kv->pool.num_pages(), d.n_layers, d.n_kv_heads, d.head_dim, seq_id, length,
                          const_cast<void*>(d_k), const_cast<void*>(d_v), s));
   return LASER_OK;
@@ -852,7 +861,7 @@ extern "C" laser_status laser_kv_export(const laser_kv* kvc, int seq_id, void* d
   laser_status st = flush_pending(kv, m, s);
   if (st != LASER_OK) return st;
   const laser_model_desc& d = m->desc;
-  HIP_TRY(launch_kv_copy(d.dtype == LASER_DTYPE_BF16, 0, kv->kpool, kv->vpool, kv->bt, kv->pool.max_pages_per_seq(),
+  HIP_TRY(launch_kv_copy(m->kv_es, 0, kv->kpool, kv->vpool, kv->bt, kv->pool.max_pages_per_seq(),
                          kv->pool.num_pages(), d.n_layers, d.n_kv_heads, d.head_dim, seq_id, kv->pool.len(seq_id), d_k, d_v, s));
   return LASER_OK;
 }
@@ -1100,7 +1109,7 @@ extern "C" laser_status laser_kv_fork(laser_kv* kv, int src_seq, int dst_seq, vo
     const laser_model_desc& d = m->desc;
     TimingScope scope(m);
     const hipError_t e = timed(m, LASER_K_OTHER, s, [&] {
-      return launch_page_copy(d.dtype == LASER_DTYPE_BF16, kv->kpool, kv->vpool, kv->pool.num_pages(), d.n_layers,
+      return launch_page_copy(m->kv_es, kv->kpool, kv->vpool, kv->pool.num_pages(), d.n_layers,
                               d.n_kv_heads, d.head_dim, c.src, c.dst, s);
     });
     if (e != hipSuccess) return laser_fail(LASER_ERR_HIP, "page copy: %s", hipGetErrorString(e));

@@ -14,7 +14,7 @@ from typing import Dict, Optional, Sequence
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "lib", "liblaser.so")
 
 OK, ERR_INVALID_ARG, ERR_OUT_OF_PAGES, ERR_HIP, ERR_UNSUPPORTED, ERR_STATE = 0, -1, -2, -3, -4, -5
-DTYPE_F32, DTYPE_BF16 = 0, 1
+DTYPE_F32, DTYPE_BF16, DTYPE_FP8_E4M3 = 0, 1, 2
 CONTINUE, EARLY_EXIT, BUDGET_EXHAUSTED = 0, 1, 2
 K_EMBED, K_QKV, K_ATTN, K_OPROJ, K_GATEUP, K_DOWN, K_LMHEAD, K_OTHER = range(8)
 KERNEL_CLASSES = {"embed": 0, "qkv": 1, "attn": 2, "oproj": 3, "gateup": 4, "down": 5, "lmhead": 6, "other": 7}
@@ -38,7 +38,7 @@ class laser_load_state(C.Structure):
 class laser_model_desc(C.Structure):
     _fields_ = [(n, C.c_int) for n in ("n_layers", "d_model", "n_q_heads", "n_kv_heads", "head_dim", "d_ffn", "vocab",
                                        "tied_embeddings", "qkv_bias", "dtype")] + [
-        ("rope_theta", C.c_float), ("rms_eps", C.c_float), ("max_positions", C.c_int)]
+        ("rope_theta", C.c_float), ("rms_eps", C.c_float), ("max_positions", C.c_int), ("kv_dtype", C.c_int)]
 
 
 class laser_sim_config(C.Structure):
@@ -245,7 +245,8 @@ def desc_from_shape(shape, max_positions: int = 16640) -> laser_model_desc:
     return laser_model_desc(
         shape.n_layers, shape.d_model, shape.n_q_heads, shape.n_kv_heads, shape.head_dim, shape.d_ffn, shape.vocab,
         int(shape.tied_embeddings), int(shape.qkv_bias), DTYPE_BF16 if shape.dtype == "bf16" else DTYPE_F32,
-        float(shape.rope_theta), float(shape.rms_eps), int(max_positions))
+        float(shape.rope_theta), float(shape.rms_eps), int(max_positions),
+        DTYPE_FP8_E4M3 if getattr(shape, "kv_dtype", "") == "fp8" else 0)
 
 
 def _stream_ptr(stream) -> Optional[int]:

@@ -43,6 +43,12 @@ def _tdtype(shape: ModelShape) -> torch.dtype:
     return torch.bfloat16 if shape.dtype == "bf16" else torch.float32
 
 
+def _kv_tdtype(shape: ModelShape) -> torch.dtype:
+    if shape.kv_storage == "fp8":
+        return torch.float8_e4m3fn
+    return _tdtype(shape)
+
+
 def tensor_specs(shape: ModelShape) -> List[tuple]:
     """(name, dims, kind) in the fixed order that defines each tensor's seed.
 
@@ -91,12 +97,13 @@ def make_weights(shape: ModelShape, device="cpu", seed_base: int = 1000, std: fl
 
 
 def make_prefill_kv(shape: ModelShape, length: int, request: int, device="cpu", seed_base: int = 2000):
-    """Pre-filled (K, V) for one request: two tensors [n_layers, length, n_kv_heads, head_dim], ~N(0,1)."""
+    """Pre-filled (K, V) for one request: two tensors [n_layers, length, n_kv_heads, head_dim], ~N(0,1),
+    in the KV-cache storage type."""
     g = torch.Generator(device=device)
     g.manual_seed(seed_base + request)
     dims = (shape.n_layers, length, shape.n_kv_heads, shape.head_dim)
-    k = torch.randn(dims, generator=g, device=device, dtype=torch.float32).to(_tdtype(shape))
-    v = torch.randn(dims, generator=g, device=device, dtype=torch.float32).to(_tdtype(shape))
+    k = torch.randn(dims, generator=g, device=device, dtype=torch.float32).to(_kv_tdtype(shape))
+    v = torch.randn(dims, generator=g, device=device, dtype=torch.float32).to(_kv_tdtype(shape))
     return k, v
 
 
@@ -136,9 +143,12 @@ def bf16_bits(t: torch.Tensor):
 
 
 def to_numpy(t: torch.Tensor):
-    """Host copy of a tensor for the oracle: bf16 tensors come back as uint16 bit patterns, fp32 as float32."""
+    """Host copy of a tensor for the oracle: bf16 tensors come back as uint16 bit patterns, fp8 (E4M3)
+    tensors as uint8 bit patterns, fp32 as float32."""
     if t.dtype == torch.bfloat16:
         return bf16_bits(t)
+    if t.dtype == torch.float8_e4m3fn:
+        return t.detach().view(torch.uint8).cpu().numpy()
     return t.detach().cpu().numpy()
 
 
