@@ -86,7 +86,15 @@ def main():
     log(f"workload {wl.name}: generating weights")
     weights = synth.make_weights(shape, device=dev)
     R = args.probe_rows
-    model = L.Model(shape, weights, max_rows=max(B + B * R, B * S), max_positions=max_pos)
+    if wl.mixed:  # every step: decode for the batch + probe chunks of a seeded half, one forward
+        schedule = synth.make_mixed_schedule(B, total_steps + 64)
+        rows = max(B + max(len(x) for x in schedule) * S, B * S)
+    else:
+        rows = max(B + B * R, B * S)
+    if rows > 64:
+        log(f"{rows} rows per forward exceed the 64-row maximum; use fewer probe rows")
+        sys.exit(2)
+    model = L.Model(shape, weights, max_rows=rows, max_positions=max_pos)
     pps = max_pos // PAGE + 1
     num_pages = sum((n + 2 * total_steps + S + T) // PAGE + 2 for n in lens) + B * ((S + T) // PAGE + 3) + 8
     num_pages += (COST_CTX + 512) // PAGE + 4  # the cost-model pass (a shorter request in a fork slot)
@@ -120,6 +128,15 @@ def main():
         n_probes[0] += 1
 
     def step(i, timed_probe):
+        if wl.mixed:  # the probes of this step run in the same forwards as its decode
+            pidx = schedule[i % len(schedule)]
+            L.laser_step_mixed(model, kv, seqs, tokens, nxt, pmax, pidx, suffix, T, conf, argm)
+            tokens.copy_(nxt)
+            c = conf.cpu().numpy()
+            for j in range(len(pidx)):
+                L.laser_exit_decision(params, load_state, float(c[j]), B, 0, 10)
+            n_probes[0] += len(pidx)
+            return
         at_atp = wl.probe_every and i % wl.probe_every == 0
         if args.probe_mode == "separate":
             L.laser_decode_step(model, kv, seqs, tokens, nxt, pmax)
@@ -279,8 +296,13 @@ def main():
         "decode_only_ms_per_step": round(dec_ms, 4),
         "decode_only_tok_s": round(B / (dec_ms / 1e3), 2),
         "probe_latency_ms": {"mean": round(float(np.mean(probe_ms)), 3) if probe_ms else None,
-                             "max": round(float(np.max(probe_ms)), 3) if probe_ms else None, "n": len(probe_ms)},
-        "probe": {"mode": args.probe_mode, "rows_per_forward": R if args.probe_mode == "riding" else S,
+                             "max": round(float(np.max(probe_ms)), 3) if probe_ms else None, "n": len(probe_ms)}
+        if not wl.mixed else {"mean": round(ms_per_step, 3), "max": None, "n": probes_timed},
+        "probe": {"mode": "mixed", "probes_in_timed_region": probes_timed,
+                  "latency_meaning": "each step's probes finish within it: one forward with the decode rows and the "
+                                     "probing half's suffix chunks, then T-1 forwards of trial rows",
+                  "separate_probe_latency_ms": round(float(np.mean(sep_ms)), 3)} if wl.mixed else
+                 {"mode": args.probe_mode, "rows_per_forward": R if args.probe_mode == "riding" else S,
                   "forwards_per_probe": (-(-S // R) + T - 1) if args.probe_mode == "riding" else 1 + T - 1,
                   "probes_in_timed_region": probes_timed,
                   "latency_meaning": "device time from the ATP fork to the confidence, decode forwards included"

@@ -91,6 +91,7 @@ WORKLOADS = {
         Workload("7B-b1-kv14336", QWEN_7B, 1, (14336,), 256, 64),
         Workload("7B-b1-kv14336-fp8kv", QWEN_7B_FP8KV, 1, (14336,), 256, 64),
         Workload("8B-b8-mixed", LLAMA_8B, 8, (), 64, 1, mixed=True),
+        Workload("8B-b8-mixed-fp8kv", LLAMA_8B_FP8KV, 8, (), 64, 1, mixed=True),
     )
 }
 
