@@ -42,6 +42,7 @@ def parse():
                     help="riding: each probe's rows ride along with the next decode forwards on a fork of the "
                          "request; separate: the probe runs as its own forwards between decode steps")
     ap.add_argument("--probe-rows", type=int, default=8, help="probe rows per forward in riding mode")
+    ap.add_argument("--no-tiles", action="store_true", help="MFMA path reads the row-major weights (no tile copy)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 256 MiB device-to-device copy three times (scale for HBM byte counters)")
     return ap.parse_args()
@@ -94,7 +95,7 @@ def main():
     if rows > 64:
         log(f"{rows} rows per forward exceed the 64-row maximum; use fewer probe rows")
         sys.exit(2)
-    model = L.Model(shape, weights, max_rows=rows, max_positions=max_pos)
+    model = L.Model(shape, weights, max_rows=rows, max_positions=max_pos, tiles=not args.no_tiles)
     pps = max_pos // PAGE + 1
     num_pages = sum((n + 2 * total_steps + S + T) // PAGE + 2 for n in lens) + B * ((S + T) // PAGE + 3) + 8
     num_pages += (COST_CTX + 512) // PAGE + 4  # the cost-model pass (a shorter request in a fork slot)

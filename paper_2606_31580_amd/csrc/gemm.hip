@@ -459,7 +459,7 @@ __global__ __launch_bounds__(64 * kMfmaMaxWaves) void k_gemm_mfma(GemmArgs a) {
   constexpr int RW = rows_per_group(EPI, true);
   constexpr int NLD = (int)sizeof(WT) / 2;  // 16-byte loads per step (bf16: 1, fp32: 2)
   // steps kept in flight per wave
-  constexpr int U = MT == 1 ? (NR == 1 ? 6 : (NR == 2 ? 4 : 3)) : (MT == 2 ? 4 : 2);
+  constexpr int U = MT == 1 ? (NR == 1 ? 6 : 4) : (MT == 2 ? 4 : 2);
   constexpr int WMAX = NR == 1 ? kMfmaMaxWaves : 4;  // several groups: always 4 waves
   constexpr int YN = 16 * MT * RW;                   // outputs of one group
   const int W = blockDim.x >> 6;                     // waves splitting K
@@ -473,9 +473,14 @@ __global__ __launch_bounds__(64 * kMfmaMaxWaves) void k_gemm_mfma(GemmArgs a) {
   const int M = a.M;
   const bool norm = a.gain != nullptr;
   const int n = l & 15, kg = 8 * (l >> 4);
-  const char* wp[NR];
+  const char* wp[NR];  // row-major: this lane's row; tiled: this lane's bytes in the group's first block
+  constexpr int BLK = 1024 * NLD;
+  const bool tiled = a.wtile != nullptr;
 #pragma unroll
-  for (int r = 0; r < NR; ++r) wp[r] = weight_row<WT, EPI, RW>(a, g0 + (r < nlive ? r : 0), n);
+  for (int r = 0; r < NR; ++r) {
+    const int g = g0 + (r < nlive ? r : 0);
+    wp[r] = tiled ? a.wtile + (size_t)g * a.tsteps * BLK + 16 * l : weight_row<WT, EPI, RW>(a, g, n);
+  }
   const float* xr[MT];
   bool own[MT];  // this lane's A row is a real row (rows past M repeat row M-1)
 #pragma unroll
@@ -508,10 +513,12 @@ __global__ __launch_bounds__(64 * kMfmaMaxWaves) void k_gemm_mfma(GemmArgs a) {
   };
   auto issue = [&](int it, Step& st) {
     const int k = kof(it), kk = k < 0 ? 0 : k;
+    const size_t woff = tiled ? (size_t)(k < 0 ? 0 : step_of(it)) * BLK : (size_t)kk * sizeof(WT);
+    const int qs = tiled ? 1024 : 16;  // offset of a lane's second 16 bytes (fp32)
 #pragma unroll
     for (int r = 0; r < NR; ++r)
 #pragma unroll
-      for (int q = 0; q < NLD; ++q) st.wv[r][q] = ld_nt16(wp[r] + (size_t)kk * sizeof(WT) + 16 * q);
+      for (int q = 0; q < NLD; ++q) st.wv[r][q] = ld_nt16(wp[r] + woff + qs * q);
     if (norm)
 #pragma unroll
       for (int q = 0; q < NLD; ++q) st.gv[q] = *(const u32x4*)((const char*)a.gain + (size_t)kk * sizeof(WT) + 16 * q);
@@ -641,6 +648,44 @@ __global__ __launch_bounds__(64 * kMfmaMaxWaves) void k_gemm_mfma(GemmArgs a) {
   for (int r = 0; r < nlive; ++r) run_epilogue<WT, EPI, RW>(a, g0 + r, M, Y + r * YN);
 }
 
+// ----------------------------------------------------------------------------- weight tiles
+
+// One block (group g, step s) per workgroup of 64 lanes: lane (n = l % 16, q = l / 16) gets
+// the 8 columns 32 s + 8 q .. + 7 of the group's row n (zeros past K), as the MFMA path's
+// B operand takes them.  fp32 weights: 16 bytes at l * 16 and 16 more at 1024 + l * 16.
+template <class WT, int EPI>
+__global__ __launch_bounds__(64) void k_tile_weights(GemmArgs a, char* dst) {
+  constexpr int NLD = (int)sizeof(WT) / 2;
+  constexpr int CH = 8;  // columns per lane
+  const int g = blockIdx.y, s = blockIdx.x, l = threadIdx.x;
+  const int n = l & 15, k0 = 32 * s + CH * (l >> 4);
+  const char* row = weight_row<WT, EPI, 16>(a, g, n);
+  char* out = dst + ((size_t)g * gridDim.x + s) * (1024 * NLD) + 16 * l;
+#pragma unroll
+  for (int q = 0; q < NLD; ++q) {
+    u32x4 v = u32x4{0u, 0u, 0u, 0u};
+    const int kq = k0 + q * (CH / NLD);  // first column of these 16 bytes
+    if (kq + CH / NLD <= a.K) v = *(const u32x4*)(row + (size_t)kq * sizeof(WT));
+    *(u32x4*)(out + 1024 * q) = v;
+  }
+}
+
+template <class WT>
+static hipError_t launch_tiles(int epi, const GemmArgs& a, char* dst, hipStream_t s) {
+  const dim3 grid((a.K + 31) / 32, a.n_groups);
+  switch (epi) {
+    case EPI_QKV: return launch_k(k_tile_weights<WT, EPI_QKV>, grid, dim3(64), s, a, dst);
+    case EPI_RESID: return launch_k(k_tile_weights<WT, EPI_RESID>, grid, dim3(64), s, a, dst);
+    case EPI_SWIGLU: return launch_k(k_tile_weights<WT, EPI_SWIGLU>, grid, dim3(64), s, a, dst);
+    case EPI_LMHEAD: return launch_k(k_tile_weights<WT, EPI_LMHEAD>, grid, dim3(64), s, a, dst);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+hipError_t launch_tile_weights(int dtype, int epi, const GemmArgs& a, char* dst, hipStream_t s) {
+  return dtype == 1 ? launch_tiles<bf16_t>(epi, a, dst, s) : launch_tiles<float>(epi, a, dst, s);
+}
+
 // ----------------------------------------------------------------------------- launch
 
 template <class WT, int MT, int NR>
@@ -673,13 +718,12 @@ static hipError_t launch_epi(int epi, int rw, const GemmArgs& a, hipStream_t s) 
     constexpr int MT = MODE - 4;
     if (rw != rows_per_group(epi, true)) return hipErrorInvalidValue;
     const int nr = a.nr < 1 ? 1 : a.nr;
-    if (nr != 1 && (MT > 1 || (nr != 2 && nr != 4))) return hipErrorInvalidValue;
+    if (nr != 1 && (MT > 1 || nr != 2)) return hipErrorInvalidValue;
     const dim3 mgrid((a.n_groups + nr - 1) / nr);
     // few row groups (the O, down and QKV projections): 8 waves split K more finely
     if (nr == 1 && a.n_groups < 512) block = dim3(64 * kMfmaMaxWaves);
     if constexpr (MT == 1) {
       if (nr == 2) return launch_mfma<WT, MT, 2>(epi, mgrid, block, a, s);
-      if (nr == 4) return launch_mfma<WT, MT, 4>(epi, mgrid, block, a, s);
     }
     return launch_mfma<WT, MT, 1>(epi, mgrid, block, a, s);
   }

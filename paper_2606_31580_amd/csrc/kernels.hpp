@@ -72,7 +72,11 @@ struct GemmArgs {
   const void* w1;
   const void* w2;
   int K, N, M, n_groups;
-  int nr;  // MFMA path: row groups per workgroup (1; 2 or 4 with one 16-row activation tile)
+  int nr;  // MFMA path: row groups per workgroup (1, or 2 with one 16-row activation tile)
+  // MFMA path: the weights in tile order (null: read the row-major tensors).  Group g, step s
+  // (32 columns) is a block of 64 lanes x 16 bytes (x 2 for fp32) at (g * tsteps + s) blocks.
+  const char* wtile;
+  int tsteps;
   // A operand: fp32 activation rows [row][ldx]; optional RMSNorm over the full row (gain)
   const float* x;
   int ldx;
@@ -141,6 +145,9 @@ inline hipError_t launch_k(K kernel, dim3 grid, dim3 block, hipStream_t s, Args.
 // dtype: 0 fp32, 1 bf16.  mode: 1..4 VALU rows per forward, 5..8 MFMA with 1..4 m-tiles.
 // rw: rows per workgroup (VALU: QKV 6 or 8, residual 6, 7 or 8, others 8; MFMA: 16).
 hipError_t launch_gemm(int dtype, int mode, int epi, int rw, const GemmArgs& a, hipStream_t s);
+// Writes the tile-order copy of one projection's weights (the MFMA path's 16-row groups of
+// `a`, as weight_row maps them) to dst: a.n_groups groups x ceil(K/32) steps.
+hipError_t launch_tile_weights(int dtype, int epi, const GemmArgs& a, char* dst, hipStream_t s);
 // dtype: the KV element type, 0 fp32, 1 bf16, 2 fp8 (E4M3).
 hipError_t launch_attn(int dtype, int hd, int nt, const AttnArgs& a, dim3 grid, hipStream_t s);
 hipError_t launch_attn_merge(const AttnArgs& a, int M, int hd, hipStream_t s);

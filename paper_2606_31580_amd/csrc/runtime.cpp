@@ -131,6 +131,13 @@ struct laser_model {
   int ev_used = 0;
   int last_stop = -1;  // pool index bound to the most recent launch's end
   bool use_graphs = true;
+  // tile-order weight copies for the MFMA path (laser_model_set_tiles)
+  struct Tiles {
+    const char *qkv, *o, *gu, *down;
+  };
+  std::vector<Tiles> tiles;
+  const char* lm_tile = nullptr;
+  bool tiles_on = false;
   hipStream_t cap_stream = nullptr;  // private stream that forwards are captured on
   std::vector<GraphEntry> graphs;
   uint64_t graph_clock = 0;
@@ -198,14 +205,13 @@ static int proj_rw(int epi, int rows, int M, int cus) {
 
 static int groups_lm(const laser_model_desc& d, int M) { return ceil_div(d.vocab, M > 4 ? 16 : 8); }
 
-// Row groups per MFMA workgroup: several (so each activation fragment serves several row
-// groups) when there are still at least two workgroups per compute unit; one for the
-// narrow projections and for more than one 16-row activation tile.
+// Row groups per MFMA workgroup: two (so each activation fragment serves both) when there
+// are still at least two workgroups per compute unit; one for the narrow projections and
+// for more than one 16-row activation tile.  (Four groups measured slower: more concurrent
+// weight streams per wave.)
 static int mfma_nr(int n_groups, int M, int cus) {
   if (M <= 4 || M > 16) return 1;
-  if (n_groups / 4 >= 2 * cus) return 4;
-  if (n_groups / 2 >= 2 * cus) return 2;
-  return 1;
+  return n_groups / 2 >= 2 * cus ? 2 : 1;
 }
 
 static Layout make_layout(const laser_model_desc& d, int max_rows) {
@@ -392,6 +398,102 @@ extern "C" laser_status laser_model_finalize(laser_model* m, int max_rows, void*
   m->h_plans = hp;
   m->max_rows = max_rows;
   m->finalized = true;
+  return LASER_OK;
+}
+
+// ----------------------------------------------------------------------------- weight tiles
+
+namespace {
+// One projection's MFMA-path geometry: 16-row groups over K columns, and its tile bytes.
+struct TileProj {
+  int epi, groups, K;
+  size_t bytes(int es) const { return (size_t)groups * ((K + 31) / 32) * 1024 * (es / 2); }
+};
+TileProj tile_qkv(const laser_model_desc& d) {
+  return {EPI_QKV, proj_groups(EPI_QKV, (d.n_q_heads + 2 * d.n_kv_heads) * d.head_dim, 16), d.d_model};
+}
+TileProj tile_o(const laser_model_desc& d) { return {EPI_RESID, proj_groups(EPI_RESID, d.d_model, 16), d.n_q_heads * d.head_dim}; }
+TileProj tile_gu(const laser_model_desc& d) { return {EPI_SWIGLU, proj_groups(EPI_SWIGLU, 2 * d.d_ffn, 16), d.d_model}; }
+TileProj tile_down(const laser_model_desc& d) { return {EPI_RESID, proj_groups(EPI_RESID, d.d_model, 16), d.d_ffn}; }
+TileProj tile_lm(const laser_model_desc& d) { return {EPI_LMHEAD, groups_lm(d, 16), d.d_model}; }
+
+size_t tile_total(const laser_model* m) {
+  const laser_model_desc& d = m->desc;
+  const size_t per_layer = tile_qkv(d).bytes(m->es) + tile_o(d).bytes(m->es) + tile_gu(d).bytes(m->es) +
+                           tile_down(d).bytes(m->es);
+  return per_layer * d.n_layers + tile_lm(d).bytes(m->es);
+}
+
+void drop_graphs(laser_model* m) {
+  for (auto& g : m->graphs) (void)hipGraphExecDestroy(g.exec);
+  m->graphs.clear();
+}
+}  // namespace
+
+extern "C" laser_status laser_model_tile_bytes(const laser_model* m, size_t* bytes) {
+  if (!handle_live(m)) return laser_fail(LASER_ERR_STATE, "invalid or destroyed model");
+  if (!bytes) return laser_fail(LASER_ERR_INVALID_ARG, "bytes is NULL");
+  *bytes = tile_total(m);
+  return LASER_OK;
+}
+
+extern "C" laser_status laser_model_set_tiles(laser_model* m, void* d_buf, size_t bytes, void* stream) {
+  if (!model_of(m)) return laser_fail(LASER_ERR_STATE, "invalid or destroyed model");
+  if (!m->finalized) return laser_fail(LASER_ERR_STATE, "model not finalized");
+  if (!d_buf) {  // back to the row-major tensors
+    m->tiles_on = false;
+    drop_graphs(m);
+    return LASER_OK;
+  }
+  if (bytes < tile_total(m)) return laser_fail(LASER_ERR_INVALID_ARG, "tile buffer of %zu bytes needed", tile_total(m));
+  const laser_model_desc& d = m->desc;
+  const int dt = d.dtype == LASER_DTYPE_BF16 ? 1 : 0;
+  hipStream_t s = (hipStream_t)stream;
+  char* p = (char*)d_buf;
+  GemmArgs base{};
+  base.hq = d.n_q_heads;
+  base.hkv = d.n_kv_heads;
+  base.hd = d.head_dim;
+  base.F = d.d_ffn;
+  auto tile = [&](const TileProj& tp, GemmArgs a, int N) -> const char* {
+    a.K = tp.K;
+    a.N = N;
+    a.n_groups = tp.groups;
+    const hipError_t e = launch_tile_weights(dt, tp.epi, a, p, s);
+    if (e != hipSuccess) return nullptr;
+    const char* out = p;
+    p += tp.bytes(m->es);
+    return out;
+  };
+  std::vector<laser_model::Tiles> tiles(d.n_layers);
+  for (int li = 0; li < d.n_layers; ++li) {
+    const LayerW& W = m->layers[li];
+    GemmArgs a = base;
+    a.w0 = W.wq;
+    a.w1 = W.wk;
+    a.w2 = W.wv;
+    tiles[li].qkv = tile(tile_qkv(d), a, (d.n_q_heads + 2 * d.n_kv_heads) * d.head_dim);
+    a = base;
+    a.w0 = W.wo;
+    tiles[li].o = tile(tile_o(d), a, d.d_model);
+    a = base;
+    a.w0 = W.w_gate;
+    a.w1 = W.w_up;
+    tiles[li].gu = tile(tile_gu(d), a, 2 * d.d_ffn);
+    a = base;
+    a.w0 = W.w_down;
+    tiles[li].down = tile(tile_down(d), a, d.d_model);
+    if (!tiles[li].qkv || !tiles[li].o || !tiles[li].gu || !tiles[li].down)
+      return laser_fail(LASER_ERR_HIP, "weight tiles: %s", hipGetErrorString(hipGetLastError()));
+  }
+  GemmArgs a = base;
+  a.w0 = d.tied_embeddings ? m->embed : m->lm_head;
+  const char* lm = tile(tile_lm(d), a, d.vocab);
+  if (!lm) return laser_fail(LASER_ERR_HIP, "weight tiles: %s", hipGetErrorString(hipGetLastError()));
+  m->tiles = std::move(tiles);
+  m->lm_tile = lm;
+  m->tiles_on = true;
+  drop_graphs(m);
   return LASER_OK;
 }
 
@@ -699,13 +801,18 @@ static laser_status launch_forward(laser_model* m, laser_kv* kv, const FwdKey& k
   base.F = d.d_ffn;
 
   // rows: output rows of the projection (SwiGLU: gate and up rows together)
-  auto gemm = [&](int cls, int epi, GemmArgs a, int K, int N, int rows, int M) -> laser_status {
+  // tile: the projection's tile-order weights (used on the MFMA path when tiles are on)
+  auto gemm = [&](int cls, int epi, GemmArgs a, int K, int N, int rows, int M, const char* tile) -> laser_status {
     const int rw = proj_rw(epi, rows, M, m->cus);
     a.K = K;
     a.N = N;
     a.n_groups = proj_groups(epi, rows, rw);
     a.nr = mfma_nr(a.n_groups, M, m->cus);
     a.M = M;
+    if (M > 4 && m->tiles_on) {
+      a.wtile = tile;
+      a.tsteps = (K + 31) / 32;
+    }
     const int mode = gemm_mode(M);
     HIP_TRY(timed(m, cls, s, [&] { return launch_gemm(dt, mode, epi, rw, a, s); }));
     return LASER_OK;
@@ -742,8 +849,9 @@ static laser_status launch_forward(laser_model* m, laser_kv* kv, const FwdKey& k
     a.ldx = d.d_model;
     a.gain = W.attn_norm;
     a.layer = li;
+    const laser_model::Tiles* T = m->tiles_on ? &m->tiles[li] : nullptr;
     st = gemm(LASER_K_QKV, EPI_QKV, a, d.d_model, (d.n_q_heads + 2 * d.n_kv_heads) * hd,
-              (d.n_q_heads + 2 * d.n_kv_heads) * hd, key.M);
+              (d.n_q_heads + 2 * d.n_kv_heads) * hd, key.M, T ? T->qkv : nullptr);
     if (st != LASER_OK) return st;
 
     aa.layer = li;
@@ -758,7 +866,7 @@ static laser_status launch_forward(laser_model* m, laser_kv* kv, const FwdKey& k
     a.x = m->wsp<float>(L.o);
     a.ldx = d.n_q_heads * hd;
     a.gain = nullptr;
-    st = gemm(LASER_K_OPROJ, EPI_RESID, a, d.n_q_heads * hd, d.d_model, d.d_model, key.M);
+    st = gemm(LASER_K_OPROJ, EPI_RESID, a, d.n_q_heads * hd, d.d_model, d.d_model, key.M, T ? T->o : nullptr);
     if (st != LASER_OK) return st;
 
     a = base;
@@ -767,7 +875,7 @@ static laser_status launch_forward(laser_model* m, laser_kv* kv, const FwdKey& k
     a.x = h;
     a.ldx = d.d_model;
     a.gain = W.mlp_norm;
-    st = gemm(LASER_K_GATEUP, EPI_SWIGLU, a, d.d_model, 2 * d.d_ffn, 2 * d.d_ffn, key.M);
+    st = gemm(LASER_K_GATEUP, EPI_SWIGLU, a, d.d_model, 2 * d.d_ffn, 2 * d.d_ffn, key.M, T ? T->gu : nullptr);
     if (st != LASER_OK) return st;
 
     a = base;
@@ -775,7 +883,7 @@ static laser_status launch_forward(laser_model* m, laser_kv* kv, const FwdKey& k
     a.x = m->wsp<float>(L.act);
     a.ldx = d.d_ffn;
     a.gain = nullptr;
-    st = gemm(LASER_K_DOWN, EPI_RESID, a, d.d_ffn, d.d_model, d.d_model, key.M);
+    st = gemm(LASER_K_DOWN, EPI_RESID, a, d.d_ffn, d.d_model, d.d_model, key.M, T ? T->down : nullptr);
     if (st != LASER_OK) return st;
   }
   if (key.n_out > 0) {
@@ -791,6 +899,10 @@ static laser_status launch_forward(laser_model* m, laser_kv* kv, const FwdKey& k
     a.n_groups = groups_lm(d, key.n_out);
     a.nr = mfma_nr(a.n_groups, key.n_out, m->cus);
     a.M = key.n_out;
+    if (key.n_out > 4 && m->tiles_on) {
+      a.wtile = m->lm_tile;
+      a.tsteps = (d.d_model + 31) / 32;
+    }
     HIP_TRY(timed(m, LASER_K_LMHEAD, s, [&] {
       hipError_t e = launch_gemm(dt, gemm_mode(key.n_out), EPI_LMHEAD, key.n_out > 4 ? 16 : 8, a, s);
       if (e == hipSuccess) e = launch_lm_reduce(dp, a.lm_part, a.n_groups, key.n_out, s);

@@ -113,6 +113,8 @@ _SIGS = {
     "laser_timing_enable": (_I, [_P, _I, _I]),
     "laser_timing_read": (_I, [_P, _I, C.POINTER(C.c_double), C.POINTER(_I)]),
     "laser_model_set_graphs": (_I, [_P, _I]),
+    "laser_model_tile_bytes": (_I, [_P, C.POINTER(C.c_size_t)]),
+    "laser_model_set_tiles": (_I, [_P, _P, C.c_size_t, _P]),
     "laser_atp_bitmap": (_I, [_P, _I, _I, _P]),
     "laser_atp_match": (_I, [_P, _I, _P, _I, _P, _P]),
     "laser_simulate": (_I, [C.POINTER(laser_params), C.POINTER(laser_sim_config), _I, C.POINTER(laser_sim_request),
@@ -260,7 +262,7 @@ class Model:
     """A finalized model over device weights (dict name -> torch tensor on the GPU)."""
 
     def __init__(self, shape, weights: Dict[str, "object"], max_rows: int = 16, max_positions: int = 16640, stream=None,
-                 poison: bool = False):
+                 poison: bool = False, tiles: bool = True):
         import torch
         self.shape = shape
         self.weights = weights  # kept alive: the library borrows them
@@ -278,6 +280,21 @@ class Model:
         if poison:  # tests: NaN bytes everywhere, so any read of unwritten workspace shows
             self.workspace.fill_(0xFF)
         _call("laser_model_finalize", self.h, max_rows, self.workspace.data_ptr(), nbytes.value, _stream_ptr(stream))
+        self.tile_buf = None
+        if tiles:
+            self.set_tiles(True, stream)
+
+    def set_tiles(self, on: bool, stream=None):
+        """Matrix-core weight tiles for forwards of more than 4 rows (a second copy of the weights)."""
+        import torch
+        if on and self.tile_buf is None:
+            nb = C.c_size_t()
+            _call("laser_model_tile_bytes", self.h, C.byref(nb))
+            self.tile_buf = torch.empty(nb.value, dtype=torch.uint8, device=self.workspace.device)
+        if on:
+            _call("laser_model_set_tiles", self.h, self.tile_buf.data_ptr(), self.tile_buf.numel(), _stream_ptr(stream))
+        else:
+            _call("laser_model_set_tiles", self.h, None, 0, _stream_ptr(stream))
 
     def set_graphs(self, on: bool):
         """Replay forwards from captured HIP graphs (default) or launch kernels one by one."""
