@@ -229,19 +229,36 @@ __global__ __launch_bounds__(64 * kAttnWaves) void k_attn(AttnArgs a) {
   static_for<D>([&](auto b) {
     if (p0 + (int)b < p1) load_page(p0 + (int)b, b);
   });
-  // queries are staged while the first pages are in flight
-  for (int idx = tid; idx < NC * HD; idx += blockDim.x) {
-    const int c = idx / HD, d = idx - c * HD;
-    float v = 0.f;
-    if (c < NQ) {
-      const int row = gd.row0 + c / a.G;
-      const int head = kvh * a.G + c % a.G;
-      v = a.q[((size_t)row * a.hq + head) * HD + d];
+  // Queries are staged while the first pages are in flight: every load of a thread is
+  // issued before any is used (a loop that used each load before the next would pay one
+  // memory round trip per iteration), 4 consecutive dims per load.
+  {
+    constexpr int Q4 = NC * HD / 4 / (64 * kAttnWaves);  // float4 loads per thread
+    static_assert(Q4 * 4 * 64 * kAttnWaves == NC * HD, "query tile");
+    float4 qv[Q4];
+#pragma unroll
+    for (int i = 0; i < Q4; ++i) {
+      const int idx = 4 * (tid + i * 64 * kAttnWaves);
+      const int c = idx / HD, d = idx - c * HD;
+      qv[i] = float4{0.f, 0.f, 0.f, 0.f};
+      if (c < NQ) {
+        const int row = gd.row0 + c / a.G;
+        const int head = kvh * a.G + c % a.G;
+        qv[i] = *(const float4*)(a.q + ((size_t)row * a.hq + head) * HD + d);
+      }
     }
-    uint16_t hi, lo;
-    split_bf16(v, hi, lo);
-    s_qh[idx] = hi;
-    s_ql[idx] = lo;
+#pragma unroll
+    for (int i = 0; i < Q4; ++i) {
+      const int idx = 4 * (tid + i * 64 * kAttnWaves);
+      const float x[4] = {qv[i].x, qv[i].y, qv[i].z, qv[i].w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        uint16_t hi, lo;
+        split_bf16(x[e], hi, lo);
+        s_qh[idx + e] = hi;
+        s_ql[idx + e] = lo;
+      }
+    }
   }
   for (int c = tid; c < NC; c += blockDim.x) s_pos[c] = c < NQ ? a.plan->rows[gd.row0 + c / a.G].pos : -1;
   __syncthreads();
