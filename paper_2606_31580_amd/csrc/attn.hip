@@ -81,6 +81,31 @@ __global__ __launch_bounds__(64 * kAttnWaves) void k_attn(AttnArgs a) {
   const size_t layer_base = (size_t)a.layer * a.num_pages;
   const size_t blk_elems = (size_t)16 * HD;
 
+  // The page ids of this wave's run are read up front, together with the queries, so no
+  // page load waits behind another page's data (vector-memory counters complete in order).
+  // (Named values, not an array: an indexed array goes to scratch memory, whose accesses
+  // share the in-order counter with the page loads.)
+  const int plast = max(p1 - 1, 0);  // clamped, branch-free: the loads issue back to back
+  const int pid0 = btrow[min(p0, plast)], pid1 = btrow[min(p0 + 1, plast)];
+  const int pid2 = btrow[min(p0 + 2, plast)], pid3 = btrow[min(p0 + 3, plast)];
+  auto page_id = [&](int pg) -> int {  // pg is wave-uniform
+    const int k = pg - p0;
+    return k == 0 ? pid0 : k == 1 ? pid1 : k == 2 ? pid2 : k == 3 ? pid3 : btrow[pg];
+  };
+  constexpr int Q4 = NC * HD / 4 / (64 * kAttnWaves);  // query float4 loads per thread
+  static_assert(Q4 * 4 * 64 * kAttnWaves == NC * HD, "query tile");
+  float4 qv[Q4];
+#pragma unroll
+  for (int i = 0; i < Q4; ++i) {  // padding columns load the last real one, zeroed when staged
+    const int idx = 4 * (tid + i * 64 * kAttnWaves);
+    const int c = min(idx / HD, NQ - 1), d = idx % HD;
+    const int row = gd.row0 + c / a.G;
+    const int head = kvh * a.G + c % a.G;
+    qv[i] = *(const float4*)(a.q + ((size_t)row * a.hq + head) * HD + d);
+  }
+  static_assert(NC <= 64 * kAttnWaves, "one position per thread");
+  const int cpos_loaded = a.plan->rows[gd.row0 + min(tid, NQ - 1) / a.G].pos;  // column tid's position
+
   // Page operands are loaded D pages ahead of their use into a ring of raw buffers (bf16
   // bits; fp32 pools are split into bf16 hi/lo when used).  A decode split is usually two
   // pages, so its whole run is in flight at once.
@@ -90,7 +115,7 @@ __global__ __launch_bounds__(64 * kAttnWaves) void k_attn(AttnArgs a) {
   u32x4 vraw[D][ND];  // bf16: only the low 8 bytes are used; fp8: the low 4
   auto load_page = [&](int pg, auto bufc) {
     constexpr int buf = decltype(bufc)::value;
-    const int pid = btrow[pg];
+    const int pid = page_id(pg);
     const size_t blk = ((layer_base + pid) * a.hkv + kvh) * blk_elems;
     if (sizeof(KT) == 1) {
       const uint8_t* kb = (const uint8_t*)a.kpool + blk;
@@ -226,31 +251,17 @@ __global__ __launch_bounds__(64 * kAttnWaves) void k_attn(AttnArgs a) {
     }
   };
 
-  static_for<D>([&](auto b) {
-    if (p0 + (int)b < p1) load_page(p0 + (int)b, b);
-  });
-  // Queries are staged while the first pages are in flight: every load of a thread is
-  // issued before any is used (a loop that used each load before the next would pay one
-  // memory round trip per iteration), 4 consecutive dims per load.
+  // The first D pages load unconditionally (a run shorter than D loads its last page again,
+  // unused): a branch here would make the wait for page 1's id also wait for page 0's data.
+  static_for<D>([&](auto b) { load_page(min(p0 + (int)b, plast), b); });
+  // Queries (loaded above, with the page ids) are split into bf16 hi/lo in LDS while the
+  // first pages are in flight.
   {
-    constexpr int Q4 = NC * HD / 4 / (64 * kAttnWaves);  // float4 loads per thread
-    static_assert(Q4 * 4 * 64 * kAttnWaves == NC * HD, "query tile");
-    float4 qv[Q4];
 #pragma unroll
     for (int i = 0; i < Q4; ++i) {
       const int idx = 4 * (tid + i * 64 * kAttnWaves);
-      const int c = idx / HD, d = idx - c * HD;
-      qv[i] = float4{0.f, 0.f, 0.f, 0.f};
-      if (c < NQ) {
-        const int row = gd.row0 + c / a.G;
-        const int head = kvh * a.G + c % a.G;
-        qv[i] = *(const float4*)(a.q + ((size_t)row * a.hq + head) * HD + d);
-      }
-    }
-#pragma unroll
-    for (int i = 0; i < Q4; ++i) {
-      const int idx = 4 * (tid + i * 64 * kAttnWaves);
-      const float x[4] = {qv[i].x, qv[i].y, qv[i].z, qv[i].w};
+      const bool real = idx / HD < NQ;
+      const float x[4] = {real ? qv[i].x : 0.f, real ? qv[i].y : 0.f, real ? qv[i].z : 0.f, real ? qv[i].w : 0.f};
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         uint16_t hi, lo;
@@ -260,7 +271,7 @@ __global__ __launch_bounds__(64 * kAttnWaves) void k_attn(AttnArgs a) {
       }
     }
   }
-  for (int c = tid; c < NC; c += blockDim.x) s_pos[c] = c < NQ ? a.plan->rows[gd.row0 + c / a.G].pos : -1;
+  if (tid < NC) s_pos[tid] = tid < NQ ? cpos_loaded : -1;
   __syncthreads();
 
   if constexpr (NT == 1) {
