@@ -72,8 +72,17 @@ __device__ __forceinline__ void split_trunc2(float x0, float x1, uint32_t& hi, u
   lo = __builtin_amdgcn_perm(r1, r0, 0x07060302u);
 }
 
-__device__ __forceinline__ u32x4 ld_nt16(const void* p) { return __builtin_nontemporal_load((const u32x4*)p); }
-__device__ __forceinline__ u32x2 ld_nt8(const void* p) { return __builtin_nontemporal_load((const u32x2*)p); }
+// Loads through the global address space.  A pointer built by arithmetic, or picked among
+// several tensors, is otherwise read with flat instructions, which count against the LDS and
+// scalar-load counter as well: every later wait on that counter then covers them too.
+template <class T>
+using global_ptr = const __attribute__((address_space(1))) T*;
+template <class T>
+__device__ __forceinline__ T ld_global(const void* p) {
+  return *(global_ptr<T>)p;
+}
+__device__ __forceinline__ u32x4 ld_nt16(const void* p) { return __builtin_nontemporal_load((global_ptr<u32x4>)p); }
+__device__ __forceinline__ u32x2 ld_nt8(const void* p) { return __builtin_nontemporal_load((global_ptr<u32x2>)p); }
 
 // Cross-lane primitives of gfx950 (no LDS traffic): DPP inside 16-lane rows, and the
 // permlane swaps across rows.  permlane16_swap(a, b) leaves (a.r0, b.r0, a.r2, b.r2) and

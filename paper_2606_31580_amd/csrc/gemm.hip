@@ -150,49 +150,64 @@ __device__ __forceinline__ int transpose_index(int lane) {
 struct EpiItem {
   bool live = false;
   int m = 0, j = 0;          // activation row; pair (QKV) or row (residual) within the group
-  float v0 = 0.f, v1 = 0.f;  // QKV: bias of the pair's two dims; residual: current h
+  // QKV: bias of the pair's two dims as stored (bf16 bits or fp32 bits, decoded when
+  // applied, so no wait is forced at fetch time); residual: current h in v0
+  uint32_t b0 = 0u, b1 = 0u;
+  float v0 = 0.f;
   int pos = 0, seq = 0;      // QKV: the row's position and request
   float2 cs = {1.f, 0.f};    // QKV: cos/sin of the pair's rotation at pos
   int page = 0;              // QKV: KV page that holds pos
 };
 
-// First fetch: what depends only on the item (row descriptor, bias, current h).
+// First fetch: what depends only on the item (row descriptor, bias, current h).  Every
+// load is unconditional, on a clamped index (items past the end read item 0's inputs and
+// stay dead): a load inside a branch makes the compiler wait for all earlier loads, the
+// weight stream included, where the branches meet.
 template <class WT, int EPI, int RW>
 __device__ __forceinline__ void epi_fetch_a(const GemmArgs& a, int g, int M, int idx, EpiItem& it) {
   constexpr int P = RW / 2;
   if (EPI == EPI_QKV) {
-    if (idx >= M * P) return;
-    it.m = idx / P;
-    it.j = idx - it.m * P;
+    const bool in = idx < M * P;
+    const int ic = in ? idx : 0;
+    it.m = ic / P;
+    it.j = ic - it.m * P;
     const int gp = P * g + it.j;
-    it.live = gp < (a.hq + 2 * a.hkv) * (a.hd >> 1);
-    if (!it.live) return;
-    const QkvPair q = qkv_pair(a, gp);
-    if (q.bias != nullptr) {
-      it.v0 = ldw<WT>(q.bias, (size_t)q.hh * a.hd + q.i);
-      it.v1 = ldw<WT>(q.bias, (size_t)q.hh * a.hd + (a.hd >> 1) + q.i);
+    it.live = in && gp < (a.hq + 2 * a.hkv) * (a.hd >> 1);
+    const QkvPair q = qkv_pair(a, it.live ? gp : 0);
+    const bool has_bias = a.b0 != nullptr;  // the three biases are set together
+    const char* bias = has_bias ? (const char*)q.bias : (const char*)a.plan;  // the plan: any valid address
+    const size_t e0 = has_bias ? (size_t)q.hh * a.hd + q.i : 0, e1 = has_bias ? e0 + (a.hd >> 1) : 0;
+    if (sizeof(WT) == 2) {
+      it.b0 = ld_global<uint16_t>(bias + 2 * e0);
+      it.b1 = ld_global<uint16_t>(bias + 2 * e1);
+    } else {
+      it.b0 = ld_global<uint32_t>(bias + 4 * e0);
+      it.b1 = ld_global<uint32_t>(bias + 4 * e1);
     }
+    if (!has_bias) it.b0 = it.b1 = 0u;  // +0 in either storage type
     const RowDesc rd = a.plan->rows[it.m];
     it.pos = rd.pos;
     it.seq = rd.seq;
   } else if (EPI == EPI_RESID) {
-    if (idx >= M * RW) return;
-    it.m = idx / RW;
-    it.j = idx - it.m * RW;
+    const bool in = idx < M * RW;
+    const int ic = in ? idx : 0;
+    it.m = ic / RW;
+    it.j = ic - it.m * RW;
     const int r = RW * g + it.j;
-    it.live = r < a.N;
-    if (it.live) it.v0 = a.h[(size_t)it.m * a.N + r];
+    it.live = in && r < a.N;
+    it.v0 = a.h[(size_t)it.m * a.N + (it.live ? r : 0)];
   }
 }
 
-// Second fetch (QKV): what is addressed by the row's position (rotation, KV page).
+// Second fetch (QKV): what is addressed by the row's position (rotation, KV page), loaded
+// for every item whether or not it uses it (same reason as above).
 template <class WT, int EPI, int RW>
 __device__ __forceinline__ void epi_fetch_b(const GemmArgs& a, int g, EpiItem& it) {
-  if (EPI != EPI_QKV || !it.live) return;
+  if (EPI != EPI_QKV) return;
   constexpr int P = RW / 2;
-  const QkvPair q = qkv_pair(a, P * g + it.j);
-  if (q.isq || q.isk) it.cs = a.rope[(size_t)it.pos * (a.hd >> 1) + q.i];
-  if (!q.isq) it.page = a.bt[(size_t)it.seq * a.max_pps + (it.pos >> 4)];
+  const QkvPair q = qkv_pair(a, it.live ? P * g + it.j : 0);
+  it.cs = a.rope[(size_t)it.pos * (a.hd >> 1) + q.i];
+  it.page = a.bt[(size_t)it.seq * a.max_pps + (it.pos >> 4)];
 }
 
 // Bias, rotation and stores of one item; Y holds the group's outputs [m][RW].
@@ -203,7 +218,9 @@ __device__ __forceinline__ void epi_apply(const GemmArgs& a, int g, const EpiIte
   if (EPI == EPI_QKV) {
     const QkvPair q = qkv_pair(a, P * g + it.j);
     const int dlo = q.i, dhi = (a.hd >> 1) + q.i;
-    float ylo = Y[it.m * RW + it.j] + it.v0, yhi = Y[it.m * RW + P + it.j] + it.v1;
+    const float bias0 = sizeof(WT) == 2 ? bf2f((uint16_t)it.b0) : __uint_as_float(it.b0);
+    const float bias1 = sizeof(WT) == 2 ? bf2f((uint16_t)it.b1) : __uint_as_float(it.b1);
+    float ylo = Y[it.m * RW + it.j] + bias0, yhi = Y[it.m * RW + P + it.j] + bias1;
     if (q.isq || q.isk) {
       const float rlo = ylo * it.cs.x - yhi * it.cs.y;
       const float rhi = yhi * it.cs.x + ylo * it.cs.y;
@@ -332,7 +349,7 @@ __global__ __launch_bounds__(kGemvMaxThreads) void k_gemv(GemmArgs a) {
   __shared__ float s_scale[M];
   const int tid = threadIdx.x, w = tid >> 6, l = tid & 63;
   const int g = blockIdx.x;
-  const bool norm = a.gain != nullptr;
+  constexpr bool norm = EPI != EPI_RESID;  // every other epilogue follows an RMSNorm (gain checked at launch)
   const int nch = a.K / CH;
   const char* wp[RW];
 #pragma unroll
@@ -348,72 +365,76 @@ __global__ __launch_bounds__(kGemvMaxThreads) void k_gemv(GemmArgs a) {
     for (int r = 0; r < RW; ++r) acc[r][m] = 0.f;
   }
   constexpr bool kPre = EPI == EPI_QKV || EPI == EPI_RESID;  // at most one item per thread here
+  // The epilogue's first inputs load ahead of the weight stream, the position-addressed ones
+  // right behind its first loads; nothing waits for them until the epilogue.
   EpiItem item;
   if (kPre) epi_fetch_a<WT, EPI, RW>(a, g, M, tid, item);
-  bool need_b = kPre && item.live;
-  for (int c0 = tid; c0 < nch; c0 += U * T) {
+  // One pass over chunks c0 and c0 + T of every row.  All loads come first and none is
+  // conditional (a chunk past the end re-reads the last one and leaves the sums as they
+  // are), so the waits before each use count exactly; the first pass is peeled so that the
+  // weight stream never waits behind the epilogue's loads at a loop header.
+  auto pass = [&](int c0, auto first) {
     u32x4 wv[U][RW];
     float4 xv[U][M][CH / 4];
     u32x4 gv[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      const int c = c0 + u * T;
-      if (c < nch) {
+      const int c = min(c0 + u * T, nch - 1);
 #pragma unroll
-        for (int r = 0; r < RW; ++r) wv[u][r] = ld_nt16(wp[r] + (size_t)c * 16);
+      for (int r = 0; r < RW; ++r) wv[u][r] = ld_nt16(wp[r] + (size_t)c * 16);
 #pragma unroll
-        for (int m = 0; m < M; ++m)
+      for (int m = 0; m < M; ++m)
 #pragma unroll
-          for (int e4 = 0; e4 < CH / 4; ++e4) xv[u][m][e4] = *(const float4*)(xr[m] + c * CH + 4 * e4);
-        if (norm) gv[u] = *(const u32x4*)((const char*)a.gain + (size_t)c * 16);
-      }
+        for (int e4 = 0; e4 < CH / 4; ++e4) xv[u][m][e4] = *(const float4*)(xr[m] + c * CH + 4 * e4);
+      if (norm) gv[u] = *(const u32x4*)((const char*)a.gain + (size_t)c * 16);
     }
-    if (need_b) {  // issued behind the first weight loads
-      epi_fetch_b<WT, EPI, RW>(a, g, item);
-      need_b = false;
-    }
+    // every load above is issued before any use (the scheduler would otherwise trade loads
+    // in flight for registers)
+    __builtin_amdgcn_sched_barrier(0);
+    if constexpr (decltype(first)::value && kPre) epi_fetch_b<WT, EPI, RW>(a, g, item);
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      const int c = c0 + u * T;
-      if (c < nch) {
-        float gf[CH];
-        if (norm) unpack16<WT>(gv[u], gf);
+      const bool valid = c0 + u * T < nch;
+      float gf[CH];
+      if (norm) unpack16<WT>(gv[u], gf);
 #pragma unroll
-        for (int m = 0; m < M; ++m) {
-          float xe[CH];
+      for (int m = 0; m < M; ++m) {
+        float xe[CH];
 #pragma unroll
-          for (int e4 = 0; e4 < CH / 4; ++e4) {
-            xe[4 * e4 + 0] = xv[u][m][e4].x;
-            xe[4 * e4 + 1] = xv[u][m][e4].y;
-            xe[4 * e4 + 2] = xv[u][m][e4].z;
-            xe[4 * e4 + 3] = xv[u][m][e4].w;
+        for (int e4 = 0; e4 < CH / 4; ++e4) {
+          xe[4 * e4 + 0] = xv[u][m][e4].x;
+          xe[4 * e4 + 1] = xv[u][m][e4].y;
+          xe[4 * e4 + 2] = xv[u][m][e4].z;
+          xe[4 * e4 + 3] = xv[u][m][e4].w;
+        }
+        if (norm) {
+          float q2 = sq[m];
+#pragma unroll
+          for (int e = 0; e < CH; ++e) {
+            q2 = fmaf(xe[e], xe[e], q2);
+            xe[e] *= gf[e];
           }
-          if (norm) {
+          sq[m] = valid ? q2 : sq[m];
+        }
 #pragma unroll
-            for (int e = 0; e < CH; ++e) {
-              sq[m] = fmaf(xe[e], xe[e], sq[m]);
-              xe[e] *= gf[e];
+        for (int r = 0; r < RW; ++r) {
+          float s = acc[r][m];
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            if (sizeof(WT) == 2) {
+              s = fmaf(__uint_as_float(wv[u][r][q] << 16), xe[2 * q], s);
+              s = fmaf(__uint_as_float(wv[u][r][q] & 0xffff0000u), xe[2 * q + 1], s);
+            } else {
+              s = fmaf(__uint_as_float(wv[u][r][q]), xe[q], s);
             }
           }
-#pragma unroll
-          for (int r = 0; r < RW; ++r) {
-            float s = acc[r][m];
-#pragma unroll
-            for (int q = 0; q < 4; ++q) {
-              if (sizeof(WT) == 2) {
-                s = fmaf(__uint_as_float(wv[u][r][q] << 16), xe[2 * q], s);
-                s = fmaf(__uint_as_float(wv[u][r][q] & 0xffff0000u), xe[2 * q + 1], s);
-              } else {
-                s = fmaf(__uint_as_float(wv[u][r][q]), xe[q], s);
-              }
-            }
-            acc[r][m] = s;
-          }
+          acc[r][m] = valid ? s : acc[r][m];
         }
       }
     }
-  }
-  if (need_b) epi_fetch_b<WT, EPI, RW>(a, g, item);
+  };
+  pass(tid, std::true_type{});
+  for (int c0 = tid + U * T; c0 < nch; c0 += U * T) pass(c0, std::false_type{});
   // wave totals, then the waves in fixed order
 #pragma unroll
   for (int m = 0; m < M; ++m) {
@@ -745,6 +766,7 @@ static hipError_t launch_mode(int mode, int epi, int rw, const GemmArgs& a, hipS
 }
 
 hipError_t launch_gemm(int dtype, int mode, int epi, int rw, const GemmArgs& a, hipStream_t s) {
+  if ((a.gain != nullptr) != (epi != EPI_RESID)) return hipErrorInvalidValue;  // only the residual GEMMs skip the norm
   if (dtype == 1) return launch_mode<bf16_t>(mode, epi, rw, a, s);
   return launch_mode<float>(mode, epi, rw, a, s);
 }
