@@ -95,7 +95,8 @@ def main():
     if rows > 64:
         log(f"{rows} rows per forward exceed the 64-row maximum; use fewer probe rows")
         sys.exit(2)
-    model = L.Model(shape, weights, max_rows=rows, max_positions=max_pos, tiles=not args.no_tiles)
+    # the workspace takes the full 64 rows so that prompt prefills run in 64-token chunks
+    model = L.Model(shape, weights, max_rows=64, max_positions=max_pos, tiles=not args.no_tiles)
     pps = max_pos // PAGE + 1
     num_pages = sum((n + 2 * total_steps + S + T) // PAGE + 2 for n in lens) + B * ((S + T) // PAGE + 3) + 8
     num_pages += (COST_CTX + 512) // PAGE + 4  # the cost-model pass (a shorter request in a fork slot)
