@@ -481,7 +481,7 @@ __global__ __launch_bounds__(64 * kMfmaMaxWaves) void k_gemm_mfma(GemmArgs a) {
   constexpr int NLD = (int)sizeof(WT) / 2;  // 16-byte loads per step (bf16: 1, fp32: 2)
   // steps kept in flight per wave
   constexpr int U = MT == 1 ? (NR == 1 ? 6 : 4) : (MT == 2 ? 4 : 2);
-  constexpr int WMAX = NR == 1 ? kMfmaMaxWaves : 4;  // several groups: always 4 waves
+  constexpr int WMAX = kMfmaMaxWaves;
   constexpr int YN = 16 * MT * RW;                   // outputs of one group
   const int W = blockDim.x >> 6;                     // waves splitting K
   __shared__ float s_red[WMAX][NR * YN];
@@ -741,8 +741,8 @@ static hipError_t launch_epi(int epi, int rw, const GemmArgs& a, hipStream_t s) 
     const int nr = a.nr < 1 ? 1 : a.nr;
     if (nr != 1 && (MT > 1 || nr != 2)) return hipErrorInvalidValue;
     const dim3 mgrid((a.n_groups + nr - 1) / nr);
-    // few row groups (the O, down and QKV projections): 8 waves split K more finely
-    if (nr == 1 && a.n_groups < 512) block = dim3(64 * kMfmaMaxWaves);
+    // few workgroups (the O, down and QKV projections): 8 waves split K more finely
+    if (mgrid.x < 512) block = dim3(64 * kMfmaMaxWaves);
     if constexpr (MT == 1) {
       if (nr == 2) return launch_mfma<WT, MT, 2>(epi, mgrid, block, a, s);
     }

@@ -209,9 +209,17 @@ static int groups_lm(const laser_model_desc& d, int M) { return ceil_div(d.vocab
 // are still at least two workgroups per compute unit; one for the narrow projections and
 // for more than one 16-row activation tile.  (Four groups measured slower: more concurrent
 // weight streams per wave.)
-static int mfma_nr(int n_groups, int M, int cus) {
+// Row groups per workgroup on the MFMA path with one 16-row activation tile (M 5..16).  A
+// workgroup reads its groups' weights and the activation rows over all of K, so two groups
+// per workgroup halve the activation reads per weight byte but also halve the workgroups.
+// The choice minimises the bytes read by the busiest compute unit (workgroups are dealt
+// round-robin): two groups for gate/up and the LM head, and for QKV at the 7B and 8B shapes
+// (288 or 384 groups: 1.2-1.5 workgroups per CU with one group each).
+static int mfma_nr(int n_groups, int M, int K, int es, int cus) {
   if (M <= 4 || M > 16) return 1;
-  return n_groups / 2 >= 2 * cus ? 2 : 1;
+  const double w = 16.0 * K * es, act = 4.0 * M * K;
+  auto cost = [&](int nr) { return (double)ceil_div(ceil_div(n_groups, nr), cus) * (nr * w + act); };
+  return cost(2) < cost(1) ? 2 : 1;
 }
 
 static Layout make_layout(const laser_model_desc& d, int max_rows) {
@@ -807,7 +815,7 @@ static laser_status launch_forward(laser_model* m, laser_kv* kv, const FwdKey& k
     a.K = K;
     a.N = N;
     a.n_groups = proj_groups(epi, rows, rw);
-    a.nr = mfma_nr(a.n_groups, M, m->cus);
+    a.nr = mfma_nr(a.n_groups, M, K, (int)m->es, m->cus);
     a.M = M;
     if (M > 4 && m->tiles_on) {
       a.wtile = tile;
@@ -897,7 +905,7 @@ static laser_status launch_forward(laser_model* m, laser_kv* kv, const FwdKey& k
     a.K = d.d_model;
     a.N = d.vocab;
     a.n_groups = groups_lm(d, key.n_out);
-    a.nr = mfma_nr(a.n_groups, key.n_out, m->cus);
+    a.nr = mfma_nr(a.n_groups, key.n_out, d.d_model, (int)m->es, m->cus);
     a.M = key.n_out;
     if (key.n_out > 4 && m->tiles_on) {
       a.wtile = m->lm_tile;
