@@ -73,6 +73,13 @@ constexpr int kMaxT = 16;   // trial tokens per probe
 #define LASER_ATTN_TARGET_WAVES 2048
 #endif
 constexpr int kTargetAttnWaves = LASER_ATTN_TARGET_WAVES;  // attention waves a forward aims for
+// A wave walks its pages with two in flight, so a long run is a chain of memory round trips:
+// past the wave target, more waves of at most 4 pages beat longer runs (batch 8 at 68k
+// positions: attention + merge 78 -> 61 us per layer; 2 pages: 68 us, 8 pages: 73 us).
+#ifndef LASER_ATTN_MAX_PPS
+#define LASER_ATTN_MAX_PPS 4
+#endif
+constexpr int kMaxPagesPerWave = LASER_ATTN_MAX_PPS;
 
 struct Layout {
   size_t rope, h, q, o, act, lm_part, attn_part, attn_ml, plans, probe_p, tok_buf, p_buf, total;
@@ -702,7 +709,8 @@ static void plan_groups(const laser_model* m, Plan& p) {
     units += (long long)g.npages * d.n_kv_heads * ceil_div(ceil_div(g.nrows * G, 16), 2);
     r = e;
   }
-  const int base = std::max(1, (int)((units + kTargetAttnWaves - 1) / kTargetAttnWaves));
+  const int base =
+      std::min(kMaxPagesPerWave, std::max(1, (int)((units + kTargetAttnWaves - 1) / kTargetAttnWaves)));
   for (int i = 0; i < p.n_groups; ++i) {
     GroupDesc& g = p.groups[i];
     g.pps = std::max(base, ceil_div(g.npages, kAttnMaxWG * kAttnWaves));
