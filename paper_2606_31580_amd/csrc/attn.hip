@@ -520,10 +520,7 @@ __global__ __launch_bounds__(64 * kMergeWaves) void k_attn_merge(AttnArgs a, int
     o0[i] = a.part[sb * hd + l];
     o1[i] = (l + 64 < hd) ? a.part[sb * hd + l + 64] : 0.f;
   }
-  const Plan* plan = a.plan;
-  int z = 0;
-  while (z + 1 < plan->n_groups && plan->groups[z + 1].row0 <= row) ++z;
-  const int nwg = plan->groups[z].nwg;
+  const int nwg = a.plan->groups[a.plan->row_group[row]].nwg;
   if (nwg <= 1) return;  // written directly by the attention kernel
 #pragma unroll
   for (int i = 0; i < PER; ++i)

@@ -49,6 +49,7 @@ struct Plan {
   PlanIO io;
   RowDesc rows[kMaxRows];
   GroupDesc groups[kMaxRows];
+  int row_group[kMaxRows];  // group of each row
   OutDesc outs[kMaxRows];
   BtUpdate bt[kMaxBt];
 };

@@ -699,6 +699,7 @@ static void plan_groups(const laser_model* m, Plan& p) {
     while (e < p.M && p.rows[e].seq == p.rows[r].seq && e - r < cap) ++e;
     int maxpos = 0;
     for (int q = r; q < e; ++q) maxpos = std::max(maxpos, p.rows[q].pos);
+    for (int q = r; q < e; ++q) p.row_group[q] = p.n_groups;
     GroupDesc& g = p.groups[p.n_groups++];
     g.seq = p.rows[r].seq;
     g.row0 = r;
