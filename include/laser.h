@@ -276,8 +276,8 @@ laser_status laser_workspace_size(const laser_model* m, int max_rows, size_t* by
 laser_status laser_model_finalize(laser_model* m, int max_rows, void* d_workspace, size_t bytes, void* stream);
 laser_status laser_model_destroy(laser_model* m);
 
-/* Matrix-core weight tiles (optional).  Forwards of more than 4 rows (probe chunks, batches
- * of 5 or more, prompt prefill) run the projections on the matrix cores, whose operand takes
+/* Matrix-core weight tiles (optional).  Forwards of more than 2 rows (probe chunks, batches
+ * of 3 or more, prompt prefill) run the projections on the matrix cores, whose operand takes
  * each 16-row group of a weight matrix as 64 lanes x 16 bytes per 32-column step: from a
  * row-major tensor that is 64 bytes of each of 16 rows per load instruction.  With tiles set,
  * those forwards read a copy of every projection and LM-head weight kept in that order
@@ -288,7 +288,7 @@ laser_status laser_model_destroy(laser_model* m);
  * the projection and LM-head weights); laser_model_set_tiles fills the caller's buffer on
  * `stream` from the model's tensors (after laser_model_finalize; the tensors must not change
  * afterwards) and switches the MFMA path to it; d_buf = NULL switches back to the row-major
- * tensors.  The buffer must stay allocated while tiles are on.  Forwards with at most 4 rows
+ * tensors.  The buffer must stay allocated while tiles are on.  Forwards with at most 2 rows
  * always read the row-major tensors. */
 laser_status laser_model_tile_bytes(const laser_model* m, size_t* bytes);
 laser_status laser_model_set_tiles(laser_model* m, void* d_buf, size_t bytes, void* stream);

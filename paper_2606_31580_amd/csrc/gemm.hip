@@ -13,12 +13,12 @@
 // epilogue stays inside the workgroup: the four waves split K and are reduced through LDS,
 // with no synchronisation between workgroups and results that do not depend on scheduling.
 // Main loops:
-//   M <= 4  (decode)      VALU: each thread streams 16-byte non-temporal loads of the 8
-//                         rows, two chunks at a time (a wave instruction reads 1 KB
-//                         contiguous of one row).
-//   M > 4   (probe chunk) MFMA 16x16x32 bf16: weights are the B operand, activations the
-//                         A operand split into bf16 hi + lo so the product keeps ~16
-//                         significand bits of fp32 activations; fp32 weights are split too.
+//   VALU (decode: 1-4 rows; the runtime uses it up to 2): each thread streams 16-byte
+//       non-temporal loads of the group's rows, two chunks at a time (a wave instruction
+//       reads 1 KB contiguous of one row).
+//   MFMA (more rows: batches, probe chunks, prefill) 16x16x32 bf16: weights are the B
+//       operand, activations the A operand split into bf16 hi + lo so the product keeps
+//       ~16 significand bits of fp32 activations; fp32 weights are split too.
 #include <type_traits>
 
 #include "device_common.hpp"

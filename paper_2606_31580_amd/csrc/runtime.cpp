@@ -181,18 +181,27 @@ namespace {
 static int ceil_div(int a, int b) { return (a + b - 1) / b; }
 static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
-static int gemm_mode(int M) { return M <= 4 ? M : 4 + ceil_div(M, 16); }
+// Projections of up to this many rows run on the VALU path, larger ones on the matrix cores.
+// Measured at the 7B shape: at 2 rows the VALU path is faster (riding-probe latency 13.9 vs
+// 14.7 ms); at 4 rows the matrix cores are (batch-4 decode step 3.57 vs 4.17 ms: gate/up
+// 47.1 vs 58.5 us, LM head 179 vs 295 us).
+#ifndef LASER_VALU_MAX_ROWS
+#define LASER_VALU_MAX_ROWS 2
+#endif
+constexpr int kValuMaxRows = LASER_VALU_MAX_ROWS;
+static_assert(kValuMaxRows >= 1 && kValuMaxRows <= 4, "VALU kernels exist for 1-4 rows");
+static int gemm_mode(int M) { return M <= kValuMaxRows ? M : 4 + ceil_div(M, 16); }
 
 // Workgroups of a projection with `rows` output rows (SwiGLU: gate + up rows) at rw rows each.
 static int proj_groups(int epi, int rows, int rw) {
   return epi == EPI_SWIGLU ? ceil_div(rows / 2, rw / 2) : ceil_div(rows, rw);
 }
 
-// Rows per workgroup: 16 on the MFMA path (M > 4).  On the VALU path the candidate that
+// Rows per workgroup: 16 on the MFMA path (M > kValuMaxRows).  On the VALU path the candidate that
 // puts the fewest rows on the busiest compute unit (workgroups dealt round-robin over
 // `cus`), larger groups first on ties; QKV groups must tile the rotary pairs exactly.
 static int proj_rw(int epi, int rows, int M, int cus) {
-  if (M > 4) return rows_per_group(epi, true);
+  if (M > kValuMaxRows) return rows_per_group(epi, true);
   static const int kQkv[] = {8, 6}, kResid[] = {8, 7, 6}, kOther[] = {8};
   const int* cand = epi == EPI_QKV ? kQkv : (epi == EPI_RESID ? kResid : kOther);
   const int nc = epi == EPI_QKV ? 2 : (epi == EPI_RESID ? 3 : 1);
@@ -210,20 +219,20 @@ static int proj_rw(int epi, int rows, int M, int cus) {
   return best;
 }
 
-static int groups_lm(const laser_model_desc& d, int M) { return ceil_div(d.vocab, M > 4 ? 16 : 8); }
+static int groups_lm(const laser_model_desc& d, int M) { return ceil_div(d.vocab, M > kValuMaxRows ? 16 : 8); }
 
 // Row groups per MFMA workgroup: two (so each activation fragment serves both) when there
 // are still at least two workgroups per compute unit; one for the narrow projections and
 // for more than one 16-row activation tile.  (Four groups measured slower: more concurrent
 // weight streams per wave.)
-// Row groups per workgroup on the MFMA path with one 16-row activation tile (M 5..16).  A
+// Row groups per workgroup on the MFMA path with one 16-row activation tile (M up to 16).  A
 // workgroup reads its groups' weights and the activation rows over all of K, so two groups
 // per workgroup halve the activation reads per weight byte but also halve the workgroups.
 // The choice minimises the bytes read by the busiest compute unit (workgroups are dealt
 // round-robin): two groups for gate/up and the LM head, and for QKV at the 7B and 8B shapes
 // (288 or 384 groups: 1.2-1.5 workgroups per CU with one group each).
 static int mfma_nr(int n_groups, int M, int K, int es, int cus) {
-  if (M <= 4 || M > 16) return 1;
+  if (M <= kValuMaxRows || M > 16) return 1;
   const double w = 16.0 * K * es, act = 4.0 * M * K;
   auto cost = [&](int nr) { return (double)ceil_div(ceil_div(n_groups, nr), cus) * (nr * w + act); };
   return cost(2) < cost(1) ? 2 : 1;
@@ -826,7 +835,7 @@ static laser_status launch_forward(laser_model* m, laser_kv* kv, const FwdKey& k
     a.n_groups = proj_groups(epi, rows, rw);
     a.nr = mfma_nr(a.n_groups, M, K, (int)m->es, m->cus);
     a.M = M;
-    if (M > 4 && m->tiles_on) {
+    if (M > kValuMaxRows && m->tiles_on) {
       a.wtile = tile;
       a.tsteps = (K + 31) / 32;
     }
@@ -916,12 +925,12 @@ static laser_status launch_forward(laser_model* m, laser_kv* kv, const FwdKey& k
     a.n_groups = groups_lm(d, key.n_out);
     a.nr = mfma_nr(a.n_groups, key.n_out, d.d_model, (int)m->es, m->cus);
     a.M = key.n_out;
-    if (key.n_out > 4 && m->tiles_on) {
+    if (key.n_out > kValuMaxRows && m->tiles_on) {
       a.wtile = m->lm_tile;
       a.tsteps = (d.d_model + 31) / 32;
     }
     HIP_TRY(timed(m, LASER_K_LMHEAD, s, [&] {
-      hipError_t e = launch_gemm(dt, gemm_mode(key.n_out), EPI_LMHEAD, key.n_out > 4 ? 16 : 8, a, s);
+      hipError_t e = launch_gemm(dt, gemm_mode(key.n_out), EPI_LMHEAD, key.n_out > kValuMaxRows ? 16 : 8, a, s);
       if (e == hipSuccess) e = launch_lm_reduce(dp, a.lm_part, a.n_groups, key.n_out, s);
       return e;
     }));
