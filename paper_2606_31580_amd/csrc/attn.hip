@@ -44,13 +44,17 @@ __global__ __launch_bounds__(64 * kAttnWaves) void k_attn(AttnArgs a) {
   // in two rounds through two slots that reuse the query space.
   constexpr int NSLOT = NT == 1 ? 3 : 2;
   constexpr bool ALIAS = NT != 1;
-  constexpr int QBYTES = NC * HD * 2 * 2;
-  constexpr int SBYTES = NSLOT * NC * HD * 4;
+  // Rows are padded by 16 bytes, so the 16 columns a wave reads at once (row stride) fall in
+  // 16 different bank groups instead of one.
+  constexpr int QS = HD + 8;  // query row stride (bf16 elements)
+  constexpr int OS = HD + 4;  // merge-slot row stride (floats)
+  constexpr int QBYTES = NC * QS * 2 * 2;
+  constexpr int SBYTES = NSLOT * NC * OS * 4;
   constexpr int LBYTES = ALIAS ? (QBYTES > SBYTES ? QBYTES : SBYTES) : QBYTES + SBYTES;
   __shared__ __align__(16) char s_raw[LBYTES];
   uint16_t* s_qh = (uint16_t*)s_raw;
-  uint16_t* s_ql = s_qh + NC * HD;
-  float* const s_of = (float*)(s_raw + (ALIAS ? 0 : QBYTES));  // slot k at s_of + k * NC * HD
+  uint16_t* s_ql = s_qh + NC * QS;
+  float* const s_of = (float*)(s_raw + (ALIAS ? 0 : QBYTES));  // slot k at s_of + k * NC * OS
   __shared__ int s_pos[NC];
   __shared__ float s_m[NSLOT][NC];
   __shared__ float s_l[NSLOT][NC];
@@ -266,8 +270,8 @@ __global__ __launch_bounds__(64 * kAttnWaves) void k_attn(AttnArgs a) {
       for (int e = 0; e < 4; ++e) {
         uint16_t hi, lo;
         split_bf16(x[e], hi, lo);
-        s_qh[idx + e] = hi;
-        s_ql[idx + e] = lo;
+        s_qh[(idx / HD) * QS + idx % HD + e] = hi;
+        s_ql[(idx / HD) * QS + idx % HD + e] = lo;
       }
     }
   }
@@ -280,8 +284,8 @@ __global__ __launch_bounds__(64 * kAttnWaves) void k_attn(AttnArgs a) {
     bf16x8 qh[NS], ql[NS];
 #pragma unroll
     for (int s = 0; s < NS; ++s) {
-      qh[s] = *(const bf16x8*)(s_qh + lc * HD + 32 * s + 8 * lg);
-      ql[s] = *(const bf16x8*)(s_ql + lc * HD + 32 * s + 8 * lg);
+      qh[s] = *(const bf16x8*)(s_qh + lc * QS + 32 * s + 8 * lg);
+      ql[s] = *(const bf16x8*)(s_ql + lc * QS + 32 * s + 8 * lg);
     }
     const int cpos = s_pos[lc];
     auto pair = [&](int pgA, auto ca, auto cbB) {
@@ -342,7 +346,7 @@ __global__ __launch_bounds__(64 * kAttnWaves) void k_attn(AttnArgs a) {
     // ---- one-round merge: waves 1-3 publish, wave 0 absorbs in order and stores
     if (w > 0) {
 #pragma unroll
-      for (int dt = 0; dt < ND; ++dt) *(f32x4*)(s_of + (w - 1) * NC * HD + lc * HD + 16 * dt + 4 * lg) = o[0][dt];
+      for (int dt = 0; dt < ND; ++dt) *(f32x4*)(s_of + (w - 1) * NC * OS + lc * OS + 16 * dt + 4 * lg) = o[0][dt];
       if (lg == 0) {
         s_m[w - 1][lc] = m_run[0];
         s_l[w - 1][lc] = l_run[0];
@@ -360,7 +364,7 @@ __global__ __launch_bounds__(64 * kAttnWaves) void k_attn(AttnArgs a) {
       m_run[0] = mm;
 #pragma unroll
       for (int dt = 0; dt < ND; ++dt) {
-        const f32x4 x = *(const f32x4*)(s_of + u * NC * HD + lc * HD + 16 * dt + 4 * lg);
+        const f32x4 x = *(const f32x4*)(s_of + u * NC * OS + lc * OS + 16 * dt + 4 * lg);
         o[0][dt] = o[0][dt] * ca + x * cb2;
       }
     }
@@ -389,7 +393,7 @@ __global__ __launch_bounds__(64 * kAttnWaves) void k_attn(AttnArgs a) {
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt) {
         if (nt * 16 >= NQ) break;
-        const int qrow = (nt * 16 + lc) * HD;
+        const int qrow = (nt * 16 + lc) * QS;
         bf16x8 qh[NS], ql[NS];
 #pragma unroll
         for (int s = 0; s < NS; ++s) {
@@ -441,7 +445,7 @@ __global__ __launch_bounds__(64 * kAttnWaves) void k_attn(AttnArgs a) {
       for (int nt = 0; nt < NT; ++nt) {
         const int c = nt * 16 + lc;
 #pragma unroll
-        for (int dt = 0; dt < ND; ++dt) *(f32x4*)(s_of + slot * NC * HD + c * HD + 16 * dt + 4 * lg) = o[nt][dt];
+        for (int dt = 0; dt < ND; ++dt) *(f32x4*)(s_of + slot * NC * OS + c * OS + 16 * dt + 4 * lg) = o[nt][dt];
         if (lg == 0) {
           s_m[slot][c] = m_run[nt];
           s_l[slot][c] = l_run[nt];
@@ -460,7 +464,7 @@ __global__ __launch_bounds__(64 * kAttnWaves) void k_attn(AttnArgs a) {
         m_run[nt] = mm;
 #pragma unroll
         for (int dt = 0; dt < ND; ++dt)
-          o[nt][dt] = o[nt][dt] * ca + *(const f32x4*)(s_of + slot * NC * HD + c * HD + 16 * dt + 4 * lg) * cb2;
+          o[nt][dt] = o[nt][dt] * ca + *(const f32x4*)(s_of + slot * NC * OS + c * OS + 16 * dt + 4 * lg) * cb2;
       }
     };
     __syncthreads();  // every wave is done with Q before the slots overwrite it
@@ -481,12 +485,13 @@ __global__ __launch_bounds__(64 * kAttnWaves) void k_attn(AttnArgs a) {
       for (int idx = tid; idx < NQ * HD; idx += blockDim.x) {
         const int c = idx / HD, d = idx - c * HD;
         const int row = gd.row0 + c / a.G, head = kvh * a.G + c % a.G;
-        a.o[((size_t)row * a.hq + head) * HD + d] = s_of[1 * NC * HD + c * HD + d] / s_l[1][c];
+        a.o[((size_t)row * a.hq + head) * HD + d] = s_of[1 * NC * OS + c * OS + d] / s_l[1][c];
       }
       return;
     }
     const size_t slot_base = ((size_t)kvh * kAttnMaxWG + wg) * ncols + (size_t)gd.row0 * a.G;
-    for (int idx = tid; idx < NQ * HD; idx += blockDim.x) a.part[slot_base * HD + idx] = s_of[1 * NC * HD + idx];
+    for (int idx = tid; idx < NQ * HD; idx += blockDim.x)
+      a.part[slot_base * HD + idx] = s_of[1 * NC * OS + (idx / HD) * OS + idx % HD];
     for (int c = tid; c < NQ; c += blockDim.x) {
       a.ml[(slot_base + c) * 2 + 0] = s_m[1][c];
       a.ml[(slot_base + c) * 2 + 1] = s_l[1][c];
