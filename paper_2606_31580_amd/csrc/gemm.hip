@@ -475,13 +475,26 @@ __global__ __launch_bounds__(kGemvMaxThreads) void k_gemv(GemmArgs a) {
 // 32-column steps (so a wave reads 256 contiguous bytes of every row it streams).  Each
 // activation fragment is split into bf16 hi/lo once per step and used for all NR groups,
 // which is what keeps the per-step load and VALU work small when M is small.
+// Row groups per workgroup allowed with MT 16-row activation tiles: four only for 2-3
+// tiles (with 4 tiles their reduction slots would leave one workgroup per CU).
+template <int MT>
+constexpr bool mfma_nr_ok(int nr) {
+  return nr == 1 || nr == 2 || (nr == 4 && MT >= 2 && MT <= 3);
+}
+// Waves of an MFMA workgroup at most: several row groups over several tiles keep 4 waves, so
+// that the per-wave reduction slots fit in LDS.
+template <int MT, int NR>
+constexpr int mfma_wmax() {
+  return NR >= 2 && MT >= 2 ? 4 : kMfmaMaxWaves;
+}
+
 template <class WT, int MT, int EPI, int NR>
 __global__ __launch_bounds__(64 * kMfmaMaxWaves) void k_gemm_mfma(GemmArgs a) {
   constexpr int RW = rows_per_group(EPI, true);
   constexpr int NLD = (int)sizeof(WT) / 2;  // 16-byte loads per step (bf16: 1, fp32: 2)
   // steps kept in flight per wave
-  constexpr int U = MT == 1 ? (NR == 1 ? 6 : 4) : (MT == 2 ? 4 : 2);
-  constexpr int WMAX = kMfmaMaxWaves;
+  constexpr int U = MT == 1 ? (NR == 1 ? 6 : 4) : (MT == 2 && NR <= 2 ? 4 : 2);
+  constexpr int WMAX = mfma_wmax<MT, NR>();
   constexpr int YN = 16 * MT * RW;                   // outputs of one group
   const int W = blockDim.x >> 6;                     // waves splitting K
   __shared__ float s_red[WMAX][NR * YN];
@@ -739,14 +752,16 @@ static hipError_t launch_epi(int epi, int rw, const GemmArgs& a, hipStream_t s) 
     constexpr int MT = MODE - 4;
     if (rw != rows_per_group(epi, true)) return hipErrorInvalidValue;
     const int nr = a.nr < 1 ? 1 : a.nr;
-    if (nr != 1 && (MT > 1 || nr != 2)) return hipErrorInvalidValue;
+    if (!mfma_nr_ok<MT>(nr)) return hipErrorInvalidValue;
     const dim3 mgrid((a.n_groups + nr - 1) / nr);
     // few workgroups (the O, down and QKV projections): 8 waves split K more finely
-    if (mgrid.x < 512) block = dim3(64 * kMfmaMaxWaves);
-    if constexpr (MT == 1) {
-      if (nr == 2) return launch_mfma<WT, MT, 2>(epi, mgrid, block, a, s);
+    const int waves = mgrid.x < 512 ? kMfmaMaxWaves : kGemmThreads / 64;
+    auto blk = [&](int wmax) { return dim3(64 * (waves < wmax ? waves : wmax)); };
+    if (nr == 2) return launch_mfma<WT, MT, 2>(epi, mgrid, blk(mfma_wmax<MT, 2>()), a, s);
+    if constexpr (mfma_nr_ok<MT>(4)) {
+      if (nr == 4) return launch_mfma<WT, MT, 4>(epi, mgrid, blk(mfma_wmax<MT, 4>()), a, s);
     }
-    return launch_mfma<WT, MT, 1>(epi, mgrid, block, a, s);
+    return launch_mfma<WT, MT, 1>(epi, mgrid, blk(mfma_wmax<MT, 1>()), a, s);
   }
 }
 

@@ -225,17 +225,24 @@ static int groups_lm(const laser_model_desc& d, int M) { return ceil_div(d.vocab
 // are still at least two workgroups per compute unit; one for the narrow projections and
 // for more than one 16-row activation tile.  (Four groups measured slower: more concurrent
 // weight streams per wave.)
-// Row groups per workgroup on the MFMA path with one 16-row activation tile (M up to 16).  A
-// workgroup reads its groups' weights and the activation rows over all of K, so two groups
-// per workgroup halve the activation reads per weight byte but also halve the workgroups.
-// The choice minimises the bytes read by the busiest compute unit (workgroups are dealt
-// round-robin): two groups for gate/up and the LM head, and for QKV at the 7B and 8B shapes
-// (288 or 384 groups: 1.2-1.5 workgroups per CU with one group each).
+// Row groups per workgroup on the MFMA path.  A workgroup reads its groups' weights and the
+// activation rows over all of K, so several groups per workgroup cut the activation reads per
+// weight byte but also the number of workgroups.  The choice minimises the bytes read by the
+// busiest compute unit (workgroups are dealt round-robin): at one 16-row tile two groups for
+// gate/up and the LM head, and for QKV at the 7B and 8B shapes (288 or 384 groups: 1.2-1.5
+// workgroups per CU with one group each); with 2-3 tiles up to four groups (gate/up of a
+// 40-row mixed step); at 4 tiles up to two.
 static int mfma_nr(int n_groups, int M, int K, int es, int cus) {
-  if (M <= kValuMaxRows || M > 16) return 1;
+  if (M <= kValuMaxRows || M > 64) return 1;
+  const int mt = ceil_div(M, 16);
   const double w = 16.0 * K * es, act = 4.0 * M * K;
   auto cost = [&](int nr) { return (double)ceil_div(ceil_div(n_groups, nr), cus) * (nr * w + act); };
-  return cost(2) < cost(1) ? 2 : 1;
+  int best = 1;
+  for (int nr : {2, 4}) {
+    if (nr == 4 && (mt < 2 || mt > 3)) continue;
+    if (cost(nr) < cost(best)) best = nr;
+  }
+  return best;
 }
 
 static Layout make_layout(const laser_model_desc& d, int max_rows) {

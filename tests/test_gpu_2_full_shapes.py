@@ -177,3 +177,47 @@ def test_llama8b_b8_mixed_step_state_injection():
         st.compare_probe(b, arg[i], d_conf[i].item())
     st.check_tables()
     st.release()
+
+
+def test_qwen1p5b_prefill_64row_chunks():
+    # A 100-token prompt in chunks of 64 and 36 rows: matrix-core projections over four and
+    # three 16-row tiles, with two and four row groups per workgroup for gate/up.
+    T0[0] = time.time()
+    dev = require_gpu()
+    shape, n, max_pos = QWEN_1P5B, 100, 256
+    model, orc, _ = make_pair(shape, max_rows=64, max_positions=max_pos, weights_on_device=True, cache_oracle=True)
+    kv = L.KVCache(model, 32, 1, max_pos // 16 + 1, poison=True)
+    opool = OraclePool(32)
+    kv.add_seq(0, 0)
+    opool.add_seq(0, 0)
+    prompt = synth.make_tokens(n, shape.vocab, 3007)
+    st = SeqState(shape, max_pos)
+    for t in prompt:
+        ref = orc.decode_token(st, int(t))
+    log(f"oracle prefill of {n} tokens done")
+    d_last = torch.zeros(shape.vocab, device=dev)
+    L.laser_prefill(model, kv, 0, prompt.to(dev), d_last)
+    opool.append(0, n)
+    torch.cuda.synchronize()
+    err = compare_logits(d_last.cpu().numpy(), ref, "prefill")
+    check_token(int(torch.argmax(d_last).item()), ref, "prefill")
+    assert kv.page_table(0) == opool.tables[0] and kv.seq_len(0) == n
+    log(f"prefill logits err {err:.3g}")
+    # one decode step on the prefilled cache
+    tok = lm_stats(ref)[0]
+    d_tok = torch.tensor([tok], dtype=torch.int32, device=dev)
+    d_next = torch.zeros(1, dtype=torch.int32, device=dev)
+    d_p = torch.zeros(1, device=dev)
+    d_logits = torch.zeros(1, shape.vocab, device=dev)
+    L.laser_decode_step(model, kv, [0], d_tok, d_next, d_p, d_logits)
+    torch.cuda.synchronize()
+    ref = orc.decode_token(st, tok)
+    err = compare_logits(d_logits[0].cpu().numpy(), ref, "decode after prefill")
+    check_token(d_next.item(), ref, "decode after prefill")
+    assert abs(d_p.item() - lm_stats(ref)[1]) <= PROB_TOL
+    log(f"decode after prefill: logits err {err:.3g}")
+    kv.destroy()
+    model.destroy()
+    del orc, st
+    gc.collect()
+    torch.cuda.empty_cache()
