@@ -502,7 +502,9 @@ __global__ __launch_bounds__(64 * kMfmaMaxWaves) void k_gemm_mfma(GemmArgs a) {
   __shared__ float Y[NR * YN];
   __shared__ float s_scale[16 * MT];
   const int tid = threadIdx.x, w = tid >> 6, l = tid & 63;
-  const int g0 = blockIdx.x * NR;
+  const int ksplit = EPI == EPI_RESID && a.ksplit > 1 ? a.ksplit : 1;  // K shares of a row group (adjacent workgroups)
+  const int ks = (int)blockIdx.x % ksplit;
+  const int g0 = (int)blockIdx.x / ksplit * NR;
   const int nlive = min(NR, a.n_groups - g0);  // groups past n_groups read clamped rows, unused
   const int M = a.M;
   const bool norm = a.gain != nullptr;
@@ -522,10 +524,14 @@ __global__ __launch_bounds__(64 * kMfmaMaxWaves) void k_gemm_mfma(GemmArgs a) {
     own[mt] = 16 * mt + n < M;
     xr[mt] = a.x + (size_t)a_src_row(a, min(16 * mt + n, M - 1)) * a.ldx;
   }
-  const int nsteps = (a.K + 31) >> 5;
-  const int nblk = (nsteps + 3) >> 2;
+  // This workgroup's 32-column steps [s0, s1): all of K, or a share of whole 4-step blocks.
+  const int nsteps_all = (a.K + 31) >> 5;
+  const int sps = ksplit > 1 ? (((nsteps_all + ksplit - 1) / ksplit + 3) & ~3) : nsteps_all;
+  const int s0 = ks * sps, s1 = min(nsteps_all, s0 + sps);
+  const int kend = min(a.K, 32 * s1);
+  const int nblk = (max(s1 - s0, 0) + 3) >> 2;
   const int niter = nblk > w ? 4 * ((nblk - w + W - 1) / W) : 0;  // this wave's steps
-  auto step_of = [&](int it) { return 4 * (w + W * (it >> 2)) + (it & 3); };
+  auto step_of = [&](int it) { return s0 + 4 * (w + W * (it >> 2)) + (it & 3); };
   f32x4 acc[NR][MT];
   float sq[MT];
 #pragma unroll
@@ -537,7 +543,7 @@ __global__ __launch_bounds__(64 * kMfmaMaxWaves) void k_gemm_mfma(GemmArgs a) {
   // K offset of this lane's 8 elements at iteration it, or -1 past the end of K
   auto kof = [&](int it) {
     const int k = 32 * step_of(it) + kg;
-    return k < a.K ? k : -1;
+    return k < kend ? k : -1;
   };
   // Every operand of a step (weights, activations, gain) is loaded U steps ahead of its use.
   struct Step {
@@ -629,7 +635,7 @@ __global__ __launch_bounds__(64 * kMfmaMaxWaves) void k_gemm_mfma(GemmArgs a) {
   // Steps whose 32 columns all lie inside K need no end check; they come first.  With K a
   // multiple of 128 (all model shapes but the tiny one) that is every step.
   int nfull = niter;
-  while (nfull > 0 && step_of(nfull - 1) >= (a.K >> 5)) --nfull;
+  while (nfull > 0 && step_of(nfull - 1) >= min(a.K >> 5, s1)) --nfull;
   using Check = std::integral_constant<bool, true>;
   using NoCheck = std::integral_constant<bool, false>;
   int it0 = 0;
@@ -679,7 +685,29 @@ __global__ __launch_bounds__(64 * kMfmaMaxWaves) void k_gemm_mfma(GemmArgs a) {
     Y[idx] = norm ? v * s_scale[j / RW] : v;
   }
   __syncthreads();
+  if (EPI == EPI_RESID && ksplit > 1) {  // partial sums of this K share (no norm on this path)
+    for (int r = 0; r < nlive; ++r)
+      for (int idx = tid; idx < M * RW; idx += blockDim.x) {
+        const int m = idx / RW, row = RW * (g0 + r) + (idx - m * RW);
+        if (row < a.N) a.kpart[((size_t)ks * M + m) * a.N + row] = Y[r * YN + idx];
+      }
+    return;
+  }
   for (int r = 0; r < nlive; ++r) run_epilogue<WT, EPI, RW>(a, g0 + r, M, Y + r * YN);
+}
+
+// h[i] += kpart[0][i] + kpart[1][i] + ... (K shares in order), i < M * N.
+__global__ void k_ksplit_reduce(float* h, const float* kpart, int ksplit, int n) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  float s = 0.f;
+  for (int k = 0; k < ksplit; ++k) s += kpart[(size_t)k * n + i];
+  h[i] += s;
+}
+
+hipError_t launch_ksplit_reduce(const GemmArgs& a, hipStream_t s) {
+  const int n = a.M * a.N;
+  return launch_k(k_ksplit_reduce, dim3((n + 255) / 256), dim3(256), s, a.h, (const float*)a.kpart, a.ksplit, n);
 }
 
 // ----------------------------------------------------------------------------- weight tiles
@@ -753,7 +781,9 @@ static hipError_t launch_epi(int epi, int rw, const GemmArgs& a, hipStream_t s) 
     if (rw != rows_per_group(epi, true)) return hipErrorInvalidValue;
     const int nr = a.nr < 1 ? 1 : a.nr;
     if (!mfma_nr_ok<MT>(nr)) return hipErrorInvalidValue;
-    const dim3 mgrid((a.n_groups + nr - 1) / nr);
+    const int ksplit = a.ksplit < 1 ? 1 : a.ksplit;
+    if (ksplit > 1 && (epi != EPI_RESID || a.kpart == nullptr || ksplit > kMaxKsplit)) return hipErrorInvalidValue;
+    const dim3 mgrid((a.n_groups + nr - 1) / nr * ksplit);
     // few workgroups (the O, down and QKV projections): 8 waves split K more finely
     const int waves = mgrid.x < 512 ? kMfmaMaxWaves : kGemmThreads / 64;
     auto blk = [&](int wmax) { return dim3(64 * (waves < wmax ? waves : wmax)); };
@@ -782,6 +812,7 @@ static hipError_t launch_mode(int mode, int epi, int rw, const GemmArgs& a, hipS
 
 hipError_t launch_gemm(int dtype, int mode, int epi, int rw, const GemmArgs& a, hipStream_t s) {
   if ((a.gain != nullptr) != (epi != EPI_RESID)) return hipErrorInvalidValue;  // only the residual GEMMs skip the norm
+  if (mode <= 4 && a.ksplit > 1) return hipErrorInvalidValue;                  // K shares: MFMA path only
   if (dtype == 1) return launch_mode<bf16_t>(mode, epi, rw, a, s);
   return launch_mode<float>(mode, epi, rw, a, s);
 }

@@ -16,6 +16,7 @@ constexpr int kAttnMaxWG = 128;   // attention workgroups per (group, kv head)
 constexpr int kGemmThreads = 256; // 4 waves
 constexpr int kGemvMaxThreads = 512;
 constexpr int kMfmaMaxWaves = 8;    // waves of an MFMA projection workgroup with few row groups
+constexpr int kMaxKsplit = 4;       // K shares of a residual projection on the MFMA path
 
 // One row of a forward: request slot, position, and where its input token id lives.
 struct RowDesc {
@@ -99,6 +100,10 @@ struct GemmArgs {
   int kv_fp8;  // K/V stored as E4M3 (else in the weight type)
   // EPI_RESID
   float* h;  // [M][N]
+  // MFMA path, EPI_RESID only: K split across `ksplit` workgroups per row group (1: none).
+  // Each writes its partial outputs to kpart[ks][M][N]; launch_ksplit_reduce adds them to h.
+  int ksplit;
+  float* kpart;
   // EPI_SWIGLU
   float* act;  // [M][F]
   int F;
@@ -146,6 +151,7 @@ inline hipError_t launch_k(K kernel, dim3 grid, dim3 block, hipStream_t s, Args.
 // dtype: 0 fp32, 1 bf16.  mode: 1..4 VALU rows per forward, 5..8 MFMA with 1..4 m-tiles.
 // rw: rows per workgroup (VALU: QKV 6 or 8, residual 6, 7 or 8, others 8; MFMA: 16).
 hipError_t launch_gemm(int dtype, int mode, int epi, int rw, const GemmArgs& a, hipStream_t s);
+hipError_t launch_ksplit_reduce(const GemmArgs& a, hipStream_t s);
 // Writes the tile-order copy of one projection's weights (the MFMA path's 16-row groups of
 // `a`, as weight_row maps them) to dst: a.n_groups groups x ceil(K/32) steps.
 hipError_t launch_tile_weights(int dtype, int epi, const GemmArgs& a, char* dst, hipStream_t s);

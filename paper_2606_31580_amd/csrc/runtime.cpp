@@ -82,7 +82,7 @@ constexpr int kTargetAttnWaves = LASER_ATTN_TARGET_WAVES;  // attention waves a 
 constexpr int kMaxPagesPerWave = LASER_ATTN_MAX_PPS;
 
 struct Layout {
-  size_t rope, h, q, o, act, lm_part, attn_part, attn_ml, plans, probe_p, tok_buf, p_buf, total;
+  size_t rope, h, q, o, act, kpart, lm_part, attn_part, attn_ml, plans, probe_p, tok_buf, p_buf, total;
 };
 
 // Launch signature of a forward.  With the plan in its fixed device slot and the caller's
@@ -225,22 +225,34 @@ static int groups_lm(const laser_model_desc& d, int M) { return ceil_div(d.vocab
 // are still at least two workgroups per compute unit; one for the narrow projections and
 // for more than one 16-row activation tile.  (Four groups measured slower: more concurrent
 // weight streams per wave.)
-// Row groups per workgroup on the MFMA path.  A workgroup reads its groups' weights and the
-// activation rows over all of K, so several groups per workgroup cut the activation reads per
-// weight byte but also the number of workgroups.  The choice minimises the bytes read by the
-// busiest compute unit (workgroups are dealt round-robin): at one 16-row tile two groups for
-// gate/up and the LM head, and for QKV at the 7B and 8B shapes (288 or 384 groups: 1.2-1.5
-// workgroups per CU with one group each); with 2-3 tiles up to four groups (gate/up of a
-// 40-row mixed step); at 4 tiles up to two.
-static int mfma_nr(int n_groups, int M, int K, int es, int cus) {
-  if (M <= kValuMaxRows || M > 64) return 1;
+// Row groups per workgroup, and K shares per row group, on the MFMA path.  A workgroup reads
+// its groups' weights and the activation rows over its K range, so several groups per
+// workgroup cut the activation reads per weight byte but also the number of workgroups, and
+// splitting K (residual projections only: the others normalise over the whole row) restores
+// the workgroups at the price of a reduce kernel.  The choice minimises the bytes read by the
+// busiest compute unit (workgroups are dealt round-robin), the reduce counted as
+// kKsplitPenalty bytes.  At one 16-row tile: two groups for gate/up and the LM head, and for
+// QKV at the 7B and 8B shapes (288 or 384 groups: 1.2-1.5 workgroups per CU with one group
+// each); with 2-3 tiles up to four groups (gate/up of a 40-row mixed step); at 4 tiles up to
+// two.  O-proj and down split K where the activation rows outweigh the weights (M >= 8 at
+// the 7B down projection, the 40-row mixed step).
+struct MfmaShape {
+  int nr, ks;
+};
+constexpr double kKsplitPenalty = 160e3;
+static MfmaShape mfma_shape(int epi, int n_groups, int M, int K, int es, int cus) {
+  if (M <= kValuMaxRows || M > 64) return {1, 1};
   const int mt = ceil_div(M, 16);
   const double w = 16.0 * K * es, act = 4.0 * M * K;
-  auto cost = [&](int nr) { return (double)ceil_div(ceil_div(n_groups, nr), cus) * (nr * w + act); };
-  int best = 1;
-  for (int nr : {2, 4}) {
+  auto cost = [&](int nr, int ks) {
+    const double wgs = (double)ceil_div(ceil_div(n_groups, nr) * ks, cus);
+    return wgs * (nr * w + act) / ks + (ks > 1 ? kKsplitPenalty : 0.0);
+  };
+  MfmaShape best{1, 1};
+  for (int nr : {1, 2, 4}) {
     if (nr == 4 && (mt < 2 || mt > 3)) continue;
-    if (cost(nr) < cost(best)) best = nr;
+    for (int ks = 1; ks <= (epi == EPI_RESID ? kMaxKsplit : 1); ks *= 2)
+      if (cost(nr, ks) < cost(best.nr, best.ks)) best = {nr, ks};
   }
   return best;
 }
@@ -259,6 +271,7 @@ static Layout make_layout(const laser_model_desc& d, int max_rows) {
   L.q = take((size_t)max_rows * d.n_q_heads * hd * 4);
   L.o = take((size_t)max_rows * d.n_q_heads * hd * 4);
   L.act = take((size_t)max_rows * d.d_ffn * 4);
+  L.kpart = take((size_t)kMaxKsplit * max_rows * d.d_model * 4);  // K-share partials of O-proj / down
   L.lm_part = take((size_t)groups_lm(d, 1) * kMaxRows * sizeof(LmPart));  // the VALU path has the most groups
   L.attn_part = take((size_t)d.n_kv_heads * kAttnMaxWG * max_rows * G * hd * 4);
   L.attn_ml = take((size_t)d.n_kv_heads * kAttnMaxWG * max_rows * G * 2 * 4);
@@ -840,14 +853,21 @@ static laser_status launch_forward(laser_model* m, laser_kv* kv, const FwdKey& k
     a.K = K;
     a.N = N;
     a.n_groups = proj_groups(epi, rows, rw);
-    a.nr = mfma_nr(a.n_groups, M, K, (int)m->es, m->cus);
+    const MfmaShape ms = mfma_shape(epi, a.n_groups, M, K, (int)m->es, m->cus);
+    a.nr = ms.nr;
+    a.ksplit = ms.ks;
+    a.kpart = m->wsp<float>(L.kpart);
     a.M = M;
     if (M > kValuMaxRows && m->tiles_on) {
       a.wtile = tile;
       a.tsteps = (K + 31) / 32;
     }
     const int mode = gemm_mode(M);
-    HIP_TRY(timed(m, cls, s, [&] { return launch_gemm(dt, mode, epi, rw, a, s); }));
+    HIP_TRY(timed(m, cls, s, [&] {
+      hipError_t e = launch_gemm(dt, mode, epi, rw, a, s);
+      if (e == hipSuccess && a.ksplit > 1) e = launch_ksplit_reduce(a, s);
+      return e;
+    }));
     return LASER_OK;
   };
 
@@ -930,7 +950,8 @@ static laser_status launch_forward(laser_model* m, laser_kv* kv, const FwdKey& k
     a.K = d.d_model;
     a.N = d.vocab;
     a.n_groups = groups_lm(d, key.n_out);
-    a.nr = mfma_nr(a.n_groups, key.n_out, d.d_model, (int)m->es, m->cus);
+    a.nr = mfma_shape(EPI_LMHEAD, a.n_groups, key.n_out, d.d_model, (int)m->es, m->cus).nr;
+    a.ksplit = 1;
     a.M = key.n_out;
     if (key.n_out > kValuMaxRows && m->tiles_on) {
       a.wtile = m->lm_tile;
