@@ -38,26 +38,18 @@ template <class KT, int HD, int NT>
 __global__ __launch_bounds__(64 * kAttnWaves) void k_attn(AttnArgs a) {
   constexpr int NS = HD / 32;  // QK k-steps
   constexpr int ND = HD / 16;  // PV d-tiles
-  constexpr int NC = 16 * NT;  // padded query columns
-  // LDS: queries (bf16 hi/lo) and the merge slots of the waves.  One query tile merges in
-  // one round (waves 1-3 publish, wave 0 absorbs) with separate slots; wider tiles merge
-  // in two rounds through two slots that reuse the query space.
-  constexpr int NSLOT = NT == 1 ? 3 : 2;
-  constexpr bool ALIAS = NT != 1;
-  // Rows are padded by 16 bytes, so the 16 columns a wave reads at once (row stride) fall in
-  // 16 different bank groups instead of one.
+  constexpr int NC = 16 * NT;  // padded query columns staged (up to NT tiles of 16)
+  // LDS: the group's queries (bf16 hi/lo) and, for page-parallel groups, the merge slots of
+  // waves 1-3 (one tile).  Rows are padded by 16 bytes, so the 16 columns a wave reads at
+  // once (row stride) fall in 16 different bank groups instead of one.
   constexpr int QS = HD + 8;  // query row stride (bf16 elements)
   constexpr int OS = HD + 4;  // merge-slot row stride (floats)
-  constexpr int QBYTES = NC * QS * 2 * 2;
-  constexpr int SBYTES = NSLOT * NC * OS * 4;
-  constexpr int LBYTES = ALIAS ? (QBYTES > SBYTES ? QBYTES : SBYTES) : QBYTES + SBYTES;
-  __shared__ __align__(16) char s_raw[LBYTES];
-  uint16_t* s_qh = (uint16_t*)s_raw;
-  uint16_t* s_ql = s_qh + NC * QS;
-  float* const s_of = (float*)(s_raw + (ALIAS ? 0 : QBYTES));  // slot k at s_of + k * NC * OS
+  __shared__ __align__(16) uint16_t s_qh[NC * QS];
+  __shared__ __align__(16) uint16_t s_ql[NC * QS];
+  __shared__ __align__(16) float s_of[3 * 16 * OS];  // slot k at s_of + k * 16 * OS
   __shared__ int s_pos[NC];
-  __shared__ float s_m[NSLOT][NC];
-  __shared__ float s_l[NSLOT][NC];
+  __shared__ float s_m[3][16];
+  __shared__ float s_l[3][16];
 
   const GroupDesc gd = a.plan->groups[blockIdx.z];
   const int wg = blockIdx.x;
@@ -68,17 +60,20 @@ __global__ __launch_bounds__(64 * kAttnWaves) void k_attn(AttnArgs a) {
   const int lc = l & 15, lg = l >> 4;
   const int NQ = gd.nrows * a.G;
 
-  float m_run[NT], l_run[NT];
-  f32x4 o[NT][ND];
+  // One 16-column query tile per wave.  A group of one tile splits its pages over the
+  // waves (page-parallel: wave w walks run 4 wg + w, then the waves merge through LDS); a
+  // wider group gives wave w tile w and every wave the workgroup's run (tile-parallel: each
+  // wave stores its own columns).  Either way a wave holds one tile's running sums.
+  const int ntile = (NQ + 15) >> 4;
+  const bool tpar = ntile > 1;
+  const int tile = tpar ? w : 0;
+  const bool active = tile < ntile;  // tile-parallel groups of fewer than 4 tiles idle a wave
+  float m_run = -INFINITY, l_run = 0.f;
+  f32x4 o[ND];
 #pragma unroll
-  for (int nt = 0; nt < NT; ++nt) {
-    m_run[nt] = -INFINITY;
-    l_run[nt] = 0.f;
-#pragma unroll
-    for (int dt = 0; dt < ND; ++dt) o[nt][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
-  }
+  for (int dt = 0; dt < ND; ++dt) o[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  const int split = wg * kAttnWaves + w;
+  const int split = tpar ? wg : wg * kAttnWaves + w;
   const int p0 = split * gd.pps;
   const int p1 = min(p0 + gd.pps, gd.npages);
   const int* btrow = a.bt + (size_t)gd.seq * a.max_pps;
@@ -115,24 +110,28 @@ __global__ __launch_bounds__(64 * kAttnWaves) void k_attn(AttnArgs a) {
   // pages, so its whole run is in flight at once.
   constexpr int D = 2;
   constexpr int KW = sizeof(KT) == 4 ? 2 : 1;  // 16-byte K loads per k-step (fp8: one 8-byte load)
-  u32x4 kraw[D][NS][KW];
-  u32x4 vraw[D][ND];  // bf16: only the low 8 bytes are used; fp8: the low 4
+  // raw page words per lane, sized to what each storage type loads (registers are what
+  // limits how many waves a CU holds)
+  using KRaw = std::conditional_t<sizeof(KT) == 1, u32x2, u32x4>;
+  using VRaw = std::conditional_t<sizeof(KT) == 1, uint32_t, std::conditional_t<sizeof(KT) == 2, u32x2, u32x4>>;
+  KRaw kraw[D][NS][KW];
+  VRaw vraw[D][ND];
   auto load_page = [&](int pg, auto bufc) {
     constexpr int buf = decltype(bufc)::value;
     const int pid = page_id(pg);
     const size_t blk = ((layer_base + pid) * a.hkv + kvh) * blk_elems;
-    if (sizeof(KT) == 1) {
+    if constexpr (sizeof(KT) == 1) {
       const uint8_t* kb = (const uint8_t*)a.kpool + blk;
       const uint8_t* vb = (const uint8_t*)a.vpool + blk;
 #pragma unroll
       for (int s = 0; s < NS; ++s) {
         const u32x2 t = ld_nt8(kb + s * 512 + 8 * l);
-        kraw[buf][s][0] = u32x4{t[0], t[1], 0u, 0u};
+        kraw[buf][s][0] = t;
       }
 #pragma unroll
       for (int dt = 0; dt < ND; ++dt)
-        vraw[buf][dt] = u32x4{__builtin_nontemporal_load((const uint32_t*)(vb + dt * 256 + 4 * l)), 0u, 0u, 0u};
-    } else if (sizeof(KT) == 2) {
+        vraw[buf][dt] = __builtin_nontemporal_load((const uint32_t*)(vb + dt * 256 + 4 * l));
+    } else if constexpr (sizeof(KT) == 2) {
       const uint16_t* kb = (const uint16_t*)a.kpool + blk;
       const uint16_t* vb = (const uint16_t*)a.vpool + blk;
 #pragma unroll
@@ -140,7 +139,7 @@ __global__ __launch_bounds__(64 * kAttnWaves) void k_attn(AttnArgs a) {
 #pragma unroll
       for (int dt = 0; dt < ND; ++dt) {
         const u32x2 t = ld_nt8(vb + dt * 256 + 4 * l);
-        vraw[buf][dt] = u32x4{t[0], t[1], 0u, 0u};
+        vraw[buf][dt] = t;
       }
     } else {
       const float* kb = (const float*)a.kpool + blk;
@@ -164,7 +163,7 @@ __global__ __launch_bounds__(64 * kAttnWaves) void k_attn(AttnArgs a) {
   };
   auto unpack = [&](int pg, auto cbc, PageOps& P) {
     constexpr int cb = decltype(cbc)::value;
-    if (sizeof(KT) == 1) {  // E4M3 -> bf16 is exact: no lo part
+    if constexpr (sizeof(KT) == 1) {  // E4M3 -> bf16 is exact: no lo part
 #pragma unroll
       for (int s = 0; s < NS; ++s) {
         uint32_t w0, w1, w2, w3;
@@ -175,14 +174,14 @@ __global__ __launch_bounds__(64 * kAttnWaves) void k_attn(AttnArgs a) {
 #pragma unroll
       for (int dt = 0; dt < ND; ++dt) {
         uint32_t w0, w1;
-        fp8x4_to_bf16x4(vraw[cb][dt][0], w0, w1);
+        fp8x4_to_bf16x4(vraw[cb][dt], w0, w1);
         P.vhi[dt] = __builtin_bit_cast(s16x4, u32x2{w0, w1});
       }
-    } else if (sizeof(KT) == 2) {
+    } else if constexpr (sizeof(KT) == 2) {
 #pragma unroll
       for (int s = 0; s < NS; ++s) P.khi[s] = __builtin_bit_cast(bf16x8, kraw[cb][s][0]);
 #pragma unroll
-      for (int dt = 0; dt < ND; ++dt) P.vhi[dt] = __builtin_bit_cast(s16x4, u32x2{vraw[cb][dt][0], vraw[cb][dt][1]});
+      for (int dt = 0; dt < ND; ++dt) P.vhi[dt] = __builtin_bit_cast(s16x4, vraw[cb][dt]);
     } else {
 #pragma unroll
       for (int s = 0; s < NS; ++s) {
@@ -227,15 +226,17 @@ __global__ __launch_bounds__(64 * kAttnWaves) void k_attn(AttnArgs a) {
     }
   };
   // S^T tile of one page: lane (c = lc, lg) gets the scores of positions 16pg + 4lg + i.
+  // (The hi and lo query parts accumulate in two chains, summed at the end, so that
+  // consecutive matrix-core ops do not wait for each other's results.)
   auto scores = [&](const PageOps& P, const bf16x8* qh, const bf16x8* ql) {
-    f32x4 sacc = f32x4{0.f, 0.f, 0.f, 0.f};
+    f32x4 shi = f32x4{0.f, 0.f, 0.f, 0.f}, slo = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int s = 0; s < NS; ++s) {
-      sacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(P.khi[s], qh[s], sacc, 0, 0, 0);
-      sacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(P.khi[s], ql[s], sacc, 0, 0, 0);
-      if (sizeof(KT) == 4) sacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(P.klo[s], qh[s], sacc, 0, 0, 0);
+      shi = __builtin_amdgcn_mfma_f32_16x16x32_bf16(P.khi[s], qh[s], shi, 0, 0, 0);
+      slo = __builtin_amdgcn_mfma_f32_16x16x32_bf16(P.khi[s], ql[s], slo, 0, 0, 0);
+      if (sizeof(KT) == 4) slo = __builtin_amdgcn_mfma_f32_16x16x32_bf16(P.klo[s], qh[s], slo, 0, 0, 0);
     }
-    return sacc;
+    return shi + slo;
   };
   // O^T += V^T P^T for one page; P^T comes straight from the score accumulator layout.
   auto accumulate = [&](const PageOps& P, const float* pv, f32x4* acc) {
@@ -278,78 +279,80 @@ __global__ __launch_bounds__(64 * kAttnWaves) void k_attn(AttnArgs a) {
   if (tid < NC) s_pos[tid] = tid < NQ ? cpos_loaded : -1;
   __syncthreads();
 
-  if constexpr (NT == 1) {
-    // ---- one query tile: queries in registers, pages in pairs (one max and one sum
-    // reduction across the lane groups per 32 positions)
-    bf16x8 qh[NS], ql[NS];
-#pragma unroll
-    for (int s = 0; s < NS; ++s) {
-      qh[s] = *(const bf16x8*)(s_qh + lc * QS + 32 * s + 8 * lg);
-      ql[s] = *(const bf16x8*)(s_ql + lc * QS + 32 * s + 8 * lg);
-    }
-    const int cpos = s_pos[lc];
-    auto pair = [&](int pgA, auto ca, auto cbB) {
-      const int pgB = pgA + 1;
-      const bool hasB = pgB < p1;  // wave-uniform
-      PageOps A, B;
-      unpack(pgA, ca, A);
-      const f32x4 sa = scores(A, qh, ql);
-      f32x4 sb = f32x4{0.f, 0.f, 0.f, 0.f};
-      if (hasB) {
-        unpack(pgB, cbB, B);
-        sb = scores(B, qh, ql);
-      }
-      float sv[8];
-      float mloc = -INFINITY;
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int ta = pgA * 16 + 4 * lg + i, tb = pgB * 16 + 4 * lg + i;
-        sv[i] = (ta <= cpos) ? sa[i] * a.scale_log2 : -INFINITY;
-        sv[4 + i] = (hasB && tb <= cpos) ? sb[i] * a.scale_log2 : -INFINITY;
-        mloc = fmaxf(mloc, fmaxf(sv[i], sv[4 + i]));
-      }
-      mloc = max_x16(mloc);
-      mloc = max_x32(mloc);
-      const float m_new = fmaxf(m_run[0], mloc);
-      // o and l are still zero while m_run is -inf, so they need no rescale then
-      const bool grow = m_run[0] != -INFINITY && m_new != m_run[0];
-      const float alpha = grow ? __builtin_amdgcn_exp2f(m_run[0] - m_new) : 1.f;
-      float pv[8], ls = 0.f;
-#pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        pv[i] = (sv[i] == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(sv[i] - m_new);
-        ls += pv[i];
-      }
-      ls = sum_x16(ls);
-      ls = sum_x32(ls);
-      l_run[0] = l_run[0] * alpha + ls;
-      m_run[0] = m_new;
-      if (__builtin_amdgcn_read_exec() & __ballot(grow)) {  // any lane whose max moved
-#pragma unroll
-        for (int dt = 0; dt < ND; ++dt) o[0][dt] *= alpha;
-      }
-      accumulate(A, pv, o[0]);
-      if (hasB) accumulate(B, pv + 4, o[0]);
-    };
-    for (int base = p0; base < p1; base += D) {
-      static_for<D / 2>([&](auto h) {
-        constexpr int bA = 2 * decltype(h)::value;
-        const int pg = base + bA;
-        if (pg < p1) {
-          pair(pg, std::integral_constant<int, bA>{}, std::integral_constant<int, bA + 1>{});
-          if (pg + D < p1) load_page(pg + D, std::integral_constant<int, bA>{});
-          if (pg + 1 + D < p1) load_page(pg + 1 + D, std::integral_constant<int, bA + 1>{});
-        }
-      });
-    }
+  if (!active) return;  // (after the last barrier of a tile-parallel group)
 
-    // ---- one-round merge: waves 1-3 publish, wave 0 absorbs in order and stores
+  // pages in pairs: one max and one sum reduction across the lane groups per 32 positions
+  const int c = tile * 16 + lc;  // this lane's query column
+  bf16x8 qh[NS], ql[NS];
+#pragma unroll
+  for (int s = 0; s < NS; ++s) {
+    qh[s] = *(const bf16x8*)(s_qh + c * QS + 32 * s + 8 * lg);
+    ql[s] = *(const bf16x8*)(s_ql + c * QS + 32 * s + 8 * lg);
+  }
+  const int cpos = s_pos[c];
+  auto pair = [&](int pgA, auto ca, auto cbB) {
+    const int pgB = pgA + 1;
+    const bool hasB = pgB < p1;  // wave-uniform
+    PageOps A, B;
+    unpack(pgA, ca, A);
+    const f32x4 sa = scores(A, qh, ql);
+    f32x4 sb = f32x4{0.f, 0.f, 0.f, 0.f};
+    if (hasB) {
+      unpack(pgB, cbB, B);
+      sb = scores(B, qh, ql);
+    }
+    float sv[8];
+    float mloc = -INFINITY;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int ta = pgA * 16 + 4 * lg + i, tb = pgB * 16 + 4 * lg + i;
+      sv[i] = (ta <= cpos) ? sa[i] * a.scale_log2 : -INFINITY;
+      sv[4 + i] = (hasB && tb <= cpos) ? sb[i] * a.scale_log2 : -INFINITY;
+      mloc = fmaxf(mloc, fmaxf(sv[i], sv[4 + i]));
+    }
+    mloc = max_x16(mloc);
+    mloc = max_x32(mloc);
+    const float m_new = fmaxf(m_run, mloc);
+    // o and l are still zero while m_run is -inf, so they need no rescale then
+    const bool grow = m_run != -INFINITY && m_new != m_run;
+    const float alpha = grow ? __builtin_amdgcn_exp2f(m_run - m_new) : 1.f;
+    float pv[8], ls = 0.f;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      pv[i] = (sv[i] == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(sv[i] - m_new);
+      ls += pv[i];
+    }
+    ls = sum_x16(ls);
+    ls = sum_x32(ls);
+    l_run = l_run * alpha + ls;
+    m_run = m_new;
+    if (__builtin_amdgcn_read_exec() & __ballot(grow)) {  // any lane whose max moved
+#pragma unroll
+      for (int dt = 0; dt < ND; ++dt) o[dt] *= alpha;
+    }
+    accumulate(A, pv, o);
+    if (hasB) accumulate(B, pv + 4, o);
+  };
+  for (int base = p0; base < p1; base += D) {
+    static_for<D / 2>([&](auto h) {
+      constexpr int bA = 2 * decltype(h)::value;
+      const int pg = base + bA;
+      if (pg < p1) {
+        pair(pg, std::integral_constant<int, bA>{}, std::integral_constant<int, bA + 1>{});
+        if (pg + D < p1) load_page(pg + D, std::integral_constant<int, bA>{});
+        if (pg + 1 + D < p1) load_page(pg + 1 + D, std::integral_constant<int, bA + 1>{});
+      }
+    });
+  }
+
+  if (!tpar) {
+    // ---- one-round merge of the page-parallel waves: 1-3 publish, 0 absorbs in order
     if (w > 0) {
 #pragma unroll
-      for (int dt = 0; dt < ND; ++dt) *(f32x4*)(s_of + (w - 1) * NC * OS + lc * OS + 16 * dt + 4 * lg) = o[0][dt];
+      for (int dt = 0; dt < ND; ++dt) *(f32x4*)(s_of + (w - 1) * 16 * OS + lc * OS + 16 * dt + 4 * lg) = o[dt];
       if (lg == 0) {
-        s_m[w - 1][lc] = m_run[0];
-        s_l[w - 1][lc] = l_run[0];
+        s_m[w - 1][lc] = m_run;
+        s_l[w - 1][lc] = l_run;
       }
     }
     __syncthreads();
@@ -357,145 +360,35 @@ __global__ __launch_bounds__(64 * kAttnWaves) void k_attn(AttnArgs a) {
 #pragma unroll
     for (int u = 0; u < 3; ++u) {
       const float m2 = s_m[u][lc], l2 = s_l[u][lc];
-      const float mm = fmaxf(m_run[0], m2);
-      const float ca = (mm == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(m_run[0] - mm);
+      const float mm = fmaxf(m_run, m2);
+      const float ca = (mm == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(m_run - mm);
       const float cb2 = (mm == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(m2 - mm);
-      l_run[0] = l_run[0] * ca + l2 * cb2;
-      m_run[0] = mm;
+      l_run = l_run * ca + l2 * cb2;
+      m_run = mm;
 #pragma unroll
       for (int dt = 0; dt < ND; ++dt) {
-        const f32x4 x = *(const f32x4*)(s_of + u * NC * OS + lc * OS + 16 * dt + 4 * lg);
-        o[0][dt] = o[0][dt] * ca + x * cb2;
+        const f32x4 x = *(const f32x4*)(s_of + u * 16 * OS + lc * OS + 16 * dt + 4 * lg);
+        o[dt] = o[dt] * ca + x * cb2;
       }
     }
-    if (lc >= NQ) return;
-    const int row = gd.row0 + lc / a.G, head = kvh * a.G + lc % a.G;
-    if (gd.nwg == 1) {
-      float* out = a.o + ((size_t)row * a.hq + head) * HD;
-      const float inv = 1.f / l_run[0];
+  }
+  // ---- this wave's columns: the output (one workgroup) or the workgroup's partial
+  if (c >= NQ) return;
+  const int row = gd.row0 + c / a.G, head = kvh * a.G + c % a.G;
+  if (gd.nwg == 1) {
+    float* out = a.o + ((size_t)row * a.hq + head) * HD;
+    const float inv = 1.f / l_run;
 #pragma unroll
-      for (int dt = 0; dt < ND; ++dt) *(f32x4*)(out + 16 * dt + 4 * lg) = o[0][dt] * inv;
-      return;
-    }
-    const size_t ncols = (size_t)a.max_rows * a.G;
-    const size_t col = ((size_t)kvh * kAttnMaxWG + wg) * ncols + (size_t)gd.row0 * a.G + lc;
+    for (int dt = 0; dt < ND; ++dt) *(f32x4*)(out + 16 * dt + 4 * lg) = o[dt] * inv;
+    return;
+  }
+  const size_t ncols = (size_t)a.max_rows * a.G;
+  const size_t col = ((size_t)kvh * kAttnMaxWG + wg) * ncols + (size_t)gd.row0 * a.G + c;
 #pragma unroll
-    for (int dt = 0; dt < ND; ++dt) *(f32x4*)(a.part + col * HD + 16 * dt + 4 * lg) = o[0][dt];
-    if (lg == 0) {
-      a.ml[col * 2 + 0] = m_run[0];
-      a.ml[col * 2 + 1] = l_run[0];
-    }
-  } else {
-    // ---- several query tiles: one page at a time, queries read from LDS
-    auto process_page = [&](int pg, auto cbc) {
-      PageOps P;
-      unpack(pg, cbc, P);
-#pragma unroll
-      for (int nt = 0; nt < NT; ++nt) {
-        if (nt * 16 >= NQ) break;
-        const int qrow = (nt * 16 + lc) * QS;
-        bf16x8 qh[NS], ql[NS];
-#pragma unroll
-        for (int s = 0; s < NS; ++s) {
-          qh[s] = *(const bf16x8*)(s_qh + qrow + 32 * s + 8 * lg);
-          ql[s] = *(const bf16x8*)(s_ql + qrow + 32 * s + 8 * lg);
-        }
-        const f32x4 sacc = scores(P, qh, ql);
-        const int cpos = s_pos[nt * 16 + lc];
-        float sv[4];
-        float mloc = -INFINITY;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int tg = pg * 16 + 4 * lg + i;
-          sv[i] = (tg <= cpos) ? sacc[i] * a.scale_log2 : -INFINITY;
-          mloc = fmaxf(mloc, sv[i]);
-        }
-        mloc = max_x16(mloc);
-        mloc = max_x32(mloc);
-        const float m_new = fmaxf(m_run[nt], mloc);
-        const float alpha = (m_new == -INFINITY) ? 1.f : safe_exp2(m_run[nt] - m_new);
-        float pv[4], ls = 0.f;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          pv[i] = (sv[i] == -INFINITY) ? 0.f : exp2f(sv[i] - m_new);
-          ls += pv[i];
-        }
-        ls = sum_x16(ls);
-        ls = sum_x32(ls);
-        l_run[nt] = l_run[nt] * alpha + ls;
-        m_run[nt] = m_new;
-#pragma unroll
-        for (int dt = 0; dt < ND; ++dt) o[nt][dt] *= alpha;
-        accumulate(P, pv, o[nt]);
-      }
-    };
-    for (int base = p0; base < p1; base += D) {
-      static_for<D>([&](auto b) {
-        const int pg = base + (int)b;
-        if (pg < p1) {
-          process_page(pg, b);
-          if (pg + D < p1) load_page(pg + D, b);
-        }
-      });
-    }
-
-    // ---- merge the 4 waves in two rounds through 2 LDS slots
-    auto publish = [&](int slot) {
-#pragma unroll
-      for (int nt = 0; nt < NT; ++nt) {
-        const int c = nt * 16 + lc;
-#pragma unroll
-        for (int dt = 0; dt < ND; ++dt) *(f32x4*)(s_of + slot * NC * OS + c * OS + 16 * dt + 4 * lg) = o[nt][dt];
-        if (lg == 0) {
-          s_m[slot][c] = m_run[nt];
-          s_l[slot][c] = l_run[nt];
-        }
-      }
-    };
-    auto absorb = [&](int slot) {
-#pragma unroll
-      for (int nt = 0; nt < NT; ++nt) {
-        const int c = nt * 16 + lc;
-        const float m2 = s_m[slot][c], l2 = s_l[slot][c];
-        const float mm = fmaxf(m_run[nt], m2);
-        const float ca = (mm == -INFINITY) ? 0.f : safe_exp2(m_run[nt] - mm);
-        const float cb2 = (mm == -INFINITY) ? 0.f : safe_exp2(m2 - mm);
-        l_run[nt] = l_run[nt] * ca + l2 * cb2;
-        m_run[nt] = mm;
-#pragma unroll
-        for (int dt = 0; dt < ND; ++dt)
-          o[nt][dt] = o[nt][dt] * ca + *(const f32x4*)(s_of + slot * NC * OS + c * OS + 16 * dt + 4 * lg) * cb2;
-      }
-    };
-    __syncthreads();  // every wave is done with Q before the slots overwrite it
-    if (w >= 2) publish(w - 2);
-    __syncthreads();
-    if (w < 2) absorb(w);
-    __syncthreads();
-    if (w == 1) publish(0);
-    __syncthreads();
-    if (w == 0) {
-      absorb(0);
-      publish(1);  // workgroup result (unnormalised) in slot 1
-    }
-    __syncthreads();
-
-    const int ncols = a.max_rows * a.G;
-    if (gd.nwg == 1) {
-      for (int idx = tid; idx < NQ * HD; idx += blockDim.x) {
-        const int c = idx / HD, d = idx - c * HD;
-        const int row = gd.row0 + c / a.G, head = kvh * a.G + c % a.G;
-        a.o[((size_t)row * a.hq + head) * HD + d] = s_of[1 * NC * OS + c * OS + d] / s_l[1][c];
-      }
-      return;
-    }
-    const size_t slot_base = ((size_t)kvh * kAttnMaxWG + wg) * ncols + (size_t)gd.row0 * a.G;
-    for (int idx = tid; idx < NQ * HD; idx += blockDim.x)
-      a.part[slot_base * HD + idx] = s_of[1 * NC * OS + (idx / HD) * OS + idx % HD];
-    for (int c = tid; c < NQ; c += blockDim.x) {
-      a.ml[(slot_base + c) * 2 + 0] = s_m[1][c];
-      a.ml[(slot_base + c) * 2 + 1] = s_l[1][c];
-    }
+  for (int dt = 0; dt < ND; ++dt) *(f32x4*)(a.part + col * HD + 16 * dt + 4 * lg) = o[dt];
+  if (lg == 0) {
+    a.ml[col * 2 + 0] = m_run;
+    a.ml[col * 2 + 1] = l_run;
   }
 }
 

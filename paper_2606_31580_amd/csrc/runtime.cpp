@@ -735,16 +735,18 @@ static void plan_groups(const laser_model* m, Plan& p) {
     g.nrows = e - r;
     g.npages = maxpos / kPage + 1;
     g.maxpos = maxpos;
-    // wider query tiles make a page costlier: weight by half the group's 16-column tiles
-    units += (long long)g.npages * d.n_kv_heads * ceil_div(ceil_div(g.nrows * G, 16), 2);
+    // a group of one 16-column tile spreads its pages over the 4 waves of a workgroup; a
+    // wider one runs the same pages on all 4 waves, one tile each
+    units += (long long)g.npages * d.n_kv_heads * (ceil_div(g.nrows * G, 16) > 1 ? kAttnWaves : 1);
     r = e;
   }
   const int base =
       std::min(kMaxPagesPerWave, std::max(1, (int)((units + kTargetAttnWaves - 1) / kTargetAttnWaves)));
   for (int i = 0; i < p.n_groups; ++i) {
     GroupDesc& g = p.groups[i];
-    g.pps = std::max(base, ceil_div(g.npages, kAttnMaxWG * kAttnWaves));
-    g.nwg = ceil_div(g.npages, kAttnWaves * g.pps);
+    const int runs_per_wg = ceil_div(g.nrows * G, 16) > 1 ? 1 : kAttnWaves;  // page runs per workgroup
+    g.pps = std::max(base, ceil_div(g.npages, kAttnMaxWG * runs_per_wg));
+    g.nwg = ceil_div(g.npages, runs_per_wg * g.pps);
   }
 }
 
