@@ -2,19 +2,19 @@
 //
 // Work: grid (workgroup split, kv head, row group).  A row group is the rows of one request
 // in this forward (1 decode row, or the S rows of a probe chunk); its query columns are
-// (row, query head of this kv head) pairs, padded to 16*NT.  Each of the 4 waves of a
-// workgroup walks its own run of pages (split-K), so every K/V page is read once for all
-// query columns of the request.  Per page (16 positions):
+// (row, query head of this kv head) pairs, staged for up to NT 16-column tiles.  Each wave
+// holds one tile.  A group of one tile is page-parallel: each of the 4 waves walks its own
+// run of pages (split-K) and the waves merge (m, l, O) in one LDS round.  A wider group is
+// tile-parallel: wave w takes tile w and all waves walk the workgroup's run, so each page is
+// fetched from HBM once for all query columns.  Per page (16 positions):
 //   S^T[t][c] = K[t][:] . Q[c][:]   v_mfma_f32_16x16x32_bf16, A = K page, B = Q^T (bf16 hi+lo)
 //   online softmax over t per column (exp2 domain), causal mask t <= pos(c)
 //   O^T[d][c] += V^T[d][t] P^T[t][c] v_mfma_f32_16x16x16_bf16, B = P^T taken straight from
 //                                    the S^T accumulator layout (bf16 hi+lo)
 // The KV page layout makes every operand load a contiguous 1 KB (K) / 512 B (V) per wave
-// instruction.  With one query tile (decode rows) the queries stay in registers and pages
-// are taken in pairs, so the cross-lane max and sum reductions run once per 32 positions,
-// and the four waves merge (m, l, O) in one LDS round; wider tiles (probe chunks) take one
-// page at a time and merge in two rounds.  When a (group, kv head) spans several
-// workgroups their fp32 partials are combined by k_attn_merge, launched next.
+// instruction.  A wave's query tile stays in registers and pages are taken in pairs, so the
+// cross-lane max and sum reductions run once per 32 positions.  When a (group, kv head)
+// spans several workgroups their fp32 partials are combined by k_attn_merge, launched next.
 #include <type_traits>
 
 #include "device_common.hpp"

@@ -9,16 +9,21 @@
 //             EPI_SWIGLU silu(gate) * up;
 //             EPI_LMHEAD logits and per-group (max, sum exp, argmax) for k_lm_reduce,
 //                        stored [row][group].
-// A workgroup owns complete output rows (8 on the VALU path, 16 on the MFMA path), so every
-// epilogue stays inside the workgroup: the four waves split K and are reduced through LDS,
-// with no synchronisation between workgroups and results that do not depend on scheduling.
+// A workgroup owns complete output rows (6-8 on the VALU path, 1, 2 or 4 groups of 16 on the
+// MFMA path), so every epilogue stays inside the workgroup: its waves split K and are
+// reduced through LDS in a fixed order, with no synchronisation between workgroups and
+// results that do not depend on scheduling.  The one exception is the MFMA path's residual
+// projections, which may split K over 2-4 workgroups: each writes its partial rows and
+// k_ksplit_reduce adds them to h, again in a fixed order.
 // Main loops:
 //   VALU (decode: 1-4 rows; the runtime uses it up to 2): each thread streams 16-byte
 //       non-temporal loads of the group's rows, two chunks at a time (a wave instruction
 //       reads 1 KB contiguous of one row).
 //   MFMA (more rows: batches, probe chunks, prefill) 16x16x32 bf16: weights are the B
-//       operand, activations the A operand split into bf16 hi + lo so the product keeps
-//       ~16 significand bits of fp32 activations; fp32 weights are split too.
+//       operand (optionally read from the tile-order copy), activations the A operand split
+//       into bf16 hi + lo so the product keeps ~16 significand bits of fp32 activations;
+//       fp32 weights are split too.  One activation fragment feeds every row group of the
+//       workgroup.
 #include <type_traits>
 
 #include "device_common.hpp"
