@@ -280,6 +280,15 @@ def main():
         if rec.get("gemm_hip_sha256_16") == cur and rec.get("workload") == wl.name:
             traffic = rec.get("bytes_per_launch")
 
+    # host exit decision (EMA, Eq. 5, Algorithm 1), timed outside the timed region through the
+    # Python binding (the C call is scalar arithmetic; ctypes dominates)
+    dec_state = L.laser_load_state(0.0)
+    n_dec = 20000
+    t0 = time.perf_counter()
+    for i in range(n_dec):
+        L.laser_exit_decision(params, dec_state, 0.9, 8, 0, 10)
+    host_decision_us = (time.perf_counter() - t0) / n_dec * 1e6
+
     out = {
         "metric": "decode tok/s + probe latency, achieved HBM GB/s vs peak, 1 GPU",
         "value": round(value, 2),
@@ -298,8 +307,10 @@ def main():
         "decode_only_ms_per_step": round(dec_ms, 4),
         "decode_only_tok_s": round(B / (dec_ms / 1e3), 2),
         "probe_latency_ms": {"mean": round(float(np.mean(probe_ms)), 3) if probe_ms else None,
+                             "p50": round(float(np.median(probe_ms)), 3) if probe_ms else None,
                              "max": round(float(np.max(probe_ms)), 3) if probe_ms else None, "n": len(probe_ms)}
-        if not wl.mixed else {"mean": round(ms_per_step, 3), "max": None, "n": probes_timed},
+        if not wl.mixed else {"mean": round(ms_per_step, 3), "p50": None, "max": None, "n": probes_timed},
+        "host_decision_us": round(host_decision_us, 3),
         "probe": {"mode": "mixed", "probes_in_timed_region": probes_timed,
                   "latency_meaning": "each step's probes finish within it: one forward with the decode rows and the "
                                      "probing half's suffix chunks, then T-1 forwards of trial rows",
