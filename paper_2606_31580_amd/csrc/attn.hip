@@ -398,7 +398,7 @@ __global__ __launch_bounds__(64 * kAttnWaves) void k_attn(AttnArgs a) {
 // (all loads of a wave issued together, before the plan lookup), lanes take dims; the
 // waves are then combined in LDS in fixed order.
 constexpr int kMergeWaves = 16;
-__global__ __launch_bounds__(64 * kMergeWaves) void k_attn_merge(AttnArgs a, int hd) {
+__global__ __launch_bounds__(64 * kMergeWaves) void k_attn_merge(AttnArgs a, int hd, int nslots) {
   constexpr int PER = kAttnMaxWG / kMergeWaves;
   __shared__ float s_m[kMergeWaves], s_l[kMergeWaves];
   __shared__ float s_o[kMergeWaves][128];
@@ -407,12 +407,14 @@ __global__ __launch_bounds__(64 * kMergeWaves) void k_attn_merge(AttnArgs a, int
   const int kvh = head / a.G, gi = head - kvh * a.G;
   const size_t ncols = (size_t)a.max_rows * a.G;
   const size_t col = (size_t)row * a.G + gi;
-  // every slot is loaded before the group's workgroup count is known (slots past it are
-  // replaced below, never combined), so the loads overlap the plan lookup
+  // Every slot is loaded before the row's own workgroup count is known (slots past it are
+  // replaced below, never combined), so the loads overlap the plan lookup.  Slots at or past
+  // nslots (the launch's bound on every group's count) read slot nslots - 1 again, a cached
+  // line, instead of stale partials; the loads stay unconditional so none waits for another.
   float mv[PER], lv[PER], o0[PER], o1[PER];
 #pragma unroll
   for (int i = 0; i < PER; ++i) {
-    const size_t sb = ((size_t)kvh * kAttnMaxWG + v + kMergeWaves * i) * ncols + col;
+    const size_t sb = ((size_t)kvh * kAttnMaxWG + min(v + kMergeWaves * i, nslots - 1)) * ncols + col;
     mv[i] = a.ml[sb * 2];
     lv[i] = a.ml[sb * 2 + 1];
     o0[i] = a.part[sb * hd + l];
@@ -463,8 +465,9 @@ __global__ __launch_bounds__(64 * kMergeWaves) void k_attn_merge(AttnArgs a, int
   }
 }
 
-hipError_t launch_attn_merge(const AttnArgs& a, int M, int hd, hipStream_t s) {
-  return launch_k(k_attn_merge, dim3(M, a.hq), dim3(64 * kMergeWaves), s, a, hd);
+hipError_t launch_attn_merge(const AttnArgs& a, int M, int hd, int nslots, hipStream_t s) {
+  if (nslots < 1 || nslots > kAttnMaxWG) return hipErrorInvalidValue;
+  return launch_k(k_attn_merge, dim3(M, a.hq), dim3(64 * kMergeWaves), s, a, hd, nslots);
 }
 
 template <class KT, int HD>

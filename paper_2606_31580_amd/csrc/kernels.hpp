@@ -157,7 +157,7 @@ hipError_t launch_ksplit_reduce(const GemmArgs& a, hipStream_t s);
 hipError_t launch_tile_weights(int dtype, int epi, const GemmArgs& a, char* dst, hipStream_t s);
 // dtype: the KV element type, 0 fp32, 1 bf16, 2 fp8 (E4M3).
 hipError_t launch_attn(int dtype, int hd, int nt, const AttnArgs& a, dim3 grid, hipStream_t s);
-hipError_t launch_attn_merge(const AttnArgs& a, int M, int hd, hipStream_t s);
+hipError_t launch_attn_merge(const AttnArgs& a, int M, int hd, int nslots, hipStream_t s);  // nslots >= every group's nwg
 hipError_t launch_lm_reduce(const Plan* plan, const LmPart* part, int n_groups, int n_out, hipStream_t s);
 hipError_t launch_embed(int dtype, const Plan* plan, int M, const void* embed, int d, int vocab, float* h, int* bt,
                         int max_pps, hipStream_t s);

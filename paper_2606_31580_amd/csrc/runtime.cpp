@@ -912,7 +912,7 @@ static laser_status launch_forward(laser_model* m, laser_kv* kv, const FwdKey& k
     aa.layer = li;
     HIP_TRY(timed(m, LASER_K_ATTN, s, [&] {
       hipError_t e = launch_attn(m->kv_fp8 ? 2 : dt, hd, key.nt, aa, agrid, s);
-      if (e == hipSuccess && key.merge) e = launch_attn_merge(aa, key.M, hd, s);
+      if (e == hipSuccess && key.merge) e = launch_attn_merge(aa, key.M, hd, key.agx, s);
       return e;
     }));
 
