@@ -89,7 +89,10 @@ def main():
     R = args.probe_rows
     if wl.mixed:  # every step: decode for the batch + probe chunks of a seeded half, one forward
         schedule = synth.make_mixed_schedule(B, total_steps + 64)
-        rows = max(B + max(len(x) for x in schedule) * S, B * S)
+        if args.probe_mode == "riding":  # decode rows + new suffix chunks + one trial row per probe in flight
+            rows = B + max(len(x) for x in schedule) * (S + T - 1)
+        else:
+            rows = max(B + max(len(x) for x in schedule) * S, B * S)
     else:
         rows = max(B + B * R, B * S)
     if rows > 64:
@@ -100,7 +103,11 @@ def main():
     pps = max_pos // PAGE + 1
     num_pages = sum((n + 2 * total_steps + S + T) // PAGE + 2 for n in lens) + B * ((S + T) // PAGE + 3) + 8
     num_pages += (COST_CTX + 512) // PAGE + 4  # the cost-model pass (a shorter request in a fork slot)
-    kv = L.KVCache(model, num_pages, 2 * B, pps)  # slots B..2B-1 hold the probes' forks
+    # fork slots after the B requests: one per request, or (mixed workload, riding probes) one per
+    # probe in flight: a seeded half of the batch starts a probe every step and each lives T forwards
+    P_SLOTS = max(len(x) for x in schedule) * T if (wl.mixed and args.probe_mode == "riding") else B
+    num_pages += P_SLOTS * ((S + T) // PAGE + 3)
+    kv = L.KVCache(model, num_pages, B + P_SLOTS, pps)
     for i, n in enumerate(lens):
         k0, v0 = synth.make_prefill_kv(shape, n, i, device=dev)
         kv.add_seq(i, n)
@@ -129,7 +136,57 @@ def main():
             L.laser_exit_decision(params, load_state, float(c[b]), B, 0, 10)
         n_probes[0] += 1
 
+    # mixed workload, riding probes: each probe is a fork of its request (slot B + f) whose S
+    # suffix rows ride in one forward and whose T-1 trial rows ride in the next forwards, all
+    # beside the batch's decode rows.  tokbuf = [suffix | T trial tokens per slot]; the
+    # trial tokens are written and read there, their probabilities at the same offsets of pbuf.
+    tokbuf = torch.zeros(S + P_SLOTS * T, dtype=torch.int32, device=dev)
+    tokbuf[:S].copy_(suffix)
+    pbuf = torch.zeros(S + P_SLOTS * T, device=dev)
+    free_slots = list(range(P_SLOTS))
+    inflight = []  # [slot, request, trials done, fork event]
+    skipped = [0]
+
+    def step_mixed_riding(i, timed_probe, new_probes=True):
+        spans = [L.span(b, 1, 0, b, out=(0, b)) for b in seqs]
+        for pr in inflight:  # one trial row per probe in flight, fed its previous trial token
+            f, j = pr[0], pr[2] + 1
+            spans.append(L.span(B + f, 1, 1, S + f * T + j - 1, out=(1, S + f * T + j)))
+            pr[2] = j
+        if new_probes:
+            for b in schedule[i % len(schedule)]:
+                if not free_slots:
+                    skipped[0] += 1
+                    continue
+                f = free_slots.pop()
+                ev0 = torch.cuda.Event(enable_timing=True)
+                ev0.record(stream)
+                kv.fork(b, B + f)
+                spans.append(L.span(B + f, S, 1, 0, out=(1, S + f * T)))
+                inflight.append([f, b, 0, ev0])
+        L.laser_forward(model, kv, spans, tokens, tokbuf, nxt, pmax, tokbuf, pbuf)
+        tokens.copy_(nxt)
+        done = [pr for pr in inflight if pr[2] == T - 1]
+        if not done:
+            return
+        for k, pr in enumerate(done):
+            L.laser_confidence(model, pbuf[S + pr[0] * T:], T, 1, conf[k:])
+        ev1 = torch.cuda.Event(enable_timing=True)
+        ev1.record(stream)
+        c = conf.cpu().numpy()
+        for k, pr in enumerate(done):
+            L.laser_exit_decision(params, load_state, float(c[k]), B, 0, 10)
+            kv.free_seq(B + pr[0])
+            free_slots.append(pr[0])
+            inflight.remove(pr)
+            if timed_probe:  # device time from the fork to the confidence (the decode forwards included)
+                probe_ms.append(pr[3].elapsed_time(ev1))
+        n_probes[0] += len(done)
+
     def step(i, timed_probe):
+        if wl.mixed and args.probe_mode == "riding":
+            step_mixed_riding(i, timed_probe)
+            return
         if wl.mixed:  # the probes of this step run in the same forwards as its decode
             pidx = schedule[i % len(schedule)]
             L.laser_step_mixed(model, kv, seqs, tokens, nxt, pmax, pidx, suffix, T, conf, argm)
@@ -190,12 +247,16 @@ def main():
         step(i, False)
     while ride:  # no probe crosses into the timed region
         step(-1, False)
+    while inflight:
+        step_mixed_riding(-1, False, new_probes=False)
     torch.cuda.synchronize()
     n_probes[0] = 0
 
     if args.profile_only:  # the timed loop's work (decode steps with their probes), nothing else
         for i in range(args.steps):
             step(args.warmup + i, False)
+        while inflight:
+            step_mixed_riding(-1, False, new_probes=False)
         torch.cuda.synchronize()
         log("profile loop done")
         return
@@ -216,6 +277,8 @@ def main():
     probes_timed = n_probes[0]
     while ride:  # a probe still riding: finish it outside the timed region
         step(-1, False)
+    while inflight:
+        step_mixed_riding(-1, False, new_probes=False)
     # reference: the probe run as separate forwards (the cost it has when nothing rides along)
     sep_ms = []
     for _ in range(2):
@@ -309,9 +372,17 @@ def main():
         "probe_latency_ms": {"mean": round(float(np.mean(probe_ms)), 3) if probe_ms else None,
                              "p50": round(float(np.median(probe_ms)), 3) if probe_ms else None,
                              "max": round(float(np.max(probe_ms)), 3) if probe_ms else None, "n": len(probe_ms)}
-        if not wl.mixed else {"mean": round(ms_per_step, 3), "p50": None, "max": None, "n": probes_timed},
+        if not (wl.mixed and args.probe_mode == "separate")
+        else {"mean": round(ms_per_step, 3), "p50": None, "max": None, "n": probes_timed},
         "host_decision_us": round(host_decision_us, 3),
-        "probe": {"mode": "mixed", "probes_in_timed_region": probes_timed,
+        "probe": {"mode": "mixed, riding", "probes_in_timed_region": probes_timed, "forwards_per_probe": T,
+                  "probes_skipped_no_slot": skipped[0],
+                  "latency_meaning": "device time from the fork to the confidence: the probing half's suffix chunks "
+                                     "ride in one forward with the batch's decode rows, each trial row in one of the "
+                                     "next T-1",
+                  "separate_probe_latency_ms": round(float(np.mean(sep_ms)), 3)}
+        if wl.mixed and args.probe_mode == "riding" else
+                 {"mode": "mixed", "probes_in_timed_region": probes_timed,
                   "latency_meaning": "each step's probes finish within it: one forward with the decode rows and the "
                                      "probing half's suffix chunks, then T-1 forwards of trial rows",
                   "separate_probe_latency_ms": round(float(np.mean(sep_ms)), 3)} if wl.mixed else

@@ -126,3 +126,81 @@ def test_riding_probe_1p5b_bf16():
     suffix = [int(t) for t in synth.make_suffix(S, shape.vocab)]
     # the benchmark's setting: the 8 suffix rows ride in one forward (9 rows: the MFMA path)
     riding_probe_run(shape, model, orc, kv, opool, states, [0], [0], [2], 8, toks, suffix, "1.5B")
+
+
+def test_riding_probes_staggered_tiny():
+    # A new probe starts on every forward (rotating over the requests, so one request has
+    # several forks in flight); each probe's suffix chunk rides in its first forward and its
+    # trial rows in the next T-1, all beside the decode rows (the batch serving pattern).
+    require_gpu()
+    model, orc, _ = make_pair(TINY, max_rows=32, max_positions=1024)
+    P = T  # probe slots: one probe starts per forward and lives T forwards
+    kv, opool = kv_pair(model, TINY, num_pages=200, max_seqs=3 + P, max_pages_per_seq=64)
+    lens = [30, 64, 131]
+    states = []
+    for s, n in enumerate(lens):
+        K0, V0 = synth.make_prefill_kv(TINY, n, 40 + s)
+        kv.add_seq(s, n)
+        opool.add_seq(s, n)
+        kv.import_kv(s, K0.cuda(), V0.cuda())
+        states.append(SeqState.from_prefill(TINY, K0.numpy(), V0.numpy(), 1024))
+    seqs = [0, 1, 2]
+    suffix = [int(t) for t in synth.make_suffix(S, TINY.vocab)]
+    d_tok = torch.tensor([int(t) for t in synth.make_tokens(3, TINY.vocab, 3011)], dtype=torch.int32, device="cuda")
+    d_next = torch.zeros(3, dtype=torch.int32, device="cuda")
+    d_p = torch.zeros(3, device="cuda")
+    tokbuf = torch.zeros(S + P * T, dtype=torch.int32, device="cuda")
+    tokbuf[:S] = torch.tensor(suffix, dtype=torch.int32)
+    pbuf = torch.zeros(S + P * T, device="cuda")
+    d_conf = torch.zeros(1, device="cuda")
+    free, inflight, checked = list(range(P)), [], 0
+    n_fwd = 10
+    for fwd in range(n_fwd + T - 1):
+        spans = [L.span(b, 1, 0, i, out=(0, i)) for i, b in enumerate(seqs)]
+        fork_rows = []  # (fork slot, rows) in span order: pages are taken in that order
+        for pr in inflight:  # [slot, request, trials done, request state at the fork]
+            f, j = pr[0], pr[2] + 1
+            spans.append(L.span(3 + f, 1, 1, S + f * T + j - 1, out=(1, S + f * T + j)))
+            fork_rows.append((3 + f, 1))
+            pr[2] = j
+        if fwd < n_fwd:
+            b = seqs[fwd % 3]
+            f = free.pop()
+            kv.fork(b, 3 + f)
+            opool.fork(b, 3 + f)
+            assert kv.page_table(3 + f) == opool.tables[3 + f], f"fork table at forward {fwd}"
+            spans.append(L.span(3 + f, S, 1, 0, out=(1, S + f * T)))
+            fork_rows.append((3 + f, S))
+            inflight.append([f, b, 0, states[b].copy()])
+        L.laser_forward(model, kv, spans, d_tok, tokbuf, d_next, d_p, tokbuf, pbuf)
+        torch.cuda.synchronize()
+        for b in seqs:
+            opool.append(b, 1)
+        for f, n in fork_rows:
+            opool.append(f, n)
+        for i, b in enumerate(seqs):
+            ref = orc.decode_token(states[b], int(d_tok[i].item()))
+            check_token(d_next[i].item(), ref, f"staggered: decode seq {b} forward {fwd}")
+            assert abs(d_p[i].item() - lm_stats(ref)[1]) <= PROB_TOL
+            assert kv.page_table(b) == opool.tables[b]
+        for pr in inflight:
+            assert kv.page_table(3 + pr[0]) == opool.tables[3 + pr[0]], f"fork table after forward {fwd}"
+        d_tok.copy_(d_next)
+        for pr in [p for p in inflight if p[2] == T - 1]:
+            f, b = pr[0], pr[1]
+            L.laser_confidence(model, pbuf[S + f * T:], T, 1, d_conf)
+            torch.cuda.synchronize()
+            res = orc.probe(pr[3], suffix, T)
+            got = [int(x) for x in tokbuf[S + f * T:S + (f + 1) * T].cpu().numpy()]
+            if got == res.tokens:
+                assert abs(d_conf.item() - res.confidence) <= PROB_TOL, f"probe of seq {b} (slot {f})"
+            else:
+                assert any(m <= 1e-2 for m in res.margins), f"probe of seq {b}: trials {got} vs {res.tokens}"
+            kv.free_seq(3 + f)
+            opool.free_seq(3 + f)
+            free.append(f)
+            inflight.remove(pr)
+            checked += 1
+    assert checked == n_fwd and not inflight
+    for b in seqs:
+        assert kv.page_table(b) == opool.tables[b] and kv.seq_len(b) == states[b].length
