@@ -74,7 +74,7 @@ __global__ __launch_bounds__(64 * kAttnWaves) void k_attn(AttnArgs a) {
   for (int dt = 0; dt < ND; ++dt) o[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
 
   const int split = tpar ? wg : wg * kAttnWaves + w;
-  const int p0 = split * gd.pps;
+  const int p0 = gd.pbeg + split * gd.pps;
   const int p1 = min(p0 + gd.pps, gd.npages);
   const int* btrow = a.bt + (size_t)gd.seq * a.max_pps;
   const size_t layer_base = (size_t)a.layer * a.num_pages;
@@ -375,7 +375,7 @@ __global__ __launch_bounds__(64 * kAttnWaves) void k_attn(AttnArgs a) {
   // ---- this wave's columns: the output (one workgroup) or the workgroup's partial
   if (c >= NQ) return;
   const int row = gd.row0 + c / a.G, head = kvh * a.G + c % a.G;
-  if (gd.nwg == 1) {
+  if (gd.direct) {
     float* out = a.o + ((size_t)row * a.hq + head) * HD;
     const float inv = 1.f / l_run;
 #pragma unroll
@@ -383,7 +383,7 @@ __global__ __launch_bounds__(64 * kAttnWaves) void k_attn(AttnArgs a) {
     return;
   }
   const size_t ncols = (size_t)a.max_rows * a.G;
-  const size_t col = ((size_t)kvh * kAttnMaxWG + wg) * ncols + (size_t)gd.row0 * a.G + c;
+  const size_t col = ((size_t)kvh * kAttnMaxWG + gd.slot0 + wg) * ncols + (size_t)gd.row0 * a.G + c;
 #pragma unroll
   for (int dt = 0; dt < ND; ++dt) *(f32x4*)(a.part + col * HD + 16 * dt + 4 * lg) = o[dt];
   if (lg == 0) {
@@ -420,7 +420,7 @@ __global__ __launch_bounds__(64 * kMergeWaves) void k_attn_merge(AttnArgs a, int
     o0[i] = a.part[sb * hd + l];
     o1[i] = (l + 64 < hd) ? a.part[sb * hd + l + 64] : 0.f;
   }
-  const int nwg = a.plan->groups[a.plan->row_group[row]].nwg;
+  const int nwg = a.plan->row_nslots[row];
   if (nwg <= 1) return;  // written directly by the attention kernel
 #pragma unroll
   for (int i = 0; i < PER; ++i)

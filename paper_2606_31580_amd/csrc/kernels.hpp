@@ -22,10 +22,15 @@ constexpr int kMaxKsplit = 4;       // K shares of a residual projection on the 
 struct RowDesc {
   int seq, pos, tok_sel, tok_off;  // token = tok_base[tok_sel][tok_off]
 };
-// Rows of one request that share its KV pages in attention (contiguous rows).
+// Contiguous rows that attend over pages [pbeg, npages) of sequence seq's block table: the
+// rows of one request, or (shared prefix) the rows of a request and its forks over the full
+// pages they share, whose own later pages are then separate groups.
 struct GroupDesc {
-  int seq, row0, nrows, npages, pps, nwg;  // pps: pages per wave split; nwg: workgroups
+  int seq, row0, nrows, npages, pps, nwg;  // npages: end page; pps: pages per wave split; nwg: workgroups
   int maxpos;                              // last position any row of the group sees
+  int pbeg;                                // first page
+  int slot0;                               // first partial slot of the group's workgroups
+  int direct;                              // the group alone covers its rows in one workgroup: no merge
 };
 // LM-head output row: activation row, destination (sel, off) for token / prob / logits.
 struct OutDesc {
@@ -50,7 +55,7 @@ struct Plan {
   PlanIO io;
   RowDesc rows[kMaxRows];
   GroupDesc groups[kMaxRows];
-  int row_group[kMaxRows];  // group of each row
+  int row_nslots[kMaxRows];  // attention partial slots of each row (over all its groups)
   OutDesc outs[kMaxRows];
   BtUpdate bt[kMaxBt];
 };

@@ -89,11 +89,11 @@ struct Layout {
 // buffers inside the plan, these values fix every kernel launch of the forward and all of
 // its arguments, so one captured graph serves every forward with the same key.
 struct FwdKey {
-  int M, n_out, n_groups, nt, agx, merge;
+  int M, n_out, n_groups, nt, agx, mslots, merge;
   uint64_t kv_id;
   bool operator==(const FwdKey& o) const {
-    return M == o.M && n_out == o.n_out && n_groups == o.n_groups && nt == o.nt && agx == o.agx && merge == o.merge &&
-           kv_id == o.kv_id;
+    return M == o.M && n_out == o.n_out && n_groups == o.n_groups && nt == o.nt && agx == o.agx &&
+           mslots == o.mslots && merge == o.merge && kv_id == o.kv_id;
   }
 };
 
@@ -716,38 +716,144 @@ static laser_status flush_pending(laser_kv* kv, laser_model* m, hipStream_t s) {
   return LASER_OK;
 }
 
-// Fill row groups (contiguous rows of one request) and their attention splits.
-static void plan_groups(const laser_model* m, Plan& p) {
+// Row groups and their attention splits.  Rows come in runs of one sequence (spans).  Runs
+// whose sequences start with the same page are a request and its forks: they share their
+// leading full pages, so one group over those pages holds the rows of all of them (each
+// shared page is read once for every row), and each run keeps a group of its own for its
+// later pages.  A row's partials from the two are merged like any split.  The rows are
+// reordered so that a family's runs are contiguous (outputs follow their rows).
+static void plan_groups(const laser_model* m, const laser_kv* kv, Plan& p) {
   const laser_model_desc& d = m->desc;
   const int G = d.n_q_heads / d.n_kv_heads;
-  const int cap = std::max(1, 64 / G);  // query columns of a group fit 4 MFMA n-tiles
-  p.n_groups = 0;
-  long long units = 0;
+  const int cap = std::max(1, 64 / G);  // rows whose query columns fit 4 MFMA n-tiles
+  struct Run {
+    int seq, r0, r1, family;
+  };
+  std::vector<Run> runs;
   for (int r = 0; r < p.M;) {
     int e = r + 1;
-    while (e < p.M && p.rows[e].seq == p.rows[r].seq && e - r < cap) ++e;
-    int maxpos = 0;
-    for (int q = r; q < e; ++q) maxpos = std::max(maxpos, p.rows[q].pos);
-    for (int q = r; q < e; ++q) p.row_group[q] = p.n_groups;
-    GroupDesc& g = p.groups[p.n_groups++];
-    g.seq = p.rows[r].seq;
-    g.row0 = r;
-    g.nrows = e - r;
-    g.npages = maxpos / kPage + 1;
-    g.maxpos = maxpos;
-    // a group of one 16-column tile spreads its pages over the 4 waves of a workgroup; a
-    // wider one runs the same pages on all 4 waves, one tile each
-    units += (long long)g.npages * d.n_kv_heads * (ceil_div(g.nrows * G, 16) > 1 ? kAttnWaves : 1);
+    while (e < p.M && p.rows[e].seq == p.rows[r].seq) ++e;
+    runs.push_back({p.rows[r].seq, r, e, -1});
     r = e;
+  }
+  struct Family {
+    std::vector<int> members;  // runs
+    int shared;                // leading full pages shared by every member (0: none)
+  };
+  std::vector<Family> fams;
+  for (size_t i = 0; i < runs.size(); ++i) {
+    if (runs[i].family >= 0) continue;
+    const std::vector<int>& ti = kv->pool.table(runs[i].seq);
+    runs[i].family = (int)fams.size();
+    Family f{{(int)i}, 0};
+    for (size_t j = i + 1; j < runs.size() && !ti.empty(); ++j) {
+      const std::vector<int>& tj = kv->pool.table(runs[j].seq);
+      if (runs[j].family < 0 && !tj.empty() && tj[0] == ti[0]) {
+        runs[j].family = (int)fams.size();
+        f.members.push_back((int)j);
+      }
+    }
+    if (f.members.size() > 1) {
+      int sh = (int)ti.size();
+      for (int k : f.members) {
+        const std::vector<int>& t = kv->pool.table(runs[k].seq);
+        int n = 0, minpos = p.rows[runs[k].r0].pos;
+        while (n < (int)t.size() && n < (int)ti.size() && t[n] == ti[n]) ++n;
+        for (int r = runs[k].r0; r < runs[k].r1; ++r) minpos = std::min(minpos, p.rows[r].pos);
+        // only pages wholly below the run's first position (every row sees all of them)
+        sh = std::min(sh, std::min(n, minpos / kPage));
+        if (runs[k].r1 - runs[k].r0 > cap) sh = 0;  // a long run keeps its own groups
+      }
+      f.shared = sh;
+    }
+    fams.push_back(f);
+  }
+  // family by family, runs in their order
+  std::vector<int> order, newrow(p.M);
+  for (const Family& f : fams)
+    for (int k : f.members)
+      for (int r = runs[k].r0; r < runs[k].r1; ++r) {
+        newrow[r] = (int)order.size();
+        order.push_back(r);
+      }
+  bool moved = false;
+  for (int i = 0; i < p.M; ++i) moved |= order[i] != i;
+  if (moved) {
+    std::vector<RowDesc> old(p.rows, p.rows + p.M);
+    for (int i = 0; i < p.M; ++i) p.rows[i] = old[order[i]];
+    for (int o = 0; o < p.n_out; ++o) p.outs[o].row = newrow[p.outs[o].row];
+    for (Run& rn : runs) {
+      const int n = rn.r1 - rn.r0;
+      rn.r0 = newrow[rn.r0];
+      rn.r1 = rn.r0 + n;
+    }
+  }
+
+  p.n_groups = 0;
+  long long units = 0;
+  std::vector<int> row_prefix(p.M, -1), row_own(p.M, -1);
+  auto add_group = [&](int seq, int r0, int r1, int pbeg, bool prefix) {
+    int maxpos = 0;
+    for (int q = r0; q < r1; ++q) maxpos = std::max(maxpos, p.rows[q].pos);
+    const int gi = p.n_groups++;
+    GroupDesc& g = p.groups[gi];
+    g.seq = seq;
+    g.row0 = r0;
+    g.nrows = r1 - r0;
+    g.pbeg = pbeg;
+    g.npages = prefix ? pbeg : maxpos / kPage + 1;  // (a prefix group's end is set by its caller)
+    g.maxpos = maxpos;
+    g.slot0 = 0;
+    g.direct = 0;
+    for (int q = r0; q < r1; ++q) (prefix ? row_prefix : row_own)[q] = gi;
+    return gi;
+  };
+  for (const Family& f : fams) {
+    if (f.shared > 0) {  // groups of whole runs over the shared pages, at most cap rows each
+      size_t k = 0;
+      while (k < f.members.size()) {
+        const int r0 = runs[f.members[k]].r0;
+        int r1 = runs[f.members[k]].r1;
+        size_t e = k + 1;
+        while (e < f.members.size() && runs[f.members[e]].r1 - r0 <= cap) r1 = runs[f.members[e++]].r1;
+        const int gi = add_group(runs[f.members[k]].seq, r0, r1, 0, true);
+        p.groups[gi].npages = f.shared;
+        k = e;
+      }
+    }
+    for (int k : f.members)  // each run's own pages, at most cap rows per group
+      for (int r = runs[k].r0; r < runs[k].r1; r += cap)
+        add_group(runs[k].seq, r, std::min(runs[k].r1, r + cap), f.shared, false);
+  }
+  // a group of one 16-column tile spreads its pages over the 4 waves of a workgroup; a wider
+  // one runs the same pages on all 4 waves, one tile each
+  auto runs_per_wg = [&](const GroupDesc& g) { return ceil_div(g.nrows * G, 16) > 1 ? 1 : kAttnWaves; };
+  for (int i = 0; i < p.n_groups; ++i) {
+    const GroupDesc& g = p.groups[i];
+    units += (long long)(g.npages - g.pbeg) * d.n_kv_heads * (runs_per_wg(g) == 1 ? kAttnWaves : 1);
   }
   const int base =
       std::min(kMaxPagesPerWave, std::max(1, (int)((units + kTargetAttnWaves - 1) / kTargetAttnWaves)));
+  // partial slots of a row: its shared-pages group's workgroups, then its own group's; own
+  // groups next to a shared one get at most kOwnSlots workgroups
+  constexpr int kOwnSlots = 8;
   for (int i = 0; i < p.n_groups; ++i) {
     GroupDesc& g = p.groups[i];
-    const int runs_per_wg = ceil_div(g.nrows * G, 16) > 1 ? 1 : kAttnWaves;  // page runs per workgroup
-    g.pps = std::max(base, ceil_div(g.npages, kAttnMaxWG * runs_per_wg));
-    g.nwg = ceil_div(g.npages, runs_per_wg * g.pps);
+    const bool shares = row_prefix[g.row0] >= 0;
+    const bool is_prefix = row_prefix[g.row0] == i;
+    const int max_wg = is_prefix ? kAttnMaxWG - kOwnSlots : (shares ? kOwnSlots : kAttnMaxWG);
+    const int npg = g.npages - g.pbeg;
+    g.pps = std::max(base, ceil_div(npg, max_wg * runs_per_wg(g)));
+    g.nwg = ceil_div(npg, runs_per_wg(g) * g.pps);
   }
+  for (int i = 0; i < p.n_groups; ++i) {
+    GroupDesc& g = p.groups[i];
+    const int pre = row_prefix[g.row0];
+    if (pre >= 0 && pre != i) g.slot0 = p.groups[pre].nwg;
+    g.direct = pre < 0 && g.nwg == 1;
+  }
+  for (int q = 0; q < p.M; ++q)
+    p.row_nslots[q] = p.groups[row_own[q]].nwg + (row_prefix[q] >= 0 ? p.groups[row_prefix[q]].nwg : 0);
 }
 
 static laser_status launch_forward(laser_model* m, laser_kv* kv, const FwdKey& key, hipStream_t s);
@@ -759,22 +865,26 @@ static laser_status run_forward(laser_model* m, laser_kv* kv, Plan& p, const Pla
                                 bool allow_graph = true) {
   const laser_model_desc& d = m->desc;
   const int G = d.n_q_heads / d.n_kv_heads;
-  plan_groups(m, p);
+  plan_groups(m, kv, p);
   p.io = io;
   FwdKey key{};
   key.M = p.M;
   key.n_out = p.n_out;
   key.n_groups = p.n_groups;
-  int max_nwg = 1, nt = 1;
+  int max_nwg = 1, nt = 1, max_slots = 1;
+  bool merge = false;
   for (int i = 0; i < p.n_groups; ++i) {
     max_nwg = std::max(max_nwg, p.groups[i].nwg);
     nt = std::max(nt, ceil_div(p.groups[i].nrows * G, 16));
+    merge |= !p.groups[i].direct;
   }
+  for (int q = 0; q < p.M; ++q) max_slots = std::max(max_slots, p.row_nslots[q]);
   key.nt = nt == 3 ? 4 : nt;
-  // the grid is rounded up (extra workgroups exit at once) so that a growing context keeps
-  // the same key for a while
+  // the grid and the merge's slot bound are rounded up (extra workgroups exit at once) so
+  // that a growing context keeps the same key for a while
   key.agx = max_nwg == 1 ? 1 : std::min(kAttnMaxWG, ceil_div(max_nwg, 8) * 8);
-  key.merge = max_nwg > 1;
+  key.mslots = std::min(kAttnMaxWG, ceil_div(max_slots, 8) * 8);
+  key.merge = merge;
   key.kv_id = kv->id;
   Plan* dp = nullptr;
   laser_status st = upload_plan(m, p, s, &dp);
@@ -912,7 +1022,7 @@ static laser_status launch_forward(laser_model* m, laser_kv* kv, const FwdKey& k
     aa.layer = li;
     HIP_TRY(timed(m, LASER_K_ATTN, s, [&] {
       hipError_t e = launch_attn(m->kv_fp8 ? 2 : dt, hd, key.nt, aa, agrid, s);
-      if (e == hipSuccess && key.merge) e = launch_attn_merge(aa, key.M, hd, key.agx, s);
+      if (e == hipSuccess && key.merge) e = launch_attn_merge(aa, key.M, hd, key.mslots, s);
       return e;
     }));
 
