@@ -1,12 +1,13 @@
 // Paged grouped-query attention over the KV cache (decode rows and probe chunks).
 //
-// Work: grid (workgroup split, kv head, row group).  A row group is the rows of one request
-// in this forward (1 decode row, or the S rows of a probe chunk); its query columns are
-// (row, query head of this kv head) pairs, staged for up to NT 16-column tiles.  Each wave
-// holds one tile.  A group of one tile is page-parallel: each of the 4 waves walks its own
-// run of pages (split-K) and the waves merge (m, l, O) in one LDS round.  A wider group is
-// tile-parallel: wave w takes tile w and all waves walk the workgroup's run, so each page is
-// fetched from HBM once for all query columns.  Per page (16 positions):
+// Work: grid (work item, kv head).  A row group is contiguous rows over one page range of one
+// block table (the rows of a request in this forward, or of a request and its forks over
+// their shared pages); its query columns are (row, query head of this kv head) pairs in
+// 16-column tiles.  A work item is one tile of a group over one page split: each of the
+// workgroup's 4 waves walks its own run of pages (split-K) and the waves merge (m, l, O) in
+// one LDS round.  The host lists the tiles of one split 8 items apart: workgroups go to the
+// 8 XCDs in turn, so these land on one XCD and each page comes from HBM once into that XCD's
+// L2 for all of the group's columns.  Per page (16 positions):
 //   S^T[t][c] = K[t][:] . Q[c][:]   v_mfma_f32_16x16x32_bf16, A = K page, B = Q^T (bf16 hi+lo)
 //   online softmax over t per column (exp2 domain), causal mask t <= pos(c)
 //   O^T[d][c] += V^T[d][t] P^T[t][c] v_mfma_f32_16x16x16_bf16, B = P^T taken straight from
@@ -34,13 +35,12 @@ __device__ __forceinline__ void static_for(F&& f) {
 
 __device__ __forceinline__ float safe_exp2(float x) { return x == -INFINITY ? 0.f : exp2f(x); }
 
-template <class KT, int HD, int NT>
+template <class KT, int HD>
 __global__ __launch_bounds__(64 * kAttnWaves) void k_attn(AttnArgs a) {
   constexpr int NS = HD / 32;  // QK k-steps
   constexpr int ND = HD / 16;  // PV d-tiles
-  constexpr int NC = 16 * NT;  // padded query columns staged (up to NT tiles of 16)
-  // LDS: the group's queries (bf16 hi/lo) and, for page-parallel groups, the merge slots of
-  // waves 1-3 (one tile).  Rows are padded by 16 bytes, so the 16 columns a wave reads at
+  constexpr int NC = 16;       // query columns of the tile
+  // LDS: the tile's queries (bf16 hi/lo) and the merge slots of waves 1-3.  Rows are padded by 16 bytes, so the 16 columns a wave reads at
   // once (row stride) fall in 16 different bank groups instead of one.
   constexpr int QS = HD + 8;  // query row stride (bf16 elements)
   constexpr int OS = HD + 4;  // merge-slot row stride (floats)
@@ -51,32 +51,25 @@ __global__ __launch_bounds__(64 * kAttnWaves) void k_attn(AttnArgs a) {
   __shared__ float s_m[3][16];
   __shared__ float s_l[3][16];
 
-  const GroupDesc gd = a.plan->groups[blockIdx.z];
-  const int wg = blockIdx.x;
-  if (wg >= gd.nwg) return;
+  const AttnItem wi = a.plan->items[blockIdx.x];
+  if (wi.nrows == 0) return;  // padding item
+  const int NQ = wi.nrows * a.G;
   const int kvh = blockIdx.y;
   const int tid = threadIdx.x;
   const int w = tid >> 6, l = tid & 63;
   const int lc = l & 15, lg = l >> 4;
-  const int NQ = gd.nrows * a.G;
+  const int col0 = (wi.info & 0xff) * 16;  // the tile's first query column
 
-  // One 16-column query tile per wave.  A group of one tile splits its pages over the
-  // waves (page-parallel: wave w walks run 4 wg + w, then the waves merge through LDS); a
-  // wider group gives wave w tile w and every wave the workgroup's run (tile-parallel: each
-  // wave stores its own columns).  Either way a wave holds one tile's running sums.
-  const int ntile = (NQ + 15) >> 4;
-  const bool tpar = ntile > 1;
-  const int tile = tpar ? w : 0;
-  const bool active = tile < ntile;  // tile-parallel groups of fewer than 4 tiles idle a wave
+  // Wave w walks its run of the item's pages for the tile's 16 columns, then the waves merge
+  // through LDS.
   float m_run = -INFINITY, l_run = 0.f;
   f32x4 o[ND];
 #pragma unroll
   for (int dt = 0; dt < ND; ++dt) o[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  const int split = tpar ? wg : wg * kAttnWaves + w;
-  const int p0 = gd.pbeg + split * gd.pps;
-  const int p1 = min(p0 + gd.pps, gd.npages);
-  const int* btrow = a.bt + (size_t)gd.seq * a.max_pps;
+  const int p0 = wi.p0 + w * wi.pps;
+  const int p1 = min(p0 + wi.pps, wi.pend);
+  const int* btrow = a.bt + (size_t)wi.seq * a.max_pps;
   const size_t layer_base = (size_t)a.layer * a.num_pages;
   const size_t blk_elems = (size_t)16 * HD;
 
@@ -97,13 +90,13 @@ __global__ __launch_bounds__(64 * kAttnWaves) void k_attn(AttnArgs a) {
 #pragma unroll
   for (int i = 0; i < Q4; ++i) {  // padding columns load the last real one, zeroed when staged
     const int idx = 4 * (tid + i * 64 * kAttnWaves);
-    const int c = min(idx / HD, NQ - 1), d = idx % HD;
-    const int row = gd.row0 + c / a.G;
+    const int c = min(col0 + idx / HD, NQ - 1), d = idx % HD;
+    const int row = wi.row0 + c / a.G;
     const int head = kvh * a.G + c % a.G;
     qv[i] = *(const float4*)(a.q + ((size_t)row * a.hq + head) * HD + d);
   }
   static_assert(NC <= 64 * kAttnWaves, "one position per thread");
-  const int cpos_loaded = a.plan->rows[gd.row0 + min(tid, NQ - 1) / a.G].pos;  // column tid's position
+  const int cpos_loaded = a.plan->rows[wi.row0 + min(col0 + tid, NQ - 1) / a.G].pos;  // column tid's position
 
   // Page operands are loaded D pages ahead of their use into a ring of raw buffers (bf16
   // bits; fp32 pools are split into bf16 hi/lo when used).  A decode split is usually two
@@ -214,12 +207,12 @@ __global__ __launch_bounds__(64 * kAttnWaves) void k_attn(AttnArgs a) {
         P.vlo[dt] = l4;
       }
     }
-    if (pg * 16 + 15 > gd.maxpos) {
+    if (pg * 16 + 15 > wi.maxpos) {
 #pragma unroll
       for (int dt = 0; dt < ND; ++dt)
 #pragma unroll
         for (int j = 0; j < 4; ++j)
-          if (pg * 16 + 4 * lg + j > gd.maxpos) {
+          if (pg * 16 + 4 * lg + j > wi.maxpos) {
             P.vhi[dt][j] = 0;
             if (sizeof(KT) == 4) P.vlo[dt][j] = 0;
           }
@@ -265,7 +258,7 @@ __global__ __launch_bounds__(64 * kAttnWaves) void k_attn(AttnArgs a) {
 #pragma unroll
     for (int i = 0; i < Q4; ++i) {
       const int idx = 4 * (tid + i * 64 * kAttnWaves);
-      const bool real = idx / HD < NQ;
+      const bool real = col0 + idx / HD < NQ;
       const float x[4] = {real ? qv[i].x : 0.f, real ? qv[i].y : 0.f, real ? qv[i].z : 0.f, real ? qv[i].w : 0.f};
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
@@ -276,20 +269,18 @@ __global__ __launch_bounds__(64 * kAttnWaves) void k_attn(AttnArgs a) {
       }
     }
   }
-  if (tid < NC) s_pos[tid] = tid < NQ ? cpos_loaded : -1;
+  if (tid < NC) s_pos[tid] = col0 + tid < NQ ? cpos_loaded : -1;
   __syncthreads();
 
-  if (!active) return;  // (after the last barrier of a tile-parallel group)
-
   // pages in pairs: one max and one sum reduction across the lane groups per 32 positions
-  const int c = tile * 16 + lc;  // this lane's query column
+  const int c = col0 + lc;  // this lane's query column
   bf16x8 qh[NS], ql[NS];
 #pragma unroll
   for (int s = 0; s < NS; ++s) {
-    qh[s] = *(const bf16x8*)(s_qh + c * QS + 32 * s + 8 * lg);
-    ql[s] = *(const bf16x8*)(s_ql + c * QS + 32 * s + 8 * lg);
+    qh[s] = *(const bf16x8*)(s_qh + lc * QS + 32 * s + 8 * lg);
+    ql[s] = *(const bf16x8*)(s_ql + lc * QS + 32 * s + 8 * lg);
   }
-  const int cpos = s_pos[c];
+  const int cpos = s_pos[lc];
   auto pair = [&](int pgA, auto ca, auto cbB) {
     const int pgB = pgA + 1;
     const bool hasB = pgB < p1;  // wave-uniform
@@ -345,37 +336,35 @@ __global__ __launch_bounds__(64 * kAttnWaves) void k_attn(AttnArgs a) {
     });
   }
 
-  if (!tpar) {
-    // ---- one-round merge of the page-parallel waves: 1-3 publish, 0 absorbs in order
-    if (w > 0) {
+  // ---- one-round merge of the page-parallel waves: 1-3 publish, 0 absorbs in order
+  if (w > 0) {
 #pragma unroll
-      for (int dt = 0; dt < ND; ++dt) *(f32x4*)(s_of + (w - 1) * 16 * OS + lc * OS + 16 * dt + 4 * lg) = o[dt];
-      if (lg == 0) {
-        s_m[w - 1][lc] = m_run;
-        s_l[w - 1][lc] = l_run;
-      }
-    }
-    __syncthreads();
-    if (w != 0) return;
-#pragma unroll
-    for (int u = 0; u < 3; ++u) {
-      const float m2 = s_m[u][lc], l2 = s_l[u][lc];
-      const float mm = fmaxf(m_run, m2);
-      const float ca = (mm == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(m_run - mm);
-      const float cb2 = (mm == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(m2 - mm);
-      l_run = l_run * ca + l2 * cb2;
-      m_run = mm;
-#pragma unroll
-      for (int dt = 0; dt < ND; ++dt) {
-        const f32x4 x = *(const f32x4*)(s_of + u * 16 * OS + lc * OS + 16 * dt + 4 * lg);
-        o[dt] = o[dt] * ca + x * cb2;
-      }
+    for (int dt = 0; dt < ND; ++dt) *(f32x4*)(s_of + (w - 1) * 16 * OS + lc * OS + 16 * dt + 4 * lg) = o[dt];
+    if (lg == 0) {
+      s_m[w - 1][lc] = m_run;
+      s_l[w - 1][lc] = l_run;
     }
   }
-  // ---- this wave's columns: the output (one workgroup) or the workgroup's partial
+  __syncthreads();
+  if (w != 0) return;
+#pragma unroll
+  for (int u = 0; u < 3; ++u) {
+    const float m2 = s_m[u][lc], l2 = s_l[u][lc];
+    const float mm = fmaxf(m_run, m2);
+    const float ca = (mm == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(m_run - mm);
+    const float cb2 = (mm == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(m2 - mm);
+    l_run = l_run * ca + l2 * cb2;
+    m_run = mm;
+#pragma unroll
+    for (int dt = 0; dt < ND; ++dt) {
+      const f32x4 x = *(const f32x4*)(s_of + u * 16 * OS + lc * OS + 16 * dt + 4 * lg);
+      o[dt] = o[dt] * ca + x * cb2;
+    }
+  }
+  // ---- the tile's columns: the output (one workgroup) or the workgroup's partial
   if (c >= NQ) return;
-  const int row = gd.row0 + c / a.G, head = kvh * a.G + c % a.G;
-  if (gd.direct) {
+  const int row = wi.row0 + c / a.G, head = kvh * a.G + c % a.G;
+  if (wi.info & (1 << 24)) {
     float* out = a.o + ((size_t)row * a.hq + head) * HD;
     const float inv = 1.f / l_run;
 #pragma unroll
@@ -383,7 +372,7 @@ __global__ __launch_bounds__(64 * kAttnWaves) void k_attn(AttnArgs a) {
     return;
   }
   const size_t ncols = (size_t)a.max_rows * a.G;
-  const size_t col = ((size_t)kvh * kAttnMaxWG + gd.slot0 + wg) * ncols + (size_t)gd.row0 * a.G + c;
+  const size_t col = ((size_t)kvh * kAttnMaxWG + ((wi.info >> 8) & 0xffff)) * ncols + (size_t)wi.row0 * a.G + c;
 #pragma unroll
   for (int dt = 0; dt < ND; ++dt) *(f32x4*)(a.part + col * HD + 16 * dt + 4 * lg) = o[dt];
   if (lg == 0) {
@@ -471,26 +460,20 @@ hipError_t launch_attn_merge(const AttnArgs& a, int M, int hd, int nslots, hipSt
 }
 
 template <class KT, int HD>
-static hipError_t launch_nt(int nt, const AttnArgs& a, dim3 grid, hipStream_t s) {
-  const dim3 block(64 * kAttnWaves);
-  switch (nt) {
-    case 1: return launch_k(k_attn<KT, HD, 1>, grid, block, s, a);
-    case 2: return launch_k(k_attn<KT, HD, 2>, grid, block, s, a);
-    case 4: return launch_k(k_attn<KT, HD, 4>, grid, block, s, a);
-    default: return hipErrorInvalidValue;
-  }
+static hipError_t launch_hd(const AttnArgs& a, dim3 grid, hipStream_t s) {
+  return launch_k(k_attn<KT, HD>, grid, dim3(64 * kAttnWaves), s, a);
 }
 
-hipError_t launch_attn(int dtype, int hd, int nt, const AttnArgs& a, dim3 grid, hipStream_t s) {
+hipError_t launch_attn(int dtype, int hd, const AttnArgs& a, dim3 grid, hipStream_t s) {
   if (dtype == 2) {
-    if (hd == 128) return launch_nt<fp8_t, 128>(nt, a, grid, s);
-    if (hd == 64) return launch_nt<fp8_t, 64>(nt, a, grid, s);
+    if (hd == 128) return launch_hd<fp8_t, 128>(a, grid, s);
+    if (hd == 64) return launch_hd<fp8_t, 64>(a, grid, s);
   } else if (dtype == 1) {
-    if (hd == 128) return launch_nt<bf16_t, 128>(nt, a, grid, s);
-    if (hd == 64) return launch_nt<bf16_t, 64>(nt, a, grid, s);
+    if (hd == 128) return launch_hd<bf16_t, 128>(a, grid, s);
+    if (hd == 64) return launch_hd<bf16_t, 64>(a, grid, s);
   } else {
-    if (hd == 128) return launch_nt<float, 128>(nt, a, grid, s);
-    if (hd == 64) return launch_nt<float, 64>(nt, a, grid, s);
+    if (hd == 128) return launch_hd<float, 128>(a, grid, s);
+    if (hd == 64) return launch_hd<float, 64>(a, grid, s);
   }
   return hipErrorInvalidValue;
 }

@@ -12,7 +12,9 @@ constexpr int kMaxRows = 64;      // rows (tokens) of one forward
 constexpr int kPage = 16;         // positions per KV page
 constexpr int kMaxBt = 1024;      // block-table updates carried by one plan
 constexpr int kAttnWaves = 4;     // waves per attention workgroup (one split each)
-constexpr int kAttnMaxWG = 128;   // attention workgroups per (group, kv head)
+constexpr int kAttnMaxWG = 128;   // attention workgroups (page splits) per (group, kv head)
+constexpr int kMaxGroups = 2 * kMaxRows;  // own groups (one per run of rows) + shared-page groups
+constexpr int kMaxAttnItems = 8192;       // attention workgroups per kv head
 constexpr int kGemmThreads = 256; // 4 waves
 constexpr int kGemvMaxThreads = 512;
 constexpr int kMfmaMaxWaves = 8;    // waves of an MFMA projection workgroup with few row groups
@@ -32,6 +34,14 @@ struct GroupDesc {
   int slot0;                               // first partial slot of the group's workgroups
   int direct;                              // the group alone covers its rows in one workgroup: no merge
 };
+// One attention workgroup (per kv head): a group's 16-column query tile over 4 runs of pages,
+// wave w's run [p0 + w pps, min(p0 + (w + 1) pps, pend)).  nrows == 0: padding, no work.
+struct AttnItem {
+  int seq, row0, nrows;  // the group's block table and rows
+  int p0, pend, pps;
+  int maxpos;            // last position any row of the group sees
+  int info;              // tile (bits 0-7) | partial slot (bits 8-23) | direct output (bit 24)
+};
 // LM-head output row: activation row, destination (sel, off) for token / prob / logits.
 struct OutDesc {
   int row, sel, off, pad;
@@ -49,15 +59,17 @@ struct PlanIO {
   float* logits[2];       // optional logits rows [..][vocab], same index; may be null
 };
 
-// Everything the kernels of one forward need that changes per call; uploaded once.
+// Everything the kernels of one forward need that changes per call; uploaded once (the used
+// part of each array).
 struct Plan {
-  int M, n_groups, n_out, n_bt;
+  int M, n_groups, n_out, n_bt, n_items;
   PlanIO io;
   RowDesc rows[kMaxRows];
-  GroupDesc groups[kMaxRows];
   int row_nslots[kMaxRows];  // attention partial slots of each row (over all its groups)
   OutDesc outs[kMaxRows];
+  AttnItem items[kMaxAttnItems];
   BtUpdate bt[kMaxBt];
+  GroupDesc groups[kMaxGroups];  // (host side: the kernels read the work items)
 };
 
 // Softmax statistics of one group of vocabulary rows for one output row.
@@ -161,7 +173,7 @@ hipError_t launch_ksplit_reduce(const GemmArgs& a, hipStream_t s);
 // `a`, as weight_row maps them) to dst: a.n_groups groups x ceil(K/32) steps.
 hipError_t launch_tile_weights(int dtype, int epi, const GemmArgs& a, char* dst, hipStream_t s);
 // dtype: the KV element type, 0 fp32, 1 bf16, 2 fp8 (E4M3).
-hipError_t launch_attn(int dtype, int hd, int nt, const AttnArgs& a, dim3 grid, hipStream_t s);
+hipError_t launch_attn(int dtype, int hd, const AttnArgs& a, dim3 grid, hipStream_t s);
 hipError_t launch_attn_merge(const AttnArgs& a, int M, int hd, int nslots, hipStream_t s);  // nslots >= every group's nwg
 hipError_t launch_lm_reduce(const Plan* plan, const LmPart* part, int n_groups, int n_out, hipStream_t s);
 hipError_t launch_embed(int dtype, const Plan* plan, int M, const void* embed, int d, int vocab, float* h, int* bt,

@@ -89,11 +89,11 @@ struct Layout {
 // buffers inside the plan, these values fix every kernel launch of the forward and all of
 // its arguments, so one captured graph serves every forward with the same key.
 struct FwdKey {
-  int M, n_out, n_groups, nt, agx, mslots, merge;
+  int M, n_out, agx, mslots, merge;  // agx: attention work items (grid width)
   uint64_t kv_id;
-  bool operator==(const FwdKey& o) const {
-    return M == o.M && n_out == o.n_out && n_groups == o.n_groups && nt == o.nt && agx == o.agx &&
-           mslots == o.mslots && merge == o.merge && kv_id == o.kv_id;
+  // same launches apart from the attention grid width
+  bool same_shape(const FwdKey& o) const {
+    return M == o.M && n_out == o.n_out && mslots == o.mslots && merge == o.merge && kv_id == o.kv_id;
   }
 };
 
@@ -683,10 +683,14 @@ static laser_status upload_plan(laser_model* m, const Plan& p, hipStream_t s, Pl
   m->ring_pos = (m->ring_pos + 1) % kRing;
   if (m->ring_used[slot]) HIP_TRY(hipEventSynchronize(m->ring_ev[slot]));
   Plan* hp = m->h_plans + slot;
-  const size_t bytes = offsetof(Plan, bt) + sizeof(BtUpdate) * (size_t)p.n_bt;
+  // the used parts: everything up to the last work item, then the block-table updates
+  const size_t bytes = offsetof(Plan, items) + sizeof(AttnItem) * (size_t)p.n_items;
+  const size_t bt_bytes = sizeof(BtUpdate) * (size_t)p.n_bt;
   std::memcpy(hp, &p, bytes);
+  std::memcpy(hp->bt, p.bt, bt_bytes);
   Plan* dp = m->wsp<Plan>(m->lay.plans);  // stream order keeps forwards off each other's plan
   HIP_TRY(hipMemcpyAsync(dp, hp, bytes, hipMemcpyHostToDevice, s));
+  if (bt_bytes) HIP_TRY(hipMemcpyAsync(dp->bt, hp->bt, bt_bytes, hipMemcpyHostToDevice, s));
   HIP_TRY(hipEventRecord(m->ring_ev[slot], s));
   m->ring_used[slot] = true;
   *d_out = dp;
@@ -699,7 +703,7 @@ static laser_status flush_pending(laser_kv* kv, laser_model* m, hipStream_t s) {
   while (i < kv->pending.size()) {
     Plan* p = new (std::nothrow) Plan;
     if (!p) return laser_fail(LASER_ERR_INVALID_ARG, "allocation failed");
-    p->M = p->n_groups = p->n_out = 0;
+    p->M = p->n_groups = p->n_out = p->n_items = 0;
     p->n_bt = 0;
     while (i < kv->pending.size() && p->n_bt < kMaxBt) {
       const PageUpdate& u = kv->pending[i++];
@@ -716,16 +720,15 @@ static laser_status flush_pending(laser_kv* kv, laser_model* m, hipStream_t s) {
   return LASER_OK;
 }
 
-// Row groups and their attention splits.  Rows come in runs of one sequence (spans).  Runs
-// whose sequences start with the same page are a request and its forks: they share their
-// leading full pages, so one group over those pages holds the rows of all of them (each
-// shared page is read once for every row), and each run keeps a group of its own for its
-// later pages.  A row's partials from the two are merged like any split.  The rows are
-// reordered so that a family's runs are contiguous (outputs follow their rows).
+// Row groups, their attention splits and the attention work items.  Rows come in runs of one
+// sequence (spans).  Runs whose sequences start with the same page are a request and its
+// forks: they share their leading full pages, so one group over those pages holds the rows
+// of all of them (each shared page is read once for every row), and each run keeps a group
+// of its own for its later pages.  A row's partials from the two are merged like any split.
+// The rows are reordered so that a family's runs are contiguous (outputs follow their rows).
 static void plan_groups(const laser_model* m, const laser_kv* kv, Plan& p) {
   const laser_model_desc& d = m->desc;
   const int G = d.n_q_heads / d.n_kv_heads;
-  const int cap = std::max(1, 64 / G);  // rows whose query columns fit 4 MFMA n-tiles
   struct Run {
     int seq, r0, r1, family;
   };
@@ -762,7 +765,6 @@ static void plan_groups(const laser_model* m, const laser_kv* kv, Plan& p) {
         for (int r = runs[k].r0; r < runs[k].r1; ++r) minpos = std::min(minpos, p.rows[r].pos);
         // only pages wholly below the run's first position (every row sees all of them)
         sh = std::min(sh, std::min(n, minpos / kPage));
-        if (runs[k].r1 - runs[k].r0 > cap) sh = 0;  // a long run keeps its own groups
       }
       f.shared = sh;
     }
@@ -790,7 +792,6 @@ static void plan_groups(const laser_model* m, const laser_kv* kv, Plan& p) {
   }
 
   p.n_groups = 0;
-  long long units = 0;
   std::vector<int> row_prefix(p.M, -1), row_own(p.M, -1);
   auto add_group = [&](int seq, int r0, int r1, int pbeg, bool prefix) {
     int maxpos = 0;
@@ -809,42 +810,45 @@ static void plan_groups(const laser_model* m, const laser_kv* kv, Plan& p) {
     return gi;
   };
   for (const Family& f : fams) {
-    if (f.shared > 0) {  // groups of whole runs over the shared pages, at most cap rows each
-      size_t k = 0;
-      while (k < f.members.size()) {
-        const int r0 = runs[f.members[k]].r0;
-        int r1 = runs[f.members[k]].r1;
-        size_t e = k + 1;
-        while (e < f.members.size() && runs[f.members[e]].r1 - r0 <= cap) r1 = runs[f.members[e++]].r1;
-        const int gi = add_group(runs[f.members[k]].seq, r0, r1, 0, true);
-        p.groups[gi].npages = f.shared;
-        k = e;
-      }
+    if (f.shared > 0) {  // the rows of all members over the shared pages
+      const int gi = add_group(runs[f.members[0]].seq, runs[f.members[0]].r0, runs[f.members.back()].r1, 0, true);
+      p.groups[gi].npages = f.shared;
     }
-    for (int k : f.members)  // each run's own pages, at most cap rows per group
-      for (int r = runs[k].r0; r < runs[k].r1; r += cap)
-        add_group(runs[k].seq, r, std::min(runs[k].r1, r + cap), f.shared, false);
+    for (int k : f.members) add_group(runs[k].seq, runs[k].r0, runs[k].r1, f.shared, false);  // own pages
   }
-  // a group of one 16-column tile spreads its pages over the 4 waves of a workgroup; a wider
-  // one runs the same pages on all 4 waves, one tile each
-  auto runs_per_wg = [&](const GroupDesc& g) { return ceil_div(g.nrows * G, 16) > 1 ? 1 : kAttnWaves; };
-  for (int i = 0; i < p.n_groups; ++i) {
-    const GroupDesc& g = p.groups[i];
-    units += (long long)(g.npages - g.pbeg) * d.n_kv_heads * (runs_per_wg(g) == 1 ? kAttnWaves : 1);
-  }
-  const int base =
-      std::min(kMaxPagesPerWave, std::max(1, (int)((units + kTargetAttnWaves - 1) / kTargetAttnWaves)));
-  // partial slots of a row: its shared-pages group's workgroups, then its own group's; own
-  // groups next to a shared one get at most kOwnSlots workgroups
+  // A work item (workgroup) takes one 16-column query tile of a group and spreads a split of
+  // its pages over its 4 waves.  Splits of at most kMaxPagesPerWave pages per wave, enough
+  // of them to give about kTargetAttnWaves waves; a group of several tiles lists its splits
+  // in chunks of 8, tile by tile, so that the tiles of one split are 8 items apart (workgroups
+  // go to the 8 XCDs in turn: they share one XCD's L2).  Partial slots of a row: its
+  // shared-pages group's splits, then its own group's; own groups next to a shared one get at
+  // most kOwnSlots splits.
+  auto ntiles = [&](const GroupDesc& g) { return ceil_div(g.nrows * G, 16); };
+  long long units = 0;
+  for (int i = 0; i < p.n_groups; ++i)
+    units += (long long)(p.groups[i].npages - p.groups[i].pbeg) * d.n_kv_heads * ntiles(p.groups[i]);
   constexpr int kOwnSlots = 8;
-  for (int i = 0; i < p.n_groups; ++i) {
-    GroupDesc& g = p.groups[i];
-    const bool shares = row_prefix[g.row0] >= 0;
-    const bool is_prefix = row_prefix[g.row0] == i;
-    const int max_wg = is_prefix ? kAttnMaxWG - kOwnSlots : (shares ? kOwnSlots : kAttnMaxWG);
-    const int npg = g.npages - g.pbeg;
-    g.pps = std::max(base, ceil_div(npg, max_wg * runs_per_wg(g)));
-    g.nwg = ceil_div(npg, runs_per_wg(g) * g.pps);
+  int base = std::min(kMaxPagesPerWave, std::max(1, (int)((units + kTargetAttnWaves - 1) / kTargetAttnWaves)));
+  auto item_count = [&]() {
+    int n = 0;
+    for (int i = 0; i < p.n_groups; ++i) {
+      const GroupDesc& g = p.groups[i];
+      const int T = ntiles(g);
+      n = (T == 1 || g.nwg < 8) ? n + g.nwg * T : ceil_div(n, 8) * 8 + ceil_div(g.nwg, 8) * 8 * T;
+    }
+    return n;
+  };
+  for (;; base *= 2) {  // (more pages per wave only if the items would not fit)
+    for (int i = 0; i < p.n_groups; ++i) {
+      GroupDesc& g = p.groups[i];
+      const bool shares = row_prefix[g.row0] >= 0;
+      const bool is_prefix = row_prefix[g.row0] == i;
+      const int max_wg = is_prefix ? kAttnMaxWG - kOwnSlots : (shares ? kOwnSlots : kAttnMaxWG);
+      const int npg = g.npages - g.pbeg;
+      g.pps = std::max(base, ceil_div(npg, max_wg * kAttnWaves));
+      g.nwg = ceil_div(npg, kAttnWaves * g.pps);
+    }
+    if (item_count() <= kMaxAttnItems) break;
   }
   for (int i = 0; i < p.n_groups; ++i) {
     GroupDesc& g = p.groups[i];
@@ -854,6 +858,41 @@ static void plan_groups(const laser_model* m, const laser_kv* kv, Plan& p) {
   }
   for (int q = 0; q < p.M; ++q)
     p.row_nslots[q] = p.groups[row_own[q]].nwg + (row_prefix[q] >= 0 ? p.groups[row_prefix[q]].nwg : 0);
+
+  p.n_items = 0;
+  auto push = [&](const GroupDesc* g, int wg, int tile) {
+    AttnItem& it = p.items[p.n_items++];
+    if (!g) {
+      it = AttnItem{0, 0, 0, 0, 0, 0, 0, 0};
+      return;
+    }
+    it.seq = g->seq;
+    it.row0 = g->row0;
+    it.nrows = g->nrows;
+    it.p0 = g->pbeg + wg * kAttnWaves * g->pps;
+    it.pend = g->npages;
+    it.pps = g->pps;
+    it.maxpos = g->maxpos;
+    it.info = tile | (g->slot0 + wg) << 8 | (g->direct ? 1 << 24 : 0);
+  };
+  for (int i = 0; i < p.n_groups; ++i) {
+    const GroupDesc& g = p.groups[i];
+    const int T = ntiles(g);
+    if (T == 1 || g.nwg < 8) {
+      for (int t = 0; t < T; ++t)
+        for (int wg = 0; wg < g.nwg; ++wg) push(&g, wg, t);
+      continue;
+    }
+    while (p.n_items % 8) push(nullptr, 0, 0);
+    for (int c = 0; c < g.nwg; c += 8)
+      for (int t = 0; t < T; ++t)
+        for (int j = 0; j < 8; ++j) push(c + j < g.nwg ? &g : nullptr, c + j, t);
+  }
+}
+
+// Pads the work items with empty ones up to n (the grid width of the launch).
+static void pad_items(Plan& p, int n) {
+  while (p.n_items < n) p.items[p.n_items++] = AttnItem{0, 0, 0, 0, 0, 0, 0, 0};
 }
 
 static laser_status launch_forward(laser_model* m, laser_kv* kv, const FwdKey& key, hipStream_t s);
@@ -863,41 +902,43 @@ static laser_status launch_forward(laser_model* m, laser_kv* kv, const FwdKey& k
 // class is being timed).
 static laser_status run_forward(laser_model* m, laser_kv* kv, Plan& p, const PlanIO& io, hipStream_t s,
                                 bool allow_graph = true) {
-  const laser_model_desc& d = m->desc;
-  const int G = d.n_q_heads / d.n_kv_heads;
   plan_groups(m, kv, p);
   p.io = io;
   FwdKey key{};
   key.M = p.M;
   key.n_out = p.n_out;
-  key.n_groups = p.n_groups;
-  int max_nwg = 1, nt = 1, max_slots = 1;
+  int max_slots = 1;
   bool merge = false;
-  for (int i = 0; i < p.n_groups; ++i) {
-    max_nwg = std::max(max_nwg, p.groups[i].nwg);
-    nt = std::max(nt, ceil_div(p.groups[i].nrows * G, 16));
-    merge |= !p.groups[i].direct;
-  }
+  for (int i = 0; i < p.n_groups; ++i) merge |= !p.groups[i].direct;
   for (int q = 0; q < p.M; ++q) max_slots = std::max(max_slots, p.row_nslots[q]);
-  key.nt = nt == 3 ? 4 : nt;
-  // the grid and the merge's slot bound are rounded up (extra workgroups exit at once) so
-  // that a growing context keeps the same key for a while
-  key.agx = max_nwg == 1 ? 1 : std::min(kAttnMaxWG, ceil_div(max_nwg, 8) * 8);
+  // the merge's slot bound is rounded up so that a growing context keeps the same key for a
+  // while (the merge reads the row's own count)
   key.mslots = std::min(kAttnMaxWG, ceil_div(max_slots, 8) * 8);
   key.merge = merge;
   key.kv_id = kv->id;
+  // The attention grid is at least the item count, a multiple of 8 (so that item i runs on
+  // XCD i mod 8), padded with empty items.  A captured forward of the same shape whose grid
+  // is at most 1/8 (+64) wider is reused; a new one is captured 1/8 wider, so a growing
+  // context or a changing mix of probes does not recapture at every step.
+  const int need = std::max(8, ceil_div(p.n_items, 8) * 8);
+  const bool timing = timing_session(m);
+  const bool graphs = allow_graph && m->use_graphs && !timing;
+  GraphEntry* ge = nullptr;
+  if (graphs)
+    for (auto& g : m->graphs)
+      if (g.key.same_shape(key) && g.key.agx >= need && g.key.agx <= need + need / 8 + 64 &&
+          (!ge || g.key.agx < ge->key.agx))
+        ge = &g;
+  key.agx = ge ? ge->key.agx : graphs ? std::min(kMaxAttnItems, ceil_div(need + need / 8, 64) * 64) : need;
+  pad_items(p, key.agx);
   Plan* dp = nullptr;
   laser_status st = upload_plan(m, p, s, &dp);
   if (st != LASER_OK) return st;
-  const bool timing = timing_session(m);
-  if (!allow_graph || !m->use_graphs || timing) {
+  if (!graphs) {
     TimingScope scope(m);
     return launch_forward(m, kv, key, s);
   }
 
-  GraphEntry* ge = nullptr;
-  for (auto& g : m->graphs)
-    if (g.key == key) ge = &g;
   if (!ge) {
     hipGraph_t graph = nullptr;
     HIP_TRY(hipStreamBeginCapture(m->cap_stream, hipStreamCaptureModeThreadLocal));
@@ -999,7 +1040,7 @@ static laser_status launch_forward(laser_model* m, laser_kv* kv, const FwdKey& k
   aa.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)hd));
   aa.part = m->wsp<float>(L.attn_part);
   aa.ml = m->wsp<float>(L.attn_ml);
-  const dim3 agrid(key.agx, d.n_kv_heads, key.n_groups);
+  const dim3 agrid(key.agx, d.n_kv_heads);
 
   for (int li = 0; li < d.n_layers; ++li) {
     const LayerW& W = m->layers[li];
@@ -1021,7 +1062,7 @@ static laser_status launch_forward(laser_model* m, laser_kv* kv, const FwdKey& k
 
     aa.layer = li;
     HIP_TRY(timed(m, LASER_K_ATTN, s, [&] {
-      hipError_t e = launch_attn(m->kv_fp8 ? 2 : dt, hd, key.nt, aa, agrid, s);
+      hipError_t e = launch_attn(m->kv_fp8 ? 2 : dt, hd, aa, agrid, s);
       if (e == hipSuccess && key.merge) e = launch_attn_merge(aa, key.M, hd, key.mslots, s);
       return e;
     }));
