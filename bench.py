@@ -43,6 +43,8 @@ def parse():
                          "request; separate: the probe runs as its own forwards between decode steps")
     ap.add_argument("--probe-rows", type=int, default=8, help="probe rows per forward in riding mode")
     ap.add_argument("--no-tiles", action="store_true", help="MFMA path reads the row-major weights (no tile copy)")
+    ap.add_argument("--gemm-kernel", type=int, choices=[0, 1, 2], default=0,
+                    help="matrix-core projections: 0 by cost, 1 K-split waves only, 2 row waves where they apply")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 256 MiB device-to-device copy three times (scale for HBM byte counters)")
     return ap.parse_args()
@@ -100,6 +102,7 @@ def main():
         sys.exit(2)
     # the workspace takes the full 64 rows so that prompt prefills run in 64-token chunks
     model = L.Model(shape, weights, max_rows=64, max_positions=max_pos, tiles=not args.no_tiles)
+    model.set_gemm_kernel(args.gemm_kernel)
     pps = max_pos // PAGE + 1
     num_pages = sum((n + 2 * total_steps + S + T) // PAGE + 2 for n in lens) + B * ((S + T) // PAGE + 3) + 8
     num_pages += (COST_CTX + 512) // PAGE + 4  # the cost-model pass (a shorter request in a fork slot)

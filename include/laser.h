@@ -431,8 +431,8 @@ laser_status laser_timing_read(laser_model* m, int kernel_class, double* total_m
 /* Graph replay                                                               */
 /* ========================================================================== */
 /* With graphs on (the default), the kernels of a decode, probe or mixed forward are
- * captured once per launch signature (rows, outputs, request groups, attention grid, KV
- * cache) into a HIP graph and replayed; per-call data (positions, pages, the caller's
+ * captured once per launch signature (rows, outputs, attention grid width and merge
+ * bound, KV cache) into a HIP graph and replayed; per-call data (positions, pages, the caller's
  * token and output buffers) travels in the plan each forward uploads.  Results are
  * bitwise identical to launching the kernels one by one, which is what happens with
  * graphs off, while any kernel class is being timed, and for laser_prefill.  Up to 16
@@ -440,6 +440,18 @@ laser_status laser_timing_read(laser_model* m, int kernel_class, double* total_m
  * Forwards of one model must be ordered (one stream, or synchronised between streams):
  * they share the model's workspace and its one device plan slot. */
 laser_status laser_model_set_graphs(laser_model* m, int enable);
+
+/* Projection kernel choice on the matrix-core path (forwards of 3 to 64 rows; the linear
+ * maps of the transformer block, §4.1's decode and probe forwards).  Two kernels compute
+ * the same products: one splits K over the waves of a workgroup (1-4 row groups of 16
+ * weight rows per workgroup), the other gives each of 4 waves its own row groups and stages
+ * the activations once per workgroup in LDS.  mode 0 (the default) takes the second for the
+ * gate/up projection of forwards of 33 to 64 rows when it has enough row groups, and the
+ * first elsewhere; 1 uses only the first kernel; 2 the second wherever it applies (K a
+ * multiple of 8).  The summation order differs between them, so
+ * results may differ in the last bits.  Captured forwards are released when the mode
+ * changes.  Errors: LASER_ERR_STATE (bad model), LASER_ERR_INVALID_ARG (mode). */
+laser_status laser_model_set_gemm_kernel(laser_model* m, int mode);
 
 #ifdef __cplusplus
 }

@@ -23,16 +23,6 @@
 
 namespace laser {
 
-// Calls f(integral_constant<int, i>) for i = 0 .. N-1 (compile-time ring-buffer indices, so
-// register arrays are never indexed dynamically).
-template <int N, int I = 0, class F>
-__device__ __forceinline__ void static_for(F&& f) {
-  if constexpr (I < N) {
-    f(std::integral_constant<int, I>{});
-    static_for<N, I + 1>(f);
-  }
-}
-
 __device__ __forceinline__ float safe_exp2(float x) { return x == -INFINITY ? 0.f : exp2f(x); }
 
 template <class KT, int HD>

@@ -701,6 +701,252 @@ __global__ __launch_bounds__(64 * kMfmaMaxWaves) void k_gemm_mfma(GemmArgs a) {
   for (int r = 0; r < nlive; ++r) run_epilogue<WT, EPI, RW>(a, g0 + r, M, Y + r * YN);
 }
 
+// ----------------------------------------------------------------------------- MFMA GEMM, row waves
+
+// The K-split kernel above reads every activation row once per workgroup, besides its one or
+// two row groups' weights; with several 16-row activation tiles that is most of what a
+// workgroup reads.  Here the 4 waves of a workgroup own different row groups (NRW each, 4 NRW
+// in all) over the whole of the workgroup's K range, and the activations are staged once per
+// workgroup in LDS, in 128-column chunks: loaded from global, scaled by the norm gain, split
+// into bf16 hi/lo and written in MFMA fragment order, while the previous chunk is multiplied.
+// So a workgroup reads its activations once for 4 NRW row groups.  Each wave sums its K range
+// in step order (one MFMA chain per group and tile); K shares (residual projections) go
+// through the K-share partials as in the kernel above.
+constexpr int kRwSteps = 4;  // 32-column steps per staged activation chunk
+#ifndef LASER_RW_RING
+#define LASER_RW_RING 8
+#endif
+constexpr int kRwRing = LASER_RW_RING;  // bf16 weight steps in flight per wave (fp32: half)
+
+template <class WT, int MT, int EPI, int NRW>
+__global__ __launch_bounds__(256) void k_gemm_mfma_rw(GemmArgs a) {
+  constexpr int RW = rows_per_group(EPI, true);
+  constexpr int NLD = (int)sizeof(WT) / 2;  // 16-byte weight loads per step (bf16: 1, fp32: 2)
+  constexpr int CS = kRwSteps, U = kRwRing / NLD < 2 * CS ? 2 * CS : kRwRing / NLD;
+  constexpr int NQ = U / CS;  // chunks per turn of the weight ring
+  static_assert(U % CS == 0 && NQ % 2 == 0, "whole chunks per ring turn, two activation buffers");
+  constexpr int NG = 4 * NRW;                 // row groups of the workgroup
+  constexpr int YN = 16 * MT * RW;            // outputs of one group
+  constexpr int ABUF = MT * CS * 2 * 1024;    // one staged chunk: tiles x steps x (hi, lo) x 1 KB
+  constexpr int YBYTES = NG * YN * 4;
+  constexpr int SMEM = 2 * ABUF > YBYTES ? 2 * ABUF : YBYTES;
+  __shared__ __align__(16) char smem[SMEM];  // two activation chunks; after the loop, Y
+  __shared__ float s_sq[16 * MT], s_scale[16 * MT];
+  const int tid = threadIdx.x, w = tid >> 6, l = tid & 63;
+  const int ksplit = EPI == EPI_RESID && a.ksplit > 1 ? a.ksplit : 1;
+  const int ks = (int)blockIdx.x % ksplit;
+  const int gw0 = (int)blockIdx.x / ksplit * NG;  // the workgroup's first group
+  const int M = a.M;
+  constexpr bool norm = EPI != EPI_RESID;  // every other epilogue follows an RMSNorm (gain checked at launch)
+  const int n = l & 15;
+  const bool tiled = a.wtile != nullptr;
+  constexpr int BLK = 1024 * NLD;
+  const char* wp[NRW];  // this lane's bytes of its wave's groups (groups past n_groups: clamped, not stored)
+#pragma unroll
+  for (int r = 0; r < NRW; ++r) {
+    const int g = min(gw0 + w * NRW + r, a.n_groups - 1);
+    wp[r] = tiled ? a.wtile + (size_t)g * a.tsteps * BLK + 16 * l : weight_row<WT, EPI, RW>(a, g, n);
+  }
+  // the workgroup's 32-column steps [s0, s1): all of K, or a share of whole chunks
+  const int nsteps_all = (a.K + 31) >> 5;
+  const int sps = ksplit > 1 ? ((nsteps_all + ksplit - 1) / ksplit + CS - 1) / CS * CS : nsteps_all;
+  const int s0 = ks * sps, s1 = min(nsteps_all, s0 + sps);
+  const int nst = max(s1 - s0, 0);
+  const int nch = (nst + CS - 1) / CS;
+  const int kend = min(a.K, 32 * s1);
+
+  // Staging: thread t takes row 16 mt + t/16 of every tile, columns 8 (t % 16) .. + 7 of the
+  // chunk (16 threads read 512 contiguous bytes of a row); those 8 columns are the operand of
+  // lane (t/16) + 16 q of step j, where 8 (t % 16) = 32 j + 8 q.
+  const int srow = tid >> 4, sc8 = 8 * (tid & 15);
+  const int sj = sc8 >> 5, slane = srow + 16 * ((sc8 & 31) >> 3);
+  const float* xs[MT];
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt) xs[mt] = a.x + (size_t)a_src_row(a, min(16 * mt + srow, M - 1)) * a.ldx;
+  float4 xv[MT][2];
+  u32x4 gv[NLD];
+  float sq[MT];
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt) sq[mt] = 0.f;
+  // column of this thread's 8 values in chunk c (-1: past the end of K); chunks past the
+  // last reload the last one (in bounds, unused)
+  auto scol = [&](int c) {
+    const int k = 32 * (s0 + min(c, nch - 1) * CS) + sc8;
+    return k < kend ? k : -1;
+  };
+  auto aload = [&](int c) {
+    const int k = scol(c), kk = k < 0 ? 0 : k;
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) {
+      xv[mt][0] = *(const float4*)(xs[mt] + kk);
+      xv[mt][1] = *(const float4*)(xs[mt] + kk + 4);
+    }
+    if (norm)
+#pragma unroll
+      for (int q = 0; q < NLD; ++q) gv[q] = *(const u32x4*)((const char*)a.gain + (size_t)kk * sizeof(WT) + 16 * q);
+  };
+  auto astore = [&](int c, auto bufc) {
+    constexpr int buf = decltype(bufc)::value;
+    const bool live = scol(c) >= 0;
+    float gf[8];
+    if (norm) {
+      unpack16<WT>(gv[0], gf);
+      if (sizeof(WT) == 4) unpack16<WT>(gv[NLD - 1], gf + 4);
+    }
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) {
+      const float4 x0 = xv[mt][0], x1 = xv[mt][1];
+      float xe[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
+#pragma unroll
+      for (int e = 0; e < 8; ++e) xe[e] = live ? xe[e] : 0.f;
+      if (norm) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          sq[mt] = fmaf(xe[e], xe[e], sq[mt]);
+          xe[e] *= gf[e];
+        }
+      }
+      u32x4 ph, pl;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        uint32_t h, lo;
+        split_trunc2(xe[2 * q], xe[2 * q + 1], h, lo);
+        ph[q] = h;
+        pl[q] = lo;
+      }
+      char* dst = smem + buf * ABUF + ((mt * CS + sj) * 2) * 1024 + 16 * slane;
+      *(u32x4*)dst = ph;
+      *(u32x4*)(dst + 1024) = pl;
+    }
+  };
+
+  // weights: a ring of U steps; steps past the last reload the last one (in bounds, unused)
+  u32x4 wv[U][NRW][NLD];
+  auto wissue = [&](int it, auto slotc) {
+    constexpr int slot = decltype(slotc)::value;
+    const int st = s0 + min(it, nst - 1);
+    const int k = 32 * st + 8 * (l >> 4);
+    const size_t woff = tiled ? (size_t)st * BLK : (size_t)(k < kend ? k : 0) * sizeof(WT);
+    const int qs = tiled ? 1024 : 16;
+#pragma unroll
+    for (int r = 0; r < NRW; ++r)
+#pragma unroll
+      for (int q = 0; q < NLD; ++q) wv[slot][r][q] = ld_nt16(wp[r] + woff + qs * q);
+  };
+  f32x4 acc[NRW][MT];
+#pragma unroll
+  for (int r = 0; r < NRW; ++r)
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) acc[r][mt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  auto compute = [&](auto slotc, auto bufc, auto jc) {
+    constexpr int slot = decltype(slotc)::value, buf = decltype(bufc)::value, j = decltype(jc)::value;
+    bf16x8 bhi[NRW], blo[NRW];
+#pragma unroll
+    for (int r = 0; r < NRW; ++r) {
+      if (NLD == 1) {
+        bhi[r] = __builtin_bit_cast(bf16x8, wv[slot][r][0]);
+      } else {
+        u32x4 ph, pl;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          uint16_t h0, l0, h1, l1;
+          split_bf16(__uint_as_float(wv[slot][r][q >> 1][(q & 1) * 2 + 0]), h0, l0);
+          split_bf16(__uint_as_float(wv[slot][r][q >> 1][(q & 1) * 2 + 1]), h1, l1);
+          ph[q] = (uint32_t)h0 | ((uint32_t)h1 << 16);
+          pl[q] = (uint32_t)l0 | ((uint32_t)l1 << 16);
+        }
+        bhi[r] = __builtin_bit_cast(bf16x8, ph);
+        blo[r] = __builtin_bit_cast(bf16x8, pl);
+      }
+    }
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) {
+      const char* src = smem + buf * ABUF + ((mt * CS + j) * 2) * 1024 + 16 * l;
+      const bf16x8 ahi = *(const bf16x8*)src, alo = *(const bf16x8*)(src + 1024);
+#pragma unroll
+      for (int r = 0; r < NRW; ++r) {
+        acc[r][mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ahi, bhi[r], acc[r][mt], 0, 0, 0);
+        acc[r][mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(alo, bhi[r], acc[r][mt], 0, 0, 0);
+        if (NLD == 2) acc[r][mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ahi, blo[r], acc[r][mt], 0, 0, 0);
+      }
+    }
+  };
+  // chunk c (the q-th of a ring turn): its CS steps from LDS buffer q % 2 (ring slots q*CS ..),
+  // each slot refilled U steps ahead; then the next chunk's activations (loaded a chunk ago)
+  // go to the other buffer, and the one after is loaded.  `checked`: the last chunks, where
+  // steps and chunks may be missing; elsewhere nothing is conditional, so that no load waits
+  // for a later one at a branch merge (vector-memory counters complete in order).
+  auto chunk = [&](int c, auto qc, auto checkedc) {
+    constexpr int q = decltype(qc)::value, buf = q & 1;
+    constexpr bool checked = decltype(checkedc)::value;
+    static_for<CS>([&](auto jc) {
+      constexpr int j = decltype(jc)::value;
+      const int it = c * CS + j;
+      if (!checked || it < nst) {
+        compute(std::integral_constant<int, q * CS + j>{}, std::integral_constant<int, buf>{}, jc);
+        wissue(it + U, std::integral_constant<int, q * CS + j>{});
+      }
+    });
+    if (!checked || c + 1 < nch) astore(c + 1, std::integral_constant<int, buf ^ 1>{});
+    __syncthreads();
+    if (!checked || c + 2 < nch) aload(c + 2);
+  };
+  if (nch > 0) {
+    aload(0);
+    astore(0, std::integral_constant<int, 0>{});
+    if (nch > 1) aload(1);
+    static_for<U>([&](auto u) { wissue((int)decltype(u)::value, u); });
+    __syncthreads();
+    int c = 0;
+    // whole ring turns whose chunks are full and followed by two more chunks
+    for (; c + NQ + 1 < nch; c += NQ)
+      static_for<NQ>([&](auto q) { chunk(c + (int)decltype(q)::value, q, std::false_type{}); });
+    for (; c < nch; c += NQ)
+      static_for<NQ>([&](auto q) {
+        if (c + (int)decltype(q)::value < nch) chunk(c + (int)decltype(q)::value, q, std::true_type{});
+      });
+  }
+  // the rows' sums of squares: the 16 threads of a row are 16 consecutive lanes
+  if (norm) {
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) {
+      float v = sq[mt];
+      v += __shfl_xor(v, 1);
+      v += __shfl_xor(v, 2);
+      v += __shfl_xor(v, 4);
+      v += __shfl_xor(v, 8);
+      if ((tid & 15) == 0) s_sq[16 * mt + srow] = v;
+    }
+  }
+  // lane (n, l/16): acc[r][mt][i] = Y_r[m = 16mt + 4(l/16) + i][n]  (the loop ended with a barrier)
+  float* Y = (float*)smem;
+#pragma unroll
+  for (int r = 0; r < NRW; ++r)
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) Y[(w * NRW + r) * YN + (16 * mt + 4 * (l >> 4) + i) * RW + n] = acc[r][mt][i];
+  __syncthreads();
+  if (norm && tid < M) s_scale[tid] = rsqrtf(s_sq[tid] / (float)a.K + a.eps);
+  __syncthreads();
+  const int nlive = min(NG, a.n_groups - gw0);
+  if (norm)
+    for (int idx = tid; idx < NG * YN; idx += blockDim.x) {
+      const int j = idx % YN;
+      if (j < M * RW) Y[idx] *= s_scale[j / RW];
+    }
+  __syncthreads();
+  if (EPI == EPI_RESID && ksplit > 1) {  // partial sums of this K share (no norm on this path)
+    for (int r = 0; r < nlive; ++r)
+      for (int idx = tid; idx < M * RW; idx += blockDim.x) {
+        const int m = idx / RW, row = RW * (gw0 + r) + (idx - m * RW);
+        if (row < a.N) a.kpart[((size_t)ks * M + m) * a.N + row] = Y[r * YN + idx];
+      }
+    return;
+  }
+  for (int r = 0; r < nlive; ++r) run_epilogue<WT, EPI, RW>(a, gw0 + r, M, Y + r * YN);
+}
+
 // h[i] += kpart[0][i] + kpart[1][i] + ... (K shares in order), i < M * N.
 __global__ void k_ksplit_reduce(float* h, const float* kpart, int ksplit, int n) {
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
@@ -766,6 +1012,18 @@ static hipError_t launch_mfma(int epi, dim3 grid, dim3 block, const GemmArgs& a,
   }
 }
 
+template <class WT, int MT, int NRW>
+static hipError_t launch_mfma_rw(int epi, dim3 grid, const GemmArgs& a, hipStream_t s) {
+  const dim3 block(256);
+  switch (epi) {
+    case EPI_QKV: return launch_k(k_gemm_mfma_rw<WT, MT, EPI_QKV, NRW>, grid, block, s, a);
+    case EPI_RESID: return launch_k(k_gemm_mfma_rw<WT, MT, EPI_RESID, NRW>, grid, block, s, a);
+    case EPI_SWIGLU: return launch_k(k_gemm_mfma_rw<WT, MT, EPI_SWIGLU, NRW>, grid, block, s, a);
+    case EPI_LMHEAD: return launch_k(k_gemm_mfma_rw<WT, MT, EPI_LMHEAD, NRW>, grid, block, s, a);
+    default: return hipErrorInvalidValue;
+  }
+}
+
 template <class WT, int MODE>
 static hipError_t launch_epi(int epi, int rw, const GemmArgs& a, hipStream_t s) {
   const dim3 grid(a.n_groups);
@@ -788,6 +1046,11 @@ static hipError_t launch_epi(int epi, int rw, const GemmArgs& a, hipStream_t s) 
     if (!mfma_nr_ok<MT>(nr)) return hipErrorInvalidValue;
     const int ksplit = a.ksplit < 1 ? 1 : a.ksplit;
     if (ksplit > 1 && (epi != EPI_RESID || a.kpart == nullptr || ksplit > kMaxKsplit)) return hipErrorInvalidValue;
+    if (a.nrw > 0) {  // row-wave kernel: 8-column activation segments, so K a multiple of 8
+      if ((a.nrw != 1 && a.nrw != 2) || a.K % 8 != 0 || a.M < 1 || a.M > 16 * MT) return hipErrorInvalidValue;
+      const dim3 grid((a.n_groups + 4 * a.nrw - 1) / (4 * a.nrw) * ksplit);
+      return a.nrw == 2 ? launch_mfma_rw<WT, MT, 2>(epi, grid, a, s) : launch_mfma_rw<WT, MT, 1>(epi, grid, a, s);
+    }
     const dim3 mgrid((a.n_groups + nr - 1) / nr * ksplit);
     // few workgroups (the O, down and QKV projections): 8 waves split K more finely
     const int waves = mgrid.x < 512 ? kMfmaMaxWaves : kGemmThreads / 64;

@@ -138,6 +138,7 @@ struct laser_model {
   int ev_used = 0;
   int last_stop = -1;  // pool index bound to the most recent launch's end
   bool use_graphs = true;
+  int gemm_kernel = 0;  // MFMA-path kernel choice (laser_model_set_gemm_kernel)
   // tile-order weight copies for the MFMA path (laser_model_set_tiles)
   struct Tiles {
     const char *qkv, *o, *gu, *down;
@@ -236,24 +237,55 @@ static int groups_lm(const laser_model_desc& d, int M) { return ceil_div(d.vocab
 // each); with 2-3 tiles up to four groups (gate/up of a 40-row mixed step); at 4 tiles up to
 // two.  O-proj and down split K where the activation rows outweigh the weights (M >= 8 at
 // the 7B down projection, the 40-row mixed step).
+// MFMA-path kernel and its shape.  nrw = 0: the K-split kernel with nr row groups per
+// workgroup; nrw = 1, 2: the row-wave kernel (4 waves of nrw groups each).  ks: K shares.
 struct MfmaShape {
-  int nr, ks;
+  int nr, ks, nrw;
 };
 constexpr double kKsplitPenalty = 160e3;
-static MfmaShape mfma_shape(int epi, int n_groups, int M, int K, int es, int cus) {
-  if (M <= kValuMaxRows || M > 64) return {1, 1};
+#ifndef LASER_RW_MAX_NRW
+#define LASER_RW_MAX_NRW 2
+#endif
+constexpr int kRwMaxGroups = LASER_RW_MAX_NRW;  // row groups per wave of the row-wave kernel, at most
+// gemm_kernel: 0 the choice below, 1 only the K-split kernel, 2 the row-wave kernel wherever
+// it applies (its shape by the cost below).  The row-wave kernel reads the activations once
+// per 8 row groups instead of once per 1-4, but streams each group's weights from one wave
+// and has few workgroups; measured, it wins for gate/up over 3-4 activation tiles (52 rows at
+// 8B: 80 vs 118 us) and loses where the K-split kernel has many workgroups and few
+// activation rows (QKV, the LM head, one tile).  So by default it takes gate/up at 3-4 tiles
+// when it fills the CUs with 8 groups per workgroup.  The cost for the K-split kernel is the
+// bytes the busiest CU reads: ceil(workgroups / CUs) times a workgroup's weights (its groups'
+// 16 K es each) and activations (M K 4), over the K shares, plus a fixed penalty for the
+// K-share reduce.
+static MfmaShape mfma_shape(int epi, int n_groups, int M, int K, int es, int cus, int gemm_kernel) {
+  if (M <= kValuMaxRows || M > 64) return {1, 1, 0};
   const int mt = ceil_div(M, 16);
+  if (gemm_kernel == 0 && epi == EPI_SWIGLU && mt >= 3 && K % 8 == 0 && ceil_div(n_groups, 8) >= cus * 7 / 8)
+    return {1, 1, 2};
   const double w = 16.0 * K * es, act = 4.0 * M * K;
-  auto cost = [&](int nr, int ks) {
-    const double wgs = (double)ceil_div(ceil_div(n_groups, nr) * ks, cus);
-    return wgs * (nr * w + act) / ks + (ks > 1 ? kKsplitPenalty : 0.0);
+  auto cost = [&](int groups_per_wg, int ks) {
+    const double wgs = (double)ceil_div(ceil_div(n_groups, groups_per_wg) * ks, cus);
+    return wgs * (groups_per_wg * w + act) / ks + (ks > 1 ? kKsplitPenalty : 0.0);
   };
-  MfmaShape best{1, 1};
-  for (int nr : {1, 2, 4}) {
-    if (nr == 4 && (mt < 2 || mt > 3)) continue;
-    for (int ks = 1; ks <= (epi == EPI_RESID ? kMaxKsplit : 1); ks *= 2)
-      if (cost(nr, ks) < cost(best.nr, best.ks)) best = {nr, ks};
-  }
+  const int max_ks = epi == EPI_RESID ? kMaxKsplit : 1;
+  MfmaShape best{1, 1, 0};
+  double best_cost = 1e300;
+  if (gemm_kernel != 2 || K % 8 != 0)  // (mode 2 falls back to it where K is not a multiple of 8)
+    for (int nr : {1, 2, 4}) {
+      if (nr == 4 && (mt < 2 || mt > 3)) continue;
+      for (int ks = 1; ks <= max_ks; ks *= 2)
+        if (cost(nr, ks) < best_cost) {
+          best = {nr, ks, 0};
+          best_cost = cost(nr, ks);
+        }
+    }
+  if (gemm_kernel == 2 && K % 8 == 0)
+    for (int nrw = 1; nrw <= kRwMaxGroups; ++nrw)
+      for (int ks = 1; ks <= max_ks; ks *= 2)
+        if (cost(4 * nrw, ks) < best_cost) {
+          best = {1, ks, nrw};
+          best_cost = cost(4 * nrw, ks);
+        }
   return best;
 }
 
@@ -1006,9 +1038,10 @@ static laser_status launch_forward(laser_model* m, laser_kv* kv, const FwdKey& k
     a.K = K;
     a.N = N;
     a.n_groups = proj_groups(epi, rows, rw);
-    const MfmaShape ms = mfma_shape(epi, a.n_groups, M, K, (int)m->es, m->cus);
+    const MfmaShape ms = mfma_shape(epi, a.n_groups, M, K, (int)m->es, m->cus, m->gemm_kernel);
     a.nr = ms.nr;
     a.ksplit = ms.ks;
+    a.nrw = ms.nrw;
     a.kpart = m->wsp<float>(L.kpart);
     a.M = M;
     if (M > kValuMaxRows && m->tiles_on) {
@@ -1103,7 +1136,9 @@ static laser_status launch_forward(laser_model* m, laser_kv* kv, const FwdKey& k
     a.K = d.d_model;
     a.N = d.vocab;
     a.n_groups = groups_lm(d, key.n_out);
-    a.nr = mfma_shape(EPI_LMHEAD, a.n_groups, key.n_out, d.d_model, (int)m->es, m->cus).nr;
+    const MfmaShape ms = mfma_shape(EPI_LMHEAD, a.n_groups, key.n_out, d.d_model, (int)m->es, m->cus, m->gemm_kernel);
+    a.nr = ms.nr;
+    a.nrw = ms.nrw;
     a.ksplit = 1;
     a.M = key.n_out;
     if (key.n_out > kValuMaxRows && m->tiles_on) {
@@ -1527,6 +1562,14 @@ extern "C" laser_status laser_atp_match(const int32_t* d_tokens, int n, const ui
 extern "C" laser_status laser_model_set_graphs(laser_model* m, int enable) {
   if (!model_of(m)) return laser_fail(LASER_ERR_STATE, "invalid or destroyed model");
   m->use_graphs = enable != 0;
+  return LASER_OK;
+}
+
+extern "C" laser_status laser_model_set_gemm_kernel(laser_model* m, int mode) {
+  if (!model_of(m)) return laser_fail(LASER_ERR_STATE, "invalid or destroyed model");
+  if (mode < 0 || mode > 2) return laser_fail(LASER_ERR_INVALID_ARG, "gemm kernel mode must be 0, 1 or 2");
+  if (mode != m->gemm_kernel) drop_graphs(m);  // captured forwards hold the previous choice
+  m->gemm_kernel = mode;
   return LASER_OK;
 }
 

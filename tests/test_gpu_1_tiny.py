@@ -104,10 +104,14 @@ def test_tiny_full_run():
     assert np.max(np.abs(K - st.K[:, :256])) < 1e-4
 
 
-def test_tiny_batched_decode_probe_and_mixed():
+# gemm_kernel: the matrix-core projections with the K-split kernel (1) and the row-wave kernel
+# (2), fp32 weights (two 16-byte loads per step, split into hi/lo)
+@pytest.mark.parametrize("gemm_kernel", [1, 2])
+def test_tiny_batched_decode_probe_and_mixed(gemm_kernel):
     require_gpu()
     V = TINY.vocab
     model, orc, _ = make_pair(TINY, max_rows=64, max_positions=1024)
+    model.set_gemm_kernel(gemm_kernel)
     kv, opool = kv_pair(model, TINY, num_pages=200, max_seqs=8, max_pages_per_seq=64)
     lens = [15, 16, 37, 250]  # page-boundary edge cases and a longer context
     states = []

@@ -179,13 +179,16 @@ def test_llama8b_b8_mixed_step_state_injection():
     st.release()
 
 
-def test_qwen1p5b_prefill_64row_chunks():
+@pytest.mark.parametrize("gemm_kernel", [1, 2])
+def test_qwen1p5b_prefill_64row_chunks(gemm_kernel):
     # A 100-token prompt in chunks of 64 and 36 rows: matrix-core projections over four and
-    # three 16-row tiles, with two and four row groups per workgroup for gate/up.
+    # three 16-row tiles, with the K-split kernel (two and four row groups per workgroup for
+    # gate/up) and the row-wave kernel (K shares for O-proj and down).
     T0[0] = time.time()
     dev = require_gpu()
     shape, n, max_pos = QWEN_1P5B, 100, 256
     model, orc, _ = make_pair(shape, max_rows=64, max_positions=max_pos, weights_on_device=True, cache_oracle=True)
+    model.set_gemm_kernel(gemm_kernel)
     kv = L.KVCache(model, 32, 1, max_pos // 16 + 1, poison=True)
     opool = OraclePool(32)
     kv.add_seq(0, 0)
