@@ -950,7 +950,7 @@ static laser_status run_forward(laser_model* m, laser_kv* kv, Plan& p, const Pla
   key.kv_id = kv->id;
   // The attention grid is at least the item count, a multiple of 8 (so that item i runs on
   // XCD i mod 8), padded with empty items.  A captured forward of the same shape whose grid
-  // is at most 1/8 (+64) wider is reused; a new one is captured 1/8 wider, so a growing
+  // is at most 1/4 (+8) wider is reused; a new one is captured 1/8 wider, so a growing
   // context or a changing mix of probes does not recapture at every step.
   const int need = std::max(8, ceil_div(p.n_items, 8) * 8);
   const bool timing = timing_session(m);
@@ -958,10 +958,10 @@ static laser_status run_forward(laser_model* m, laser_kv* kv, Plan& p, const Pla
   GraphEntry* ge = nullptr;
   if (graphs)
     for (auto& g : m->graphs)
-      if (g.key.same_shape(key) && g.key.agx >= need && g.key.agx <= need + need / 8 + 64 &&
+      if (g.key.same_shape(key) && g.key.agx >= need && g.key.agx <= need + need / 4 + 8 &&
           (!ge || g.key.agx < ge->key.agx))
         ge = &g;
-  key.agx = ge ? ge->key.agx : graphs ? std::min(kMaxAttnItems, ceil_div(need + need / 8, 64) * 64) : need;
+  key.agx = ge ? ge->key.agx : graphs ? std::min(kMaxAttnItems, ceil_div(need + need / 8, 8) * 8) : need;
   pad_items(p, key.agx);
   Plan* dp = nullptr;
   laser_status st = upload_plan(m, p, s, &dp);
