@@ -446,8 +446,8 @@ laser_status laser_model_set_graphs(laser_model* m, int enable);
  * the same products: one splits K over the waves of a workgroup (1-4 row groups of 16
  * weight rows per workgroup), the other gives each of 4 waves its own row groups and stages
  * the activations once per workgroup in LDS.  mode 0 (the default) takes the second for the
- * gate/up projection of forwards of 33 to 64 rows when it has enough row groups, and the
- * first elsewhere; 1 uses only the first kernel; 2 the second wherever it applies (K a
+ * gate/up projection of forwards of 33 to 64 rows when it has enough row groups and for
+ * the O and down projections of forwards of 49 to 64 rows, and the first elsewhere; 1 uses only the first kernel; 2 the second wherever it applies (K a
  * multiple of 8).  The summation order differs between them, so
  * results may differ in the last bits.  Captured forwards are released when the mode
  * changes.  Errors: LASER_ERR_STATE (bad model), LASER_ERR_INVALID_ARG (mode). */

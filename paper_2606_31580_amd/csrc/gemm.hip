@@ -725,13 +725,14 @@ __global__ __launch_bounds__(256) void k_gemm_mfma_rw(GemmArgs a) {
   constexpr int CS = kRwSteps, U = kRwRing / NLD < 2 * CS ? 2 * CS : kRwRing / NLD;
   constexpr int NQ = U / CS;  // chunks per turn of the weight ring
   static_assert(U % CS == 0 && NQ % 2 == 0, "whole chunks per ring turn, two activation buffers");
+  static_assert(CS == 4, "each of the 4 waves stages one step of a chunk");
   constexpr int NG = 4 * NRW;                 // row groups of the workgroup
   constexpr int YN = 16 * MT * RW;            // outputs of one group
   constexpr int ABUF = MT * CS * 2 * 1024;    // one staged chunk: tiles x steps x (hi, lo) x 1 KB
   constexpr int YBYTES = NG * YN * 4;
   constexpr int SMEM = 2 * ABUF > YBYTES ? 2 * ABUF : YBYTES;
   __shared__ __align__(16) char smem[SMEM];  // two activation chunks; after the loop, Y
-  __shared__ float s_sq[16 * MT], s_scale[16 * MT];
+  __shared__ float s_sqp[4][16 * MT], s_scale[16 * MT];
   const int tid = threadIdx.x, w = tid >> 6, l = tid & 63;
   const int ksplit = EPI == EPI_RESID && a.ksplit > 1 ? a.ksplit : 1;
   const int ks = (int)blockIdx.x % ksplit;
@@ -755,11 +756,11 @@ __global__ __launch_bounds__(256) void k_gemm_mfma_rw(GemmArgs a) {
   const int nch = (nst + CS - 1) / CS;
   const int kend = min(a.K, 32 * s1);
 
-  // Staging: thread t takes row 16 mt + t/16 of every tile, columns 8 (t % 16) .. + 7 of the
-  // chunk (16 threads read 512 contiguous bytes of a row); those 8 columns are the operand of
-  // lane (t/16) + 16 q of step j, where 8 (t % 16) = 32 j + 8 q.
-  const int srow = tid >> 4, sc8 = 8 * (tid & 15);
-  const int sj = sc8 >> 5, slane = srow + 16 * ((sc8 & 31) >> 3);
+  // Staging: wave w stages step w of the chunk, lane l the operand of fragment lane l: row
+  // 16 mt + l % 16 of every tile, columns 32 w + 8 (l / 16) .. + 7.  So each wave's LDS
+  // writes are 1 KB contiguous (no bank conflicts).
+  const int srow = l & 15, sc8 = 32 * w + 8 * (l >> 4);
+  const int sj = w, slane = l;
   const float* xs[MT];
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt) xs[mt] = a.x + (size_t)a_src_row(a, min(16 * mt + srow, M - 1)) * a.ldx;
@@ -906,16 +907,14 @@ __global__ __launch_bounds__(256) void k_gemm_mfma_rw(GemmArgs a) {
         if (c + (int)decltype(q)::value < nch) chunk(c + (int)decltype(q)::value, q, std::true_type{});
       });
   }
-  // the rows' sums of squares: the 16 threads of a row are 16 consecutive lanes
+  // the rows' sums of squares: lanes l, l ^ 16, l ^ 32, l ^ 48 of every wave hold row l % 16
   if (norm) {
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
       float v = sq[mt];
-      v += __shfl_xor(v, 1);
-      v += __shfl_xor(v, 2);
-      v += __shfl_xor(v, 4);
-      v += __shfl_xor(v, 8);
-      if ((tid & 15) == 0) s_sq[16 * mt + srow] = v;
+      v += __shfl_xor(v, 16);
+      v += __shfl_xor(v, 32);
+      if (l < 16) s_sqp[w][16 * mt + l] = v;
     }
   }
   // lane (n, l/16): acc[r][mt][i] = Y_r[m = 16mt + 4(l/16) + i][n]  (the loop ended with a barrier)
@@ -927,7 +926,7 @@ __global__ __launch_bounds__(256) void k_gemm_mfma_rw(GemmArgs a) {
 #pragma unroll
       for (int i = 0; i < 4; ++i) Y[(w * NRW + r) * YN + (16 * mt + 4 * (l >> 4) + i) * RW + n] = acc[r][mt][i];
   __syncthreads();
-  if (norm && tid < M) s_scale[tid] = rsqrtf(s_sq[tid] / (float)a.K + a.eps);
+  if (norm && tid < M) s_scale[tid] = rsqrtf((s_sqp[0][tid] + s_sqp[1][tid] + s_sqp[2][tid] + s_sqp[3][tid]) / (float)a.K + a.eps);
   __syncthreads();
   const int nlive = min(NG, a.n_groups - gw0);
   if (norm)

@@ -249,11 +249,13 @@ constexpr double kKsplitPenalty = 160e3;
 constexpr int kRwMaxGroups = LASER_RW_MAX_NRW;  // row groups per wave of the row-wave kernel, at most
 // gemm_kernel: 0 the choice below, 1 only the K-split kernel, 2 the row-wave kernel wherever
 // it applies (its shape by the cost below).  The row-wave kernel reads the activations once
-// per 8 row groups instead of once per 1-4, but streams each group's weights from one wave
+// per 4-8 row groups instead of once per 1-4, but streams each group's weights from one wave
 // and has few workgroups; measured, it wins for gate/up over 3-4 activation tiles (52 rows at
-// 8B: 80 vs 118 us) and loses where the K-split kernel has many workgroups and few
-// activation rows (QKV, the LM head, one tile).  So by default it takes gate/up at 3-4 tiles
-// when it fills the CUs with 8 groups per workgroup.  The cost for the K-split kernel is the
+// 8B: 69 vs 118 us) and for O-proj / down over 4 tiles (32 vs 38 us), and loses where the
+// K-split kernel has many workgroups and few activation rows (QKV, the LM head, one tile).
+// So by default it takes gate/up at 3-4 tiles when it fills the CUs with 8 groups per
+// workgroup, and O-proj / down at 4 tiles (4 groups per workgroup, 4 K shares).  The cost
+// for the K-split kernel is the
 // bytes the busiest CU reads: ceil(workgroups / CUs) times a workgroup's weights (its groups'
 // 16 K es each) and activations (M K 4), over the K shares, plus a fixed penalty for the
 // K-share reduce.
@@ -262,6 +264,7 @@ static MfmaShape mfma_shape(int epi, int n_groups, int M, int K, int es, int cus
   const int mt = ceil_div(M, 16);
   if (gemm_kernel == 0 && epi == EPI_SWIGLU && mt >= 3 && K % 8 == 0 && ceil_div(n_groups, 8) >= cus * 7 / 8)
     return {1, 1, 2};
+  if (gemm_kernel == 0 && epi == EPI_RESID && mt >= 4 && K % 8 == 0) return {1, kMaxKsplit, 1};
   const double w = 16.0 * K * es, act = 4.0 * M * K;
   auto cost = [&](int groups_per_wg, int ks) {
     const double wgs = (double)ceil_div(ceil_div(n_groups, groups_per_wg) * ks, cus);
