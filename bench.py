@@ -267,6 +267,7 @@ def main():
     # ---- whole job: decode + probes + host exit decisions (forwards replay captured graphs)
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
+    cap0 = model.graph_stats()[0]
     e0.record(stream)
     w0 = time.perf_counter()
     for i in range(args.steps):
@@ -276,6 +277,7 @@ def main():
     wall = time.perf_counter() - w0
     ms_total = e0.elapsed_time(e1)
     ms_per_step = ms_total / args.steps
+    captures_timed = model.graph_stats()[0] - cap0  # forwards captured into new graphs while timed
     value = args.steps * B / (ms_total / 1e3)
     probes_timed = n_probes[0]
     while ride:  # a probe still riding: finish it outside the timed region
@@ -378,6 +380,7 @@ def main():
         if not (wl.mixed and args.probe_mode == "separate")
         else {"mean": round(ms_per_step, 3), "p50": None, "max": None, "n": probes_timed},
         "host_decision_us": round(host_decision_us, 3),
+        "graph_captures_timed": captures_timed,
         "probe": {"mode": "mixed, riding", "probes_in_timed_region": probes_timed, "forwards_per_probe": T,
                   "probes_skipped_no_slot": skipped[0],
                   "latency_meaning": "device time from the fork to the confidence: the probing half's suffix chunks "

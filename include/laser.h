@@ -441,6 +441,11 @@ laser_status laser_timing_read(laser_model* m, int kernel_class, double* total_m
  * they share the model's workspace and its one device plan slot. */
 laser_status laser_model_set_graphs(laser_model* m, int enable);
 
+/* Graph cache statistics (for callers that want to see recaptures): *captures = forwards
+ * captured into graphs since the model was created, *cached = graphs held now (at most 16).
+ * Host-side only.  Errors: LASER_ERR_STATE (bad model), LASER_ERR_INVALID_ARG (null). */
+laser_status laser_model_graph_stats(const laser_model* m, long long* captures, int* cached);
+
 /* Projection kernel choice on the matrix-core path (forwards of 3 to 64 rows; the linear
  * maps of the transformer block, §4.1's decode and probe forwards).  Two kernels compute
  * the same products: one splits K over the waves of a workgroup (1-4 row groups of 16

@@ -860,17 +860,31 @@ __global__ __launch_bounds__(256) void k_gemm_mfma_rw(GemmArgs a) {
         blo[r] = __builtin_bit_cast(bf16x8, pl);
       }
     }
+    bf16x8 ahi[MT], alo[MT];
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
       const char* src = smem + buf * ABUF + ((mt * CS + j) * 2) * 1024 + 16 * l;
-      const bf16x8 ahi = *(const bf16x8*)src, alo = *(const bf16x8*)(src + 1024);
-#pragma unroll
-      for (int r = 0; r < NRW; ++r) {
-        acc[r][mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ahi, bhi[r], acc[r][mt], 0, 0, 0);
-        acc[r][mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(alo, bhi[r], acc[r][mt], 0, 0, 0);
-        if (NLD == 2) acc[r][mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ahi, blo[r], acc[r][mt], 0, 0, 0);
-      }
+      ahi[mt] = *(const bf16x8*)src;
+      alo[mt] = *(const bf16x8*)(src + 1024);
     }
+    // every accumulator's hi product, then every lo product: consecutive matrix-core ops
+    // feed different accumulators (each accumulator still sums hi before lo)
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+      for (int r = 0; r < NRW; ++r)
+        acc[r][mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ahi[mt], bhi[r], acc[r][mt], 0, 0, 0);
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+      for (int r = 0; r < NRW; ++r)
+        acc[r][mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(alo[mt], bhi[r], acc[r][mt], 0, 0, 0);
+    if (NLD == 2)
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int r = 0; r < NRW; ++r)
+          acc[r][mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ahi[mt], blo[r], acc[r][mt], 0, 0, 0);
   };
   // chunk c (the q-th of a ring turn): its CS steps from LDS buffer q % 2 (ring slots q*CS ..),
   // each slot refilled U steps ahead; then the next chunk's activations (loaded a chunk ago)

@@ -149,6 +149,7 @@ struct laser_model {
   hipStream_t cap_stream = nullptr;  // private stream that forwards are captured on
   std::vector<GraphEntry> graphs;
   uint64_t graph_clock = 0;
+  long long graph_captures = 0;  // forwards captured into graphs since creation
 
   template <class T>
   T* wsp(size_t off) const { return (T*)(ws + off); }
@@ -995,6 +996,7 @@ static laser_status run_forward(laser_model* m, laser_kv* kv, Plan& p, const Pla
       m->graphs.erase(lru);
     }
     m->graphs.push_back(GraphEntry{key, exec, 0});
+    ++m->graph_captures;
     ge = &m->graphs.back();
   }
   ge->last_use = ++m->graph_clock;
@@ -1565,6 +1567,14 @@ extern "C" laser_status laser_atp_match(const int32_t* d_tokens, int n, const ui
 extern "C" laser_status laser_model_set_graphs(laser_model* m, int enable) {
   if (!model_of(m)) return laser_fail(LASER_ERR_STATE, "invalid or destroyed model");
   m->use_graphs = enable != 0;
+  return LASER_OK;
+}
+
+extern "C" laser_status laser_model_graph_stats(const laser_model* m, long long* captures, int* cached) {
+  if (!model_of(const_cast<laser_model*>(m))) return laser_fail(LASER_ERR_STATE, "invalid or destroyed model");
+  if (!captures || !cached) return laser_fail(LASER_ERR_INVALID_ARG, "null output pointer");
+  *captures = m->graph_captures;
+  *cached = (int)m->graphs.size();
   return LASER_OK;
 }
 

@@ -114,6 +114,7 @@ _SIGS = {
     "laser_timing_read": (_I, [_P, _I, C.POINTER(C.c_double), C.POINTER(_I)]),
     "laser_model_set_graphs": (_I, [_P, _I]),
     "laser_model_set_gemm_kernel": (_I, [_P, _I]),
+    "laser_model_graph_stats": (_I, [_P, C.POINTER(C.c_longlong), C.POINTER(C.c_int)]),
     "laser_model_tile_bytes": (_I, [_P, C.POINTER(C.c_size_t)]),
     "laser_model_set_tiles": (_I, [_P, _P, C.c_size_t, _P]),
     "laser_atp_bitmap": (_I, [_P, _I, _I, _P]),
@@ -300,6 +301,12 @@ class Model:
     def set_graphs(self, on: bool):
         """Replay forwards from captured HIP graphs (default) or launch kernels one by one."""
         _call("laser_model_set_graphs", self.h, int(on))
+
+    def graph_stats(self):
+        """(forwards captured into graphs so far, graphs cached now)."""
+        n, c = C.c_longlong(), C.c_int()
+        _call("laser_model_graph_stats", self.h, C.byref(n), C.byref(c))
+        return n.value, c.value
 
     def set_gemm_kernel(self, mode: int):
         """Matrix-core projection kernel: 0 by cost (default), 1 K-split waves, 2 row waves."""
