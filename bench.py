@@ -130,7 +130,7 @@ def main():
     load_state = L.laser_load_state(0.0)
     stream = torch.cuda.current_stream()
 
-    probe_ms = []  # riding: ATP to exit decision (wall, the decode forwards included); separate: the probe
+    probe_ms = []  # riding: fork to confidence (device time, the decode forwards included); separate: the probe
     n_probes = [0]
     ride = {}  # progress of the riding probes in flight: suffix rows and trial tokens done
 
@@ -138,6 +138,36 @@ def main():
         for b in range(B):  # the controller needs the confidence on the host
             L.laser_exit_decision(params, load_state, float(c[b]), B, 0, 10)
         n_probes[0] += 1
+
+    # Riding probes: the confidences go to the host by an asynchronous copy, and the exit
+    # decisions are taken once the next forward is queued (settle), so the GPU never waits
+    # for the host round trip.  A request that exits is told one decode step later.  Two
+    # pinned buffers in turn; at most one copy is pending at a time.
+    conf_h = [torch.empty(max(B, 1), pin_memory=True) for _ in range(2)]
+    pend = []  # [copy event, host buffer, confidences, per-request decisions?, (fork, conf) events, timed]
+    turn = [0]
+
+    def send(n, per_request, evs, timed):
+        hb = conf_h[turn[0]]
+        turn[0] ^= 1
+        hb[:n].copy_(conf[:n], non_blocking=True)
+        ev = torch.cuda.Event()
+        ev.record(stream)
+        pend.append((ev, hb, n, per_request, evs, timed))
+
+    def settle():
+        while pend:
+            ev, hb, n, per_request, evs, timed = pend.pop(0)
+            ev.synchronize()
+            c = hb[:n].numpy()
+            if per_request:
+                decide(c)
+            else:
+                for k in range(n):
+                    L.laser_exit_decision(params, load_state, float(c[k]), B, 0, 10)
+                n_probes[0] += n
+            if timed:  # device time from the fork to the confidence (the decode forwards included)
+                probe_ms.extend(e0.elapsed_time(e1) for e0, e1 in evs)
 
     # mixed workload, riding probes: each probe is a fork of its request (slot B + f) whose S
     # suffix rows ride in one forward and whose T-1 trial rows ride in the next forwards, all
@@ -169,6 +199,7 @@ def main():
                 inflight.append([f, b, 0, ev0])
         L.laser_forward(model, kv, spans, tokens, tokbuf, nxt, pmax, tokbuf, pbuf)
         tokens.copy_(nxt)
+        settle()  # the previous step's decisions, this step's forward being queued
         done = [pr for pr in inflight if pr[2] == T - 1]
         if not done:
             return
@@ -176,15 +207,11 @@ def main():
             L.laser_confidence(model, pbuf[S + pr[0] * T:], T, 1, conf[k:])
         ev1 = torch.cuda.Event(enable_timing=True)
         ev1.record(stream)
-        c = conf.cpu().numpy()
-        for k, pr in enumerate(done):
-            L.laser_exit_decision(params, load_state, float(c[k]), B, 0, 10)
+        send(len(done), False, [(pr[3], ev1) for pr in done], timed_probe)
+        for pr in done:  # (later forwards are stream-ordered after this one's use of the pages)
             kv.free_seq(B + pr[0])
             free_slots.append(pr[0])
             inflight.remove(pr)
-            if timed_probe:  # device time from the fork to the confidence (the decode forwards included)
-                probe_ms.append(pr[3].elapsed_time(ev1))
-        n_probes[0] += len(done)
 
     def step(i, timed_probe):
         if wl.mixed and args.probe_mode == "riding":
@@ -234,15 +261,14 @@ def main():
                 tok1 = argm
         L.laser_forward(model, kv, spans, tokens, tok1, nxt, pmax, argm, ptrial)
         tokens.copy_(nxt)
+        settle()  # the previous step's decisions, this step's forward being queued
         if ride and ride["s"] == S and ride["t"] == T - 1:
             L.laser_confidence(model, ptrial, T, B, conf)
             ev1 = torch.cuda.Event(enable_timing=True)
             ev1.record(stream)
-            decide(conf.cpu().numpy())
-            for b in seqs:
+            send(B, True, [(ride["ev0"], ev1)], timed_probe)
+            for b in seqs:  # (later forwards are stream-ordered after this one's use of the pages)
                 kv.free_seq(forks[b])
-            if timed_probe:  # device time from the fork to the confidence (decode forwards included)
-                probe_ms.append(ride["ev0"].elapsed_time(ev1))
             ride.clear()
 
     log("warmup")
@@ -252,6 +278,7 @@ def main():
         step(-1, False)
     while inflight:
         step_mixed_riding(-1, False, new_probes=False)
+    settle()
     torch.cuda.synchronize()
     n_probes[0] = 0
 
@@ -260,6 +287,7 @@ def main():
             step(args.warmup + i, False)
         while inflight:
             step_mixed_riding(-1, False, new_probes=False)
+        settle()
         torch.cuda.synchronize()
         log("profile loop done")
         return
@@ -272,6 +300,7 @@ def main():
     w0 = time.perf_counter()
     for i in range(args.steps):
         step(args.warmup + i, True)
+    settle()  # the last step's decisions
     e1.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - w0
@@ -284,6 +313,7 @@ def main():
         step(-1, False)
     while inflight:
         step_mixed_riding(-1, False, new_probes=False)
+    settle()
     # reference: the probe run as separate forwards (the cost it has when nothing rides along)
     sep_ms = []
     for _ in range(2):
@@ -386,6 +416,7 @@ def main():
                   "latency_meaning": "device time from the fork to the confidence: the probing half's suffix chunks "
                                      "ride in one forward with the batch's decode rows, each trial row in one of the "
                                      "next T-1",
+                  "exit_decision": "on the host, once the next forward is queued (a request that exits stops one step later)",
                   "separate_probe_latency_ms": round(float(np.mean(sep_ms)), 3)}
         if wl.mixed and args.probe_mode == "riding" else
                  {"mode": "mixed", "probes_in_timed_region": probes_timed,
@@ -397,6 +428,8 @@ def main():
                   "probes_in_timed_region": probes_timed,
                   "latency_meaning": "device time from the ATP fork to the confidence, decode forwards included"
                   if args.probe_mode == "riding" else "host time of the probe call with its confidence copy",
+                  "exit_decision": "on the host, once the next forward is queued (a request that exits stops one step later)"
+                  if args.probe_mode == "riding" else "on the host, after the probe's confidence copy",
                   "separate_probe_latency_ms": round(float(np.mean(sep_ms)), 3)},
         "step_hbm": {"bytes": step_bytes, "achieved_GBs": round(step_gbs, 1), "frac_of_peak": round(step_gbs / HBM_PEAK_GBS, 4)},
         "roofline": {"kernel": "gate/up projection + SwiGLU (k_gemv, EPI_SWIGLU)", "bound": "hbm",
