@@ -204,3 +204,45 @@ def test_riding_probes_staggered_tiny():
     assert checked == n_fwd and not inflight
     for b in seqs:
         assert kv.page_table(b) == opool.tables[b] and kv.seq_len(b) == states[b].length
+
+
+def test_fork_with_long_own_tail_tiny():
+    # A fork that has decoded far past its fork point: its own pages outnumber what its own
+    # row group may split into (the split count beside a shared-prefix group is bounded), so
+    # the planner lengthens that group's page runs.  Then the request and the fork decode in
+    # one forward: one group over their shared pages, one group each over its own pages,
+    # partials merged per row.  Every decode row and page table is checked.
+    require_gpu()
+    model, orc, _ = make_pair(TINY, max_rows=16, max_positions=1024)
+    kv, opool = kv_pair(model, TINY, num_pages=120, max_seqs=2, max_pages_per_seq=64)
+    K0, V0 = synth.make_prefill_kv(TINY, 100, 50)
+    kv.add_seq(0, 100)
+    opool.add_seq(0, 100)
+    kv.import_kv(0, K0.cuda(), V0.cuda())
+    states = [SeqState.from_prefill(TINY, K0.numpy(), V0.numpy(), 1024)]
+    kv.fork(0, 1)
+    opool.fork(0, 1)
+    states.append(states[0].copy())
+    assert kv.page_table(1) == opool.tables[1]
+    toks = [int(t) for t in synth.make_tokens(2, TINY.vocab, 3012)]
+
+    def steps(seqs, n, tag):
+        B = len(seqs)
+        d_tok = torch.tensor([toks[b] for b in seqs], dtype=torch.int32, device="cuda")
+        d_next = torch.zeros(B, dtype=torch.int32, device="cuda")
+        d_p = torch.zeros(B, device="cuda")
+        for step in range(n):
+            L.laser_decode_step(model, kv, seqs, d_tok, d_next, d_p)
+            torch.cuda.synchronize()
+            for i, b in enumerate(seqs):
+                opool.append(b, 1)
+                ref = orc.decode_token(states[b], toks[b])
+                check_token(d_next[i].item(), ref, f"{tag} step {step} seq {b}")
+                assert abs(d_p[i].item() - lm_stats(ref)[1]) <= PROB_TOL
+                toks[b] = lm_stats(ref)[0]
+                assert kv.page_table(b) == opool.tables[b], f"{tag} step {step}: page table of seq {b}"
+            d_tok.copy_(torch.tensor([toks[b] for b in seqs], dtype=torch.int32))
+
+    steps([1], 560, "fork alone")  # 35 own pages past the 6 shared ones
+    steps([0, 1], 4, "request and fork")
+    steps([1, 0], 2, "fork and request")
