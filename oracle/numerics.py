@@ -76,3 +76,12 @@ def as_float64(a) -> np.ndarray:
     if a.dtype == np.uint8:
         return fp8_e4m3_bits_to_float(a)
     return a.astype(np.float64)
+
+
+def as_dtype(a, dtype) -> np.ndarray:
+    """Value of a stored tensor (as as_float64) in the given float type.  bf16 bit patterns go
+    to float32 exactly (a bf16 value is the upper half of an fp32 word), then to `dtype`."""
+    a = np.asarray(a)
+    if a.dtype == np.uint16:
+        return (a.astype(np.uint32) << np.uint32(16)).view(np.float32).astype(dtype, copy=False)
+    return as_float64(a).astype(dtype, copy=False)

@@ -28,12 +28,13 @@ no worked example.
 """
 from __future__ import annotations
 
+import math
 from dataclasses import dataclass, field
 from typing import List, Mapping, Optional, Sequence
 
 import numpy as np
 
-from .numerics import as_float64, round_bf16, round_fp8_e4m3
+from .numerics import as_dtype, as_float64, round_bf16, round_fp8_e4m3
 
 
 # --------------------------------------------------------------------------- blocks
@@ -75,10 +76,14 @@ def gqa_attention(q: np.ndarray, K: np.ndarray, V: np.ndarray) -> np.ndarray:
     hkv = K.shape[1]
     G = hq // hkv
     out = np.empty_like(q)
-    for h in range(hq):
-        kv = h // G
-        scores = K[:, kv, :] @ q[h] / np.sqrt(hd)
-        out[h] = softmax(scores) @ V[:, kv, :]
+    for kv in range(hkv):
+        # the keys and values of one KV head, read by its G query heads (a contiguous copy,
+        # so each product below reads them densely)
+        Kh = np.ascontiguousarray(K[:, kv, :])
+        Vh = np.ascontiguousarray(V[:, kv, :])
+        for h in range(kv * G, (kv + 1) * G):
+            scores = Kh @ q[h] / math.sqrt(hd)  # (a Python float keeps the working precision)
+            out[h] = softmax(scores) @ Vh
     return out
 
 
@@ -163,13 +168,20 @@ class DecoderOracle:
         # cache_weights keeps each tensor's decoded value after first use (memory for speed)
         self._cache = {} if cache_weights else None
 
+    def set_weight(self, name: str, value: np.ndarray) -> None:
+        """Replaces one input tensor (same encoding as the constructor's) and drops its cached value."""
+        self.weights = dict(self.weights)
+        self.weights[name] = value
+        if self._cache is not None:
+            self._cache.pop(name, None)
+
     def W(self, name: str) -> np.ndarray:
         if self._cache is not None:
             w = self._cache.get(name)
             if w is None:
-                w = self._cache[name] = as_float64(self.weights[name]).astype(self.dtype, copy=False)
+                w = self._cache[name] = as_dtype(self.weights[name], self.dtype)
             return w
-        return as_float64(self.weights[name]).astype(self.dtype, copy=False)
+        return as_dtype(self.weights[name], self.dtype)
 
     def store_kv(self, x: np.ndarray) -> np.ndarray:
         if self.kv_storage == "bf16":
@@ -199,11 +211,12 @@ class DecoderOracle:
                 q = q + self.W(p + "bq")
                 k = k + self.W(p + "bk")
                 v = v + self.W(p + "bv")
-            q = rope(q.reshape(hq, hd), pos, s.rope_theta)
-            k = rope(k.reshape(hkv, hd), pos, s.rope_theta)
+            # (the rotation angles are float64; results are kept in the oracle's working precision)
+            q = rope(q.reshape(hq, hd), pos, s.rope_theta).astype(self.dtype, copy=False)
+            k = rope(k.reshape(hkv, hd), pos, s.rope_theta).astype(self.dtype, copy=False)
             st.K[i, pos] = self.store_kv(k)
             st.V[i, pos] = self.store_kv(v.reshape(hkv, hd))
-            o = gqa_attention(q, st.K[i, : pos + 1], st.V[i, : pos + 1])
+            o = gqa_attention(q, st.K[i, : pos + 1], st.V[i, : pos + 1]).astype(self.dtype, copy=False)
             h = h + self.W(p + "wo") @ o.reshape(hq * hd)
             x = rmsnorm(h, self.W(p + "mlp_norm"), s.rms_eps)
             a = silu(self.W(p + "w_gate") @ x) * (self.W(p + "w_up") @ x)
