@@ -13,7 +13,9 @@ weights of the named shape and pre-filled random KV (stand-ins for the paper's t
 reasoners and their chains of thought, which are not available here).
 
 Prints one JSON line.  `value` is whole-job decode throughput (tokens/s) with the
-probes and exit decisions inside the timed region.
+probes and exit decisions inside the timed region: ATPs are counted from the first timed
+step (a probe at timed step 0, then every `probe_every` steps), so any run of at least
+S/probe-rows + T - 1 steps times at least one whole riding probe.
 """
 from __future__ import annotations
 
@@ -271,6 +273,8 @@ def main():
                 kv.free_seq(forks[b])
             ride.clear()
 
+    # ATPs fall on step indices counted from the start of each phase (warm-up, timed), so the
+    # timed region begins with a probe whatever the warm-up length.
     log("warmup")
     for i in range(args.warmup):
         step(i, False)
@@ -284,7 +288,7 @@ def main():
 
     if args.profile_only:  # the timed loop's work (decode steps with their probes), nothing else
         for i in range(args.steps):
-            step(args.warmup + i, False)
+            step(i, False)
         while inflight:
             step_mixed_riding(-1, False, new_probes=False)
         settle()
@@ -299,7 +303,7 @@ def main():
     e0.record(stream)
     w0 = time.perf_counter()
     for i in range(args.steps):
-        step(args.warmup + i, True)
+        step(i, True)
     settle()  # the last step's decisions
     e1.record(stream)
     torch.cuda.synchronize()
@@ -314,14 +318,16 @@ def main():
     while inflight:
         step_mixed_riding(-1, False, new_probes=False)
     settle()
-    # reference: the probe run as separate forwards (the cost it has when nothing rides along)
+    # reference: the probe run as separate forwards (the cost it has when nothing rides along),
+    # device time between stream events around the call
     sep_ms = []
-    for _ in range(2):
+    for _ in range(3):
         torch.cuda.synchronize()
-        t0 = time.perf_counter()
+        e0.record(stream)
         L.laser_probe_confidence(model, kv, seqs, suffix, T, conf, argm)
-        conf.cpu()
-        sep_ms.append((time.perf_counter() - t0) * 1e3)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        sep_ms.append(e0.elapsed_time(e1))
     log(f"timed {args.steps} steps: {ms_per_step:.3f} ms/step, {value:.1f} tok/s (wall {wall:.2f}s)")
 
     # ---- decode only (same cache, no probes)
@@ -409,6 +415,7 @@ def main():
                              "max": round(float(np.max(probe_ms)), 3) if probe_ms else None, "n": len(probe_ms)}
         if not (wl.mixed and args.probe_mode == "separate")
         else {"mean": round(ms_per_step, 3), "p50": None, "max": None, "n": probes_timed},
+        "probe_latency_valid": (len(probe_ms) > 0) if not (wl.mixed and args.probe_mode == "separate") else probes_timed > 0,
         "host_decision_us": round(host_decision_us, 3),
         "graph_captures_timed": captures_timed,
         "probe": {"mode": "mixed, riding", "probes_in_timed_region": probes_timed, "forwards_per_probe": T,
@@ -417,12 +424,15 @@ def main():
                                      "ride in one forward with the batch's decode rows, each trial row in one of the "
                                      "next T-1",
                   "exit_decision": "on the host, once the next forward is queued (a request that exits stops one step later)",
-                  "separate_probe_latency_ms": round(float(np.mean(sep_ms)), 3)}
+                  "separate_probe_latency_ms": round(float(np.mean(sep_ms)), 3),
+                  "separate_probe_latency_meaning": "device time between stream events around laser_probe_confidence"}
         if wl.mixed and args.probe_mode == "riding" else
                  {"mode": "mixed", "probes_in_timed_region": probes_timed,
                   "latency_meaning": "each step's probes finish within it: one forward with the decode rows and the "
                                      "probing half's suffix chunks, then T-1 forwards of trial rows",
-                  "separate_probe_latency_ms": round(float(np.mean(sep_ms)), 3)} if wl.mixed else
+                  "separate_probe_latency_ms": round(float(np.mean(sep_ms)), 3),
+                  "separate_probe_latency_meaning": "device time between stream events around laser_probe_confidence"}
+        if wl.mixed else
                  {"mode": args.probe_mode, "rows_per_forward": R if args.probe_mode == "riding" else S,
                   "forwards_per_probe": (-(-S // R) + T - 1) if args.probe_mode == "riding" else 1 + T - 1,
                   "probes_in_timed_region": probes_timed,
@@ -430,7 +440,8 @@ def main():
                   if args.probe_mode == "riding" else "host time of the probe call with its confidence copy",
                   "exit_decision": "on the host, once the next forward is queued (a request that exits stops one step later)"
                   if args.probe_mode == "riding" else "on the host, after the probe's confidence copy",
-                  "separate_probe_latency_ms": round(float(np.mean(sep_ms)), 3)},
+                  "separate_probe_latency_ms": round(float(np.mean(sep_ms)), 3),
+                  "separate_probe_latency_meaning": "device time between stream events around laser_probe_confidence"},
         "step_hbm": {"bytes": step_bytes, "achieved_GBs": round(step_gbs, 1), "frac_of_peak": round(step_gbs / HBM_PEAK_GBS, 4)},
         "roofline": {"kernel": "gate/up projection + SwiGLU (k_gemv, EPI_SWIGLU)", "bound": "hbm",
                      "achieved": round(gu_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
@@ -440,7 +451,7 @@ def main():
         "sim_costs": sim_costs,
     }
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(shape, weights, kv, lens, model, dev, log)
+        out["cpu_baseline"] = cpu_baseline(shape, weights, kv, lens, model, dev, log, S, T)
     print(json.dumps(out), flush=True)
 
 
@@ -519,15 +530,31 @@ def cost_model(L, synth, model, kv, shape, dev, slot, dec_long_ms, ctx_long, suf
                        "probe_ms + probe_ms_per_ctx * context; per prompt = prefill_ms + prefill_ms_per_token * tokens"}
 
 
-def cpu_baseline(shape, weights, kv, lens, model, dev, log):
-    """The oracle, as written, timed on this host for one decode token of request 0."""
+def cpu_baseline(shape, weights, kv, lens, model, dev, log, S, T):
+    """The oracle, as written (float64 numpy), timed on this host: two decode tokens of request
+    0 at its context, BLAS threads set to the cores this process may run on.  A probe of the
+    oracle is S + T - 1 such token forwards (its suffix tokens, then the fed-back trial
+    tokens) plus a softmax statistic per trial token, so its latency is reported as that many
+    measured token times."""
+    import platform
+
     import numpy as np
     import torch
-    from threadpoolctl import threadpool_info
+    from threadpoolctl import threadpool_info, threadpool_limits
 
     from oracle.transformer import DecoderOracle, SeqState
     from paper_2606_31580_amd import synth
 
+    cores = len(os.sched_getaffinity(0))
+    cpu_model = platform.processor() or "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    cpu_model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
     log("cpu baseline: copying weights and the request's KV to the host")
     host = {k: synth.to_numpy(v) for k, v in weights.items()}
     n = kv.seq_len(0)
@@ -536,17 +563,27 @@ def cpu_baseline(shape, weights, kv, lens, model, dev, log):
     V = torch.empty_like(K)
     kv.export_kv(0, K, V)
     torch.cuda.synchronize()
-    st = SeqState.from_prefill(shape, synth.to_numpy(K), synth.to_numpy(V), n + 1)
+    st = SeqState.from_prefill(shape, synth.to_numpy(K), synth.to_numpy(V), n + 2)
     del K, V
     orc = DecoderOracle(shape, host)
-    tok = int(synth.make_tokens(1, shape.vocab, 3004)[0])
-    log("cpu baseline: one oracle decode token")
-    t0 = time.perf_counter()
-    orc.decode_token(st, tok)
-    sec = time.perf_counter() - t0
-    threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    toks = [int(t) for t in synth.make_tokens(2, shape.vocab, 3004)]
+    log(f"cpu baseline: two oracle decode tokens ({cores} cores)")
+    with threadpool_limits(limits=cores, user_api="blas"):
+        info = [i for i in threadpool_info() if i.get("user_api") == "blas"]
+        secs = []
+        for tok in toks:
+            t0 = time.perf_counter()
+            orc.decode_token(st, tok)
+            secs.append(time.perf_counter() - t0)
+    sec = float(np.mean(secs))
+    blas = ", ".join(sorted({f"{i.get('internal_api', '?')} {i.get('version', '')}".strip() for i in info})) or "unknown"
+    threads = max([i.get("num_threads", 1) for i in info] or [1])
     return {"value": round(1.0 / sec, 5), "unit": "tok/s", "cores": threads, "kind": "oracle",
-            "sample": f"1 decode token of request 0 at context {n} (float64 numpy, {sec:.1f} s)"}
+            "sample": f"2 decode tokens of request 0 at context {n}-{n + 1} (float64 numpy, {sum(secs):.1f} s)",
+            "probe_latency_ms": round((S + T - 1) * sec * 1e3, 1),
+            "probe_latency_meaning": f"{S + T - 1} oracle token forwards (S={S} suffix + T-1={T - 1} trial) at the "
+                                     f"measured token time",
+            "affinity_cores": cores, "blas_threads": threads, "blas": blas, "cpu_model": cpu_model}
 
 
 if __name__ == "__main__":

@@ -46,7 +46,7 @@
 extern "C" {
 #endif
 
-#define LASER_ABI_VERSION 2
+#define LASER_ABI_VERSION 3
 
 typedef enum {
   LASER_OK = 0,
@@ -371,7 +371,9 @@ laser_status laser_step_mixed(laser_model* m, laser_kv* kv, int batch, const int
  * spans[i].seq at its current length, with input ids (tok_sel ? d_tok1 : d_tok0)
  * [tok_off .. tok_off + n_tokens - 1]; if spans[i].out is nonzero the greedy token and
  * max-softmax probability of the span's last row go to (out_sel ? d_out_tok1 : d_out_tok0)
- * [out_off] and (out_sel ? d_out_p1 : d_out_p0)[out_off].  A decode step is a span of one
+ * [out_off] and (out_sel ? d_out_p1 : d_out_p0)[out_off], and, when the matching
+ * d_out_logits0 / d_out_logits1 ([..][vocab] floats) is not NULL, its logits to row out_off
+ * of it (for parity checks; NULL skips the write).  A decode step is a span of one
  * token per request; a prompt or probe chunk is a longer span; spans of different
  * sequences mix freely (this is how a probe rides along with decode steps on a fork of
  * the request: Section 3.1's probe, with the request's own tokens unaffected).  Sequences
@@ -382,7 +384,8 @@ typedef struct {
 } laser_span;
 laser_status laser_forward(laser_model* m, laser_kv* kv, int n_spans, const laser_span* spans,
                            const int32_t* d_tok0, const int32_t* d_tok1, int32_t* d_out_tok0, float* d_out_p0,
-                           int32_t* d_out_tok1, float* d_out_p1, void* stream);
+                           int32_t* d_out_tok1, float* d_out_p1, float* d_out_logits0, float* d_out_logits1,
+                           void* stream);
 
 /* d_conf[i] = (d_p[i*T] + ... + d_p[i*T + T-1]) / T for i < n: the confidence of
  * Section 3.1 from the trial tokens' max-softmax probabilities. */
@@ -447,13 +450,15 @@ laser_status laser_model_set_graphs(laser_model* m, int enable);
 laser_status laser_model_graph_stats(const laser_model* m, long long* captures, int* cached);
 
 /* Projection kernel choice on the matrix-core path (forwards of 3 to 64 rows; the linear
- * maps of the transformer block, §4.1's decode and probe forwards).  Two kernels compute
- * the same products: one splits K over the waves of a workgroup (1-4 row groups of 16
- * weight rows per workgroup), the other gives each of 4 waves its own row groups and stages
- * the activations once per workgroup in LDS.  mode 0 (the default) takes the second for the
+ * maps of the transformer block in the decode steps and the trial-answer probe of
+ * Section 3.1, whose costs Eq. 2 sums).  Two kernels compute the same products: one
+ * splits K over the waves of a workgroup (1-4 row groups of 16 weight rows per
+ * workgroup), the other gives each of 4 waves its own row groups and stages the
+ * activations once per workgroup in LDS.  mode 0 (the default) takes the second for the
  * gate/up projection of forwards of 33 to 64 rows when it has enough row groups and for
- * the O and down projections of forwards of 49 to 64 rows, and the first elsewhere; 1 uses only the first kernel; 2 the second wherever it applies (K a
- * multiple of 8).  The summation order differs between them, so
+ * the O and down projections of forwards of 49 to 64 rows, and the first elsewhere; 1
+ * uses only the first kernel; 2 the second wherever it applies (K a multiple of 8).  The
+ * summation order differs between them, so
  * results may differ in the last bits.  Captured forwards are released when the mode
  * changes.  Errors: LASER_ERR_STATE (bad model), LASER_ERR_INVALID_ARG (mode). */
 laser_status laser_model_set_gemm_kernel(laser_model* m, int mode);

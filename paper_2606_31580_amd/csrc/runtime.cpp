@@ -101,7 +101,17 @@ struct GraphEntry {
   FwdKey key;
   hipGraphExec_t exec;
   uint64_t last_use;
+  hipEvent_t done;  // recorded after each launch: the exec is destroyed only once it has completed
 };
+
+// Releases a captured forward after its last launch has finished.
+static void release_graph(GraphEntry& g) {
+  if (g.done) {
+    (void)hipEventSynchronize(g.done);
+    (void)hipEventDestroy(g.done);
+  }
+  (void)hipGraphExecDestroy(g.exec);
+}
 
 // Spans of one kernel class in a timing session: (end of the kernel launched before the
 // class's launch, end of the class's last kernel), as indices into the model's event pool.
@@ -505,7 +515,7 @@ size_t tile_total(const laser_model* m) {
 }
 
 void drop_graphs(laser_model* m) {
-  for (auto& g : m->graphs) (void)hipGraphExecDestroy(g.exec);
+  for (auto& g : m->graphs) release_graph(g);
   m->graphs.clear();
 }
 }  // namespace
@@ -586,7 +596,7 @@ extern "C" laser_status laser_model_destroy(laser_model* m) {
       (void)hipEventDestroy(m->ring_ev[i]);
     }
     (void)hipHostFree(m->h_plans);
-    for (auto& g : m->graphs) (void)hipGraphExecDestroy(g.exec);
+    for (auto& g : m->graphs) release_graph(g);
     if (m->cap_stream) (void)hipStreamDestroy(m->cap_stream);
   }
   for (auto e : m->ev_pool) (void)hipEventDestroy(e);
@@ -989,18 +999,25 @@ static laser_status run_forward(laser_model* m, laser_kv* kv, Plan& p, const Pla
     const hipError_t ei = hipGraphInstantiate(&exec, graph, nullptr, nullptr, 0);
     (void)hipGraphDestroy(graph);
     if (ei != hipSuccess) return laser_fail(LASER_ERR_HIP, "graph instantiate: %s", hipGetErrorString(ei));
-    if ((int)m->graphs.size() >= kMaxGraphs) {
+    hipEvent_t done = nullptr;
+    const hipError_t ee = hipEventCreateWithFlags(&done, hipEventDisableTiming);
+    if (ee != hipSuccess) {
+      (void)hipGraphExecDestroy(exec);
+      return laser_fail(LASER_ERR_HIP, "hipEventCreate: %s", hipGetErrorString(ee));
+    }
+    if ((int)m->graphs.size() >= kMaxGraphs) {  // the least recently used, once its last launch is done
       auto lru = std::min_element(m->graphs.begin(), m->graphs.end(),
                                   [](const GraphEntry& x, const GraphEntry& y) { return x.last_use < y.last_use; });
-      (void)hipGraphExecDestroy(lru->exec);  // safe while a launch of it is in flight
+      release_graph(*lru);
       m->graphs.erase(lru);
     }
-    m->graphs.push_back(GraphEntry{key, exec, 0});
+    m->graphs.push_back(GraphEntry{key, exec, 0, done});
     ++m->graph_captures;
     ge = &m->graphs.back();
   }
   ge->last_use = ++m->graph_clock;
   HIP_TRY(hipGraphLaunch(ge->exec, s));
+  HIP_TRY(hipEventRecord(ge->done, s));
   return LASER_OK;
 }
 
@@ -1478,7 +1495,8 @@ extern "C" laser_status laser_kv_fork(laser_kv* kv, int src_seq, int dst_seq, vo
 
 extern "C" laser_status laser_forward(laser_model* m, laser_kv* kv, int n_spans, const laser_span* spans,
                                       const int32_t* d_tok0, const int32_t* d_tok1, int32_t* d_out_tok0, float* d_out_p0,
-                                      int32_t* d_out_tok1, float* d_out_p1, void* stream) {
+                                      int32_t* d_out_tok1, float* d_out_p1, float* d_out_logits0,
+                                      float* d_out_logits1, void* stream) {
   laser_status st = check_ready(m, kv);
   if (st != LASER_OK) return st;
   if (n_spans < 1 || !spans) return laser_fail(LASER_ERR_INVALID_ARG, "need at least one span");
@@ -1527,6 +1545,8 @@ extern "C" laser_status laser_forward(laser_model* m, laser_kv* kv, int n_spans,
   io.tok_dst[1] = d_out_tok1;
   io.p_dst[0] = d_out_p0;
   io.p_dst[1] = d_out_p1;
+  io.logits[0] = d_out_logits0;
+  io.logits[1] = d_out_logits1;
   st = run_forward(m, kv, *p, io, s);
   delete p;
   return st;

@@ -108,7 +108,7 @@ _SIGS = {
     "laser_decode_step": (_I, [_P, _P, _I, _I32P, _P, _P, _P, _P, _P]),
     "laser_probe_confidence": (_I, [_P, _P, _I, _I32P, _P, _I, _I, _P, _P, _P, _P]),
     "laser_step_mixed": (_I, [_P, _P, _I, _I32P, _P, _P, _P, _I, _I32P, _P, _I, _I, _P, _P, _P]),
-    "laser_forward": (_I, [_P, _P, _I, _P, _P, _P, _P, _P, _P, _P, _P]),
+    "laser_forward": (_I, [_P, _P, _I, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P]),
     "laser_confidence": (_I, [_P, _P, _I, _I, _P, _P]),
     "laser_timing_enable": (_I, [_P, _I, _I]),
     "laser_timing_read": (_I, [_P, _I, C.POINTER(C.c_double), C.POINTER(_I)]),
@@ -411,10 +411,11 @@ def span(seq, n_tokens, tok_sel=0, tok_off=0, out=None):
 
 
 def laser_forward(model: Model, kv: KVCache, spans: Sequence[laser_span], d_tok0, d_tok1=None, d_out_tok0=None,
-                  d_out_p0=None, d_out_tok1=None, d_out_p1=None, stream=None):
+                  d_out_p0=None, d_out_tok1=None, d_out_p1=None, d_out_logits0=None, d_out_logits1=None, stream=None):
     arr = (laser_span * len(spans))(*spans)
     _call("laser_forward", model.h, kv.h, len(spans), arr, _ptr(d_tok0), _ptr(d_tok1), _ptr(d_out_tok0),
-          _ptr(d_out_p0), _ptr(d_out_tok1), _ptr(d_out_p1), _stream_ptr(stream))
+          _ptr(d_out_p0), _ptr(d_out_tok1), _ptr(d_out_p1), _ptr(d_out_logits0), _ptr(d_out_logits1),
+          _stream_ptr(stream))
 
 
 def laser_confidence(model: Model, d_p, T: int, n: int, d_conf, stream=None):

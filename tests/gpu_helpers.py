@@ -24,7 +24,7 @@ def require_gpu():
     return torch.device("cuda:0")
 
 
-def make_pair(shape, max_rows, max_positions, weights_on_device=False, cache_oracle=False):
+def make_pair(shape, max_rows, max_positions, weights_on_device=False, cache_oracle=False, oracle_dtype=np.float64):
     """(device weights, oracle) for `shape` from the seeded generator."""
     dev = require_gpu()
     if weights_on_device:
@@ -32,7 +32,7 @@ def make_pair(shape, max_rows, max_positions, weights_on_device=False, cache_ora
     else:
         w_dev = {k: v.to(dev) for k, v in synth.make_weights(shape).items()}
     host = {k: synth.to_numpy(v) for k, v in w_dev.items()}
-    orc = DecoderOracle(shape, host, cache_weights=cache_oracle)
+    orc = DecoderOracle(shape, host, dtype=oracle_dtype, cache_weights=cache_oracle)
     model = L.Model(shape, w_dev, max_rows=max_rows, max_positions=max_positions, poison=True)
     return model, orc, w_dev
 
@@ -63,3 +63,213 @@ def check_token(gpu_tok, ref_row, what=""):
     if margin > MARGIN:
         assert int(gpu_tok) == tok, f"{what}: token {gpu_tok} vs oracle {tok} (margin {margin})"
     return tok
+
+
+# If every logit of a row is within LOGIT_TOL of the oracle's, each term exp(l_j - l_max) of
+# p_max = 1 / sum_j exp(l_j - l_max) moves by a factor within exp(+-2 LOGIT_TOL), so p_max, and
+# the confidence (a mean of such values), are within that factor too.  At random init every
+# p_max is about 1/V, far below the absolute tolerance, so the relative bound is what gives
+# these checks their power there.
+PROB_REL_TOL = float(np.expm1(2 * LOGIT_TOL))
+
+
+def check_prob(gpu_p, ref_p, what=""):
+    """A max-softmax probability or confidence: within PROB_TOL absolute and PROB_REL_TOL relative."""
+    g, r = float(gpu_p), float(ref_p)
+    err = abs(g - r)
+    assert err <= PROB_TOL, f"{what}: {g} vs oracle {r} (|diff| {err:.3g} > {PROB_TOL})"
+    assert err <= PROB_REL_TOL * r, f"{what}: {g} vs oracle {r} (relative {err / max(r, 1e-30):.3g} > {PROB_REL_TOL:.3g})"
+    return err
+
+
+def forced_probe(model, kv, seq, fork, d_suffix, trial_inputs, T, vocab, logits=True):
+    """The probe of `seq` at its current length on the GPU, with trial token j+1's input forced
+    to trial_inputs[j] (the oracle's t_1..t_{T-1}, i.e. teacher forcing), so the confidence is
+    compared even where a low-margin trial token differs.  Runs on a fork (slot `fork`, freed
+    afterwards): the suffix chunk in one forward, then one forward per trial row
+    (laser_forward), and the mean by laser_confidence.  Returns (tokens, p [T], confidence,
+    logits [T][vocab] or None)."""
+    import torch
+
+    dev = d_suffix.device
+    forced = torch.tensor([int(t) for t in trial_inputs[:T - 1]] or [0], dtype=torch.int32, device=dev)
+    tok = torch.zeros(T, dtype=torch.int32, device=dev)
+    p = torch.zeros(T, device=dev)
+    lg = torch.zeros(T, vocab, device=dev) if logits else None
+    conf = torch.zeros(1, device=dev)
+    kv.fork(seq, fork)
+    S = d_suffix.numel()
+    L.laser_forward(model, kv, [L.span(fork, S, 0, 0, out=(0, 0))], d_suffix, forced, tok, p, d_out_logits0=lg)
+    for j in range(1, T):
+        L.laser_forward(model, kv, [L.span(fork, 1, 1, j - 1, out=(0, j))], d_suffix, forced, tok, p,
+                        d_out_logits0=lg)
+    L.laser_confidence(model, p, T, 1, conf)
+    torch.cuda.synchronize()
+    kv.free_seq(fork)
+    return ([int(x) for x in tok.cpu()], p.cpu().numpy().astype(np.float64), float(conf.item()),
+            None if lg is None else lg.cpu().numpy())
+
+
+def compare_forced_probe(res, got, what=""):
+    """Checks a forced_probe result against the oracle's ProbeResult `res` (same trial inputs)."""
+    tokens, p, conf, logits = got
+    for j in range(len(res.tokens)):
+        if logits is not None and res.logits:
+            compare_logits(logits[j], res.logits[j], f"{what} trial {j}")
+        if res.margins[j] > MARGIN:
+            assert tokens[j] == res.tokens[j], f"{what} trial {j}: token {tokens[j]} vs oracle {res.tokens[j]}"
+        check_prob(p[j], res.pmax[j], f"{what} trial {j} p_max")
+    check_prob(conf, res.confidence, f"{what} confidence")
+
+
+def check_exit_decisions(pairs, what="", seed=0):
+    """Exit decisions of the library (laser_exit_decision on the GPU's confidence) against the
+    oracle controller (on the oracle's confidence), over thresholds spanning the observed
+    confidences: a grid over (0, 1) plus points 1.1e-3 to 2e-2 either side of each oracle
+    confidence, under a fixed threshold (beta 0), Eq. 5 at L_bar = L_target (lambda =
+    lambda_base exactly), and random loads with beta up to 0.5; clamps widened to [0, 1].
+    Decisions must be identical wherever |C - lambda| > 1e-3.  Returns the number compared."""
+    from oracle import controller as OC
+
+    rng = np.random.default_rng(seed)
+    grid = set(np.round(np.linspace(0.01, 0.99, 99), 6).tolist())
+    for _, co in pairs:
+        for dlt in (1.1e-3, 2e-3, 5e-3, 2e-2):
+            grid |= {co - dlt, co + dlt}
+    lams = sorted(x for x in grid if 0.0 < x < 1.0)
+    compared, outcomes = 0, set()
+    for cg, co in pairs:
+        for lam in lams:
+            regimes = [(0.0, 0.0, 1), (0.04, 10.0, 10)]
+            regimes += [(float(rng.choice([0.04, 0.2, 0.5])), float(rng.uniform(0, 30)), int(rng.integers(0, 60)))]
+            for beta, Lbar, active in regimes:
+                for k_done, B_i in ((0, 3), (2, 3)):
+                    op = OC.LaserParams(lambda_base=lam, beta=beta, lambda_min=0.0, lambda_max=1.0)
+                    d_ref, lam_ref, _ = OC.exit_decision(Lbar, co, active, k_done, B_i, op)
+                    cp = L.laser_params_default()
+                    cp.lambda_base, cp.beta, cp.lambda_min, cp.lambda_max = lam, beta, 0.0, 1.0
+                    st = L.laser_load_state(Lbar)
+                    d_gpu, lam_gpu = L.laser_exit_decision(cp, st, float(np.float32(cg)), active, k_done, B_i)
+                    assert abs(lam_gpu - lam_ref) <= 1e-12, f"{what}: threshold {lam_gpu} vs {lam_ref}"
+                    if abs(co - lam_ref) > 1e-3:
+                        assert d_gpu == d_ref, (f"{what}: decision {d_gpu} vs oracle {d_ref} at lambda {lam_ref} "
+                                                f"(C gpu {cg}, oracle {co}, k {k_done}/{B_i})")
+                        compared += 1
+                        outcomes.add(d_ref)
+    # both sides of the threshold were exercised
+    assert {OC.EARLY_EXIT, OC.CONTINUE, OC.BUDGET_EXHAUSTED} <= outcomes, f"{what}: outcomes {outcomes}"
+    return compared
+
+
+def set_final_gain(model, orc, gain):
+    """Sets every element of the final RMSNorm gain to `gain` on the device tensor the model
+    borrows and in the oracle's copy (a power of two is exact in bf16, so both hold the same
+    value).  The norm's output feeds the LM head linearly, so every logit scales by `gain`."""
+    import torch
+
+    w = model.weights["final_norm"]
+    w.fill_(gain)
+    torch.cuda.synchronize()
+    orc.set_weight("final_norm", synth.to_numpy(w))
+
+
+def riding_forwards(model, orc, kv, opool, states, seqs, starts, checked, fork_slots, suffix, S, T, tok_seed,
+                    what, check_rows=None, log=print):
+    """Decode forwards of the requests `seqs` with probes riding along on forks.
+
+    Forward f feeds every request a seeded random input token (a decode row) and starts a
+    probe on each request of starts[f]: the request is forked into the next slot of
+    fork_slots, the fork's S suffix rows ride in forward f and its T-1 trial rows one per
+    forward in f+1 .. f+T-1 (spans in that order: decode rows, trial rows, suffix rows).
+    Probes in `checked` ((forward, request) pairs) are compared with the oracle's probe of the
+    request's state at the fork, their trial inputs forced to the oracle's tokens; the others
+    get seeded random trial inputs.  Decode rows of check_rows (default: every request) are
+    compared with the oracle after every forward (logits, greedy token, max-probability); page
+    tables of every request and live fork with the oracle page model.  Forks of probes that
+    have not finished after the last forward are freed unchecked.  Returns the
+    (GPU confidence, oracle confidence) pairs of the checked probes.
+    """
+    import torch
+
+    V = model.shape.vocab
+    B = len(seqs)
+    check_rows = list(seqs) if check_rows is None else list(check_rows)
+    n_probes = sum(len(s) for s in starts)
+    assert n_probes <= len(fork_slots)
+    for f, b in checked:
+        assert b in check_rows and b in starts[f], "a checked probe needs its request's oracle state"
+    rng = np.random.default_rng(tok_seed)
+    dev = "cuda"
+    d_tok = torch.zeros(B, dtype=torch.int32, device=dev)
+    d_next = torch.zeros(B, dtype=torch.int32, device=dev)
+    d_p = torch.zeros(B, device=dev)
+    d_lg0 = torch.zeros(B, V, device=dev)
+    tok1 = torch.zeros(S + n_probes * (T - 1), dtype=torch.int32, device=dev)
+    tok1[:S] = torch.tensor([int(t) for t in suffix], dtype=torch.int32)
+    out_tok1 = torch.zeros(n_probes * T, dtype=torch.int32, device=dev)
+    out_p1 = torch.zeros(n_probes * T, device=dev)
+    out_lg1 = torch.zeros(n_probes * T, V, device=dev)
+    d_conf = torch.zeros(1, device=dev)
+    live = []  # [slot, fork seq, request, start forward, oracle ProbeResult or None]
+    pairs = []
+    slot = 0
+    for f in range(len(starts)):
+        for b in starts[f]:
+            fork = fork_slots[slot]
+            res = orc.probe(states[b], suffix, T, keep_logits=True) if (f, b) in checked else None
+            kv.fork(b, fork)
+            opool.fork(b, fork)
+            assert kv.page_table(fork) == opool.tables[fork], f"{what}: fork table of request {b} at forward {f}"
+            trial_in = res.tokens[:T - 1] if res else [int(x) for x in rng.integers(0, V, T - 1)]
+            tok1[S + slot * (T - 1):S + (slot + 1) * (T - 1)] = torch.tensor(trial_in, dtype=torch.int32)
+            live.append([slot, fork, b, f, res])
+            slot += 1
+        inputs = [int(x) for x in rng.integers(0, V, B)]
+        d_tok.copy_(torch.tensor(inputs, dtype=torch.int32))
+        spans = [L.span(b, 1, 0, i, out=(0, i)) for i, b in enumerate(seqs)]
+        grow = [(b, 1) for b in seqs]
+        for k, fork, b, f0, _ in live:
+            j = f - f0
+            if j >= 1:  # trial row j reads t_j, gives t_{j+1}
+                spans.append(L.span(fork, 1, 1, S + k * (T - 1) + j - 1, out=(1, k * T + j)))
+                grow.append((fork, 1))
+        for k, fork, b, f0, _ in live:
+            if f0 == f:
+                spans.append(L.span(fork, S, 1, 0, out=(1, k * T)))
+                grow.append((fork, S))
+        rows = sum(n for _, n in grow)
+        L.laser_forward(model, kv, spans, d_tok, tok1, d_next, d_p, out_tok1, out_p1, d_lg0, out_lg1)
+        torch.cuda.synchronize()
+        for sq, n in grow:
+            opool.append(sq, n)
+        lg0 = d_lg0.cpu().numpy()
+        for i, b in enumerate(seqs):
+            if b in check_rows:
+                ref = orc.decode_token(states[b], inputs[i])
+                err = compare_logits(lg0[i], ref, f"{what}: forward {f} ({rows} rows) decode row of request {b}")
+                check_token(d_next[i].item(), ref, f"{what}: forward {f} decode row of request {b}")
+                check_prob(d_p[i].item(), lm_stats(ref)[1], f"{what}: forward {f} p_max of request {b}")
+            assert kv.page_table(b) == opool.tables[b], f"{what}: page table of request {b} after forward {f}"
+        for k, fork, b, f0, _ in live:
+            assert kv.page_table(fork) == opool.tables[fork], f"{what}: fork table after forward {f}"
+        log(f"{what}: forward {f}: {rows} rows, decode rows checked")
+        for pr in [p for p in live if f - p[3] == T - 1]:
+            k, fork, b, f0, res = pr
+            L.laser_confidence(model, out_p1[k * T:], T, 1, d_conf)
+            torch.cuda.synchronize()
+            if res is not None:
+                got = ([int(x) for x in out_tok1[k * T:(k + 1) * T].cpu()],
+                       out_p1[k * T:(k + 1) * T].cpu().numpy().astype(np.float64), float(d_conf.item()),
+                       out_lg1[k * T:(k + 1) * T].cpu().numpy())
+                compare_forced_probe(res, got, f"{what}: probe of request {b} from forward {f0}")
+                pairs.append((got[2], res.confidence))
+                log(f"{what}: probe of request {b} from forward {f0}: conf gpu {got[2]:.6g} oracle {res.confidence:.6g}")
+            kv.free_seq(fork)
+            opool.free_seq(fork)
+            live.remove(pr)
+    for k, fork, b, f0, _ in live:
+        kv.free_seq(fork)
+        opool.free_seq(fork)
+    for b in seqs:
+        assert kv.page_table(b) == opool.tables[b], f"{what}: page table of request {b} at the end"
+    return pairs

@@ -27,7 +27,7 @@ def test_exports_every_declared_symbol(lib):
     for name in declared:
         assert hasattr(lib, name), name
     assert set(L.exported_symbols()) <= declared
-    assert lib.laser_abi_version() == 2
+    assert lib.laser_abi_version() == 3
 
 
 def _params_from(p: OC.LaserParams):

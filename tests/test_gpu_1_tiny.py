@@ -10,7 +10,7 @@ import numpy as np
 import pytest
 import torch
 
-from gpu_helpers import (LOGIT_TOL, PROB_TOL, check_token, compare_logits, export_seq, kv_pair, make_pair,
+from gpu_helpers import (LOGIT_TOL, check_prob, check_token, compare_logits, export_seq, kv_pair, make_pair,
                          require_gpu)
 from oracle.transformer import SeqState, lm_stats
 from paper_2606_31580_amd import laser as L
@@ -50,7 +50,7 @@ def probe_and_compare(model, kv, orc, states, seqs, suffix, d_suffix, what):
                 assert arg[b, j] == tok, f"{what}: trial token {j}"
             agree = arg[b, j] == tok
         if agree:
-            assert abs(conf[b] - res.confidence) <= PROB_TOL, (what, conf[b], res.confidence)
+            check_prob(conf[b], res.confidence, (what, conf[b], res.confidence))
         assert 0.0 <= conf[b] <= 1.0
         assert kv.page_table(s) == tables[b] and kv.seq_len(s) == lens[b], f"{what}: probe changed the cache state"
     return conf
@@ -94,7 +94,7 @@ def test_tiny_full_run():
         worst = max(worst, compare_logits(d_logits[0].cpu().numpy(), ref, f"step {step}"))
         rtok, rp, _ = lm_stats(ref)
         check_token(d_next.item(), ref, f"step {step}")
-        assert abs(d_p.item() - rp) <= PROB_TOL
+        check_prob(d_p.item(), rp)
         assert kv.page_table(0) == opool.tables[0] and kv.seq_len(0) == st.length
         tok = rtok
         if step % 32 == 0:
@@ -155,7 +155,7 @@ def test_tiny_batched_decode_probe_and_mixed(gemm_kernel):
     for b in seqs:
         ref = orc.decode_token(states[b], toks[b])
         check_token(d_next[b].item(), ref, f"mixed decode seq {b}")
-        assert abs(d_p[b].item() - lm_stats(ref)[1]) <= PROB_TOL
+        check_prob(d_p[b].item(), lm_stats(ref)[1])
     for i, b in enumerate(pidx):
         # scratch pages are taken after every request's committed page and returned afterwards
         opool.append(b, S + T - 1)
@@ -164,7 +164,7 @@ def test_tiny_batched_decode_probe_and_mixed(gemm_kernel):
     for i, b in enumerate(pidx):
         res = orc.probe(states[b], suffix, T)
         if list(d_arg[i * T:(i + 1) * T].cpu().numpy()) == res.tokens:
-            assert abs(d_conf[i].item() - res.confidence) <= PROB_TOL
+            check_prob(d_conf[i].item(), res.confidence)
     for b in seqs:
         assert kv.page_table(b) == opool.tables[b] and kv.seq_len(b) == states[b].length
 

@@ -13,7 +13,8 @@ import numpy as np
 import pytest
 import torch
 
-from gpu_helpers import PROB_TOL, check_token, compare_logits, make_pair, require_gpu
+from gpu_helpers import (check_prob, check_token, compare_forced_probe, compare_logits, forced_probe, make_pair,
+                         require_gpu)
 from oracle.pages import PagePool as OraclePool
 from oracle.transformer import SeqState, lm_stats
 from paper_2606_31580_amd import laser as L
@@ -41,7 +42,8 @@ class Setup:
                                             cache_oracle=True)
         pps = max_pos // 16 + 1
         num_pages = sum(n // 16 + 4 for n in lens) + 8 * len(lens) + 8
-        self.kv = L.KVCache(self.model, num_pages, len(lens), pps, poison=True)
+        self.fork_slot = len(lens)  # a free slot for teacher-forced probes
+        self.kv = L.KVCache(self.model, num_pages, len(lens) + 1, pps, poison=True)
         self.opool = OraclePool(num_pages)
         self.states = []
         for i, n in enumerate(lens):
@@ -77,7 +79,7 @@ class Setup:
                 ref = self.orc.decode_token(self.states[b], self.toks[b])
                 err = compare_logits(d_logits[b].cpu().numpy(), ref, f"step {step} seq {b}")
                 check_token(d_next[b].item(), ref, f"step {step} seq {b}")
-                assert abs(d_p[b].item() - lm_stats(ref)[1]) <= PROB_TOL
+                check_prob(d_p[b].item(), lm_stats(ref)[1])
                 self.toks[b] = lm_stats(ref)[0]
                 log(f"decode step {step} seq {b} (ctx {self.states[b].length}): logits err {err:.3g}")
             self.check_tables()
@@ -95,7 +97,12 @@ class Setup:
             if margin > 1e-2:
                 assert agree, f"probe seq {b} trial {j}: {gpu_tokens[j]} vs {tok}"
         if agree:
-            assert abs(gpu_conf - res.confidence) <= PROB_TOL
+            check_prob(gpu_conf, res.confidence, f"probe seq {b} confidence")
+        else:  # a low-margin trial token differs: rerun the probe with the oracle's trial tokens
+            got = forced_probe(self.model, self.kv, b, self.fork_slot, self.d_suffix, res.tokens, T, self.shape.vocab,
+                               logits=bool(res.logits))
+            compare_forced_probe(res, got, f"probe seq {b} (teacher-forced)")
+            log(f"probe seq {b}: trial tokens differ at a low margin; teacher-forced conf gpu {got[2]:.6g}")
         log(f"probe seq {b}: conf gpu {gpu_conf:.6g} oracle {res.confidence:.6g}")
 
     def probe(self, seqs):
@@ -168,7 +175,7 @@ def test_llama8b_b8_mixed_step_state_injection():
     for b in st.seqs:
         ref = st.orc.decode_token(st.states[b], st.toks[b])
         check_token(d_next[b].item(), ref, f"mixed decode seq {b}")
-        assert abs(d_p[b].item() - lm_stats(ref)[1]) <= PROB_TOL
+        check_prob(d_p[b].item(), lm_stats(ref)[1])
         log(f"mixed decode seq {b} ok")
     for b in probe_idx:
         st.opool.truncate(b, st.states[b].length)
@@ -217,7 +224,7 @@ def test_qwen1p5b_prefill_64row_chunks(gemm_kernel):
     ref = orc.decode_token(st, tok)
     err = compare_logits(d_logits[0].cpu().numpy(), ref, "decode after prefill")
     check_token(d_next.item(), ref, "decode after prefill")
-    assert abs(d_p.item() - lm_stats(ref)[1]) <= PROB_TOL
+    check_prob(d_p.item(), lm_stats(ref)[1])
     log(f"decode after prefill: logits err {err:.3g}")
     kv.destroy()
     model.destroy()

@@ -9,14 +9,17 @@ all suffix rows in one forward beside the decode row, then the trial rows one pe
 
 * every decode row equals plain decoding of the request (the fork's rows never touch it);
 * the confidence and trial tokens equal the oracle's probe of the request's state at the
-  ATP (Section 3.1);
+  ATP (Section 3.1): with the trial rows fed back on the device (the benchmark's way; the
+  confidence compared whenever the trial tokens agree) and teacher-forced with the oracle's
+  trial tokens (every trial's max-probability and the confidence compared);
+* decode rows take the oracle's greedy tokens as inputs (teacher forcing);
 * page tables (request, fork, and the pool after the fork is freed) equal the oracle page
   model's, bit for bit.
 """
 import pytest
 import torch
 
-from gpu_helpers import PROB_TOL, check_token, kv_pair, make_pair, require_gpu
+from gpu_helpers import check_prob, check_token, kv_pair, make_pair, require_gpu
 from oracle.transformer import SeqState, lm_stats
 from paper_2606_31580_amd import laser as L
 from paper_2606_31580_amd import synth
@@ -27,9 +30,14 @@ pytestmark = pytest.mark.gpu
 S, T = 8, 4
 
 
-def riding_probe_run(shape, model, orc, kv, opool, states, seqs, probing, forks, per_step, toks, suffix, tag):
-    """Runs decode steps for `seqs` while requests `probing` (forked into `forks`) carry their
-    probe rows, per_step rows per forward; returns (forwards, the next input tokens)."""
+def riding_probe_run(shape, model, orc, kv, opool, states, seqs, probing, forks, per_step, toks, suffix, tag,
+                     forced=False):
+    """Runs decode steps for `seqs` (inputs: the oracle's greedy tokens) while requests
+    `probing` (forked into `forks`) carry their probe rows, per_step rows per forward.  The
+    trial rows read t_j as the device wrote it (forced=False: the benchmark's feedback, the
+    confidence compared whenever every trial token agrees) or the oracle's t_j (forced=True:
+    teacher forcing, every p_j and the confidence compared).  Returns (forwards, the next
+    input tokens)."""
     V = shape.vocab
     B, P = len(seqs), len(probing)
     d_tok = torch.tensor(toks, dtype=torch.int32, device="cuda")
@@ -39,11 +47,13 @@ def riding_probe_run(shape, model, orc, kv, opool, states, seqs, probing, forks,
     d_arg = torch.zeros(P * T, dtype=torch.int32, device="cuda")
     d_pp = torch.zeros(P * T, device="cuda")
     d_conf = torch.zeros(P, device="cuda")
-    atp = {b: states[b].copy() for b in probing}
+    res = {b: orc.probe(states[b], suffix, T) for b in probing}  # the oracle's probe at the ATP
+    d_forced = torch.tensor([t for b in probing for t in res[b].tokens], dtype=torch.int32, device="cuda")
     for b, f in zip(probing, forks):
         kv.fork(b, f)
         opool.fork(b, f)
         assert kv.page_table(f) == opool.tables[f], f"{tag}: fork table"
+    toks = list(toks)
     done_s, done_t, n_fwd = 0, 0, 0
     while done_t < T - 1 or done_s < S:
         spans = [L.span(b, 1, 0, i, out=(0, i)) for i, b in enumerate(seqs)]
@@ -58,36 +68,43 @@ def riding_probe_run(shape, model, orc, kv, opool, states, seqs, probing, forks,
             done_t += 1
             for i, f in enumerate(forks):  # trial j = done_t reads t_j, writes t_{j+1}
                 spans.append(L.span(f, 1, 1, i * T + done_t - 1, out=(1, i * T + done_t)))
-            tok1, adv = d_arg, 1
+            tok1, adv = (d_forced if forced else d_arg), 1
         L.laser_forward(model, kv, spans, d_tok, tok1, d_next, d_p, d_arg, d_pp)
         torch.cuda.synchronize()
         n_fwd += 1
         for i, b in enumerate(seqs):
             opool.append(b, 1)
-            ref = orc.decode_token(states[b], int(d_tok[i].item()))
+            ref = orc.decode_token(states[b], toks[i])
             check_token(d_next[i].item(), ref, f"{tag}: decode seq {b} forward {n_fwd}")
-            assert abs(d_p[i].item() - lm_stats(ref)[1]) <= PROB_TOL
+            check_prob(d_p[i].item(), lm_stats(ref)[1], f"{tag}: decode seq {b} forward {n_fwd}")
             assert kv.page_table(b) == opool.tables[b]
+            toks[i] = lm_stats(ref)[0]
         for f in forks:
             opool.append(f, adv)
             assert kv.page_table(f) == opool.tables[f], f"{tag}: fork table after forward {n_fwd}"
-        d_tok.copy_(d_next)
+        d_tok.copy_(torch.tensor(toks, dtype=torch.int32))
     L.laser_confidence(model, d_pp, T, P, d_conf)
     torch.cuda.synchronize()
+    pp = d_pp.cpu().numpy()
     for i, b in enumerate(probing):
-        res = orc.probe(atp[b], suffix, T)
+        r = res[b]
         got = [int(x) for x in d_arg[i * T:(i + 1) * T].cpu().numpy()]
-        print(f"{tag}: probe seq {b}: conf gpu {d_conf[i].item():.6g} oracle {res.confidence:.6g}", flush=True)
-        if got == res.tokens:
-            assert abs(d_conf[i].item() - res.confidence) <= PROB_TOL
-        else:  # a trial token may differ only where the oracle's top-2 margin is tiny
-            assert any(m <= 1e-2 for m in res.margins), f"{tag}: trial tokens {got} vs {res.tokens}"
+        print(f"{tag}: probe seq {b}: conf gpu {d_conf[i].item():.6g} oracle {r.confidence:.6g}", flush=True)
+        for j in range(T):
+            if r.margins[j] > 1e-2:
+                assert got[j] == r.tokens[j], f"{tag}: trial {j} token {got[j]} vs {r.tokens[j]}"
+        if forced or got == r.tokens:
+            for j in range(T):
+                check_prob(pp[i * T + j], r.pmax[j], f"{tag}: probe seq {b} trial {j}")
+            check_prob(d_conf[i].item(), r.confidence, f"{tag}: probe seq {b} confidence")
+        else:  # device feedback: a trial token may differ only where the oracle's top-2 margin is tiny
+            assert any(m <= 1e-2 for m in r.margins), f"{tag}: trial tokens {got} vs {r.tokens}"
     for f in forks:
         kv.free_seq(f)
         opool.free_seq(f)
     for b in seqs:
         assert kv.page_table(b) == opool.tables[b] and kv.seq_len(b) == states[b].length
-    return n_fwd, [int(x) for x in d_tok.cpu().numpy()]
+    return n_fwd, toks
 
 
 def test_riding_probe_tiny():
@@ -104,9 +121,9 @@ def test_riding_probe_tiny():
         states.append(SeqState.from_prefill(TINY, K0.numpy(), V0.numpy(), 1024))
     toks = [int(t) for t in synth.make_tokens(len(lens), TINY.vocab, 3010)]
     suffix = [int(t) for t in synth.make_suffix(S, TINY.vocab)]
-    for per_step in (1, 3, 8):
+    for per_step, forced in ((1, False), (3, False), (8, False), (3, True), (8, True)):
         n, toks = riding_probe_run(TINY, model, orc, kv, opool, states, [0, 1, 2], [0, 1], [5, 6], per_step,
-                                   toks, suffix, f"tiny per_step={per_step}")
+                                   toks, suffix, f"tiny per_step={per_step} forced={forced}", forced=forced)
         assert n == -(-S // per_step) + T - 1
 
 
@@ -146,56 +163,63 @@ def test_riding_probes_staggered_tiny():
         states.append(SeqState.from_prefill(TINY, K0.numpy(), V0.numpy(), 1024))
     seqs = [0, 1, 2]
     suffix = [int(t) for t in synth.make_suffix(S, TINY.vocab)]
-    d_tok = torch.tensor([int(t) for t in synth.make_tokens(3, TINY.vocab, 3011)], dtype=torch.int32, device="cuda")
+    toks = [int(t) for t in synth.make_tokens(3, TINY.vocab, 3011)]
+    d_tok = torch.tensor(toks, dtype=torch.int32, device="cuda")
     d_next = torch.zeros(3, dtype=torch.int32, device="cuda")
     d_p = torch.zeros(3, device="cuda")
+    # inputs: the suffix, then each slot's trial inputs (the oracle's t_1..t_{T-1}: teacher forcing)
     tokbuf = torch.zeros(S + P * T, dtype=torch.int32, device="cuda")
     tokbuf[:S] = torch.tensor(suffix, dtype=torch.int32)
-    pbuf = torch.zeros(S + P * T, device="cuda")
+    outbuf = torch.zeros(P * T, dtype=torch.int32, device="cuda")
+    pbuf = torch.zeros(P * T, device="cuda")
     d_conf = torch.zeros(1, device="cuda")
     free, inflight, checked = list(range(P)), [], 0
     n_fwd = 10
     for fwd in range(n_fwd + T - 1):
         spans = [L.span(b, 1, 0, i, out=(0, i)) for i, b in enumerate(seqs)]
         fork_rows = []  # (fork slot, rows) in span order: pages are taken in that order
-        for pr in inflight:  # [slot, request, trials done, request state at the fork]
+        for pr in inflight:  # [slot, request, trials done, the oracle's probe at the fork]
             f, j = pr[0], pr[2] + 1
-            spans.append(L.span(3 + f, 1, 1, S + f * T + j - 1, out=(1, S + f * T + j)))
+            spans.append(L.span(3 + f, 1, 1, S + f * T + j - 1, out=(1, f * T + j)))
             fork_rows.append((3 + f, 1))
             pr[2] = j
         if fwd < n_fwd:
             b = seqs[fwd % 3]
             f = free.pop()
+            res = orc.probe(states[b], suffix, T)
+            tokbuf[S + f * T:S + (f + 1) * T] = torch.tensor(res.tokens, dtype=torch.int32)
             kv.fork(b, 3 + f)
             opool.fork(b, 3 + f)
             assert kv.page_table(3 + f) == opool.tables[3 + f], f"fork table at forward {fwd}"
-            spans.append(L.span(3 + f, S, 1, 0, out=(1, S + f * T)))
+            spans.append(L.span(3 + f, S, 1, 0, out=(1, f * T)))
             fork_rows.append((3 + f, S))
-            inflight.append([f, b, 0, states[b].copy()])
-        L.laser_forward(model, kv, spans, d_tok, tokbuf, d_next, d_p, tokbuf, pbuf)
+            inflight.append([f, b, 0, res])
+        L.laser_forward(model, kv, spans, d_tok, tokbuf, d_next, d_p, outbuf, pbuf)
         torch.cuda.synchronize()
         for b in seqs:
             opool.append(b, 1)
         for f, n in fork_rows:
             opool.append(f, n)
         for i, b in enumerate(seqs):
-            ref = orc.decode_token(states[b], int(d_tok[i].item()))
+            ref = orc.decode_token(states[b], toks[i])
             check_token(d_next[i].item(), ref, f"staggered: decode seq {b} forward {fwd}")
-            assert abs(d_p[i].item() - lm_stats(ref)[1]) <= PROB_TOL
+            check_prob(d_p[i].item(), lm_stats(ref)[1], f"staggered: decode seq {b} forward {fwd}")
             assert kv.page_table(b) == opool.tables[b]
+            toks[i] = lm_stats(ref)[0]
         for pr in inflight:
             assert kv.page_table(3 + pr[0]) == opool.tables[3 + pr[0]], f"fork table after forward {fwd}"
-        d_tok.copy_(d_next)
+        d_tok.copy_(torch.tensor(toks, dtype=torch.int32))
         for pr in [p for p in inflight if p[2] == T - 1]:
-            f, b = pr[0], pr[1]
-            L.laser_confidence(model, pbuf[S + f * T:], T, 1, d_conf)
+            f, b, res = pr[0], pr[1], pr[3]
+            L.laser_confidence(model, pbuf[f * T:], T, 1, d_conf)
             torch.cuda.synchronize()
-            res = orc.probe(pr[3], suffix, T)
-            got = [int(x) for x in tokbuf[S + f * T:S + (f + 1) * T].cpu().numpy()]
-            if got == res.tokens:
-                assert abs(d_conf.item() - res.confidence) <= PROB_TOL, f"probe of seq {b} (slot {f})"
-            else:
-                assert any(m <= 1e-2 for m in res.margins), f"probe of seq {b}: trials {got} vs {res.tokens}"
+            got = [int(x) for x in outbuf[f * T:(f + 1) * T].cpu().numpy()]
+            pp = pbuf[f * T:(f + 1) * T].cpu().numpy()
+            for j in range(T):
+                if res.margins[j] > 1e-2:
+                    assert got[j] == res.tokens[j], f"probe of seq {b} (slot {f}) trial {j}"
+                check_prob(pp[j], res.pmax[j], f"probe of seq {b} (slot {f}) trial {j}")
+            check_prob(d_conf.item(), res.confidence, f"probe of seq {b} (slot {f})")
             kv.free_seq(3 + f)
             opool.free_seq(3 + f)
             free.append(f)
@@ -238,7 +262,7 @@ def test_fork_with_long_own_tail_tiny():
                 opool.append(b, 1)
                 ref = orc.decode_token(states[b], toks[b])
                 check_token(d_next[i].item(), ref, f"{tag} step {step} seq {b}")
-                assert abs(d_p[i].item() - lm_stats(ref)[1]) <= PROB_TOL
+                check_prob(d_p[i].item(), lm_stats(ref)[1])
                 toks[b] = lm_stats(ref)[0]
                 assert kv.page_table(b) == opool.tables[b], f"{tag} step {step}: page table of seq {b}"
             d_tok.copy_(torch.tensor([toks[b] for b in seqs], dtype=torch.int32))

@@ -14,7 +14,7 @@ import numpy as np
 import pytest
 import torch
 
-from gpu_helpers import PROB_TOL, check_token, require_gpu
+from gpu_helpers import check_prob, check_token, require_gpu
 from oracle.numerics import round_fp8_e4m3
 from oracle.transformer import lm_stats
 from paper_2606_31580_amd import laser as L
@@ -91,7 +91,7 @@ def test_llama8b_fp8kv_b8_mixed_step_state_injection():
     for b in st.seqs:
         ref = st.orc.decode_token(st.states[b], st.toks[b])
         check_token(d_next[b].item(), ref, f"mixed decode seq {b}")
-        assert abs(d_p[b].item() - lm_stats(ref)[1]) <= PROB_TOL
+        check_prob(d_p[b].item(), lm_stats(ref)[1])
     for b in probe_idx:
         st.opool.truncate(b, st.states[b].length)
     arg = d_arg.cpu().numpy().reshape(len(probe_idx), T)
