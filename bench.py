@@ -47,6 +47,10 @@ def parse():
     ap.add_argument("--no-tiles", action="store_true", help="MFMA path reads the row-major weights (no tile copy)")
     ap.add_argument("--gemm-kernel", type=int, choices=[0, 1, 2], default=0,
                     help="matrix-core projections: 0 by cost, 1 K-split waves only, 2 row waves where they apply")
+    ap.add_argument("--attn-merge", choices=["fused", "kernel"], default="kernel",
+                    help="one-row attention groups: merged by the attention kernel's last workgroup (fused) or "
+                         "by the separate merge kernel")
+    ap.add_argument("--attn-splits", type=int, default=56, help="split bound of a fused one-row attention group")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 256 MiB device-to-device copy three times (scale for HBM byte counters)")
     return ap.parse_args()
@@ -105,6 +109,7 @@ def main():
     # the workspace takes the full 64 rows so that prompt prefills run in 64-token chunks
     model = L.Model(shape, weights, max_rows=64, max_positions=max_pos, tiles=not args.no_tiles)
     model.set_gemm_kernel(args.gemm_kernel)
+    model.set_attn_merge(args.attn_merge == "fused", args.attn_splits)
     pps = max_pos // PAGE + 1
     num_pages = sum((n + 2 * total_steps + S + T) // PAGE + 2 for n in lens) + B * ((S + T) // PAGE + 3) + 8
     num_pages += (COST_CTX + 512) // PAGE + 4  # the cost-model pass (a shorter request in a fork slot)
@@ -407,7 +412,8 @@ def main():
         "dtype": "bf16 weights+KV, fp32 activations" if shape.dtype == "bf16" else "f32",
         "data": "synthetic: random-init weights, seeded pre-filled KV",
         "config": {"workload": wl.name, "model_shape": shape.name, "batch": B, "kv_lens": lens,
-                   "probe_every": wl.probe_every, "suffix": S, "trials": T},
+                   "probe_every": wl.probe_every, "suffix": S, "trials": T, "attn_merge": args.attn_merge,
+                   "attn_splits": args.attn_splits},
         "decode_only_ms_per_step": round(dec_ms, 4),
         "decode_only_tok_s": round(B / (dec_ms / 1e3), 2),
         "probe_latency_ms": {"mean": round(float(np.mean(probe_ms)), 3) if probe_ms else None,

@@ -463,6 +463,20 @@ laser_status laser_model_graph_stats(const laser_model* m, long long* captures, 
  * changes.  Errors: LASER_ERR_STATE (bad model), LASER_ERR_INVALID_ARG (mode). */
 laser_status laser_model_set_gemm_kernel(laser_model* m, int mode);
 
+/* Attention split merge.  The decode step's paged attention (Section 3.1's chain-of-thought
+ * decode, whose per-token cost Eq. 2 sums) splits a long context over several workgroups per
+ * KV head and combines their partial results (running max, sum of exponentials, weighted
+ * values).  fused = 0 (the default): every group's partials are combined by a separate merge
+ * kernel.  fused = 1: a group of one row (a plain decode row) is combined by the last of its
+ * workgroups to finish, inside the attention kernel, over at most max_splits splits (56 by
+ * default); other groups (probe chunks, shared-prefix families) keep the merge kernel.  The
+ * summation order differs between the two, so results may differ in the last bits.  (At the
+ * 7B shape, batch 1, 14k context the fused merge measured slower: the last workgroup's
+ * device-scope round trips cost more than the kernel boundary.)
+ * Errors: LASER_ERR_STATE (bad model), LASER_ERR_INVALID_ARG (fused not 0/1, max_splits
+ * outside [2, 128]). */
+laser_status laser_model_set_attn_merge(laser_model* m, int fused, int max_splits);
+
 #ifdef __cplusplus
 }
 #endif

@@ -15,7 +15,10 @@
 // The KV page layout makes every operand load a contiguous 1 KB (K) / 512 B (V) per wave
 // instruction.  A wave's query tile stays in registers and pages are taken in pairs, so the
 // cross-lane max and sum reductions run once per 32 positions.  When a (group, kv head)
-// spans several workgroups their fp32 partials are combined by k_attn_merge, launched next.
+// spans several workgroups their fp32 partials are combined: for a one-row group (a decode
+// row) by the group's last workgroup to finish, inside this kernel (the partials go out with
+// device-scope stores, an arrival counter tells the last one; see the fused items below);
+// otherwise by k_attn_merge, launched next.
 #include <type_traits>
 
 #include "device_common.hpp"
@@ -43,7 +46,9 @@ __global__ __launch_bounds__(64 * kAttnWaves) void k_attn(AttnArgs a) {
 
   const AttnItem wi = a.plan->items[blockIdx.x];
   if (wi.nrows == 0) return;  // padding item
-  const int NQ = wi.nrows * a.G;
+  const int nrows = wi.nrows & 0xff;
+  const int fuse_n = (wi.nrows >> 8) & 0xff;  // fused group: its split count (else 0)
+  const int NQ = nrows * a.G;
   const int kvh = blockIdx.y;
   const int tid = threadIdx.x;
   const int w = tid >> 6, l = tid & 63;
@@ -336,39 +341,93 @@ __global__ __launch_bounds__(64 * kAttnWaves) void k_attn(AttnArgs a) {
     }
   }
   __syncthreads();
-  if (w != 0) return;
+  if (w != 0 && fuse_n == 0) return;
+  const size_t ncols = (size_t)a.max_rows * a.G;
+  const __amdgpu_buffer_rsrc_t rpart = dev_rsrc(a.part, a.part_bytes), rml = dev_rsrc(a.ml, a.ml_bytes);
+  if (w == 0) {
 #pragma unroll
-  for (int u = 0; u < 3; ++u) {
-    const float m2 = s_m[u][lc], l2 = s_l[u][lc];
-    const float mm = fmaxf(m_run, m2);
-    const float ca = (mm == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(m_run - mm);
-    const float cb2 = (mm == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(m2 - mm);
-    l_run = l_run * ca + l2 * cb2;
-    m_run = mm;
+    for (int u = 0; u < 3; ++u) {
+      const float m2 = s_m[u][lc], l2 = s_l[u][lc];
+      const float mm = fmaxf(m_run, m2);
+      const float ca = (mm == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(m_run - mm);
+      const float cb2 = (mm == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(m2 - mm);
+      l_run = l_run * ca + l2 * cb2;
+      m_run = mm;
 #pragma unroll
-    for (int dt = 0; dt < ND; ++dt) {
-      const f32x4 x = *(const f32x4*)(s_of + u * 16 * OS + lc * OS + 16 * dt + 4 * lg);
-      o[dt] = o[dt] * ca + x * cb2;
+      for (int dt = 0; dt < ND; ++dt) {
+        const f32x4 x = *(const f32x4*)(s_of + u * 16 * OS + lc * OS + 16 * dt + 4 * lg);
+        o[dt] = o[dt] * ca + x * cb2;
+      }
+    }
+    // ---- the tile's columns: the output (one workgroup) or the workgroup's partial
+    if (c < NQ) {
+      const int row = wi.row0 + c / a.G, head = kvh * a.G + c % a.G;
+      const size_t col = ((size_t)kvh * kAttnMaxWG + ((wi.info >> 8) & 0xffff)) * ncols + (size_t)wi.row0 * a.G + c;
+      if (wi.info & (1 << 24)) {
+        float* out = a.o + ((size_t)row * a.hq + head) * HD;
+        const float inv = 1.f / l_run;
+#pragma unroll
+        for (int dt = 0; dt < ND; ++dt) *(f32x4*)(out + 16 * dt + 4 * lg) = o[dt] * inv;
+      } else if (fuse_n) {  // device-scope stores: another XCD's workgroup may merge them
+#pragma unroll
+        for (int dt = 0; dt < ND; ++dt) st_dev16(rpart, (uint32_t)((col * HD + 16 * dt + 4 * lg) * 4), o[dt]);
+        if (lg == 0) st_dev8(rml, (uint32_t)(col * 8), m_run, l_run);
+      } else {
+#pragma unroll
+        for (int dt = 0; dt < ND; ++dt) *(f32x4*)(a.part + col * HD + 16 * dt + 4 * lg) = o[dt];
+        if (lg == 0) {
+          a.ml[col * 2 + 0] = m_run;
+          a.ml[col * 2 + 1] = l_run;
+        }
+      }
     }
   }
-  // ---- the tile's columns: the output (one workgroup) or the workgroup's partial
-  if (c >= NQ) return;
-  const int row = wi.row0 + c / a.G, head = kvh * a.G + c % a.G;
-  if (wi.info & (1 << 24)) {
-    float* out = a.o + ((size_t)row * a.hq + head) * HD;
-    const float inv = 1.f / l_run;
-#pragma unroll
-    for (int dt = 0; dt < ND; ++dt) *(f32x4*)(out + 16 * dt + 4 * lg) = o[dt] * inv;
-    return;
+  if (fuse_n == 0) return;
+
+  // ---- fused group: count this workgroup's arrival once its partial is stored; the last of
+  // the group's fuse_n workgroups combines every split (slots 0 .. fuse_n-1, fixed order):
+  // o = sum_s O_s 2^(m_s - M) / sum_s l_s 2^(m_s - M), then re-arms the counter.
+  __shared__ unsigned s_tk;
+  unsigned* cnt = a.cnt + ((size_t)kvh * kMaxGroups + (wi.nrows >> 16)) * kAttnCntStride;
+  if (w == 0) {
+    wait_mem();
+    if (l == 0) s_tk = __hip_atomic_fetch_add(cnt, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
-  const size_t ncols = (size_t)a.max_rows * a.G;
-  const size_t col = ((size_t)kvh * kAttnMaxWG + ((wi.info >> 8) & 0xffff)) * ncols + (size_t)wi.row0 * a.G + c;
+  __syncthreads();
+  if (s_tk != (unsigned)(fuse_n - 1)) return;
+  constexpr int CH = HD / 4;  // 4-dim chunks of a column
+  if (tid < NQ * CH) {
+    const int cc = tid / CH, d4 = tid - cc * CH;
+    const size_t colb = (size_t)wi.row0 * a.G + cc;
+    float M = -INFINITY, Ls = 0.f;
+    f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+    constexpr int B = 8;  // slots loaded together
+    for (int s0 = 0; s0 < fuse_n; s0 += B) {
+      f32x4 ov[B];
+      i32x2 mv[B];
 #pragma unroll
-  for (int dt = 0; dt < ND; ++dt) *(f32x4*)(a.part + col * HD + 16 * dt + 4 * lg) = o[dt];
-  if (lg == 0) {
-    a.ml[col * 2 + 0] = m_run;
-    a.ml[col * 2 + 1] = l_run;
+      for (int j = 0; j < B; ++j) {  // past the count: slot fuse_n - 1 again (ignored below)
+        const size_t colx = ((size_t)kvh * kAttnMaxWG + min(s0 + j, fuse_n - 1)) * ncols + colb;
+        ov[j] = ld_dev16(rpart, (uint32_t)((colx * HD + 4 * d4) * 4));
+        mv[j] = ld_dev8(rml, (uint32_t)(colx * 8));
+      }
+#pragma unroll
+      for (int j = 0; j < B; ++j) {
+        if (s0 + j < fuse_n) {
+          const float ms = __int_as_float(mv[j][0]), ls = __int_as_float(mv[j][1]);
+          const float mn = fmaxf(M, ms);
+          const float ca = (M == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(M - mn);
+          const float cb = (ms == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(ms - mn);
+          Ls = Ls * ca + ls * cb;
+          acc = acc * ca + ov[j] * cb;
+          M = mn;
+        }
+      }
+    }
+    const int row = wi.row0 + cc / a.G, head = kvh * a.G + cc % a.G;
+    *(f32x4*)(a.o + ((size_t)row * a.hq + head) * HD + 4 * d4) = acc * (1.f / Ls);
   }
+  if (tid == 0) __hip_atomic_store(cnt, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 // Combines the workgroup partials (m, l, O) of every (row, query head) whose group used

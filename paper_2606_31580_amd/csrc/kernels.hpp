@@ -33,15 +33,20 @@ struct GroupDesc {
   int pbeg;                                // first page
   int slot0;                               // first partial slot of the group's workgroups
   int direct;                              // the group alone covers its rows in one workgroup: no merge
+  int fused;                               // one row, several workgroups: merged by the last of them
 };
 // One attention workgroup (per kv head): a group's 16-column query tile over 4 runs of pages,
 // wave w's run [p0 + w pps, min(p0 + (w + 1) pps, pend)).  nrows == 0: padding, no work.
+// A one-row group split over several workgroups may merge its splits itself ("fused"): then
+// nrows carries the split count in bits 8-15 and the group's arrival counter in bits 16-23,
+// and the last workgroup of the group to finish combines every split's partial.
 struct AttnItem {
-  int seq, row0, nrows;  // the group's block table and rows
+  int seq, row0, nrows;  // the group's block table and rows (bits 0-7; fused: see above)
   int p0, pend, pps;
   int maxpos;            // last position any row of the group sees
   int info;              // tile (bits 0-7) | partial slot (bits 8-23) | direct output (bit 24)
 };
+constexpr int kAttnCntStride = 16;  // arrival counters 64 bytes apart: [kv head][group]
 // LM-head output row: activation row, destination (sel, off) for token / prob / logits.
 struct OutDesc {
   int row, sel, off, pad;
@@ -141,6 +146,8 @@ struct AttnArgs {
   float scale_log2;
   float* part;  // [hkv][kAttnMaxWG][max_rows*G][hd]
   float* ml;    // [hkv][kAttnMaxWG][max_rows*G][2]
+  uint32_t part_bytes, ml_bytes;
+  unsigned* cnt;  // fused groups' arrival counters [hkv][kMaxGroups] x kAttnCntStride; zero between kernels
 };
 
 // Kernel timing hooks.  `start`/`stop` are bound to the next launch only; when `next_stop`

@@ -80,9 +80,17 @@ constexpr int kTargetAttnWaves = LASER_ATTN_TARGET_WAVES;  // attention waves a 
 #define LASER_ATTN_MAX_PPS 4
 #endif
 constexpr int kMaxPagesPerWave = LASER_ATTN_MAX_PPS;
+// Splits of a one-row group that merges inside the attention kernel: its last workgroup reads
+// every split's partial (G columns x (hd + 2) floats each), so fewer, longer splits shorten
+// that tail; the bound trades it against how many workgroups stream the group's pages.
+#ifndef LASER_ATTN_FUSED_SPLITS
+#define LASER_ATTN_FUSED_SPLITS 56
+#endif
+constexpr int kFusedMaxSplits = LASER_ATTN_FUSED_SPLITS;
 
 struct Layout {
-  size_t rope, h, q, o, act, kpart, lm_part, attn_part, attn_ml, plans, probe_p, tok_buf, p_buf, total;
+  size_t rope, h, q, o, act, kpart, lm_part, attn_part, attn_ml, attn_cnt, plans, probe_p, tok_buf, p_buf, total;
+  size_t attn_part_bytes, attn_ml_bytes, attn_cnt_bytes;
 };
 
 // Launch signature of a forward.  With the plan in its fixed device slot and the caller's
@@ -149,6 +157,10 @@ struct laser_model {
   int last_stop = -1;  // pool index bound to the most recent launch's end
   bool use_graphs = true;
   int gemm_kernel = 0;  // MFMA-path kernel choice (laser_model_set_gemm_kernel)
+  // one-row attention groups merge their splits inside the attention kernel (laser_model_set_attn_merge;
+  // off by default: measured slower than the merge kernel at the 7B shape, batch 1)
+  int attn_fuse = 0;
+  int attn_fuse_max = kFusedMaxSplits;
   // tile-order weight copies for the MFMA path (laser_model_set_tiles)
   struct Tiles {
     const char *qkv, *o, *gu, *down;
@@ -319,8 +331,12 @@ static Layout make_layout(const laser_model_desc& d, int max_rows) {
   L.act = take((size_t)max_rows * d.d_ffn * 4);
   L.kpart = take((size_t)kMaxKsplit * max_rows * d.d_model * 4);  // K-share partials of O-proj / down
   L.lm_part = take((size_t)groups_lm(d, 1) * kMaxRows * sizeof(LmPart));  // the VALU path has the most groups
-  L.attn_part = take((size_t)d.n_kv_heads * kAttnMaxWG * max_rows * G * hd * 4);
-  L.attn_ml = take((size_t)d.n_kv_heads * kAttnMaxWG * max_rows * G * 2 * 4);
+  L.attn_part_bytes = (size_t)d.n_kv_heads * kAttnMaxWG * max_rows * G * hd * 4;
+  L.attn_ml_bytes = (size_t)d.n_kv_heads * kAttnMaxWG * max_rows * G * 2 * 4;
+  L.attn_cnt_bytes = (size_t)d.n_kv_heads * kMaxGroups * kAttnCntStride * 4;
+  L.attn_part = take(L.attn_part_bytes);
+  L.attn_ml = take(L.attn_ml_bytes);
+  L.attn_cnt = take(L.attn_cnt_bytes);  // zero between kernels (fused attention merges re-arm them)
   L.plans = take(sizeof(Plan));  // the one device plan slot every forward reads
   L.probe_p = take((size_t)kMaxRows * kMaxT * 4);
   L.tok_buf = take((size_t)kMaxRows * 4);
@@ -451,6 +467,8 @@ extern "C" laser_status laser_model_finalize(laser_model* m, int max_rows, void*
   }
   Layout L = make_layout(d, max_rows);
   if (!d_workspace || bytes < L.total) return laser_fail(LASER_ERR_INVALID_ARG, "workspace of %zu bytes needed", L.total);
+  if (L.attn_part_bytes >= (1ull << 31))  // read by buffer instructions with 32-bit offsets
+    return laser_fail(LASER_ERR_UNSUPPORTED, "attention partials of %zu bytes exceed 2 GiB", L.attn_part_bytes);
   hipStream_t s = (hipStream_t)stream;
   // RoPE table: angle pos * theta^(-2i/hd), computed in double precision
   const int half = d.head_dim / 2;
@@ -482,6 +500,7 @@ extern "C" laser_status laser_model_finalize(laser_model* m, int max_rows, void*
   m->cap_stream = cs;
   char* ws = (char*)d_workspace;
   HIP_TRY(hipMemcpyAsync(ws + L.rope, rope.data(), rope.size() * sizeof(float2), hipMemcpyHostToDevice, s));
+  HIP_TRY(hipMemsetAsync(ws + L.attn_cnt, 0, L.attn_cnt_bytes, s));
   HIP_TRY(hipStreamSynchronize(s));  // the host rope table goes out of scope
   m->ws = ws;
   m->lay = L;
@@ -852,6 +871,7 @@ static void plan_groups(const laser_model* m, const laser_kv* kv, Plan& p) {
     g.maxpos = maxpos;
     g.slot0 = 0;
     g.direct = 0;
+    g.fused = 0;
     for (int q = r0; q < r1; ++q) (prefix ? row_prefix : row_own)[q] = gi;
     return gi;
   };
@@ -884,12 +904,15 @@ static void plan_groups(const laser_model* m, const laser_kv* kv, Plan& p) {
     }
     return n;
   };
+  // one-row groups with no shared-prefix group can merge their own splits (fewer, longer ones)
+  auto fusable = [&](const GroupDesc& g) { return m->attn_fuse && g.nrows == 1 && row_prefix[g.row0] < 0; };
   for (;; base *= 2) {  // (more pages per wave only if the items would not fit)
     for (int i = 0; i < p.n_groups; ++i) {
       GroupDesc& g = p.groups[i];
       const bool shares = row_prefix[g.row0] >= 0;
       const bool is_prefix = row_prefix[g.row0] == i;
-      const int max_wg = is_prefix ? kAttnMaxWG - kOwnSlots : (shares ? kOwnSlots : kAttnMaxWG);
+      const int max_wg = fusable(g) ? m->attn_fuse_max
+                                    : is_prefix ? kAttnMaxWG - kOwnSlots : (shares ? kOwnSlots : kAttnMaxWG);
       const int npg = g.npages - g.pbeg;
       g.pps = std::max(base, ceil_div(npg, max_wg * kAttnWaves));
       g.nwg = ceil_div(npg, kAttnWaves * g.pps);
@@ -901,9 +924,13 @@ static void plan_groups(const laser_model* m, const laser_kv* kv, Plan& p) {
     const int pre = row_prefix[g.row0];
     if (pre >= 0 && pre != i) g.slot0 = p.groups[pre].nwg;
     g.direct = pre < 0 && g.nwg == 1;
+    g.fused = !g.direct && fusable(g);
   }
+  // (a fused row counts as written directly: the merge kernel skips it)
   for (int q = 0; q < p.M; ++q)
-    p.row_nslots[q] = p.groups[row_own[q]].nwg + (row_prefix[q] >= 0 ? p.groups[row_prefix[q]].nwg : 0);
+    p.row_nslots[q] = p.groups[row_own[q]].fused
+                          ? 1
+                          : p.groups[row_own[q]].nwg + (row_prefix[q] >= 0 ? p.groups[row_prefix[q]].nwg : 0);
 
   p.n_items = 0;
   auto push = [&](const GroupDesc* g, int wg, int tile) {
@@ -914,7 +941,7 @@ static void plan_groups(const laser_model* m, const laser_kv* kv, Plan& p) {
     }
     it.seq = g->seq;
     it.row0 = g->row0;
-    it.nrows = g->nrows;
+    it.nrows = g->nrows | (g->fused ? g->nwg << 8 | (int)(g - p.groups) << 16 : 0);
     it.p0 = g->pbeg + wg * kAttnWaves * g->pps;
     it.pend = g->npages;
     it.pps = g->pps;
@@ -941,13 +968,32 @@ static void pad_items(Plan& p, int n) {
   while (p.n_items < n) p.items[p.n_items++] = AttnItem{0, 0, 0, 0, 0, 0, 0, 0};
 }
 
-static laser_status launch_forward(laser_model* m, laser_kv* kv, const FwdKey& key, hipStream_t s);
+// Where a forward's scratch lives: attention partials (rows laid out for `rows` rows),
+// split statistics, fused-merge arrival counters, LM-head statistics, K-share partials.
+struct Scratch {
+  float *attn_part, *attn_ml, *kpart;
+  unsigned* attn_cnt;
+  LmPart* lm_part;
+  size_t part_bytes, ml_bytes;
+  int rows;
+};
+
+// The model workspace's scratch.
+static Scratch workspace_scratch(const laser_model* m) {
+  const Layout& L = m->lay;
+  return Scratch{m->wsp<float>(L.attn_part), m->wsp<float>(L.attn_ml), m->wsp<float>(L.kpart),
+                 m->wsp<unsigned>(L.attn_cnt), m->wsp<LmPart>(L.lm_part), L.attn_part_bytes, L.attn_ml_bytes,
+                 m->max_rows};
+}
+
+static laser_status launch_forward(laser_model* m, laser_kv* kv, const FwdKey& key, hipStream_t s, const Scratch& sc);
 
 // Runs one forward: plans the attention splits, uploads the plan, then launches the
 // forward's kernels (replaying a captured graph of them when graphs are on and no kernel
 // class is being timed).
 static laser_status run_forward(laser_model* m, laser_kv* kv, Plan& p, const PlanIO& io, hipStream_t s,
-                                bool allow_graph = true) {
+                                bool allow_graph = true, const Scratch* sc_in = nullptr) {
+  const Scratch sc = sc_in ? *sc_in : workspace_scratch(m);
   plan_groups(m, kv, p);
   p.io = io;
   FwdKey key{};
@@ -955,7 +1001,7 @@ static laser_status run_forward(laser_model* m, laser_kv* kv, Plan& p, const Pla
   key.n_out = p.n_out;
   int max_slots = 1;
   bool merge = false;
-  for (int i = 0; i < p.n_groups; ++i) merge |= !p.groups[i].direct;
+  for (int i = 0; i < p.n_groups; ++i) merge |= !p.groups[i].direct && !p.groups[i].fused;
   for (int q = 0; q < p.M; ++q) max_slots = std::max(max_slots, p.row_nslots[q]);
   // the merge's slot bound is rounded up so that a growing context keeps the same key for a
   // while (the merge reads the row's own count)
@@ -982,13 +1028,13 @@ static laser_status run_forward(laser_model* m, laser_kv* kv, Plan& p, const Pla
   if (st != LASER_OK) return st;
   if (!graphs) {
     TimingScope scope(m);
-    return launch_forward(m, kv, key, s);
+    return launch_forward(m, kv, key, s, sc);
   }
 
   if (!ge) {
     hipGraph_t graph = nullptr;
     HIP_TRY(hipStreamBeginCapture(m->cap_stream, hipStreamCaptureModeThreadLocal));
-    st = launch_forward(m, kv, key, m->cap_stream);
+    st = launch_forward(m, kv, key, m->cap_stream, sc);
     const hipError_t ec = hipStreamEndCapture(m->cap_stream, &graph);
     if (st != LASER_OK) {
       if (graph) (void)hipGraphDestroy(graph);
@@ -1022,7 +1068,7 @@ static laser_status run_forward(laser_model* m, laser_kv* kv, Plan& p, const Pla
 }
 
 // Launches the kernels of one forward whose plan is in the device plan slot.
-static laser_status launch_forward(laser_model* m, laser_kv* kv, const FwdKey& key, hipStream_t s) {
+static laser_status launch_forward(laser_model* m, laser_kv* kv, const FwdKey& key, hipStream_t s, const Scratch& sc) {
   const laser_model_desc& d = m->desc;
   const Layout& L = m->lay;
   const int hd = d.head_dim, G = d.n_q_heads / d.n_kv_heads;
@@ -1064,7 +1110,7 @@ static laser_status launch_forward(laser_model* m, laser_kv* kv, const FwdKey& k
     a.nr = ms.nr;
     a.ksplit = ms.ks;
     a.nrw = ms.nrw;
-    a.kpart = m->wsp<float>(L.kpart);
+    a.kpart = sc.kpart;
     a.M = M;
     if (M > kValuMaxRows && m->tiles_on) {
       a.wtile = tile;
@@ -1091,10 +1137,13 @@ static laser_status launch_forward(laser_model* m, laser_kv* kv, const FwdKey& k
   aa.hq = d.n_q_heads;
   aa.hkv = d.n_kv_heads;
   aa.G = G;
-  aa.max_rows = m->max_rows;
+  aa.max_rows = sc.rows;
   aa.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)hd));
-  aa.part = m->wsp<float>(L.attn_part);
-  aa.ml = m->wsp<float>(L.attn_ml);
+  aa.part = sc.attn_part;
+  aa.ml = sc.attn_ml;
+  aa.part_bytes = (uint32_t)sc.part_bytes;
+  aa.ml_bytes = (uint32_t)sc.ml_bytes;
+  aa.cnt = sc.attn_cnt;
   const dim3 agrid(key.agx, d.n_kv_heads);
 
   for (int li = 0; li < d.n_layers; ++li) {
@@ -1154,7 +1203,7 @@ static laser_status launch_forward(laser_model* m, laser_kv* kv, const FwdKey& k
     a.ldx = d.d_model;
     a.gain = m->final_norm;
     a.row_map = 1;
-    a.lm_part = m->wsp<LmPart>(L.lm_part);
+    a.lm_part = sc.lm_part;
     a.K = d.d_model;
     a.N = d.vocab;
     a.n_groups = groups_lm(d, key.n_out);
@@ -1595,6 +1644,15 @@ extern "C" laser_status laser_model_graph_stats(const laser_model* m, long long*
   if (!captures || !cached) return laser_fail(LASER_ERR_INVALID_ARG, "null output pointer");
   *captures = m->graph_captures;
   *cached = (int)m->graphs.size();
+  return LASER_OK;
+}
+
+extern "C" laser_status laser_model_set_attn_merge(laser_model* m, int fused, int max_splits) {
+  if (!model_of(m)) return laser_fail(LASER_ERR_STATE, "invalid or destroyed model");
+  if ((fused != 0 && fused != 1) || max_splits < 2 || max_splits > kAttnMaxWG)
+    return laser_fail(LASER_ERR_INVALID_ARG, "fused must be 0 or 1 and max_splits in [2, %d]", kAttnMaxWG);
+  m->attn_fuse = fused;
+  m->attn_fuse_max = max_splits;
   return LASER_OK;
 }
 

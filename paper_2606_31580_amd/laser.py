@@ -114,6 +114,7 @@ _SIGS = {
     "laser_timing_read": (_I, [_P, _I, C.POINTER(C.c_double), C.POINTER(_I)]),
     "laser_model_set_graphs": (_I, [_P, _I]),
     "laser_model_set_gemm_kernel": (_I, [_P, _I]),
+    "laser_model_set_attn_merge": (_I, [_P, _I, _I]),
     "laser_model_graph_stats": (_I, [_P, C.POINTER(C.c_longlong), C.POINTER(C.c_int)]),
     "laser_model_tile_bytes": (_I, [_P, C.POINTER(C.c_size_t)]),
     "laser_model_set_tiles": (_I, [_P, _P, C.c_size_t, _P]),
@@ -307,6 +308,10 @@ class Model:
         n, c = C.c_longlong(), C.c_int()
         _call("laser_model_graph_stats", self.h, C.byref(n), C.byref(c))
         return n.value, c.value
+
+    def set_attn_merge(self, fused: bool, max_splits: int = 56):
+        """One-row attention groups merged inside the attention kernel (fused) or by the merge kernel (default)."""
+        _call("laser_model_set_attn_merge", self.h, int(fused), int(max_splits))
 
     def set_gemm_kernel(self, mode: int):
         """Matrix-core projection kernel: 0 by cost (default), 1 K-split waves, 2 row waves."""

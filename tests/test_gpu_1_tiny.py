@@ -204,3 +204,40 @@ def test_tiny_determinism_and_errors():
         L.laser_decode_step(model, kv, [0], torch.zeros(1, dtype=torch.int32, device="cuda"),
                             torch.zeros(1, dtype=torch.int32, device="cuda"), torch.zeros(1, device="cuda"))
     assert e.value.code == L.ERR_OUT_OF_PAGES and kv.seq_len(0) == 32 and kv.page_table(0) == [0, 1]
+
+
+def test_tiny_batched_decode_fused_attention_merge():
+    # One-row attention groups merged by their last workgroup inside the attention kernel
+    # (laser_model_set_attn_merge), batch 4 at 15-700 positions (1 to several splits each).
+    require_gpu()
+    V = TINY.vocab
+    model, orc, _ = make_pair(TINY, max_rows=16, max_positions=1024)
+    model.set_attn_merge(True, 4)
+    kv, opool = kv_pair(model, TINY, num_pages=200, max_seqs=4, max_pages_per_seq=64)
+    lens = [15, 130, 433, 700]
+    states = []
+    for s, n in enumerate(lens):
+        K0, V0 = synth.make_prefill_kv(TINY, n, 80 + s)
+        kv.add_seq(s, n)
+        opool.add_seq(s, n)
+        kv.import_kv(s, K0.cuda(), V0.cuda())
+        states.append(SeqState.from_prefill(TINY, K0.numpy(), V0.numpy(), 1024))
+    toks = [int(t) for t in synth.make_tokens(len(lens), V, 3040)]
+    seqs = list(range(len(lens)))
+    B = len(seqs)
+    d_tok = torch.zeros(B, dtype=torch.int32, device="cuda")
+    d_next = torch.zeros(B, dtype=torch.int32, device="cuda")
+    d_p = torch.zeros(B, device="cuda")
+    d_logits = torch.zeros(B, V, device="cuda")
+    for step in range(3):
+        d_tok.copy_(torch.tensor(toks, dtype=torch.int32))
+        L.laser_decode_step(model, kv, seqs, d_tok, d_next, d_p, d_logits)
+        torch.cuda.synchronize()
+        for b in seqs:
+            opool.append(b, 1)
+            ref = orc.decode_token(states[b], toks[b])
+            compare_logits(d_logits[b].cpu().numpy(), ref, f"fused merge step {step} seq {b}")
+            check_token(d_next[b].item(), ref, f"fused merge step {step} seq {b}")
+            check_prob(d_p[b].item(), lm_stats(ref)[1], f"fused merge step {step} seq {b}")
+            toks[b] = lm_stats(ref)[0]
+            assert kv.page_table(b) == opool.tables[b]

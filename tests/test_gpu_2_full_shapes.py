@@ -141,6 +141,18 @@ def test_qwen1p5b_kv14336_state_injection():
     st.release()
 
 
+def test_qwen1p5b_kv14336_fused_attention_merge():
+    # The optional in-kernel split merge (laser_model_set_attn_merge): a decode row's attention
+    # over 896 pages of 2 KV heads in at most 56 splits, combined by the last workgroup of
+    # each (row, KV head); plain decode steps against the oracle.
+    st = Setup(QWEN_1P5B, [14336])
+    st.model.set_attn_merge(True, 56)
+    st.decode(2)
+    st.model.set_attn_merge(True, 8)  # longer splits, fewer partials
+    st.decode(1)
+    st.release()
+
+
 def test_qwen7b_b1_kv14336_state_injection():
     st = Setup(QWEN_7B, [14336])
     st.decode(1)
