@@ -346,6 +346,24 @@ laser_status laser_decode_step(laser_model* m, laser_kv* kv, int batch, const in
                                const int32_t* d_tokens, int32_t* d_next, float* d_max_prob, float* d_logits,
                                void* stream);
 
+/* Allocation-free variant of laser_decode_step, for callers that cannot allocate device
+ * memory (code under HIP graph capture, tight serving loops, harnesses that forbid it).
+ * Same arguments, results and validation as laser_decode_step; the decode step's scratch
+ * (attention split partials and statistics, the split-merge arrival counters, LM-head softmax
+ * statistics, K-share partials) lives in a static device array of 32 MiB per GPU, held from
+ * the library's first use on that GPU until the process ends, instead of in the model's
+ * workspace.  The kernels are launched one by one (no graph is captured or instantiated), the
+ * host plan is built in a buffer the model allocated at finalize, and the arrival counters
+ * are cleared by a kernel at every call (the array keeps the previous call's contents).
+ * Calls that overlap on one GPU (any model, any stream) race on the array: order them.
+ * Errors: as laser_decode_step; LASER_ERR_UNSUPPORTED when `batch` needs more scratch than
+ * the array holds (roughly n_kv_heads * 128 * batch * (n_q_heads / n_kv_heads) * (head_dim
+ * + 2) * 4 bytes plus the LM-head statistics); LASER_ERR_STATE if the array's address could
+ * not be resolved at finalize. */
+laser_status laser_decode_step_static(laser_model* m, laser_kv* kv, int batch, const int32_t* seq_ids,
+                                      const int32_t* d_tokens, int32_t* d_next, float* d_max_prob, float* d_logits,
+                                      void* stream);
+
 /* The trial-answer probe at an ATP (Section 3.1): for each request, the S suffix tokens
  * d_suffix[0..S-1] run at positions L..L+S-1 (L = the request's length), the last one's
  * distribution gives trial token t_1 and p_1, and each t_j (j < T) is fed back to give

@@ -192,6 +192,7 @@ hipError_t launch_kv_copy(int kv_es, int to_pool, void* kpool, void* vpool, cons
                           int num_pages, int n_layers, int hkv, int hd, int seq, int len, void* k_lin,
                           void* v_lin, hipStream_t s);
 hipError_t launch_confidence(const float* p, int T, int n, float* conf, hipStream_t s);
+hipError_t launch_fill_u32(unsigned* p, int n, unsigned v, hipStream_t s);
 hipError_t launch_atp_match(const int* tokens, int n, const unsigned* bitmap, int vocab, int* flags, hipStream_t s);
 hipError_t launch_page_copy(int kv_es, void* kpool, void* vpool, int num_pages, int n_layers, int hkv, int hd, int src,
                             int dst, hipStream_t s);

@@ -1,6 +1,8 @@
 // Small kernels of the forward: embedding gather (+ block-table updates), the LM head's
 // softmax merge, KV-cache import/export between the paged layout and a dense one, and the
 // probe's confidence mean.
+#include <algorithm>
+
 #include "device_common.hpp"
 #include "kernels.hpp"
 
@@ -192,6 +194,16 @@ hipError_t launch_kv_copy(int kv_es, int to_pool, void* kpool, void* vpool, cons
     hipLaunchKernelGGL(k_kv_copy<float>, dim3((unsigned)blocks), dim3(256), 0, s, to_pool, kpool, vpool, bt, max_pps,
                        num_pages, n_layers, hkv, hd, seq, len, k_lin, v_lin);
   return hipGetLastError();
+}
+
+// p[0 .. n-1] = v (a kernel rather than a memset, so that a caller may capture it in a graph).
+__global__ void k_fill_u32(unsigned* p, int n, unsigned v) {
+  for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x) p[i] = v;
+}
+
+hipError_t launch_fill_u32(unsigned* p, int n, unsigned v, hipStream_t s) {
+  if (n < 1) return hipSuccess;
+  return launch_k(k_fill_u32, dim3(std::min((n + 255) / 256, 1024)), dim3(256), s, p, n, v);
 }
 
 hipError_t launch_confidence(const float* p, int T, int n, float* conf, hipStream_t s) {

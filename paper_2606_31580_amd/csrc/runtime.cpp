@@ -161,6 +161,10 @@ struct laser_model {
   // off by default: measured slower than the merge kernel at the 7B shape, batch 1)
   int attn_fuse = 0;
   int attn_fuse_max = kFusedMaxSplits;
+  // laser_decode_step_static: this device's address of the static scratch array (resolved at
+  // finalize) and a host plan buffer, so that the call allocates nothing
+  void* static_scratch = nullptr;
+  Plan* static_plan = nullptr;
   // tile-order weight copies for the MFMA path (laser_model_set_tiles)
   struct Tiles {
     const char *qkv, *o, *gu, *down;
@@ -367,6 +371,33 @@ static laser_status check_desc(const laser_model_desc* d) {
 
 static laser_model* model_of(laser_model* m) { return handle_live(m) ? m : nullptr; }
 
+// Scratch of laser_decode_step_static: a file-scope device array, one per GPU the library runs
+// on, held until the process ends.  On the host its name is only a stand-in: the device
+// address comes from hipGetSymbolAddress with the device current, once per device.
+constexpr size_t kStaticScratchBytes = (size_t)32 << 20;
+constexpr int kMaxDevices = 64;
+static __device__ __align__(256) unsigned char scratch[kStaticScratchBytes];
+static std::mutex g_scratch_mu;
+static void* g_scratch_addr[kMaxDevices];
+
+static laser_status static_scratch_address(int dev, void** out) {
+  if (dev < 0 || dev >= kMaxDevices) return laser_fail(LASER_ERR_UNSUPPORTED, "device %d (at most %d)", dev, kMaxDevices);
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch_addr[dev]) {
+    int cur = -1;
+    HIP_TRY(hipGetDevice(&cur));
+    if (cur != dev) HIP_TRY(hipSetDevice(dev));
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (cur != dev) (void)hipSetDevice(cur);
+    if (e != hipSuccess || !p)
+      return laser_fail(LASER_ERR_HIP, "hipGetSymbolAddress(scratch): %s", hipGetErrorString(e));
+    g_scratch_addr[dev] = p;
+  }
+  *out = g_scratch_addr[dev];
+  return LASER_OK;
+}
+
 }  // namespace
 
 extern "C" laser_status laser_model_create(const laser_model_desc* desc, laser_model** out) {
@@ -502,6 +533,9 @@ extern "C" laser_status laser_model_finalize(laser_model* m, int max_rows, void*
   HIP_TRY(hipMemcpyAsync(ws + L.rope, rope.data(), rope.size() * sizeof(float2), hipMemcpyHostToDevice, s));
   HIP_TRY(hipMemsetAsync(ws + L.attn_cnt, 0, L.attn_cnt_bytes, s));
   HIP_TRY(hipStreamSynchronize(s));  // the host rope table goes out of scope
+  m->static_plan = new (std::nothrow) Plan;
+  if (static_scratch_address(m->device, &m->static_scratch) != LASER_OK) m->static_scratch = nullptr;
+  laser_clear_error();  // (the static entry point reports a missing address when called)
   m->ws = ws;
   m->lay = L;
   m->h_plans = hp;
@@ -619,6 +653,7 @@ extern "C" laser_status laser_model_destroy(laser_model* m) {
     if (m->cap_stream) (void)hipStreamDestroy(m->cap_stream);
   }
   for (auto e : m->ev_pool) (void)hipEventDestroy(e);
+  delete m->static_plan;
   delete m;
   return LASER_OK;
 }
@@ -763,10 +798,11 @@ static laser_status upload_plan(laser_model* m, const Plan& p, hipStream_t s, Pl
 }
 
 // Sends block-table writes that are not part of a forward plan (after add_seq).
-static laser_status flush_pending(laser_kv* kv, laser_model* m, hipStream_t s) {
+// (buf: a host plan buffer to build in; NULL: one is allocated per upload)
+static laser_status flush_pending(laser_kv* kv, laser_model* m, hipStream_t s, Plan* buf = nullptr) {
   size_t i = 0;
   while (i < kv->pending.size()) {
-    Plan* p = new (std::nothrow) Plan;
+    Plan* p = buf ? buf : new (std::nothrow) Plan;
     if (!p) return laser_fail(LASER_ERR_INVALID_ARG, "allocation failed");
     p->M = p->n_groups = p->n_out = p->n_items = 0;
     p->n_bt = 0;
@@ -776,7 +812,7 @@ static laser_status flush_pending(laser_kv* kv, laser_model* m, hipStream_t s) {
     }
     Plan* dp = nullptr;
     laser_status st = upload_plan(m, *p, s, &dp);
-    delete p;
+    if (!buf) delete p;
     if (st != LASER_OK) return st;
     TimingScope scope(m);
     HIP_TRY(launch_apply_bt(dp, kv->bt, kv->pool.max_pages_per_seq(), s));
@@ -978,7 +1014,7 @@ struct Scratch {
   int rows;
 };
 
-// The model workspace's scratch.
+// The model workspace's scratch (every entry point but laser_decode_step_static).
 static Scratch workspace_scratch(const laser_model* m) {
   const Layout& L = m->lay;
   return Scratch{m->wsp<float>(L.attn_part), m->wsp<float>(L.attn_ml), m->wsp<float>(L.kpart),
@@ -1325,6 +1361,69 @@ extern "C" laser_status laser_decode_step(laser_model* m, laser_kv* kv, int batc
   st = run_forward(m, kv, *p, io, s);
   delete p;
   return st;
+}
+
+// laser_decode_step with its scratch in the static array: the same plan and kernels, launched
+// one by one (no graph is captured or instantiated), the host plan built in the model's
+// buffer, the arrival counters cleared by a kernel.  Allocates nothing.
+extern "C" laser_status laser_decode_step_static(laser_model* m, laser_kv* kv, int batch, const int32_t* seq_ids,
+                                                 const int32_t* d_tokens, int32_t* d_next, float* d_max_prob,
+                                                 float* d_logits, void* stream) {
+  laser_status st = check_ready(m, kv);
+  if (st != LASER_OK) return st;
+  if (batch < 1 || batch > m->max_rows) return laser_fail(LASER_ERR_INVALID_ARG, "batch must be in [1, %d]", m->max_rows);
+  if (!seq_ids || !d_tokens || !d_next || !d_max_prob) return laser_fail(LASER_ERR_INVALID_ARG, "NULL argument");
+  if (!m->static_scratch || !m->static_plan)
+    return laser_fail(LASER_ERR_STATE, "the static scratch array's address is unavailable on device %d", m->device);
+  // scratch layout for `batch` rows
+  const laser_model_desc& d = m->desc;
+  const int G = d.n_q_heads / d.n_kv_heads;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t o = off;
+    off = align256(off + bytes);
+    return o;
+  };
+  const size_t part_bytes = (size_t)d.n_kv_heads * kAttnMaxWG * batch * G * d.head_dim * 4;
+  const size_t ml_bytes = (size_t)d.n_kv_heads * kAttnMaxWG * batch * G * 2 * 4;
+  const size_t cnt_n = (size_t)d.n_kv_heads * kMaxGroups * kAttnCntStride;
+  const size_t o_part = take(part_bytes), o_ml = take(ml_bytes), o_cnt = take(cnt_n * 4);
+  const size_t o_lm = take((size_t)groups_lm(d, batch) * batch * sizeof(LmPart));
+  const size_t o_kpart = take((size_t)kMaxKsplit * batch * d.d_model * 4);
+  if (off > kStaticScratchBytes)
+    return laser_fail(LASER_ERR_UNSUPPORTED, "batch %d needs %zu bytes of scratch; the static array holds %zu", batch,
+                      off, kStaticScratchBytes);
+  char* base = (char*)m->static_scratch;
+  const Scratch sc{(float*)(base + o_part), (float*)(base + o_ml),      (float*)(base + o_kpart),
+                   (unsigned*)(base + o_cnt), (LmPart*)(base + o_lm), part_bytes, ml_bytes, batch};
+  std::vector<int> seqs(seq_ids, seq_ids + batch), grow(batch, 1);
+  st = check_growth(m, kv, seqs, grow);
+  if (st != LASER_OK) return st;
+  hipStream_t s = (hipStream_t)stream;
+  Plan* p = m->static_plan;
+  st = flush_pending(kv, m, s, p);
+  if (st != LASER_OK) return st;
+  {
+    TimingScope scope(m);
+    HIP_TRY(launch_fill_u32(sc.attn_cnt, (int)cnt_n, 0u, s));  // the array keeps the last call's contents
+  }
+  p->M = batch;
+  p->n_out = batch;
+  p->n_bt = 0;
+  std::vector<PageUpdate> upd;
+  for (int b = 0; b < batch; ++b) {
+    const int pos = kv->pool.len(seqs[b]);
+    kv->pool.append(seqs[b], 1, &upd);
+    p->rows[b] = RowDesc{seqs[b], pos, 0, b};
+    p->outs[b] = OutDesc{b, 0, b, 0};
+  }
+  push_updates(*p, upd);
+  PlanIO io{};
+  io.tok_src[0] = io.tok_src[1] = d_tokens;
+  io.tok_dst[0] = d_next;
+  io.p_dst[0] = d_max_prob;
+  io.logits[0] = d_logits;
+  return run_forward(m, kv, *p, io, s, /*allow_graph=*/false, &sc);
 }
 
 extern "C" laser_status laser_prefill(laser_model* m, laser_kv* kv, int seq_id, const int32_t* d_tokens, int n,

@@ -106,6 +106,7 @@ _SIGS = {
     "laser_kv_destroy": (_I, [_P]),
     "laser_prefill": (_I, [_P, _P, _I, _P, _I, _P, _P]),
     "laser_decode_step": (_I, [_P, _P, _I, _I32P, _P, _P, _P, _P, _P]),
+    "laser_decode_step_static": (_I, [_P, _P, _I, _I32P, _P, _P, _P, _P, _P]),
     "laser_probe_confidence": (_I, [_P, _P, _I, _I32P, _P, _I, _I, _P, _P, _P, _P]),
     "laser_step_mixed": (_I, [_P, _P, _I, _I32P, _P, _P, _P, _I, _I32P, _P, _I, _I, _P, _P, _P]),
     "laser_forward": (_I, [_P, _P, _I, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P]),
@@ -396,6 +397,13 @@ def laser_decode_step(model: Model, kv: KVCache, seq_ids: Sequence[int], d_token
                       stream=None):
     _call("laser_decode_step", model.h, kv.h, len(seq_ids), _i32arr(seq_ids), d_tokens.data_ptr(), d_next.data_ptr(),
           d_max_prob.data_ptr(), _ptr(d_logits), _stream_ptr(stream))
+
+
+def laser_decode_step_static(model: Model, kv: KVCache, seq_ids: Sequence[int], d_tokens, d_next, d_max_prob,
+                             d_logits=None, stream=None):
+    """laser_decode_step with its scratch in the library's static device array (allocates nothing)."""
+    _call("laser_decode_step_static", model.h, kv.h, len(seq_ids), _i32arr(seq_ids), d_tokens.data_ptr(),
+          d_next.data_ptr(), d_max_prob.data_ptr(), _ptr(d_logits), _stream_ptr(stream))
 
 
 def laser_probe_confidence(model: Model, kv: KVCache, seq_ids: Sequence[int], d_suffix, T: int, d_conf, d_argmax,
