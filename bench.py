@@ -51,6 +51,9 @@ def parse():
                     help="one-row attention groups: merged by the attention kernel's last workgroup (fused) or "
                          "by the separate merge kernel")
     ap.add_argument("--attn-splits", type=int, default=56, help="split bound of a fused one-row attention group")
+    ap.add_argument("--design-probes", action="store_true",
+                    help="only run the design-probe program (streaming read, kernel boundary, cross-workgroup "
+                         "hand-off, grid barrier, dependent products) and print its report")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 256 MiB device-to-device copy three times (scale for HBM byte counters)")
     return ap.parse_args()
@@ -62,6 +65,14 @@ def main():
         print(f"bench.py measures one GPU: this build has no multi-GPU path (asked for --gpus {args.gpus})",
               file=sys.stderr)
         sys.exit(2)
+    if args.design_probes:  # a child process: nothing here has touched the GPU
+        import subprocess
+
+        exe = os.path.join(os.path.dirname(os.path.abspath(__file__)), "paper_2606_31580_amd", "lib", "design_probes")
+        if not os.path.exists(exe):
+            print(f"{exe} is missing: build with `python -m paper_2606_31580_amd.build`", file=sys.stderr)
+            sys.exit(2)
+        sys.exit(subprocess.run([exe]).returncode)
     import numpy as np
     import torch
 

@@ -1,7 +1,8 @@
 """Builds liblaser.so for gfx950 in-tree (paper_2606_31580_amd/lib/liblaser.so).
 
 Every call recompiles: the HIP sources with hipcc --offload-arch=gfx950 (packed fp32
-instructions disabled), the C controller with gcc, then links one shared library.
+instructions disabled), the C controller with gcc, then links one shared library; and the
+stand-alone design-probe program (lib/design_probes, run by bench.py --design-probes).
 Usage: python -m paper_2606_31580_amd.build
 """
 from __future__ import annotations
@@ -18,6 +19,9 @@ INCLUDE = os.path.join(ROOT, "include")
 OBJ = os.path.join(PKG, "_build")
 LIBDIR = os.path.join(PKG, "lib")
 LIB = os.path.join(LIBDIR, "liblaser.so")
+# measurement program behind the kernel structure (bench.py --design-probes); not part of the library
+PROBES_SRC = os.path.join(PKG, "probes", "design_probes.hip")
+PROBES = os.path.join(LIBDIR, "design_probes")
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
@@ -53,13 +57,20 @@ def build(verbose: bool = False) -> str:
     os.makedirs(LIBDIR, exist_ok=True)
     jobs = min(8, max(1, len(os.sched_getaffinity(0))))
     objs, failed = [], []
+    probe_cmd = [HIPCC, *HIP_FLAGS, "-o", PROBES + ".tmp", PROBES_SRC]
     with cf.ThreadPoolExecutor(jobs) as ex:
+        probe_job = ex.submit(_run, probe_cmd)
         for src, obj, rc, out, cmd in ex.map(_compile, HIP_SOURCES + C_SOURCES):
             if rc != 0:
                 failed.append((src, out, cmd))
             elif verbose and out.strip():
                 print(f"[{src}]\n{out}")
             objs.append(obj)
+        rc, out = probe_job.result()
+        if rc != 0:
+            failed.append(("probes/design_probes.hip", out, probe_cmd))
+        else:
+            os.replace(PROBES + ".tmp", PROBES)
     if failed:
         msg = "\n".join(f"--- {s} ---\n{' '.join(c)}\n{o}" for s, o, c in failed)
         raise RuntimeError("liblaser build failed:\n" + msg)
