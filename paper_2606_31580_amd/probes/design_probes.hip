@@ -62,23 +62,25 @@ __global__ __launch_bounds__(TPB) void k_stream(const u32x4* p, size_t n16, unsi
 
 static void stream_read() {
   printf("## 1. streaming read (non-temporal 16-byte loads, 2048 workgroups of 256 threads)\n");
-  const size_t maxb = (size_t)1 << 30;
+  printf("(each launch reads the next region of a 4 GiB buffer, so nothing is served from the\n"
+         " 256 MB memory-side cache of an earlier launch)\n");
+  const size_t pool = (size_t)4 << 30;
   u32x4* p;
   unsigned* sink;
-  CK(hipMalloc(&p, maxb));
+  CK(hipMalloc(&p, pool));
   CK(hipMalloc(&sink, 64));
-  CK(hipMemset(p, 1, maxb));
+  CK(hipMemset(p, 1, pool));
   hipEvent_t a, b;
   CK(hipEventCreate(&a));
   CK(hipEventCreate(&b));
   std::vector<double> xs, ys;
   for (size_t mb : {16, 32, 64, 128, 256, 512, 1024}) {
-    const size_t bytes = mb << 20, n16 = bytes / 16;
-    for (int i = 0; i < 3; ++i) k_stream<<<2048, TPB>>>(p, n16, sink);
+    const size_t bytes = mb << 20, n16 = bytes / 16, regions = pool / bytes;
+    for (int i = 0; i < 3; ++i) k_stream<<<2048, TPB>>>(p + (i % regions) * n16, n16, sink);
     CK(hipDeviceSynchronize());
     const int reps = 20;
     CK(hipEventRecord(a));
-    for (int i = 0; i < reps; ++i) k_stream<<<2048, TPB>>>(p, n16, sink);
+    for (int i = 0; i < reps; ++i) k_stream<<<2048, TPB>>>(p + ((3 + i) % regions) * n16, n16, sink);
     CK(hipEventRecord(b));
     CK(hipDeviceSynchronize());
     const double us = time_ms(a, b) * 1e3 / reps;
@@ -471,7 +473,7 @@ static void dependent_products() {
 int main() {
   hipDeviceProp_t prop;
   CK(hipGetDeviceProperties(&prop, 0));
-  printf("# design probes on %s (%s), %d compute units\n\n", prop.name, prop.gcnArchName, prop.multiProcessorCount);
+  printf("# design probes on %s, %d compute units\n\n", prop.gcnArchName, prop.multiProcessorCount);
   stream_read();
   graph_boundary();
   {
