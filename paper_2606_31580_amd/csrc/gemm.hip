@@ -341,11 +341,11 @@ __device__ __forceinline__ void unpack16(const u32x4& raw, float* out) {
 
 // ----------------------------------------------------------------------------- VALU GEMV
 
-template <class WT, int M, int EPI, int RW>
+// U: chunks of every row in flight per thread (one pass covers U x blockDim chunks).
+template <class WT, int M, int EPI, int RW, int U>
 __global__ __launch_bounds__(kGemvMaxThreads) void k_gemv(GemmArgs a) {
   constexpr int RWP = RW <= 4 ? 4 : (RW <= 8 ? 8 : 16);  // RW padded to a power of two
   constexpr int CH = 16 / (int)sizeof(WT);  // elements per 16-byte load
-  constexpr int U = 2;                      // chunks in flight per thread
   constexpr int NV = RW * M + M;            // per-wave totals: outputs, then sums of squares
   const int T = blockDim.x;                 // 256, or 512 for long rows
   const int nw = T >> 6;
@@ -1037,20 +1037,64 @@ static hipError_t launch_mfma_rw(int epi, dim3 grid, const GemmArgs& a, hipStrea
   }
 }
 
+// VALU GEMV variants built, by chunks in flight per thread: two for every row count and
+// weight type; one (short rows) and three (long residual rows, at most one workgroup per
+// compute unit) for bf16 weights and one or two rows, where the runtime picks them.
+template <class WT, int MODE, int EPI, int U>
+constexpr bool gemv_built() {
+  if (U == 2) return true;
+  if (!std::is_same<WT, bf16_t>::value || MODE > 2) return false;
+  return U == 1 || (U == 3 && EPI == EPI_RESID);
+}
+
+template <class WT, int MODE, int EPI, int RW>
+static hipError_t launch_gemv_u(int u, dim3 grid, dim3 block, const GemmArgs& a, hipStream_t s) {
+  switch (u) {
+#define LASER_GEMV_U(UU)                                                               \
+  case UU:                                                                             \
+    if constexpr (gemv_built<WT, MODE, EPI, UU>())                                     \
+      return launch_k(k_gemv<WT, MODE, EPI, RW, UU>, grid, block, s, a);               \
+    break;
+    LASER_GEMV_U(1)
+    LASER_GEMV_U(2)
+    LASER_GEMV_U(3)
+#undef LASER_GEMV_U
+  }
+  return hipErrorInvalidValue;
+}
+
 template <class WT, int MODE>
 static hipError_t launch_epi(int epi, int rw, const GemmArgs& a, hipStream_t s) {
   const dim3 grid(a.n_groups);
   dim3 block(kGemmThreads);
   if constexpr (MODE <= 4) {
-    // long rows (the down projection) use 8 waves so each thread streams fewer chunks
-    if (a.K / (16 / (int)sizeof(WT)) > 2048) block = dim3(kGemvMaxThreads);
-    if (epi == EPI_QKV && rw == 6) return launch_k(k_gemv<WT, MODE, EPI_QKV, 6>, grid, block, s, a);
-    if (epi == EPI_QKV && rw == 8) return launch_k(k_gemv<WT, MODE, EPI_QKV, 8>, grid, block, s, a);
-    if (epi == EPI_RESID && rw == 6) return launch_k(k_gemv<WT, MODE, EPI_RESID, 6>, grid, block, s, a);
-    if (epi == EPI_RESID && rw == 7) return launch_k(k_gemv<WT, MODE, EPI_RESID, 7>, grid, block, s, a);
-    if (epi == EPI_RESID && rw == 8) return launch_k(k_gemv<WT, MODE, EPI_RESID, 8>, grid, block, s, a);
-    if (epi == EPI_SWIGLU && rw == 8) return launch_k(k_gemv<WT, MODE, EPI_SWIGLU, 8>, grid, block, s, a);
-    if (epi == EPI_LMHEAD && rw == 8) return launch_k(k_gemv<WT, MODE, EPI_LMHEAD, 8>, grid, block, s, a);
+    // threads: a.gv_threads, else 256, or 512 for long rows (the down projection) so each
+    // thread streams fewer chunks; chunks in flight per thread: a.gv_u, else 2
+    if (a.gv_threads > 0) {
+      if (a.gv_threads % 64 != 0 || a.gv_threads > kGemvMaxThreads || a.gv_threads < 64 * ((rw * MODE + 63) / 64))
+        return hipErrorInvalidValue;
+      block = dim3(a.gv_threads);
+    } else if (a.K / (16 / (int)sizeof(WT)) > 2048) {
+      block = dim3(kGemvMaxThreads);
+    }
+    const int u = a.gv_u > 0 ? a.gv_u : 2;
+    switch (epi) {
+      case EPI_QKV:
+        if (rw == 6) return launch_gemv_u<WT, MODE, EPI_QKV, 6>(u, grid, block, a, s);
+        if (rw == 8) return launch_gemv_u<WT, MODE, EPI_QKV, 8>(u, grid, block, a, s);
+        break;
+      case EPI_RESID:
+        if (rw == 6) return launch_gemv_u<WT, MODE, EPI_RESID, 6>(u, grid, block, a, s);
+        if (rw == 7) return launch_gemv_u<WT, MODE, EPI_RESID, 7>(u, grid, block, a, s);
+        if (rw == 8) return launch_gemv_u<WT, MODE, EPI_RESID, 8>(u, grid, block, a, s);
+        break;
+      case EPI_SWIGLU:
+        if (rw == 8) return launch_gemv_u<WT, MODE, EPI_SWIGLU, 8>(u, grid, block, a, s);
+        break;
+      case EPI_LMHEAD:
+        if (rw == 8) return launch_gemv_u<WT, MODE, EPI_LMHEAD, 8>(u, grid, block, a, s);
+        break;
+    }
     return hipErrorInvalidValue;
   } else {
     constexpr int MT = MODE - 4;

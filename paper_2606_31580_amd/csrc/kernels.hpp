@@ -98,6 +98,7 @@ struct GemmArgs {
   int K, N, M, n_groups;
   int nr;   // MFMA path: row groups per workgroup (1, 2, or 4 at 2-3 activation tiles)
   int nrw;  // MFMA path: 0, or row groups per wave of the row-wave kernel (1, 2; 4 waves)
+  int gv_threads, gv_u;  // VALU path: threads per workgroup and chunks in flight per thread (0: defaults)
   // MFMA path: the weights in tile order (null: read the row-major tensors).  Group g, step s
   // (32 columns) is a block of 64 lanes x 16 bytes (x 2 for fp32) at (g * tsteps + s) blocks.
   const char* wtile;
