@@ -9,10 +9,13 @@
 //   5. two dependent weight-streaming products shaped like the 7B gate/up (271.6 MB) and down
 //      (135.8 MB) projections: two kernels, or one launch whose second-stage workgroups
 //      (dispatched after every first-stage one) load their first weights, wait for a
-//      completion counter (bounded spin) and read the first stage's output.
+//      completion counter (bounded spin) and read the first stage's output;
+//   6. memory-side cache: a region streamed right after another kernel read it (plain or
+//      non-temporal loads), against the same region cold (after a 1 GiB read of other data).
 // Every access is in bounds and every wait is bounded.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cstdio>
 #include <cstdlib>
 #include <vector>
@@ -470,6 +473,71 @@ static void dependent_products() {
   printf("\n");
 }
 
+// ---------------------------------------------------------------- 6. memory-side cache
+__global__ __launch_bounds__(TPB) void k_read_plain(const u32x4* p, size_t n16, unsigned* sink) {
+  unsigned acc = 0;
+  for (size_t i = (size_t)blockIdx.x * TPB + threadIdx.x; i < n16; i += (size_t)gridDim.x * TPB) {
+    const u32x4 v = p[i];
+    acc ^= v.x ^ v.y ^ v.z ^ v.w;
+  }
+  if (acc == 0x9e3779b9u) sink[0] = acc;
+}
+
+static void cache_reuse() {
+  printf("## 6. memory-side cache: one non-temporal read of a region, timed alone (event pair)\n");
+  printf("(cold: after a 1 GiB read of other data; warm: right after a plain or non-temporal read\n"
+         " of the same region; medians of 5 regions)\n");
+  const size_t pool = (size_t)4 << 30, flush_bytes = (size_t)1 << 30;
+  u32x4* p;
+  unsigned* sink;
+  CK(hipMalloc(&p, pool));
+  CK(hipMalloc(&sink, 64));
+  CK(hipMemset(p, 1, pool));
+  CK(hipDeviceSynchronize());
+  hipEvent_t a, b;
+  CK(hipEventCreate(&a));
+  CK(hipEventCreate(&b));
+  const u32x4* flush = p + (pool - flush_bytes) / 16;  // the last GiB; the regions lie below 2 GiB
+  auto flushc = [&]() {
+    k_stream<<<2048, TPB>>>(flush, flush_bytes / 16, sink);
+    CK(hipDeviceSynchronize());
+  };
+  auto timed = [&](const u32x4* q, size_t n16) {
+    CK(hipEventRecord(a));
+    k_stream<<<2048, TPB>>>(q, n16, sink);
+    CK(hipEventRecord(b));
+    CK(hipEventSynchronize(b));
+    return (double)time_ms(a, b) * 1e3;
+  };
+  auto med = [](std::vector<double> v) {
+    std::sort(v.begin(), v.end());
+    return v[v.size() / 2];
+  };
+  printf("  size |  cold            | after plain read | after nt read\n");
+  for (size_t mb : {8, 16, 32, 64, 128, 192}) {
+    const size_t bytes = mb << 20, n16 = bytes / 16;
+    std::vector<double> c, wp, wn;
+    for (int rep = 0; rep < 5; ++rep) {
+      const u32x4* r = p + (size_t)rep * ((size_t)256 << 20) / 16;
+      flushc();
+      c.push_back(timed(r, n16));
+      flushc();
+      k_read_plain<<<2048, TPB>>>(r, n16, sink);
+      CK(hipDeviceSynchronize());
+      wp.push_back(timed(r, n16));
+      flushc();
+      k_stream<<<2048, TPB>>>(r, n16, sink);
+      CK(hipDeviceSynchronize());
+      wn.push_back(timed(r, n16));
+    }
+    printf("%4zu MiB | %7.2f us %5.0f GB/s | %7.2f us %5.0f GB/s | %7.2f us %5.0f GB/s\n", mb, med(c), bytes / med(c) / 1e3,
+           med(wp), bytes / med(wp) / 1e3, med(wn), bytes / med(wn) / 1e3);
+  }
+  printf("\n");
+  CK(hipFree(p));
+  CK(hipFree(sink));
+}
+
 int main() {
   hipDeviceProp_t prop;
   CK(hipGetDeviceProperties(&prop, 0));
@@ -501,6 +569,7 @@ int main() {
     printf("\n");
   }
   dependent_products();
+  cache_reuse();
   printf("done\n");
   return 0;
 }
