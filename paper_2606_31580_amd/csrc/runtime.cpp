@@ -254,11 +254,11 @@ static int proj_rw(int epi, int rows, int M, int cus) {
 // most one workgroup per compute unit take three chunks per thread and cover the row in
 // one pass (1.5B down, K = 8960: 7.9 -> 6.95 us).  Everything else keeps the defaults:
 // 256 threads (512 for rows over 2,048 chunks) and two chunks, which measured best at the
-// 7B shape.
-static void gemv_shape(int epi, int K, int es, int n_groups, int cus, GemmArgs& a) {
+// 7B shape.  (The other shapes are built for one and two rows of bf16 weights.)
+static void gemv_shape(int epi, int K, int es, int M, int n_groups, int cus, GemmArgs& a) {
   a.gv_threads = 0;
   a.gv_u = 0;
-  if (es != 2) return;
+  if (es != 2 || M > 2) return;
   const int nch = K / 8;
   if (nch <= 256) {
     a.gv_threads = 64 * ceil_div(nch, 64);
@@ -1170,7 +1170,7 @@ static laser_status launch_forward(laser_model* m, laser_kv* kv, const FwdKey& k
     a.nrw = ms.nrw;
     a.kpart = sc.kpart;
     a.M = M;
-    if (M <= kValuMaxRows) gemv_shape(epi, K, (int)m->es, a.n_groups, m->cus, a);
+    if (M <= kValuMaxRows) gemv_shape(epi, K, (int)m->es, M, a.n_groups, m->cus, a);
     if (M > kValuMaxRows && m->tiles_on) {
       a.wtile = tile;
       a.tsteps = (K + 31) / 32;
@@ -1271,7 +1271,7 @@ static laser_status launch_forward(laser_model* m, laser_kv* kv, const FwdKey& k
     a.nrw = ms.nrw;
     a.ksplit = 1;
     a.M = key.n_out;
-    if (key.n_out <= kValuMaxRows) gemv_shape(EPI_LMHEAD, d.d_model, (int)m->es, a.n_groups, m->cus, a);
+    if (key.n_out <= kValuMaxRows) gemv_shape(EPI_LMHEAD, d.d_model, (int)m->es, key.n_out, a.n_groups, m->cus, a);
     if (key.n_out > kValuMaxRows && m->tiles_on) {
       a.wtile = m->lm_tile;
       a.tsteps = (d.d_model + 31) / 32;
