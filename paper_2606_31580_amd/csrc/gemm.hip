@@ -1039,12 +1039,14 @@ static hipError_t launch_mfma_rw(int epi, dim3 grid, const GemmArgs& a, hipStrea
 
 // VALU GEMV variants built, by chunks in flight per thread: two for every row count and
 // weight type; one (short rows) and three (long residual rows, at most one workgroup per
-// compute unit) for bf16 weights and one or two rows, where the runtime picks them.
-template <class WT, int MODE, int EPI, int U>
+// compute unit) for bf16 weights and one or two rows, where the runtime picks them.  Four-row
+// QKV groups exist only with one chunk per thread (short rows).
+template <class WT, int MODE, int EPI, int RW, int U>
 constexpr bool gemv_built() {
+  const bool valu_bf16 = std::is_same<WT, bf16_t>::value && MODE <= 2;
+  if (RW == 4) return valu_bf16 && U == 1;
   if (U == 2) return true;
-  if (!std::is_same<WT, bf16_t>::value || MODE > 2) return false;
-  return U == 1 || (U == 3 && EPI == EPI_RESID);
+  return valu_bf16 && (U == 1 || (U == 3 && EPI == EPI_RESID));
 }
 
 template <class WT, int MODE, int EPI, int RW>
@@ -1052,7 +1054,7 @@ static hipError_t launch_gemv_u(int u, dim3 grid, dim3 block, const GemmArgs& a,
   switch (u) {
 #define LASER_GEMV_U(UU)                                                               \
   case UU:                                                                             \
-    if constexpr (gemv_built<WT, MODE, EPI, UU>())                                     \
+    if constexpr (gemv_built<WT, MODE, EPI, RW, UU>())                                 \
       return launch_k(k_gemv<WT, MODE, EPI, RW, UU>, grid, block, s, a);               \
     break;
     LASER_GEMV_U(1)
@@ -1080,6 +1082,7 @@ static hipError_t launch_epi(int epi, int rw, const GemmArgs& a, hipStream_t s) 
     const int u = a.gv_u > 0 ? a.gv_u : 2;
     switch (epi) {
       case EPI_QKV:
+        if (rw == 4) return launch_gemv_u<WT, MODE, EPI_QKV, 4>(u, grid, block, a, s);
         if (rw == 6) return launch_gemv_u<WT, MODE, EPI_QKV, 6>(u, grid, block, a, s);
         if (rw == 8) return launch_gemv_u<WT, MODE, EPI_QKV, 8>(u, grid, block, a, s);
         break;
