@@ -56,3 +56,45 @@ def test_static_scratch_decode_matches_decode_step():
     for kv in kvs:
         kv.destroy()
     model.destroy()
+
+
+def test_static_scratch_size_limit():
+    """A batch whose scratch exceeds the static array is refused before anything changes; a
+    batch just under the limit runs and matches laser_decode_step.  (A 1-layer bf16 decoder
+    with 64 query / 8 KV heads of 128: 4 MiB of attention partials per row.)"""
+    require_gpu()
+    from paper_2606_31580_amd.configs import ModelShape
+
+    wide = ModelShape("wide-heads-1L", 1, 512, 64, 8, 128, 512, 1024, False, False, "bf16", 1.0e4, 1.0e-6)
+    V = wide.vocab
+    model, _, _ = make_pair(wide, max_rows=8, max_positions=256)
+    kvs = []
+    for _ in range(2):
+        kv = L.KVCache(model, 64, 8, 16, poison=True)
+        for s in range(8):
+            K0, V0 = synth.make_prefill_kv(wide, 20 + s, 90 + s, device="cuda")
+            kv.add_seq(s, 20 + s)
+            kv.import_kv(s, K0, V0)
+        kvs.append(kv)
+    toks = synth.make_tokens(8, V, 3050).cuda()
+    nxt = torch.zeros(8, dtype=torch.int32, device="cuda")
+    p = torch.zeros(8, device="cuda")
+    with pytest.raises(L.LaserError) as e:
+        L.laser_decode_step_static(model, kvs[1], list(range(8)), toks, nxt, p)
+    assert e.value.code == L.ERR_UNSUPPORTED
+    assert all(kvs[1].seq_len(s) == 20 + s for s in range(8))
+    seqs = list(range(7))  # 28 MiB of partials: within the array
+    outs = []
+    for kv, fn in ((kvs[0], L.laser_decode_step), (kvs[1], L.laser_decode_step_static)):
+        n7 = torch.zeros(7, dtype=torch.int32, device="cuda")
+        p7 = torch.zeros(7, device="cuda")
+        lg = torch.zeros(7, V, device="cuda")
+        fn(model, kv, seqs, toks[:7], n7, p7, lg)
+        torch.cuda.synchronize()
+        outs.append((n7.cpu().numpy(), p7.cpu().numpy(), lg.cpu().numpy()))
+    (t0, p0, l0), (t1, p1, l1) = outs
+    assert np.array_equal(t0, t1)
+    assert float(np.max(np.abs(l0 - l1))) <= LOGIT_TOL and float(np.max(np.abs(p0 - p1))) <= PROB_TOL
+    for kv in kvs:
+        kv.destroy()
+    model.destroy()
