@@ -228,3 +228,15 @@ def test_model_validation_without_device(lib):
     assert lib.laser_model_finalize(h, 8, None, 0, None) in (L.ERR_STATE, L.ERR_INVALID_ARG)
     assert lib.laser_model_destroy(h) == L.OK
     assert lib.laser_model_destroy(h) == L.ERR_STATE
+
+
+def test_bench_refuses_several_gpus():
+    # one GPU only: the benchmark exits with a message before anything touches a device
+    import subprocess
+    import sys
+
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    r = subprocess.run([sys.executable, os.path.join(root, "bench.py"), "--gpus", "2"], capture_output=True, text=True,
+                       timeout=120)
+    assert r.returncode == 2
+    assert "one GPU" in r.stderr and r.stdout == ""
