@@ -390,6 +390,21 @@ def main():
     step_gbs = step_bytes / (dec_ms / 1e3) / 1e9
     gu_bytes = 2 * shape.d_ffn * shape.d_model * es + B * shape.d_model * 4 + B * shape.d_ffn * 4
     gu_gbs = gu_bytes / (gu_avg_ms / 1e3) / 1e9
+    # every class of the kernel-timing pass against the same peak: its algorithmic bytes per
+    # launch (the weights once; for attention the K and V of the context in one layer) over its
+    # average launch time
+    d, hd, F = shape.d_model, shape.head_dim, shape.d_ffn
+    cls_bytes = {
+        "qkv": (shape.n_q_heads + 2 * shape.n_kv_heads) * hd * d * es,
+        "attn+merge": sum(ctx) * kv_tok // shape.n_layers,
+        "o_proj": d * shape.n_q_heads * hd * es,
+        "gate_up": 2 * F * d * es,
+        "down": d * F * es,
+        "lm_head+reduce": shape.vocab * d * es,
+    }
+    class_hbm = {n: {"bytes_per_launch": b,
+                     "frac_of_peak": round(b / (kernel_us[n]["avg_us"] * 1e-6) / 1e9 / HBM_PEAK_GBS, 4)}
+                 for n, b in cls_bytes.items() if kernel_us[n]["avg_us"] > 0}
 
     traffic = None
     tf = os.path.join(os.path.dirname(os.path.abspath(__file__)), "profiles", "gateup_traffic.json")
@@ -465,6 +480,7 @@ def main():
                      "frac": round(gu_gbs / HBM_PEAK_GBS, 4), "traffic": traffic,
                      "avg_launch_us": round(gu_avg_ms * 1e3, 2), "launches": gu_n, "bytes_per_launch": gu_bytes},
         "kernel_us_per_launch": kernel_us,
+        "kernel_hbm_frac": class_hbm,
         "sim_costs": sim_costs,
     }
     if not args.no_cpu_baseline:
