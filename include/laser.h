@@ -474,9 +474,11 @@ laser_status laser_model_graph_stats(const laser_model* m, long long* captures, 
  * workgroup), the other gives each of 4 waves its own row groups and stages the
  * activations once per workgroup in LDS.  mode 0 (the default) takes the second for the
  * gate/up projection of forwards of 33 to 64 rows when it has enough row groups and for
- * the O and down projections of forwards of 49 to 64 rows, and the first elsewhere; 1
- * uses only the first kernel; 2 the second wherever it applies (K a multiple of 8).  The
- * summation order differs between them, so
+ * the O and down projections of forwards of 49 to 64 rows, and the first elsewhere; it
+ * also computes the QKV projection of bf16 models in forwards of 33 to 64 rows over
+ * 512-column slices of K (each slice's activations staged once in LDS for 16 row groups,
+ * the slices summed by a second kernel).  1 uses only the first kernel; 2 the second
+ * wherever it applies (K a multiple of 8).  The summation order differs between them, so
  * results may differ in the last bits.  Captured forwards are released when the mode
  * changes.  Errors: LASER_ERR_STATE (bad model), LASER_ERR_INVALID_ARG (mode). */
 laser_status laser_model_set_gemm_kernel(laser_model* m, int mode);

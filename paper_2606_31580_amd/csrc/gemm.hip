@@ -974,6 +974,242 @@ hipError_t launch_ksplit_reduce(const GemmArgs& a, hipStream_t s) {
   return launch_k(k_ksplit_reduce, dim3((n + 255) / 256), dim3(256), s, a.h, (const float*)a.kpart, a.ksplit, n);
 }
 
+// ----------------------------------------------------------------------------- QKV over K slices
+
+// QKV of wide forwards (3-4 activation tiles: batched decode with riding probe rows).  In the
+// K-split kernel every workgroup reads the fp32 activation rows over its K range for its one or
+// two row groups: at 52 rows of the 8B shape that is three times the weight bytes.  Here a
+// workgroup takes one slice of K (SS 32-column steps), stages the slice of every activation row
+// once in LDS (times the norm gain, split into bf16 hi/lo in A-operand order), and its NW waves
+// run gb = NW GPW row groups over it (wave w: groups w, w + NW, ...).  Every wave issues its
+// share of the activation loads, then all of its groups' weight loads, before it waits for
+// anything.  (Measured at 56 rows of the 8B shape: the activations that miss in L2 still arrive
+// behind much of the chip's weight traffic, 5-10 us after the start, but waiting for them
+// before requesting the weights is slower: 22.5 against 19.5 us.)  Each A fragment is read from
+// LDS once per wave for all of its groups.  Each slice's partial sums and each row's sum of
+// squares over the slice go to qpart / sqpart; k_qkv_slices_epi adds the slices in order,
+// applies the norm scale, then bias, rotation and the stores of the QKV epilogue.  Weights: the tile-order copy when there is one, else the
+// row-major tensors (the same products in the same order).  Partial sums: qpart[slice][m][16 g +
+// n], the group order of the QKV tiles (group g holds rotary pairs 8g .. 8g+7, low dims in rows
+// 0-7, high dims in rows 8-15).
+template <int MT, int SS, int GPW, int NW>
+__global__ __launch_bounds__(64 * NW) void k_qkv_slices(GemmArgs a, float* qpart, float* sqpart, int gb) {
+  constexpr int NU = MT * SS;              // (tile, step) units of the staged slice
+  constexpr int UPW = (NU + NW - 1) / NW;  // units per wave
+  __shared__ __align__(16) u32x4 s_a[MT][SS][2][64];  // [tile][step][hi, lo][lane]
+  __shared__ float s_sq[NU][16];                       // per unit: the 16 rows' sums of squares over its 32 columns
+  const int tid = threadIdx.x, w = tid >> 6, l = tid & 63;
+  const int slice = blockIdx.x, g0 = blockIdx.y * gb;
+  const int gend = min(g0 + gb, a.n_groups);
+  const int M = a.M, K = a.K, N = a.N;
+  const int k0 = slice * SS * 32;
+  const int nst = a.tsteps;  // 32-column steps of the tile-order weights
+  // Activation loads first, all in flight together: unit u = w + NW i is tile u / SS, step
+  // u % SS; lane l holds row 16 t + l % 16, 8 columns at 32 st + 8 (l / 16).  Units past NU
+  // read unit NU - 1 again (not used).  Loads through global pointers, so that the compiler
+  // need not keep them behind the LDS stores.
+  u32x4 xa[UPW], xb[UPW], gv[UPW];
+#pragma unroll
+  for (int i = 0; i < UPW; ++i) {
+    const int u = min(w + NW * i, NU - 1), t = u / SS, st = u - t * SS;
+    const int row = 16 * t + (l & 15), k = k0 + 32 * st + 8 * (l >> 4);
+    const bool in = row < M && k < K;  // K is a multiple of 8
+    const size_t off = in ? (size_t)row * a.ldx + k : 0;
+    xa[i] = ld_global<u32x4>(a.x + off);
+    xb[i] = ld_global<u32x4>(a.x + off + 4);
+    gv[i] = ld_global<u32x4>((const char*)a.gain + (in ? (size_t)k * 2 : 0));
+  }
+  // Then group j of this wave (g0 + w + j NW) over the slice, from the tile-order copy (steps
+  // past K read the last step) or the row-major tensors (lane l % 16's row; columns past K read
+  // column 0): the A operand there is zero.  Past the workgroup's groups the last one is read
+  // again (not used).
+  u32x4 wv[GPW][SS];
+#pragma unroll
+  for (int j = 0; j < GPW; ++j) {
+    const int g = min(g0 + w + j * NW, gend - 1);
+    if (a.wtile) {
+#pragma unroll
+      for (int st = 0; st < SS; ++st)
+        wv[j][st] = ld_nt16(a.wtile + ((size_t)g * nst + min(slice * SS + st, nst - 1)) * 1024 + 16 * l);
+    } else {
+      const char* rp = weight_row<bf16_t, EPI_QKV, 16>(a, g, l & 15);
+#pragma unroll
+      for (int st = 0; st < SS; ++st) {
+        const int k = k0 + 32 * st + 8 * (l >> 4);
+        wv[j][st] = ld_nt16(rp + (size_t)(k < K ? k : 0) * 2);
+      }
+    }
+  }
+  // staged units: A = x times the gain, split into bf16 hi / lo; rows past M and columns past K zero
+#pragma unroll
+  for (int i = 0; i < UPW; ++i) {
+    const int u = w + NW * i;
+    if (u >= NU) break;
+    const int t = u / SS, st = u - t * SS;
+    const int row = 16 * t + (l & 15), k = k0 + 32 * st + 8 * (l >> 4);
+    const bool in = row < M && k < K;
+    float gf[8];
+    unpack16<bf16_t>(gv[i], gf);
+    float xe[8];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      xe[e] = __uint_as_float(xa[i][e]);
+      xe[4 + e] = __uint_as_float(xb[i][e]);
+    }
+    float sq = 0.f;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      xe[e] = in ? xe[e] : 0.f;
+      sq = fmaf(xe[e], xe[e], sq);
+      xe[e] *= gf[e];
+    }
+    u32x4 ph, pl;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      uint32_t h, lo;
+      split_trunc2(xe[2 * q], xe[2 * q + 1], h, lo);
+      ph[q] = h;
+      pl[q] = lo;
+    }
+    s_a[t][st][0][l] = ph;
+    s_a[t][st][1][l] = pl;
+    sq = sum_x16(sq);  // lanes l, l+16, l+32, l+48 hold the same row
+    sq = sum_x32(sq);
+    if (l < 16) s_sq[u][l] = sq;
+  }
+  __syncthreads();
+  if (tid < M) {  // the row's sum of squares over the slice, its steps in order
+    const int t = tid >> 4;
+    float sq = 0.f;
+#pragma unroll
+    for (int st = 0; st < SS; ++st) sq += s_sq[t * SS + st][tid & 15];
+    sqpart[(size_t)slice * M + tid] = sq;
+  }
+  // each A fragment read from LDS once per wave, for all of the wave's groups;
+  // acc[j][mt][i] = Y[m = 16 mt + 4 (l / 16) + i][16 g_j + l % 16]
+  f32x4 acc[GPW][MT];
+#pragma unroll
+  for (int j = 0; j < GPW; ++j)
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) acc[j][mt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int st = 0; st < SS; ++st)
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) {
+      const bf16x8 ahi = __builtin_bit_cast(bf16x8, s_a[mt][st][0][l]);
+      const bf16x8 alo = __builtin_bit_cast(bf16x8, s_a[mt][st][1][l]);
+#pragma unroll
+      for (int j = 0; j < GPW; ++j) {
+        const bf16x8 b = __builtin_bit_cast(bf16x8, wv[j][st]);
+        acc[j][mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ahi, b, acc[j][mt], 0, 0, 0);
+        acc[j][mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(alo, b, acc[j][mt], 0, 0, 0);
+      }
+    }
+#pragma unroll
+  for (int j = 0; j < GPW; ++j) {
+    const int g = g0 + w + j * NW;
+    if (g >= gend) break;
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int m = 16 * mt + 4 * (l >> 4) + i;
+        if (m < M) qpart[((size_t)slice * M + m) * N + 16 * g + (l & 15)] = acc[j][mt][i];
+      }
+  }
+}
+
+// One thread per (row, 4 consecutive rotary pairs of a group): the slices summed in order, the
+// norm scale, then the QKV epilogue of each pair (bias, rotation of q and k, q stored, K/V
+// appended to the row's page).
+template <class WT>
+__global__ __launch_bounds__(256) void k_qkv_slices_epi(GemmArgs a, const float* qpart, const float* sqpart,
+                                                         int nslices) {
+  const int nq = a.N / 8;  // quads of pairs per row (two per group)
+  const int idx = blockIdx.x * 256 + threadIdx.x;
+  if (idx >= a.M * nq) return;
+  const int m = idx / nq, qd = idx - m * nq;
+  const int g = qd >> 1, j0 = 4 * (qd & 1);
+  // the row's descriptor, then what it addresses (rotations of the 4 pairs, the KV page) in
+  // flight with the partial sums
+  const RowDesc rd = a.plan->rows[m];
+  const int i0 = qkv_pair(a, 8 * g + j0).i;  // the 4 pairs are consecutive pairs of one head
+  float2 cs[4];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) cs[e] = a.rope[(size_t)rd.pos * (a.hd >> 1) + i0 + e];
+  const int page = a.bt[(size_t)rd.seq * a.max_pps + (rd.pos >> 4)];
+  float4 slo = {0.f, 0.f, 0.f, 0.f}, shi = {0.f, 0.f, 0.f, 0.f};
+  float sq = 0.f;
+#pragma unroll 8
+  for (int s2 = 0; s2 < nslices; ++s2) {
+    const float* pr = qpart + ((size_t)s2 * a.M + m) * a.N + 16 * g + j0;
+    const float4 lo = *(const float4*)pr, hi = *(const float4*)(pr + 8);
+    slo.x += lo.x;
+    slo.y += lo.y;
+    slo.z += lo.z;
+    slo.w += lo.w;
+    shi.x += hi.x;
+    shi.y += hi.y;
+    shi.z += hi.z;
+    shi.w += hi.w;
+    sq += sqpart[(size_t)s2 * a.M + m];
+  }
+  const float scale = rsqrtf(sq / (float)a.K + a.eps);
+  const float vlo[4] = {slo.x, slo.y, slo.z, slo.w}, vhi[4] = {shi.x, shi.y, shi.z, shi.w};
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const QkvPair q = qkv_pair(a, 8 * g + j0 + e);
+    const int dlo = q.i, dhi = (a.hd >> 1) + q.i;
+    float ylo = vlo[e] * scale, yhi = vhi[e] * scale;
+    if (a.b0 != nullptr) {  // the three biases are set together
+      const size_t e0 = (size_t)q.hh * a.hd + q.i, e1 = e0 + (a.hd >> 1);
+      ylo += bf2f(ld_global<uint16_t>((const char*)q.bias + 2 * e0));
+      yhi += bf2f(ld_global<uint16_t>((const char*)q.bias + 2 * e1));
+    }
+    if (q.isq || q.isk) {
+      const float rlo = ylo * cs[e].x - yhi * cs[e].y;
+      const float rhi = yhi * cs[e].x + ylo * cs[e].y;
+      ylo = rlo;
+      yhi = rhi;
+    }
+    if (q.isq) {
+      float* qo = a.q_out + ((size_t)m * a.hq + q.hh) * a.hd;
+      qo[dlo] = ylo;
+      qo[dhi] = yhi;
+    } else {
+      const int t = rd.pos & 15;
+      const size_t blk = (((size_t)a.layer * a.num_pages + page) * a.hkv + q.hh) * (size_t)(16 * a.hd);
+      void* pool = q.isk ? a.kpool : a.vpool;
+      const size_t olo = blk + (q.isk ? k_block_off(t, dlo) : v_block_off(t, dlo));
+      const size_t ohi = blk + (q.isk ? k_block_off(t, dhi) : v_block_off(t, dhi));
+      if (a.kv_fp8) {
+        stw<fp8_t>(pool, olo, ylo);
+        stw<fp8_t>(pool, ohi, yhi);
+      } else {
+        stw<WT>(pool, olo, ylo);
+        stw<WT>(pool, ohi, yhi);
+      }
+    }
+  }
+}
+
+hipError_t launch_qkv_slices(const GemmArgs& a, float* qpart, float* sqpart, hipStream_t s) {
+  constexpr int SS = kQSliceSteps, GPW = 2, NW = kQSliceGroups / GPW;
+  const int mt = (a.M + 15) / 16;
+  if (a.gain == nullptr || a.row_map || a.N % 16 != 0 || a.n_groups * 16 != a.N || a.K % 8 != 0 ||
+      a.tsteps != (a.K + 31) / 32 || mt < 3 || mt > 4)
+    return hipErrorInvalidValue;
+  const int nslices = (a.K + SS * 32 - 1) / (SS * 32);
+  const dim3 grid(nslices, (a.n_groups + kQSliceGroups - 1) / kQSliceGroups), block(64 * NW);
+  const hipError_t e =
+      mt == 3 ? launch_k(k_qkv_slices<3, SS, GPW, NW>, grid, block, s, a, qpart, sqpart, (int)kQSliceGroups)
+              : launch_k(k_qkv_slices<4, SS, GPW, NW>, grid, block, s, a, qpart, sqpart, (int)kQSliceGroups);
+  if (e != hipSuccess) return e;
+  const int n = a.M * (a.N / 8);
+  return launch_k(k_qkv_slices_epi<bf16_t>, dim3((n + 255) / 256), dim3(256), s, a, (const float*)qpart,
+                  (const float*)sqpart, nslices);
+}
+
 // ----------------------------------------------------------------------------- weight tiles
 
 // One block (group g, step s) per workgroup of 64 lanes: lane (n = l % 16, q = l / 16) gets

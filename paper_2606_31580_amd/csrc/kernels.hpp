@@ -178,6 +178,12 @@ inline hipError_t launch_k(K kernel, dim3 grid, dim3 block, hipStream_t s, Args.
 // rw: rows per workgroup (VALU: QKV 6 or 8, residual 6, 7 or 8, others 8; MFMA: 16).
 hipError_t launch_gemm(int dtype, int mode, int epi, int rw, const GemmArgs& a, hipStream_t s);
 hipError_t launch_ksplit_reduce(const GemmArgs& a, hipStream_t s);
+// QKV of a wide forward (bf16 weights; a.M of 33 to 64 rows) over K slices of kQSliceSteps
+// 32-column steps, kQSliceGroups row groups per workgroup: partial sums per slice in qpart
+// [ceil(K / (32 kQSliceSteps))][M][N], the rows' sums of squares per slice in sqpart [slices][M],
+// then the summing / norm / epilogue kernel.
+constexpr int kQSliceSteps = 16, kQSliceGroups = 16;
+hipError_t launch_qkv_slices(const GemmArgs& a, float* qpart, float* sqpart, hipStream_t s);
 // Writes the tile-order copy of one projection's weights (the MFMA path's 16-row groups of
 // `a`, as weight_row maps them) to dst: a.n_groups groups x ceil(K/32) steps.
 hipError_t launch_tile_weights(int dtype, int epi, const GemmArgs& a, char* dst, hipStream_t s);

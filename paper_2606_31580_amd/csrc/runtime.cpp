@@ -89,7 +89,8 @@ constexpr int kMaxPagesPerWave = LASER_ATTN_MAX_PPS;
 constexpr int kFusedMaxSplits = LASER_ATTN_FUSED_SPLITS;
 
 struct Layout {
-  size_t rope, h, q, o, act, kpart, lm_part, attn_part, attn_ml, attn_cnt, plans, probe_p, tok_buf, p_buf, total;
+  size_t rope, h, q, o, act, kpart, qpart, sqpart, lm_part, attn_part, attn_ml, attn_cnt, plans, probe_p, tok_buf, p_buf,
+      total;
   size_t attn_part_bytes, attn_ml_bytes, attn_cnt_bytes;
 };
 
@@ -350,6 +351,18 @@ static MfmaShape mfma_shape(int epi, int n_groups, int M, int K, int es, int cus
   return best;
 }
 
+// QKV over K slices (launch_qkv_slices): forwards of kQSliceMinRows to 64 rows, bf16 weights
+// (tile order when the copy is there).  Each workgroup stages a 512-column slice of K of every
+// activation row in LDS and runs 16 row groups over it.  Measured against the K-split kernel,
+// which reads all of K of every activation row for each of its one or two row groups: QKV of
+// the 8B shape at 56 rows 39.3 us against 19.5 + 6.0 us (slices, then their sum and the
+// epilogue), at 40 rows 34.0 against 17.1 + 6.0; the 7B shape at 40 rows 30.8 against 14.4 + 6.7.
+// Other slice shapes (256 columns; 12 groups per workgroup over 6 waves) measured slower.
+constexpr int kQSliceMinRows = 33;
+static bool qkv_slices_fit(const laser_model_desc& d, int max_rows) {
+  return d.dtype == LASER_DTYPE_BF16 && max_rows >= kQSliceMinRows && d.d_model % 8 == 0 && d.head_dim % 16 == 0;
+}
+
 static Layout make_layout(const laser_model_desc& d, int max_rows) {
   Layout L{};
   const int hd = d.head_dim, G = d.n_q_heads / d.n_kv_heads;
@@ -365,6 +378,11 @@ static Layout make_layout(const laser_model_desc& d, int max_rows) {
   L.o = take((size_t)max_rows * d.n_q_heads * hd * 4);
   L.act = take((size_t)max_rows * d.d_ffn * 4);
   L.kpart = take((size_t)kMaxKsplit * max_rows * d.d_model * 4);  // K-share partials of O-proj / down
+  if (qkv_slices_fit(d, max_rows)) {  // K-slice partials of the QKV projection of wide forwards
+    const size_t nsl = ceil_div(d.d_model, kQSliceSteps * 32);
+    L.qpart = take(nsl * max_rows * (size_t)(d.n_q_heads + 2 * d.n_kv_heads) * hd * 4);
+    L.sqpart = take(nsl * max_rows * 4);
+  }
   L.lm_part = take((size_t)groups_lm(d, 1) * kMaxRows * sizeof(LmPart));  // the VALU path has the most groups
   L.attn_part_bytes = (size_t)d.n_kv_heads * kAttnMaxWG * max_rows * G * hd * 4;
   L.attn_ml_bytes = (size_t)d.n_kv_heads * kAttnMaxWG * max_rows * G * 2 * 4;
@@ -1039,6 +1057,7 @@ static void pad_items(Plan& p, int n) {
 // split statistics, fused-merge arrival counters, LM-head statistics, K-share partials.
 struct Scratch {
   float *attn_part, *attn_ml, *kpart;
+  float *qpart, *sqpart;  // QKV K-slice partials (null: that kernel is not used)
   unsigned* attn_cnt;
   LmPart* lm_part;
   size_t part_bytes, ml_bytes;
@@ -1048,7 +1067,11 @@ struct Scratch {
 // The model workspace's scratch (every entry point but laser_decode_step_static).
 static Scratch workspace_scratch(const laser_model* m) {
   const Layout& L = m->lay;
-  return Scratch{m->wsp<float>(L.attn_part), m->wsp<float>(L.attn_ml), m->wsp<float>(L.kpart),
+  return Scratch{m->wsp<float>(L.attn_part),
+                 m->wsp<float>(L.attn_ml),
+                 m->wsp<float>(L.kpart),
+                 L.qpart ? m->wsp<float>(L.qpart) : nullptr,
+                 L.sqpart ? m->wsp<float>(L.sqpart) : nullptr,
                  m->wsp<unsigned>(L.attn_cnt), m->wsp<LmPart>(L.lm_part), L.attn_part_bytes, L.attn_ml_bytes,
                  m->max_rows};
 }
@@ -1184,6 +1207,12 @@ static laser_status launch_forward(laser_model* m, laser_kv* kv, const FwdKey& k
     if (M > kValuMaxRows && m->tiles_on) {
       a.wtile = tile;
       a.tsteps = (K + 31) / 32;
+    }
+    if (epi == EPI_QKV && M >= kQSliceMinRows && M <= 64 && dt == 1 && sc.qpart != nullptr && m->gemm_kernel == 0 &&
+        a.n_groups * 16 == N) {
+      a.tsteps = (K + 31) / 32;
+      HIP_TRY(timed(m, cls, s, [&] { return launch_qkv_slices(a, sc.qpart, sc.sqpart, s); }));
+      return LASER_OK;
     }
     const int mode = gemm_mode(M);
     HIP_TRY(timed(m, cls, s, [&] {
@@ -1428,7 +1457,7 @@ extern "C" laser_status laser_decode_step_static(laser_model* m, laser_kv* kv, i
     return laser_fail(LASER_ERR_UNSUPPORTED, "batch %d needs %zu bytes of scratch; the static array holds %zu", batch,
                       off, kStaticScratchBytes);
   char* base = (char*)m->static_scratch;
-  const Scratch sc{(float*)(base + o_part), (float*)(base + o_ml),      (float*)(base + o_kpart),
+  const Scratch sc{(float*)(base + o_part), (float*)(base + o_ml), (float*)(base + o_kpart), nullptr, nullptr,
                    (unsigned*)(base + o_cnt), (LmPart*)(base + o_lm), part_bytes, ml_bytes, batch};
   std::vector<int> seqs(seq_ids, seq_ids + batch), grow(batch, 1);
   st = check_growth(m, kv, seqs, grow);
