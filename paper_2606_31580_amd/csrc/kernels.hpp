@@ -66,14 +66,14 @@ struct PlanIO {
 
 // Everything the kernels of one forward need that changes per call; uploaded once (the used
 // part of each array).
-struct Plan {
+struct alignas(16) Plan {  // (16-byte aligned arrays: k_plan_fetch copies 16-byte chunks)
   int M, n_groups, n_out, n_bt, n_items;
   PlanIO io;
   RowDesc rows[kMaxRows];
   int row_nslots[kMaxRows];  // attention partial slots of each row (over all its groups)
   OutDesc outs[kMaxRows];
-  AttnItem items[kMaxAttnItems];
-  BtUpdate bt[kMaxBt];
+  alignas(16) AttnItem items[kMaxAttnItems];
+  alignas(16) BtUpdate bt[kMaxBt];
   GroupDesc groups[kMaxGroups];  // (host side: the kernels read the work items)
 };
 
@@ -194,6 +194,10 @@ hipError_t launch_lm_reduce(const Plan* plan, const LmPart* part, int n_groups, 
 hipError_t launch_embed(int dtype, const Plan* plan, int M, const void* embed, int d, int vocab, float* h, int* bt,
                         int max_pps, hipStream_t s);
 hipError_t launch_apply_bt(const Plan* plan, int* bt, int max_pps, hipStream_t s);
+// Copies a staged plan (pinned host slot) to the device plan slot; the kernel's address, so a
+// captured forward's copy can be pointed at the next slot before each replay.
+hipError_t launch_plan_fetch(const Plan* src, Plan* dst, hipStream_t s);
+const void* plan_fetch_kernel();
 // kv_es: bytes per KV element (1 fp8, 2 bf16, 4 fp32); the copy moves raw elements.
 hipError_t launch_kv_copy(int kv_es, int to_pool, void* kpool, void* vpool, const int* bt, int max_pps,
                           int num_pages, int n_layers, int hkv, int hd, int seq, int len, void* k_lin,

@@ -2,6 +2,7 @@
 // softmax merge, KV-cache import/export between the paged layout and a dense one, and the
 // probe's confidence mean.
 #include <algorithm>
+#include <cstddef>
 
 #include "device_common.hpp"
 #include "kernels.hpp"
@@ -171,6 +172,52 @@ hipError_t launch_embed(int dtype, const Plan* plan, int M, const void* embed, i
 hipError_t launch_lm_reduce(const Plan* plan, const LmPart* part, int n_groups, int n_out, hipStream_t s) {
   return launch_k(k_lm_reduce, dim3(n_out), dim3(kLmThreads), s, plan, part, n_groups);
 }
+
+// Copies the used part of a plan from its pinned host staging slot (fine-grained memory, read
+// over the bus) to the device plan slot: the fixed head and the first work items in one round
+// of loads (16 KB), then the rest of the items and the block-table updates, whose counts the
+// head gives.  One workgroup; the next kernel of the forward sees the copy after the boundary.
+constexpr int kFetchThreads = 1024;
+__global__ __launch_bounds__(kFetchThreads) void k_plan_fetch(const Plan* src, Plan* dst) {
+  const char* s = (const char*)src;
+  char* d = (char*)dst;
+  const int t = threadIdx.x;
+  __shared__ int s_cnt[2];
+  constexpr size_t R1 = 16 * kFetchThreads;
+  static_assert(offsetof(Plan, n_items) < 32 && offsetof(Plan, n_bt) < 16, "counts in the first two chunks");
+  static_assert(R1 <= offsetof(Plan, bt), "the first round stays inside the head and items");
+  const u32x4 v = ld_global<u32x4>(s + 16 * t);
+  *(u32x4*)(d + 16 * t) = v;
+  if (t == 0) s_cnt[0] = (int)v[offsetof(Plan, n_bt) / 4];
+  if (t == 1) s_cnt[1] = (int)v[(offsetof(Plan, n_items) - 16) / 4];
+  __syncthreads();
+  const int n_bt = min(max(s_cnt[0], 0), kMaxBt), n_items = min(max(s_cnt[1], 0), kMaxAttnItems);
+  const size_t items_end = (offsetof(Plan, items) + sizeof(AttnItem) * (size_t)n_items + 15) & ~(size_t)15;
+  for (size_t o = R1 + 16 * t; o < items_end; o += 4 * 16 * kFetchThreads) {
+    u32x4 w[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const size_t ou = o + (size_t)u * 16 * kFetchThreads;
+      w[u] = ld_global<u32x4>(s + (ou < items_end ? ou : o));
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const size_t ou = o + (size_t)u * 16 * kFetchThreads;
+      if (ou < items_end) *(u32x4*)(d + ou) = w[u];
+    }
+  }
+  // block-table updates: 12-byte entries from a 16-byte aligned start, whole chunks
+  static_assert(offsetof(Plan, bt) % 16 == 0, "block-table updates 16-byte aligned");
+  const size_t bt_end = offsetof(Plan, bt) + ((sizeof(BtUpdate) * (size_t)n_bt + 15) & ~(size_t)15);
+  for (size_t o = offsetof(Plan, bt) + 16 * t; o < bt_end; o += 16 * kFetchThreads)
+    *(u32x4*)(d + o) = ld_global<u32x4>(s + o);
+}
+
+hipError_t launch_plan_fetch(const Plan* src, Plan* dst, hipStream_t s) {
+  return launch_k(k_plan_fetch, dim3(1), dim3(kFetchThreads), s, src, dst);
+}
+
+const void* plan_fetch_kernel() { return reinterpret_cast<const void*>(&k_plan_fetch); }
 
 hipError_t launch_apply_bt(const Plan* plan, int* bt, int max_pps, hipStream_t s) {
   hipLaunchKernelGGL(k_apply_bt, dim3(1), dim3(256), 0, s, plan, bt, max_pps);

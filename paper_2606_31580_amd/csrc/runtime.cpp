@@ -7,6 +7,7 @@
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
+#include <cstddef>
 #include <cstring>
 #include <mutex>
 #include <new>
@@ -111,6 +112,9 @@ struct GraphEntry {
   hipGraphExec_t exec;
   uint64_t last_use;
   hipEvent_t done;  // recorded after each launch: the exec is destroyed only once it has completed
+  hipGraph_t graph;           // the captured graph (its nodes address the exec's nodes)
+  hipGraphNode_t fetch;       // the plan copy, the forward's first kernel
+  hipKernelNodeParams fetch_params;
 };
 
 // Releases a captured forward after its last launch has finished.
@@ -120,6 +124,7 @@ static void release_graph(GraphEntry& g) {
     (void)hipEventDestroy(g.done);
   }
   (void)hipGraphExecDestroy(g.exec);
+  if (g.graph) (void)hipGraphDestroy(g.graph);
 }
 
 // Spans of one kernel class in a timing session: (end of the kernel launched before the
@@ -559,7 +564,8 @@ extern "C" laser_status laser_model_finalize(laser_model* m, int max_rows, void*
       rope[(size_t)p * half + i] = make_float2((float)std::cos(ang), (float)std::sin(ang));
     }
   Plan* hp = nullptr;
-  HIP_TRY(hipHostMalloc((void**)&hp, sizeof(Plan) * kRing, hipHostMallocDefault));
+  // fine-grained: the forward's first kernel reads the staged plan over the bus, uncached
+  HIP_TRY(hipHostMalloc((void**)&hp, sizeof(Plan) * kRing, hipHostMallocCoherent));
   for (int i = 0; i < kRing; ++i) {
     hipError_t e = hipEventCreateWithFlags(&m->ring_ev[i], hipEventDisableTiming);
     if (e != hipSuccess) {
@@ -825,24 +831,26 @@ static hipError_t timed(laser_model* m, int cls, hipStream_t s, F&& f) {
   return e;
 }
 
-// Copies a plan into the next pinned staging slot and on to the device plan slot (forwards of
-// one model are ordered on its stream, so one device slot suffices); returns the device copy.
-static laser_status upload_plan(laser_model* m, const Plan& p, hipStream_t s, Plan** d_out) {
+// Copies the used part of a plan into the next pinned staging slot, once the forward that
+// last used the slot has finished.  The forward's first kernel (k_plan_fetch) copies it on to
+// the device plan slot, so a replayed forward is one graph launch with no copy command before
+// it (a host-to-device copy between graph launches cost about 20 us of idle time per step).
+// staged_done marks the slot in use until the work now on the stream has finished.
+static laser_status stage_plan(laser_model* m, const Plan& p, const Plan** hp_out, int* slot_out) {
   const int slot = m->ring_pos;
   m->ring_pos = (m->ring_pos + 1) % kRing;
   if (m->ring_used[slot]) HIP_TRY(hipEventSynchronize(m->ring_ev[slot]));
   Plan* hp = m->h_plans + slot;
-  // the used parts: everything up to the last work item, then the block-table updates
-  const size_t bytes = offsetof(Plan, items) + sizeof(AttnItem) * (size_t)p.n_items;
-  const size_t bt_bytes = sizeof(BtUpdate) * (size_t)p.n_bt;
-  std::memcpy(hp, &p, bytes);
-  std::memcpy(hp->bt, p.bt, bt_bytes);
-  Plan* dp = m->wsp<Plan>(m->lay.plans);  // stream order keeps forwards off each other's plan
-  HIP_TRY(hipMemcpyAsync(dp, hp, bytes, hipMemcpyHostToDevice, s));
-  if (bt_bytes) HIP_TRY(hipMemcpyAsync(dp->bt, hp->bt, bt_bytes, hipMemcpyHostToDevice, s));
+  std::memcpy(hp, &p, offsetof(Plan, items) + sizeof(AttnItem) * (size_t)p.n_items);
+  std::memcpy(hp->bt, p.bt, sizeof(BtUpdate) * (size_t)p.n_bt);
+  *hp_out = hp;
+  *slot_out = slot;
+  return LASER_OK;
+}
+
+static laser_status staged_done(laser_model* m, int slot, hipStream_t s) {
   HIP_TRY(hipEventRecord(m->ring_ev[slot], s));
   m->ring_used[slot] = true;
-  *d_out = dp;
   return LASER_OK;
 }
 
@@ -859,12 +867,17 @@ static laser_status flush_pending(laser_kv* kv, laser_model* m, hipStream_t s, P
       const PageUpdate& u = kv->pending[i++];
       p->bt[p->n_bt++] = BtUpdate{u.seq, u.idx, u.page};
     }
-    Plan* dp = nullptr;
-    laser_status st = upload_plan(m, *p, s, &dp);
+    const Plan* hp = nullptr;
+    int slot = 0;
+    laser_status st = stage_plan(m, *p, &hp, &slot);
     if (!buf) delete p;
     if (st != LASER_OK) return st;
+    Plan* dp = m->wsp<Plan>(m->lay.plans);  // stream order keeps forwards off each other's plan
     TimingScope scope(m);
+    HIP_TRY(launch_plan_fetch(hp, dp, s));
     HIP_TRY(launch_apply_bt(dp, kv->bt, kv->pool.max_pages_per_seq(), s));
+    st = staged_done(m, slot, s);
+    if (st != LASER_OK) return st;
   }
   kv->pending.clear();
   return LASER_OK;
@@ -1076,9 +1089,10 @@ static Scratch workspace_scratch(const laser_model* m) {
                  m->max_rows};
 }
 
-static laser_status launch_forward(laser_model* m, laser_kv* kv, const FwdKey& key, hipStream_t s, const Scratch& sc);
+static laser_status launch_forward(laser_model* m, laser_kv* kv, const FwdKey& key, hipStream_t s, const Scratch& sc,
+                                   const Plan* hp);
 
-// Runs one forward: plans the attention splits, uploads the plan, then launches the
+// Runs one forward: plans the attention splits, stages the plan, then launches the
 // forward's kernels (replaying a captured graph of them when graphs are on and no kernel
 // class is being timed).
 static laser_status run_forward(laser_model* m, laser_kv* kv, Plan& p, const PlanIO& io, hipStream_t s,
@@ -1113,32 +1127,51 @@ static laser_status run_forward(laser_model* m, laser_kv* kv, Plan& p, const Pla
         ge = &g;
   key.agx = ge ? ge->key.agx : graphs ? std::min(kMaxAttnItems, ceil_div(need + need / 8, 8) * 8) : need;
   pad_items(p, key.agx);
-  Plan* dp = nullptr;
-  laser_status st = upload_plan(m, p, s, &dp);
+  const Plan* hp = nullptr;
+  int slot = 0;
+  laser_status st = stage_plan(m, p, &hp, &slot);
   if (st != LASER_OK) return st;
   if (!graphs) {
-    TimingScope scope(m);
-    return launch_forward(m, kv, key, s, sc);
+    {
+      TimingScope scope(m);
+      st = launch_forward(m, kv, key, s, sc, hp);
+    }
+    const laser_status sd = staged_done(m, slot, s);
+    return st != LASER_OK ? st : sd;
   }
 
   if (!ge) {
     hipGraph_t graph = nullptr;
     HIP_TRY(hipStreamBeginCapture(m->cap_stream, hipStreamCaptureModeThreadLocal));
-    st = launch_forward(m, kv, key, m->cap_stream, sc);
+    st = launch_forward(m, kv, key, m->cap_stream, sc, hp);
     const hipError_t ec = hipStreamEndCapture(m->cap_stream, &graph);
     if (st != LASER_OK) {
       if (graph) (void)hipGraphDestroy(graph);
       return st;
     }
     if (ec != hipSuccess) return laser_fail(LASER_ERR_HIP, "graph capture: %s", hipGetErrorString(ec));
+    // the plan copy is the one root: every other kernel follows it in stream order
+    hipGraphNode_t fetch = nullptr;
+    size_t n_roots = 1;
+    hipKernelNodeParams fp{};
+    hipGraphNodeType ty{};
+    if (hipGraphGetRootNodes(graph, &fetch, &n_roots) != hipSuccess || n_roots != 1 ||
+        hipGraphNodeGetType(fetch, &ty) != hipSuccess || ty != hipGraphNodeTypeKernel ||
+        hipGraphKernelNodeGetParams(fetch, &fp) != hipSuccess || fp.func != plan_fetch_kernel()) {
+      (void)hipGraphDestroy(graph);
+      return laser_fail(LASER_ERR_HIP, "graph capture: the plan copy is not the forward's only root");
+    }
     hipGraphExec_t exec = nullptr;
     const hipError_t ei = hipGraphInstantiate(&exec, graph, nullptr, nullptr, 0);
-    (void)hipGraphDestroy(graph);
-    if (ei != hipSuccess) return laser_fail(LASER_ERR_HIP, "graph instantiate: %s", hipGetErrorString(ei));
+    if (ei != hipSuccess) {
+      (void)hipGraphDestroy(graph);
+      return laser_fail(LASER_ERR_HIP, "graph instantiate: %s", hipGetErrorString(ei));
+    }
     hipEvent_t done = nullptr;
     const hipError_t ee = hipEventCreateWithFlags(&done, hipEventDisableTiming);
     if (ee != hipSuccess) {
       (void)hipGraphExecDestroy(exec);
+      (void)hipGraphDestroy(graph);
       return laser_fail(LASER_ERR_HIP, "hipEventCreate: %s", hipGetErrorString(ee));
     }
     if ((int)m->graphs.size() >= kMaxGraphs) {  // the least recently used, once its last launch is done
@@ -1147,18 +1180,28 @@ static laser_status run_forward(laser_model* m, laser_kv* kv, Plan& p, const Pla
       release_graph(*lru);
       m->graphs.erase(lru);
     }
-    m->graphs.push_back(GraphEntry{key, exec, 0, done});
+    m->graphs.push_back(GraphEntry{key, exec, 0, done, graph, fetch, fp});
     ++m->graph_captures;
     ge = &m->graphs.back();
   }
   ge->last_use = ++m->graph_clock;
+  {  // the replay's plan copy reads this call's staging slot
+    Plan* dp = m->wsp<Plan>(m->lay.plans);
+    void* args[2] = {(void*)&hp, (void*)&dp};
+    hipKernelNodeParams kp = ge->fetch_params;
+    kp.kernelParams = args;
+    kp.extra = nullptr;
+    HIP_TRY(hipGraphExecKernelNodeSetParams(ge->exec, ge->fetch, &kp));
+  }
   HIP_TRY(hipGraphLaunch(ge->exec, s));
   HIP_TRY(hipEventRecord(ge->done, s));
-  return LASER_OK;
+  return staged_done(m, slot, s);
 }
 
-// Launches the kernels of one forward whose plan is in the device plan slot.
-static laser_status launch_forward(laser_model* m, laser_kv* kv, const FwdKey& key, hipStream_t s, const Scratch& sc) {
+// Launches the kernels of one forward: the copy of its staged plan (hp) to the device plan
+// slot, then the forward's kernels, which read that slot.
+static laser_status launch_forward(laser_model* m, laser_kv* kv, const FwdKey& key, hipStream_t s, const Scratch& sc,
+                                   const Plan* hp) {
   const laser_model_desc& d = m->desc;
   const Layout& L = m->lay;
   const int hd = d.head_dim, G = d.n_q_heads / d.n_kv_heads;
@@ -1167,8 +1210,9 @@ static laser_status launch_forward(laser_model* m, laser_kv* kv, const FwdKey& k
   const Plan* dp = m->wsp<Plan>(L.plans);
   laser_status st = LASER_OK;
   float* h = m->wsp<float>(L.h);
-  HIP_TRY(timed(m, LASER_K_EMBED, s, [&] {
-    return launch_embed(dt, dp, key.M, m->embed, d.d_model, d.vocab, h, kv->bt, max_pps, s);
+  HIP_TRY(timed(m, LASER_K_EMBED, s, [&] {  // the plan copy (from the staging slot hp), then the embedding gather
+    const hipError_t e = launch_plan_fetch(hp, m->wsp<Plan>(L.plans), s);
+    return e == hipSuccess ? launch_embed(dt, dp, key.M, m->embed, d.d_model, d.vocab, h, kv->bt, max_pps, s) : e;
   }));
 
   GemmArgs base{};
