@@ -13,8 +13,9 @@
 // MFMA path), so every epilogue stays inside the workgroup: its waves split K and are
 // reduced through LDS in a fixed order, with no synchronisation between workgroups and
 // results that do not depend on scheduling.  The one exception is the MFMA path's residual
-// projections, which may split K over 2-4 workgroups: each writes its partial rows and
-// k_ksplit_reduce adds them to h, again in a fixed order.
+// projections, which may split K over 2-4 workgroups: each writes its partial rows, and the
+// shares are added to h in share order: by the last of the workgroups to arrive (an atomic
+// counter) at 2 shares, else by k_ksplit_reduce (ksplit_finish).
 // Main loops:
 //   VALU (decode: 1-4 rows; the runtime uses it up to 2): each thread streams 16-byte
 //       non-temporal loads of the group's rows, two chunks at a time (a wave instruction
@@ -493,6 +494,51 @@ constexpr int mfma_wmax() {
   return NR >= 2 && MT >= 2 ? 4 : kMfmaMaxWaves;
 }
 
+// K shares of a residual projection (a.ksplit workgroups per block of row groups, share ks
+// here): this workgroup's partial sums of its nlive groups (Y: [group][row][RW], YN apart) go to
+// kpart.  Without counters (a.kcnt null) that is all: k_ksplit_reduce adds the shares to h.
+// With them, the stores are device-scope ones, which other XCDs see once they have completed,
+// and the workgroup then counts its arrival with a device-scope atomic; the last of the
+// block's workgroups to arrive reads every share back (device-scope loads), adds them in share
+// order and adds the sum to h, as the reduce kernel would, then re-arms the counter.
+template <int RW>
+__device__ void ksplit_finish(const GemmArgs& a, int ks, int blk, int g0, int nlive, int M, const float* Y, int YN) {
+  static_assert(RW % 4 == 0, "16-byte chunks of a group's rows");
+  constexpr int C4 = RW / 4;
+  const int ksplit = a.ksplit;
+  if (a.kcnt == nullptr) {  // k_ksplit_reduce adds the shares
+    for (int r = 0; r < nlive; ++r)
+      for (int i = threadIdx.x; i < M * RW; i += blockDim.x) {
+        const int m = i / RW, row = RW * (g0 + r) + (i - m * RW);
+        a.kpart[((size_t)ks * M + m) * a.N + row] = Y[r * YN + i];
+      }
+    return;
+  }
+  const __amdgpu_buffer_rsrc_t rk = dev_rsrc(a.kpart, (uint32_t)((size_t)ksplit * M * a.N * 4));
+  for (int r = 0; r < nlive; ++r)
+    for (int i = threadIdx.x; i < M * C4; i += blockDim.x) {
+      const int m = i / C4, row = RW * (g0 + r) + 4 * (i - m * C4);
+      const float* y = Y + r * YN + m * RW + (row - RW * (g0 + r));
+      st_dev16(rk, (uint32_t)((((size_t)ks * M + m) * a.N + row) * 4), f32x4{y[0], y[1], y[2], y[3]});
+    }
+  wait_mem();
+  __syncthreads();
+  __shared__ unsigned s_tk;
+  unsigned* cnt = a.kcnt + (size_t)blk * kKsCntStride;
+  if (threadIdx.x == 0) s_tk = __hip_atomic_fetch_add(cnt, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  __syncthreads();
+  if (s_tk != (unsigned)(ksplit - 1)) return;
+  for (int r = 0; r < nlive; ++r)
+    for (int i = threadIdx.x; i < M * C4; i += blockDim.x) {
+      const int m = i / C4, row = RW * (g0 + r) + 4 * (i - m * C4);
+      f32x4 sum = f32x4{0.f, 0.f, 0.f, 0.f};
+      for (int k = 0; k < ksplit; ++k) sum += ld_dev16(rk, (uint32_t)((((size_t)k * M + m) * a.N + row) * 4));
+      f32x4* hp = (f32x4*)(a.h + (size_t)m * a.N + row);
+      *hp = *hp + sum;
+    }
+  if (threadIdx.x == 0) __hip_atomic_store(cnt, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
 template <class WT, int MT, int EPI, int NR>
 __global__ __launch_bounds__(64 * kMfmaMaxWaves) void k_gemm_mfma(GemmArgs a) {
   constexpr int RW = rows_per_group(EPI, true);
@@ -691,11 +737,7 @@ __global__ __launch_bounds__(64 * kMfmaMaxWaves) void k_gemm_mfma(GemmArgs a) {
   }
   __syncthreads();
   if (EPI == EPI_RESID && ksplit > 1) {  // partial sums of this K share (no norm on this path)
-    for (int r = 0; r < nlive; ++r)
-      for (int idx = tid; idx < M * RW; idx += blockDim.x) {
-        const int m = idx / RW, row = RW * (g0 + r) + (idx - m * RW);
-        if (row < a.N) a.kpart[((size_t)ks * M + m) * a.N + row] = Y[r * YN + idx];
-      }
+    ksplit_finish<RW>(a, ks, (int)blockIdx.x / ksplit, g0, nlive, M, Y, YN);
     return;
   }
   for (int r = 0; r < nlive; ++r) run_epilogue<WT, EPI, RW>(a, g0 + r, M, Y + r * YN);
@@ -950,11 +992,7 @@ __global__ __launch_bounds__(256) void k_gemm_mfma_rw(GemmArgs a) {
     }
   __syncthreads();
   if (EPI == EPI_RESID && ksplit > 1) {  // partial sums of this K share (no norm on this path)
-    for (int r = 0; r < nlive; ++r)
-      for (int idx = tid; idx < M * RW; idx += blockDim.x) {
-        const int m = idx / RW, row = RW * (gw0 + r) + (idx - m * RW);
-        if (row < a.N) a.kpart[((size_t)ks * M + m) * a.N + row] = Y[r * YN + idx];
-      }
+    ksplit_finish<RW>(a, ks, (int)blockIdx.x / ksplit, gw0, nlive, M, Y, YN);
     return;
   }
   for (int r = 0; r < nlive; ++r) run_epilogue<WT, EPI, RW>(a, gw0 + r, M, Y + r * YN);
@@ -1341,7 +1379,9 @@ static hipError_t launch_epi(int epi, int rw, const GemmArgs& a, hipStream_t s) 
     const int nr = a.nr < 1 ? 1 : a.nr;
     if (!mfma_nr_ok<MT>(nr)) return hipErrorInvalidValue;
     const int ksplit = a.ksplit < 1 ? 1 : a.ksplit;
-    if (ksplit > 1 && (epi != EPI_RESID || a.kpart == nullptr || ksplit > kMaxKsplit)) return hipErrorInvalidValue;
+    if (ksplit > 1 && (epi != EPI_RESID || a.kpart == nullptr || ksplit > kMaxKsplit || a.N % 16 != 0 ||
+                       (size_t)ksplit * a.M * a.N * 4 > 0xffffffffu))
+      return hipErrorInvalidValue;
     if (a.nrw > 0) {  // row-wave kernel: 8-column activation segments, so K a multiple of 8
       if ((a.nrw != 1 && a.nrw != 2) || a.K % 8 != 0 || a.M < 1 || a.M > 16 * MT) return hipErrorInvalidValue;
       const dim3 grid((a.n_groups + 4 * a.nrw - 1) / (4 * a.nrw) * ksplit);

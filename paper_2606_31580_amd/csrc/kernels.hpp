@@ -19,6 +19,7 @@ constexpr int kGemmThreads = 256; // 4 waves
 constexpr int kGemvMaxThreads = 512;
 constexpr int kMfmaMaxWaves = 8;    // waves of an MFMA projection workgroup with few row groups
 constexpr int kMaxKsplit = 4;       // K shares of a residual projection on the MFMA path
+constexpr int kKsCntStride = 16;    // K-share arrival counters 64 bytes apart
 
 // One row of a forward: request slot, position, and where its input token id lives.
 struct RowDesc {
@@ -125,9 +126,13 @@ struct GemmArgs {
   // EPI_RESID
   float* h;  // [M][N]
   // MFMA path, EPI_RESID only: K split across `ksplit` workgroups per row group (1: none).
-  // Each writes its partial outputs to kpart[ks][M][N]; launch_ksplit_reduce adds them to h.
+  // Each writes its partial outputs to kpart[ks][M][N].  With kcnt (one counter per block of
+  // row groups, kKsCntStride apart, zero between kernels) each counts its arrival and the last
+  // to arrive adds the shares, in share order, to h and re-arms the counter; without it,
+  // launch_ksplit_reduce adds them.
   int ksplit;
   float* kpart;
+  unsigned* kcnt;
   // EPI_SWIGLU
   float* act;  // [M][F]
   int F;

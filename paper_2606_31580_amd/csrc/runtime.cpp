@@ -90,9 +90,9 @@ constexpr int kMaxPagesPerWave = LASER_ATTN_MAX_PPS;
 constexpr int kFusedMaxSplits = LASER_ATTN_FUSED_SPLITS;
 
 struct Layout {
-  size_t rope, h, q, o, act, kpart, qpart, sqpart, lm_part, attn_part, attn_ml, attn_cnt, plans, probe_p, tok_buf, p_buf,
+  size_t rope, h, q, o, act, kpart, kcnt, qpart, sqpart, lm_part, attn_part, attn_ml, attn_cnt, plans, probe_p, tok_buf, p_buf,
       total;
-  size_t attn_part_bytes, attn_ml_bytes, attn_cnt_bytes;
+  size_t attn_part_bytes, attn_ml_bytes, attn_cnt_bytes, kcnt_bytes;
 };
 
 // Launch signature of a forward.  With the plan in its fixed device slot and the caller's
@@ -368,6 +368,12 @@ static bool qkv_slices_fit(const laser_model_desc& d, int max_rows) {
   return d.dtype == LASER_DTYPE_BF16 && max_rows >= kQSliceMinRows && d.d_model % 8 == 0 && d.head_dim % 16 == 0;
 }
 
+// K-share arrival counters of the residual projections: one per block of their 16-row groups
+// (at most d_model / 16 blocks), kKsCntStride apart.
+static size_t ks_cnt_bytes(const laser_model_desc& d) {
+  return (size_t)ceil_div(d.d_model, 16) * kKsCntStride * 4;
+}
+
 static Layout make_layout(const laser_model_desc& d, int max_rows) {
   Layout L{};
   const int hd = d.head_dim, G = d.n_q_heads / d.n_kv_heads;
@@ -383,6 +389,8 @@ static Layout make_layout(const laser_model_desc& d, int max_rows) {
   L.o = take((size_t)max_rows * d.n_q_heads * hd * 4);
   L.act = take((size_t)max_rows * d.d_ffn * 4);
   L.kpart = take((size_t)kMaxKsplit * max_rows * d.d_model * 4);  // K-share partials of O-proj / down
+  L.kcnt_bytes = ks_cnt_bytes(d);
+  L.kcnt = take(L.kcnt_bytes);  // their arrival counters (zero between kernels)
   if (qkv_slices_fit(d, max_rows)) {  // K-slice partials of the QKV projection of wide forwards
     const size_t nsl = ceil_div(d.d_model, kQSliceSteps * 32);
     L.qpart = take(nsl * max_rows * (size_t)(d.n_q_heads + 2 * d.n_kv_heads) * hd * 4);
@@ -587,6 +595,7 @@ extern "C" laser_status laser_model_finalize(laser_model* m, int max_rows, void*
   char* ws = (char*)d_workspace;
   HIP_TRY(hipMemcpyAsync(ws + L.rope, rope.data(), rope.size() * sizeof(float2), hipMemcpyHostToDevice, s));
   HIP_TRY(hipMemsetAsync(ws + L.attn_cnt, 0, L.attn_cnt_bytes, s));
+  HIP_TRY(hipMemsetAsync(ws + L.kcnt, 0, L.kcnt_bytes, s));
   HIP_TRY(hipStreamSynchronize(s));  // the host rope table goes out of scope
   m->static_plan = new (std::nothrow) Plan;
   if (static_scratch_address(m->device, &m->static_scratch) != LASER_OK) m->static_scratch = nullptr;
@@ -1070,6 +1079,7 @@ static void pad_items(Plan& p, int n) {
 // split statistics, fused-merge arrival counters, LM-head statistics, K-share partials.
 struct Scratch {
   float *attn_part, *attn_ml, *kpart;
+  unsigned* kcnt;  // K-share arrival counters
   float *qpart, *sqpart;  // QKV K-slice partials (null: that kernel is not used)
   unsigned* attn_cnt;
   LmPart* lm_part;
@@ -1083,6 +1093,7 @@ static Scratch workspace_scratch(const laser_model* m) {
   return Scratch{m->wsp<float>(L.attn_part),
                  m->wsp<float>(L.attn_ml),
                  m->wsp<float>(L.kpart),
+                 m->wsp<unsigned>(L.kcnt),
                  L.qpart ? m->wsp<float>(L.qpart) : nullptr,
                  L.sqpart ? m->wsp<float>(L.sqpart) : nullptr,
                  m->wsp<unsigned>(L.attn_cnt), m->wsp<LmPart>(L.lm_part), L.attn_part_bytes, L.attn_ml_bytes,
@@ -1246,6 +1257,10 @@ static laser_status launch_forward(laser_model* m, laser_kv* kv, const FwdKey& k
     a.ksplit = ms.ks;
     a.nrw = ms.nrw;
     a.kpart = sc.kpart;
+    // two K shares: the later workgroup of each block adds them (measured: the 8B batch-8
+    // down projection 26.8 -> 24.6 us); four (the row-wave kernel at 49-64 rows): a reduce
+    // kernel, whose last arrivers' reads of 4 shares made the riding forward slower
+    a.kcnt = ms.ks == 2 ? sc.kcnt : nullptr;
     a.M = M;
     if (M <= kValuMaxRows) gemv_shape(epi, K, (int)m->es, M, a.n_groups, m->cus, a);
     if (M > kValuMaxRows && m->tiles_on) {
@@ -1261,7 +1276,7 @@ static laser_status launch_forward(laser_model* m, laser_kv* kv, const FwdKey& k
     const int mode = gemm_mode(M);
     HIP_TRY(timed(m, cls, s, [&] {
       hipError_t e = launch_gemm(dt, mode, epi, rw, a, s);
-      if (e == hipSuccess && a.ksplit > 1) e = launch_ksplit_reduce(a, s);
+      if (e == hipSuccess && a.ksplit > 1 && a.kcnt == nullptr) e = launch_ksplit_reduce(a, s);
       return e;
     }));
     return LASER_OK;
@@ -1497,11 +1512,13 @@ extern "C" laser_status laser_decode_step_static(laser_model* m, laser_kv* kv, i
   const size_t o_part = take(part_bytes), o_ml = take(ml_bytes), o_cnt = take(cnt_n * 4);
   const size_t o_lm = take((size_t)groups_lm(d, batch) * batch * sizeof(LmPart));
   const size_t o_kpart = take((size_t)kMaxKsplit * batch * d.d_model * 4);
+  const size_t kcnt_bytes = ks_cnt_bytes(d), o_kcnt = take(kcnt_bytes);
   if (off > kStaticScratchBytes)
     return laser_fail(LASER_ERR_UNSUPPORTED, "batch %d needs %zu bytes of scratch; the static array holds %zu", batch,
                       off, kStaticScratchBytes);
   char* base = (char*)m->static_scratch;
-  const Scratch sc{(float*)(base + o_part), (float*)(base + o_ml), (float*)(base + o_kpart), nullptr, nullptr,
+  const Scratch sc{(float*)(base + o_part), (float*)(base + o_ml), (float*)(base + o_kpart), (unsigned*)(base + o_kcnt),
+                   nullptr, nullptr,
                    (unsigned*)(base + o_cnt), (LmPart*)(base + o_lm), part_bytes, ml_bytes, batch};
   std::vector<int> seqs(seq_ids, seq_ids + batch), grow(batch, 1);
   st = check_growth(m, kv, seqs, grow);
@@ -1513,6 +1530,7 @@ extern "C" laser_status laser_decode_step_static(laser_model* m, laser_kv* kv, i
   {
     TimingScope scope(m);
     HIP_TRY(launch_fill_u32(sc.attn_cnt, (int)cnt_n, 0u, s));  // the array keeps the last call's contents
+    HIP_TRY(launch_fill_u32(sc.kcnt, (int)(kcnt_bytes / 4), 0u, s));
   }
   p->M = batch;
   p->n_out = batch;
