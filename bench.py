@@ -138,7 +138,7 @@ def main():
     seqs = list(range(B))
     forks = [B + b for b in seqs]
     tokens = synth.make_tokens(B, shape.vocab, 3003).to(dev)
-    nxt = torch.empty(B, dtype=torch.int32, device=dev)
+    nxt = tokens  # greedy feedback in place: each forward's next tokens overwrite its inputs
     pmax = torch.empty(B, device=dev)
     suffix = synth.make_suffix(S, shape.vocab).to(dev)
     conf = torch.empty(B, device=dev)
@@ -216,7 +216,6 @@ def main():
                 spans.append(L.span(B + f, S, 1, 0, out=(1, S + f * T)))
                 inflight.append([f, b, 0, ev0])
         L.laser_forward(model, kv, spans, tokens, tokbuf, nxt, pmax, tokbuf, pbuf)
-        tokens.copy_(nxt)
         settle()  # the previous step's decisions, this step's forward being queued
         done = [pr for pr in inflight if pr[2] == T - 1]
         if not done:
@@ -238,7 +237,6 @@ def main():
         if wl.mixed:  # the probes of this step run in the same forwards as its decode
             pidx = schedule[i % len(schedule)]
             L.laser_step_mixed(model, kv, seqs, tokens, nxt, pmax, pidx, suffix, T, conf, argm)
-            tokens.copy_(nxt)
             c = conf.cpu().numpy()
             for j in range(len(pidx)):
                 L.laser_exit_decision(params, load_state, float(c[j]), B, 0, 10)
@@ -247,7 +245,6 @@ def main():
         at_atp = wl.probe_every and i % wl.probe_every == 0
         if args.probe_mode == "separate":
             L.laser_decode_step(model, kv, seqs, tokens, nxt, pmax)
-            tokens.copy_(nxt)
             if at_atp:
                 if timed_probe:  # latency of the probe itself, not of decode steps still queued
                     torch.cuda.synchronize()
@@ -278,7 +275,6 @@ def main():
                 spans += [L.span(forks[b], 1, 1, b * T + j - 1, out=(1, b * T + j)) for b in seqs]
                 tok1 = argm
         L.laser_forward(model, kv, spans, tokens, tok1, nxt, pmax, argm, ptrial)
-        tokens.copy_(nxt)
         settle()  # the previous step's decisions, this step's forward being queued
         if ride and ride["s"] == S and ride["t"] == T - 1:
             L.laser_confidence(model, ptrial, T, B, conf)
@@ -353,7 +349,6 @@ def main():
     e0.record(stream)
     for i in range(n_dec):
         L.laser_decode_step(model, kv, seqs, tokens, nxt, pmax)
-        tokens.copy_(nxt)
     e1.record(stream)
     torch.cuda.synchronize()
     dec_ms = e0.elapsed_time(e1) / n_dec
@@ -368,7 +363,6 @@ def main():
     n_kt = min(args.steps, 32)
     for i in range(n_kt):
         L.laser_decode_step(model, kv, seqs, tokens, nxt, pmax)
-        tokens.copy_(nxt)
     kernel_us = {}
     for name, c in classes.items():
         tot_ms, n = model.timing_read(c)
@@ -512,14 +506,12 @@ def cost_model(L, synth, model, kv, shape, dev, slot, dec_long_ms, ctx_long, suf
     kv.import_kv(slot, k0, v0)
     del k0, v0
     tok = synth.make_tokens(1, shape.vocab, 3005).to(dev)
-    nxt = torch.empty(1, dtype=torch.int32, device=dev)
     pm = torch.empty(1, device=dev)
     conf = torch.empty(1, device=dev)
     argm = torch.empty(T, dtype=torch.int32, device=dev)
 
     def dec():
-        L.laser_decode_step(model, kv, [slot], tok, nxt, pm)
-        tok.copy_(nxt)
+        L.laser_decode_step(model, kv, [slot], tok, tok, pm)  # next token in place
 
     timed(dec, 4)
     n = 32

@@ -395,8 +395,10 @@ laser_status laser_step_mixed(laser_model* m, laser_kv* kv, int batch, const int
  * token per request; a prompt or probe chunk is a longer span; spans of different
  * sequences mix freely (this is how a probe rides along with decode steps on a fork of
  * the request: Section 3.1's probe, with the request's own tokens unaffected).  Sequences
- * are distinct across spans; the total rows are at most max_rows.  Input and output
- * arrays may alias when no output index is also read as an input of the same call. */
+ * are distinct across spans; the total rows are at most max_rows.  The call is one
+ * forward whose first kernel reads every input token before any output is written, so
+ * input and output arrays may alias, also at the same indices (a decode loop can write each
+ * request's next token over its input). */
 typedef struct {
   int32_t seq, n_tokens, tok_sel, tok_off, out, out_sel, out_off;
 } laser_span;

@@ -93,3 +93,27 @@ def test_graph_replay_matches_eager():
     model.timing_enable(L.K_GATEUP, False)
     assert n == 2 * TINY.n_layers and ms > 0  # both decodes ran inside the timing session
     assert torch.equal(lg, ref[2])
+
+
+def test_forward_next_tokens_in_place():
+    """laser_forward whose output tokens overwrite its input tokens at the same indices (the
+    forward reads every input before it writes an output) against separate output buffers."""
+    require_gpu()
+    w = {k: v.cuda() for k, v in synth.make_weights(TINY).items()}
+    model = L.Model(TINY, w, max_rows=32, max_positions=768, poison=True)
+    lens = [31, 250, 77]
+    kv_a, kv_b = _state(model, lens), _state(model, lens)
+    B = len(lens)
+    tok_a = synth.make_tokens(B, TINY.vocab, 78).cuda()
+    tok_b, nxt_b = tok_a.clone(), torch.zeros(B, dtype=torch.int32, device="cuda")
+    p_a, p_b = torch.zeros(B, device="cuda"), torch.zeros(B, device="cuda")
+    spans = [L.span(b, 1, 0, b, out=(0, b)) for b in range(B)]
+    for step in range(24):
+        L.laser_forward(model, kv_a, spans, tok_a, None, tok_a, p_a)
+        L.laser_forward(model, kv_b, spans, tok_b, None, nxt_b, p_b)
+        torch.cuda.synchronize()
+        assert torch.equal(tok_a, nxt_b) and torch.equal(p_a, p_b), f"step {step}"
+        tok_b.copy_(nxt_b)
+    kv_a.destroy()
+    kv_b.destroy()
+    model.destroy()
