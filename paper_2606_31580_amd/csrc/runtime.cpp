@@ -169,6 +169,8 @@ struct laser_model {
   hipEvent_t ring_ev[kRing] = {};
   bool ring_used[kRing] = {};
   int ring_pos = 0;
+  long long ring_turn = 0;               // turns of the staging ring so far
+  long long ring_rec_turn[kRing] = {};   // the turn in which ring_ev[slot] was last recorded
   Timer timers[LASER_K_NCLASS];
   std::vector<hipEvent_t> ev_pool;  // fence-free timing events, reused across sessions
   int ev_used = 0;
@@ -720,10 +722,8 @@ extern "C" laser_status laser_model_destroy(laser_model* m) {
   if (!model_of(m)) return laser_fail(LASER_ERR_STATE, "invalid or destroyed model");
   handle_del(m);
   if (m->finalized) {
-    for (int i = 0; i < kRing; ++i) {
-      if (m->ring_used[i]) (void)hipEventSynchronize(m->ring_ev[i]);
-      (void)hipEventDestroy(m->ring_ev[i]);
-    }
+    (void)hipDeviceSynchronize();  // forwards still queued read the staging ring (events mark only some)
+    for (int i = 0; i < kRing; ++i) (void)hipEventDestroy(m->ring_ev[i]);
     (void)hipHostFree(m->h_plans);
     for (auto& g : m->graphs) release_graph(g);
     if (m->cap_stream) (void)hipStreamDestroy(m->cap_stream);
@@ -861,8 +861,16 @@ static hipError_t timed(laser_model* m, int cls, hipStream_t s, F&& f) {
 static laser_status stage_plan(laser_model* m, const Plan& p, const Plan** hp_out, int* slot_out) {
   const int slot = m->ring_pos;
   m->ring_pos = (m->ring_pos + 1) % kRing;
+  if (slot == 0) ++m->ring_turn;
   const int last = slot + kRingEventEvery - 1;  // the block's last slot
-  if (slot % kRingEventEvery == 0 && m->ring_used[last]) HIP_TRY(hipEventSynchronize(m->ring_ev[last]));
+  if (slot % kRingEventEvery == 0 && m->ring_turn > 1) {
+    // the block was last used in the previous turn; its last forward's event covers it (one
+    // stream per model), unless that forward failed before its event was recorded
+    if (m->ring_used[last] && m->ring_rec_turn[last] == m->ring_turn - 1)
+      HIP_TRY(hipEventSynchronize(m->ring_ev[last]));
+    else
+      HIP_TRY(hipDeviceSynchronize());
+  }
   Plan* hp = m->h_plans + slot;
   std::memcpy(hp, &p, offsetof(Plan, items) + sizeof(AttnItem) * (size_t)p.n_items);
   std::memcpy(hp->bt, p.bt, sizeof(BtUpdate) * (size_t)p.n_bt);
@@ -875,6 +883,7 @@ static laser_status staged_done(laser_model* m, int slot, hipStream_t s) {
   if (slot % kRingEventEvery != kRingEventEvery - 1) return LASER_OK;
   HIP_TRY(hipEventRecord(m->ring_ev[slot], s));
   m->ring_used[slot] = true;
+  m->ring_rec_turn[slot] = m->ring_turn;
   return LASER_OK;
 }
 
