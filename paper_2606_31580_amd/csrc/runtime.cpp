@@ -321,6 +321,13 @@ struct MfmaShape {
   int nr, ks, nrw;
 };
 constexpr double kKsplitPenalty = 160e3;
+// Two shares summed inside the projection (no reduce kernel) cost one more round trip at the
+// end of it, which pays only for long rows: for K >= kKsplitLongK the penalty of two shares is
+// kKsplit2LongPenalty.  Measured: the 7B batch-4 down projection (K = 18,944) 29.8 -> 26.5 us
+// with two shares; with the same penalty at K = 4,096 the 8B batch-8 O-projection took two
+// shares and went from 10.6 to 11.4 us.
+constexpr double kKsplit2LongPenalty = 40e3;
+constexpr int kKsplitLongK = 8192;
 #ifndef LASER_RW_MAX_NRW
 #define LASER_RW_MAX_NRW 2
 #endif
@@ -346,7 +353,8 @@ static MfmaShape mfma_shape(int epi, int n_groups, int M, int K, int es, int cus
   const double w = 16.0 * K * es, act = 4.0 * M * K;
   auto cost = [&](int groups_per_wg, int ks) {
     const double wgs = (double)ceil_div(ceil_div(n_groups, groups_per_wg) * ks, cus);
-    return wgs * (groups_per_wg * w + act) / ks + (ks > 1 ? kKsplitPenalty : 0.0);
+    const double pen = ks == 2 && K >= kKsplitLongK ? kKsplit2LongPenalty : kKsplitPenalty;
+    return wgs * (groups_per_wg * w + act) / ks + (ks > 1 ? pen : 0.0);
   };
   const int max_ks = epi == EPI_RESID ? kMaxKsplit : 1;
   MfmaShape best{1, 1, 0};
