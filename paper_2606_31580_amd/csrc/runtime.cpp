@@ -308,13 +308,14 @@ static int groups_lm(const laser_model_desc& d, int M) { return ceil_div(d.vocab
 // its groups' weights and the activation rows over its K range, so several groups per
 // workgroup cut the activation reads per weight byte but also the number of workgroups, and
 // splitting K (residual projections only: the others normalise over the whole row) restores
-// the workgroups at the price of a reduce kernel.  The choice minimises the bytes read by the
-// busiest compute unit (workgroups are dealt round-robin), the reduce counted as
-// kKsplitPenalty bytes.  At one 16-row tile: two groups for gate/up and the LM head, and for
-// QKV at the 7B and 8B shapes (288 or 384 groups: 1.2-1.5 workgroups per CU with one group
-// each); with 2-3 tiles up to four groups (gate/up of a 40-row mixed step); at 4 tiles up to
-// two.  O-proj and down split K where the activation rows outweigh the weights (M >= 8 at
-// the 7B down projection, the 40-row mixed step).
+// the workgroups at the price of summing the shares.  The choice minimises the bytes read by
+// the busiest compute unit (workgroups are dealt round-robin), the sum counted as
+// kKsplitPenalty bytes (kKsplit2LongPenalty for two shares of long rows).  At one 16-row
+// tile: two groups for gate/up and the LM head, and for QKV at the 7B and 8B shapes (288 or
+// 384 groups: 1.2-1.5 workgroups per CU with one group each); with 2-3 tiles up to four
+// groups (gate/up of a 40-row mixed step); at 4 tiles up to two.  The down projection splits
+// K from 4 rows at the 7B shape (two groups, two shares) and O-proj where the activation rows
+// outweigh the weights (the 40-row mixed step).
 // MFMA-path kernel and its shape.  nrw = 0: the K-split kernel with nr row groups per
 // workgroup; nrw = 1, 2: the row-wave kernel (4 waves of nrw groups each).  ks: K shares.
 struct MfmaShape {
