@@ -117,3 +117,42 @@ def test_forward_next_tokens_in_place():
     kv_a.destroy()
     kv_b.destroy()
     model.destroy()
+
+
+def test_graph_eviction_matches_eager():
+    """More forward shapes than the captured-graph cache holds (16): evicted graphs are
+    released while later forwards are queued, and every replay still matches the eager
+    launch of the same forward bitwise."""
+    require_gpu()
+    w = {k: v.cuda() for k, v in synth.make_weights(TINY).items()}
+    model = L.Model(TINY, w, max_rows=32, max_positions=768, poison=True)
+    n = 20
+    lens = [10 + 7 * i for i in range(n)]
+
+    def caches():
+        kv = L.KVCache(model, 200, n, 48, poison=True)
+        for i, ln in enumerate(lens):
+            k0, v0 = synth.make_prefill_kv(TINY, ln, 90 + i)
+            kv.add_seq(i, ln)
+            kv.import_kv(i, k0.cuda(), v0.cuda())
+        return kv
+    kv_a, kv_b = caches(), caches()
+    tok = synth.make_tokens(n, TINY.vocab, 79).cuda()
+    for rnd in range(3):
+        for b in range(1, n + 1):  # b rows: a new graph key per batch size
+            seqs = list(range(b))
+            outs = []
+            for on, kv in ((True, kv_a), (False, kv_b)):
+                model.set_graphs(on)
+                nxt = torch.zeros(b, dtype=torch.int32, device="cuda")
+                p = torch.zeros(b, device="cuda")
+                L.laser_decode_step(model, kv, seqs, tok[:b], nxt, p)
+                outs.append((nxt, p))
+            torch.cuda.synchronize()
+            assert torch.equal(outs[0][0], outs[1][0]) and torch.equal(outs[0][1], outs[1][1]), f"round {rnd}, {b} rows"
+    model.set_graphs(True)
+    captures, cached = model.graph_stats()
+    assert captures > 16 and cached <= 16
+    kv_a.destroy()
+    kv_b.destroy()
+    model.destroy()
