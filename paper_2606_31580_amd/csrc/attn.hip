@@ -432,80 +432,99 @@ __global__ __launch_bounds__(64 * kAttnWaves) void k_attn(AttnArgs a) {
 
 // Combines the workgroup partials (m, l, O) of every (row, query head) whose group used
 // more than one attention workgroup: o = sum_w O_w 2^(m_w - M) / sum_w l_w 2^(m_w - M),
-// M = max_w m_w.  grid (rows, query heads), 16 waves: wave v takes partials w = v mod 16
-// (all loads of a wave issued together, before the plan lookup), lanes take dims; the
-// waves are then combined in LDS in fixed order.
-constexpr int kMergeWaves = 16;
-__global__ __launch_bounds__(64 * kMergeWaves) void k_attn_merge(AttnArgs a, int hd, int nslots) {
-  constexpr int PER = kAttnMaxWG / kMergeWaves;
+// M = max_w m_w.  grid (rows, query heads), 8 waves.  A slot's HD floats are read by HD/4
+// consecutive lanes with 16-byte loads, each lane also reading the slot's (m, l) pair, so
+// one wave load covers 64/(HD/4) slots; a lane takes kAttnMaxWG/(kMergeWaves x that) slots, all its
+// loads issued together before the plan lookup.  Each wave combines its slots across its
+// lanes, then the waves are combined in LDS in fixed order.
+constexpr int kMergeWaves = 8;
+template <int HD>
+__global__ __launch_bounds__(64 * kMergeWaves) void k_attn_merge(AttnArgs a, int nslots) {
+  constexpr int LPS = HD / 4;             // lanes per slot
+  constexpr int SPW = 64 / LPS;           // slots per wave load
+  constexpr int SPP = SPW * kMergeWaves;  // slots per workgroup pass
+  constexpr int PER = kAttnMaxWG / SPP;   // slots per lane
+  static_assert(PER * SPP == kAttnMaxWG, "slot passes");
   __shared__ float s_m[kMergeWaves], s_l[kMergeWaves];
-  __shared__ float s_o[kMergeWaves][128];
+  __shared__ __align__(16) float s_o[kMergeWaves][HD];
   const int row = blockIdx.x, head = blockIdx.y;
   const int v = threadIdx.x >> 6, l = threadIdx.x & 63;
+  const int d4 = l % LPS, sl = l / LPS;
   const int kvh = head / a.G, gi = head - kvh * a.G;
   const size_t ncols = (size_t)a.max_rows * a.G;
   const size_t col = (size_t)row * a.G + gi;
-  // Every slot is loaded before the row's own workgroup count is known (slots past it are
-  // replaced below, never combined), so the loads overlap the plan lookup.  Slots at or past
-  // nslots (the launch's bound on every group's count) read slot nslots - 1 again, a cached
-  // line, instead of stale partials; the loads stay unconditional so none waits for another.
-  float mv[PER], lv[PER], o0[PER], o1[PER];
+  // Slots at or past nslots (the launch's bound on every group's count) read slot
+  // nslots - 1 again, a cached line, instead of stale partials; slots past the row's own
+  // count are replaced below, never combined.  The loads stay unconditional so none waits
+  // for another.
+  float mv[PER], lv[PER];
+  f32x4 ov[PER];
 #pragma unroll
   for (int i = 0; i < PER; ++i) {
-    const size_t sb = ((size_t)kvh * kAttnMaxWG + min(v + kMergeWaves * i, nslots - 1)) * ncols + col;
-    mv[i] = a.ml[sb * 2];
-    lv[i] = a.ml[sb * 2 + 1];
-    o0[i] = a.part[sb * hd + l];
-    o1[i] = (l + 64 < hd) ? a.part[sb * hd + l + 64] : 0.f;
+    const int slot = min(SPP * i + SPW * v + sl, nslots - 1);
+    const size_t sb = ((size_t)kvh * kAttnMaxWG + slot) * ncols + col;
+    const float2 ml = *(const float2*)(a.ml + sb * 2);
+    mv[i] = ml.x;
+    lv[i] = ml.y;
+    ov[i] = *(const f32x4*)(a.part + sb * HD + 4 * d4);
   }
   const int nwg = a.plan->row_nslots[row];
   if (nwg <= 1) return;  // written directly by the attention kernel
 #pragma unroll
   for (int i = 0; i < PER; ++i)
-    if (v + kMergeWaves * i >= nwg) {
+    if (SPP * i + SPW * v + sl >= nwg) {
       mv[i] = -INFINITY;
       lv[i] = 0.f;
-      o0[i] = o1[i] = 0.f;
+      ov[i] = f32x4{0.f, 0.f, 0.f, 0.f};
     }
   float M = -INFINITY;
 #pragma unroll
   for (int i = 0; i < PER; ++i) M = fmaxf(M, mv[i]);
-  float L = 0.f, O0 = 0.f, O1 = 0.f;
+  M = wave_max(M);  // over the wave's slots
+  float L = 0.f;
+  f32x4 O = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
   for (int i = 0; i < PER; ++i) {
     const float f = (M == -INFINITY) ? 0.f : safe_exp2(mv[i] - M);
     L += lv[i] * f;
-    O0 += o0[i] * f;
-    O1 += o1[i] * f;
+    O += ov[i] * f;
   }
+  // the wave's slot lanes (LPS apart) summed, so every lane holds the wave's totals
+  if constexpr (SPW == 4) {
+    L = sum_x16(L);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) O[q] = sum_x16(O[q]);
+  }
+  L = sum_x32(L);
+#pragma unroll
+  for (int q = 0; q < 4; ++q) O[q] = sum_x32(O[q]);
+  if (l < LPS) *(f32x4*)&s_o[v][4 * d4] = O;
   if (l == 0) {
     s_m[v] = M;
     s_l[v] = L;
   }
-  s_o[v][l] = O0;
-  s_o[v][l + 64] = O1;
   __syncthreads();
-  if (v == 0) {
+  const int d = threadIdx.x;
+  if (d < HD) {
     float Mt = -INFINITY;
 #pragma unroll
     for (int u = 0; u < kMergeWaves; ++u) Mt = fmaxf(Mt, s_m[u]);
-    float Lt = 0.f, Ot0 = 0.f, Ot1 = 0.f;
+    float Lt = 0.f, Ot = 0.f;
 #pragma unroll
     for (int u = 0; u < kMergeWaves; ++u) {
       const float f = (s_m[u] == -INFINITY) ? 0.f : safe_exp2(s_m[u] - Mt);
       Lt += s_l[u] * f;
-      Ot0 += s_o[u][l] * f;
-      Ot1 += s_o[u][l + 64] * f;
+      Ot += s_o[u][d] * f;
     }
-    float* out = a.o + ((size_t)row * a.hq + head) * hd;
-    out[l] = Ot0 / Lt;
-    if (l + 64 < hd) out[l + 64] = Ot1 / Lt;
+    a.o[((size_t)row * a.hq + head) * HD + d] = Ot / Lt;
   }
 }
 
 hipError_t launch_attn_merge(const AttnArgs& a, int M, int hd, int nslots, hipStream_t s) {
   if (nslots < 1 || nslots > kAttnMaxWG) return hipErrorInvalidValue;
-  return launch_k(k_attn_merge, dim3(M, a.hq), dim3(64 * kMergeWaves), s, a, hd, nslots);
+  if (hd == 128) return launch_k(k_attn_merge<128>, dim3(M, a.hq), dim3(64 * kMergeWaves), s, a, nslots);
+  if (hd == 64) return launch_k(k_attn_merge<64>, dim3(M, a.hq), dim3(64 * kMergeWaves), s, a, nslots);
+  return hipErrorInvalidValue;
 }
 
 template <class KT, int HD>
