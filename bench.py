@@ -51,6 +51,9 @@ def parse():
                     help="one-row attention groups: merged by the attention kernel's last workgroup (fused) or "
                          "by the separate merge kernel")
     ap.add_argument("--attn-splits", type=int, default=56, help="split bound of a fused one-row attention group")
+    ap.add_argument("--oproj-merge", choices=["auto", "on", "off"], default="auto",
+                    help="split merge of 1-2 row forwards: inside the O-projection's launch (on), as its own "
+                         "kernel (off), or inside the launch for projections of at least 16 MiB of weights (auto)")
     ap.add_argument("--design-probes", action="store_true",
                     help="only run the design-probe program (streaming read, kernel boundary, cross-workgroup "
                          "hand-off, grid barrier, dependent products) and print its report")
@@ -121,6 +124,7 @@ def main():
     model = L.Model(shape, weights, max_rows=64, max_positions=max_pos, tiles=not args.no_tiles)
     model.set_gemm_kernel(args.gemm_kernel)
     model.set_attn_merge(args.attn_merge == "fused", args.attn_splits)
+    model.set_oproj_merge({"off": 0, "auto": 1, "on": 2}[args.oproj_merge])
     pps = max_pos // PAGE + 1
     num_pages = sum((n + 2 * total_steps + S + T) // PAGE + 2 for n in lens) + B * ((S + T) // PAGE + 3) + 8
     num_pages += (COST_CTX + 512) // PAGE + 4  # the cost-model pass (a shorter request in a fork slot)
@@ -433,7 +437,7 @@ def main():
         "data": "synthetic: random-init weights, seeded pre-filled KV",
         "config": {"workload": wl.name, "model_shape": shape.name, "batch": B, "kv_lens": lens,
                    "probe_every": wl.probe_every, "suffix": S, "trials": T, "attn_merge": args.attn_merge,
-                   "attn_splits": args.attn_splits},
+                   "attn_splits": args.attn_splits, "oproj_merge": args.oproj_merge},
         "decode_only_ms_per_step": round(dec_ms, 4),
         "decode_only_tok_s": round(B / (dec_ms / 1e3), 2),
         "probe_latency_ms": {"mean": round(float(np.mean(probe_ms)), 3) if probe_ms else None,

@@ -499,6 +499,18 @@ laser_status laser_model_set_gemm_kernel(laser_model* m, int mode);
  * outside [2, 128]). */
 laser_status laser_model_set_attn_merge(laser_model* m, int fused, int max_splits);
 
+/* Where the attention split merge of a forward of 1-2 rows runs (the decode step of Section
+ * 3.1, whose per-token cost Eq. 2 sums; with fused = 0 above).  mode 2: in the O-projection's
+ * launch, whose first workgroups combine the partials and publish the output while the
+ * projection's workgroups start streaming their weights, then wait for it (a bounded wait; a
+ * projection whose merge never arrived writes NaN).  mode 0: a separate merge kernel.  mode 1
+ * (the default): the O-projection's launch when the projection's weights take at least 16 MiB
+ * (long enough a stream to hide the merge: measured faster at the 7B shape, slower at 1.5B),
+ * else the merge kernel.  The two combine the partials in different orders, so results may
+ * differ in the last bits.  Not used by laser_decode_step_static.
+ * Errors: LASER_ERR_STATE (bad model), LASER_ERR_INVALID_ARG (mode not 0, 1 or 2). */
+laser_status laser_model_set_oproj_merge(laser_model* m, int mode);
+
 #ifdef __cplusplus
 }
 #endif

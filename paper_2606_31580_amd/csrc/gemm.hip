@@ -342,9 +342,23 @@ __device__ __forceinline__ void unpack16(const u32x4& raw, float* out) {
 
 // ----------------------------------------------------------------------------- VALU GEMV
 
+__device__ __forceinline__ float merge_exp2(float x) { return x == -INFINITY ? 0.f : exp2f(x); }
+
+// Split merge carried by a projection's launch (MG): polls of the merge counter before a
+// projection workgroup gives up (a fraction of a second), and partial slots per lane per round.
+constexpr unsigned kMgSpin = 1u << 18;
+constexpr int kMgPer = 16;
+
 // U: chunks of every row in flight per thread (one pass covers U x blockDim chunks).
-template <class WT, int M, int EPI, int RW, int U>
-__global__ __launch_bounds__(kGemvMaxThreads) void k_gemv(GemmArgs a) {
+// MG: the activation rows are the attention output o that the launch's first mg.nwg
+// workgroups produce (k_gemv_merged): read with device-scope loads once the workgroup's
+// replica of the layer's merge counter has reached the plan's target, which the first pass
+// waits for after issuing its weight loads.  Those loads start about 1.7 us into the
+// workgroup, so that the merge's partial loads, stores and counter updates are not queued
+// behind the projection's weight stream (7B shape, 64 counter copies: the projection with the
+// merge 10.3 us with this delay, 10.9-11.0 us with 0.4-0.85 us).  g: the row group.
+template <class WT, int M, int EPI, int RW, int U, bool MG>
+__device__ __forceinline__ void gemv_body(const GemmArgs& a, const MergeArgs& mg, const int g) {
   constexpr int RWP = RW <= 4 ? 4 : (RW <= 8 ? 8 : 16);  // RW padded to a power of two
   constexpr int CH = 16 / (int)sizeof(WT);  // elements per 16-byte load
   constexpr int NV = RW * M + M;            // per-wave totals: outputs, then sums of squares
@@ -354,7 +368,6 @@ __global__ __launch_bounds__(kGemvMaxThreads) void k_gemv(GemmArgs a) {
   __shared__ float Y[M * RW];
   __shared__ float s_scale[M];
   const int tid = threadIdx.x, w = tid >> 6, l = tid & 63;
-  const int g = blockIdx.x;
   constexpr bool norm = EPI != EPI_RESID;  // every other epilogue follows an RMSNorm (gain checked at launch)
   const int nch = a.K / CH;
   const char* wp[RW];
@@ -375,11 +388,14 @@ __global__ __launch_bounds__(kGemvMaxThreads) void k_gemv(GemmArgs a) {
   // right behind its first loads; nothing waits for them until the epilogue.
   EpiItem item;
   if (kPre) epi_fetch_a<WT, EPI, RW>(a, g, M, tid, item);
+  int mg_fail = 0;  // MG, thread 0: the merge counter never reached its target
+  const __amdgpu_buffer_rsrc_t ro = dev_rsrc(MG ? a.x : nullptr, MG ? mg.o_bytes : 0u);  // o (MG only)
   // One pass over chunks c0 and c0 + T of every row.  All loads come first and none is
   // conditional (a chunk past the end re-reads the last one and leaves the sums as they
   // are), so the waits before each use count exactly; the first pass is peeled so that the
   // weight stream never waits behind the epilogue's loads at a loop header.
   auto pass = [&](int c0, auto first) {
+    if constexpr (MG && decltype(first)::value) __builtin_amdgcn_s_sleep(64);  // 4096 cycles
     u32x4 wv[U][RW];
     float4 xv[U][M][CH / 4];
     u32x4 gv[U];
@@ -388,11 +404,44 @@ __global__ __launch_bounds__(kGemvMaxThreads) void k_gemv(GemmArgs a) {
       const int c = min(c0 + u * T, nch - 1);
 #pragma unroll
       for (int r = 0; r < RW; ++r) wv[u][r] = ld_nt16(wp[r] + (size_t)c * 16);
+      if constexpr (!MG) {
 #pragma unroll
-      for (int m = 0; m < M; ++m)
+        for (int m = 0; m < M; ++m)
 #pragma unroll
-        for (int e4 = 0; e4 < CH / 4; ++e4) xv[u][m][e4] = *(const float4*)(xr[m] + c * CH + 4 * e4);
-      if (norm) gv[u] = *(const u32x4*)((const char*)a.gain + (size_t)c * 16);
+          for (int e4 = 0; e4 < CH / 4; ++e4) xv[u][m][e4] = *(const float4*)(xr[m] + c * CH + 4 * e4);
+        if (norm) gv[u] = *(const u32x4*)((const char*)a.gain + (size_t)c * 16);
+      }
+    }
+    if constexpr (MG) {
+      if constexpr (decltype(first)::value) {
+        // thread 0 polls (its poll returns after its own weight loads: loads complete in
+        // order), the others wait at the barrier with their weight loads in flight
+        if (tid == 0) {
+          const unsigned target = a.plan->merge_target;
+          unsigned it = 0;
+          const unsigned* cnt = mg.cnt + (g % kMgReplicas) * kKsCntStride;
+          while ((int)(__hip_atomic_load(cnt, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) - target) < 0) {
+            if (++it == kMgSpin) {
+              mg_fail = 1;
+              break;
+            }
+            __builtin_amdgcn_s_sleep(2);
+          }
+        }
+        __builtin_amdgcn_s_barrier();
+        __atomic_signal_fence(__ATOMIC_SEQ_CST);  // no o load moves above the wait
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int c = min(c0 + u * T, nch - 1);
+#pragma unroll
+        for (int m = 0; m < M; ++m)
+#pragma unroll
+          for (int e4 = 0; e4 < CH / 4; ++e4) {
+            const f32x4 t = ld_dev16(ro, (uint32_t)((m * a.ldx + c * CH + 4 * e4) * 4));
+            xv[u][m][e4] = make_float4(t[0], t[1], t[2], t[3]);
+          }
+      }
     }
     // every load above is issued before any use (the scheduler would otherwise trade loads
     // in flight for registers)
@@ -455,6 +504,8 @@ __global__ __launch_bounds__(kGemvMaxThreads) void k_gemv(GemmArgs a) {
       if (l == 0) s_red[w][RW * M + m] = s;
     }
   }
+  __shared__ int s_fail;
+  if (MG && tid == 0) s_fail = mg_fail;
   __syncthreads();
   if (norm && tid < M) {
     float s = 0.f;
@@ -467,12 +518,128 @@ __global__ __launch_bounds__(kGemvMaxThreads) void k_gemv(GemmArgs a) {
     float v = 0.f;
     for (int q = 0; q < nw; ++q) v += s_red[q][tid];
     Y[m * RW + r] = norm ? v * s_scale[m] : v;
+    if (MG && s_fail) Y[m * RW + r] = __builtin_nanf("");  // a merge that never arrived shows as NaN
   }
   __syncthreads();
   if (kPre)
     epi_apply<WT, EPI, RW>(a, g, item, Y);
   else
     run_epilogue<WT, EPI, RW>(a, g, M, Y);
+}
+
+template <class WT, int M, int EPI, int RW, int U>
+__global__ __launch_bounds__(kGemvMaxThreads) void k_gemv(GemmArgs a) {
+  gemv_body<WT, M, EPI, RW, U, false>(a, MergeArgs{}, blockIdx.x);
+}
+
+// The split merge of (row b / hq, query head b % hq) in a projection's launch: o = sum_s O_s
+// 2^(m_s - M) / sum_s l_s 2^(m_s - M) over the row's slots, as k_attn_merge combines them (HD/4
+// lanes per slot, 16-byte loads, each wave's slots across its lanes, the waves in LDS in fixed
+// order), in rounds of kMgPer slots per lane (one round for up to 128 slots from 4 waves).  o
+// goes out with device-scope stores; then every replica of the layer's counter is bumped (one
+// per lane of wave 0), also by the workgroups of rows whose attention wrote o directly.
+template <int HD>
+__device__ void merge_part(const MergeArgs& mg, const Plan* plan, float* o, int b) {
+  constexpr int LPS = HD / 4, SPW = 64 / LPS;
+  __shared__ float s_m[kGemvMaxThreads / 64], s_l[kGemvMaxThreads / 64];
+  __shared__ __align__(16) float s_o[kGemvMaxThreads / 64][HD];
+  const int nw = blockDim.x >> 6, spp = SPW * nw;
+  const int row = b / mg.hq, head = b - row * mg.hq;
+  const int v = threadIdx.x >> 6, l = threadIdx.x & 63;
+  const int d4 = l % LPS, sl = l / LPS;
+  const int kvh = head / mg.G, gi = head - kvh * mg.G;
+  const size_t ncols = (size_t)mg.max_rows * mg.G;
+  const size_t col = (size_t)row * mg.G + gi;
+  const int nwg = plan->row_nslots[row];
+  if (nwg > 1) {
+    float M = -INFINITY, L = 0.f;
+    f32x4 O = {0.f, 0.f, 0.f, 0.f};
+    for (int s0 = 0; s0 < nwg; s0 += kMgPer * spp) {
+      // every load of the round issued together; slots past the launch's bound re-read the
+      // last one, slots past the row's count are dropped below
+      float mv[kMgPer], lv[kMgPer];
+      f32x4 ov[kMgPer];
+#pragma unroll
+      for (int i = 0; i < kMgPer; ++i) {
+        const int slot = min(s0 + spp * i + SPW * v + sl, mg.nslots - 1);
+        const size_t sb = ((size_t)(kvh * kAttnMaxWG + slot)) * ncols + col;
+        const float2 ml = *(const float2*)(mg.ml + sb * 2);
+        mv[i] = ml.x;
+        lv[i] = ml.y;
+        ov[i] = *(const f32x4*)(mg.part + sb * HD + 4 * d4);
+      }
+#pragma unroll
+      for (int i = 0; i < kMgPer; ++i)
+        if (s0 + spp * i + SPW * v + sl >= nwg) {
+          mv[i] = -INFINITY;
+          lv[i] = 0.f;
+          ov[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+        }
+      float Mr = M;
+#pragma unroll
+      for (int i = 0; i < kMgPer; ++i) Mr = fmaxf(Mr, mv[i]);
+      Mr = wave_max(Mr);
+      if (Mr != -INFINITY) {  // wave-uniform
+        const float c = merge_exp2(M - Mr);  // earlier rounds (0 while M is -inf)
+        L *= c;
+        O *= c;
+#pragma unroll
+        for (int i = 0; i < kMgPer; ++i) {
+          const float f = merge_exp2(mv[i] - Mr);
+          L += lv[i] * f;
+          O += ov[i] * f;
+        }
+        M = Mr;
+      }
+    }
+    if constexpr (SPW == 4) {
+      L = sum_x16(L);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) O[q] = sum_x16(O[q]);
+    }
+    L = sum_x32(L);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) O[q] = sum_x32(O[q]);
+    if (l < LPS) *(f32x4*)&s_o[v][4 * d4] = O;
+    if (l == 0) {
+      s_m[v] = M;
+      s_l[v] = L;
+    }
+    __syncthreads();
+    if ((int)threadIdx.x < LPS) {  // wave 0
+      float Mt = -INFINITY;
+      for (int u = 0; u < nw; ++u) Mt = fmaxf(Mt, s_m[u]);
+      float Lt = 0.f;
+      f32x4 Ot = {0.f, 0.f, 0.f, 0.f};
+      for (int u = 0; u < nw; ++u) {
+        const float f = merge_exp2(s_m[u] - Mt);
+        Lt += s_l[u] * f;
+        Ot += *(const f32x4*)&s_o[u][4 * threadIdx.x] * f;
+      }
+      const __amdgpu_buffer_rsrc_t ro = dev_rsrc(o, mg.o_bytes);
+      st_dev16(ro, (uint32_t)((((size_t)row * mg.hq + head) * HD + 4 * threadIdx.x) * 4), Ot / Lt);
+    }
+  }
+  static_assert(kMgReplicas == 64, "one replica per lane of wave 0");
+  if (threadIdx.x < 64) {  // wave 0: its stores complete, then the arrival
+    wait_mem();
+    __hip_atomic_fetch_add(mg.cnt + threadIdx.x * kKsCntStride, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+}
+
+// A residual projection (VALU path, M rows) whose first mg.nwg workgroups merge the attention
+// splits that produce its activation rows (see MergeArgs).  The merge workgroups come first in
+// the grid, so they are dispatched before any projection workgroup waits for them.
+template <class WT, int M, int RW, int U>
+__global__ __launch_bounds__(kGemvMaxThreads) void k_gemv_merged(GemmArgs a, MergeArgs mg) {
+  if ((int)blockIdx.x < mg.nwg) {
+    if (mg.hd == 128)
+      merge_part<128>(mg, a.plan, const_cast<float*>(a.x), blockIdx.x);
+    else
+      merge_part<64>(mg, a.plan, const_cast<float*>(a.x), blockIdx.x);
+    return;
+  }
+  gemv_body<WT, M, EPI_RESID, RW, U, true>(a, mg, (int)blockIdx.x - mg.nwg);
 }
 
 // ----------------------------------------------------------------------------- MFMA GEMM
@@ -1339,20 +1506,25 @@ static hipError_t launch_gemv_u(int u, dim3 grid, dim3 block, const GemmArgs& a,
   return hipErrorInvalidValue;
 }
 
+// Threads of a VALU GEMV workgroup: a.gv_threads, else 256, or 512 for long rows (the down
+// projection) so each thread streams fewer chunks.  0: an invalid a.gv_threads.
+template <class WT>
+static unsigned gemv_threads(const GemmArgs& a, int rw, int rows) {
+  if (a.gv_threads > 0) {
+    if (a.gv_threads % 64 != 0 || a.gv_threads > kGemvMaxThreads || a.gv_threads < 64 * ((rw * rows + 63) / 64)) return 0;
+    return (unsigned)a.gv_threads;
+  }
+  return a.K / (16 / (int)sizeof(WT)) > 2048 ? kGemvMaxThreads : kGemmThreads;
+}
+
 template <class WT, int MODE>
 static hipError_t launch_epi(int epi, int rw, const GemmArgs& a, hipStream_t s) {
   const dim3 grid(a.n_groups);
   dim3 block(kGemmThreads);
   if constexpr (MODE <= 4) {
-    // threads: a.gv_threads, else 256, or 512 for long rows (the down projection) so each
-    // thread streams fewer chunks; chunks in flight per thread: a.gv_u, else 2
-    if (a.gv_threads > 0) {
-      if (a.gv_threads % 64 != 0 || a.gv_threads > kGemvMaxThreads || a.gv_threads < 64 * ((rw * MODE + 63) / 64))
-        return hipErrorInvalidValue;
-      block = dim3(a.gv_threads);
-    } else if (a.K / (16 / (int)sizeof(WT)) > 2048) {
-      block = dim3(kGemvMaxThreads);
-    }
+    // chunks in flight per thread: a.gv_u, else 2
+    block = dim3(gemv_threads<WT>(a, rw, MODE));
+    if (block.x == 0) return hipErrorInvalidValue;
     const int u = a.gv_u > 0 ? a.gv_u : 2;
     switch (epi) {
       case EPI_QKV:
@@ -1412,6 +1584,43 @@ static hipError_t launch_mode(int mode, int epi, int rw, const GemmArgs& a, hipS
     case 8: return launch_epi<WT, 8>(epi, rw, a, s);
     default: return hipErrorInvalidValue;
   }
+}
+
+template <class WT, int M, int RW>
+static hipError_t launch_merged_u(int u, dim3 grid, dim3 block, const GemmArgs& a, const MergeArgs& mg, hipStream_t s) {
+  switch (u) {
+#define LASER_MERGED_U(UU)                                                           \
+  case UU:                                                                           \
+    if constexpr (gemv_built<WT, M, EPI_RESID, RW, UU>())                            \
+      return launch_k(k_gemv_merged<WT, M, RW, UU>, grid, block, s, a, mg);          \
+    break;
+    LASER_MERGED_U(1)
+    LASER_MERGED_U(2)
+    LASER_MERGED_U(3)
+#undef LASER_MERGED_U
+  }
+  return hipErrorInvalidValue;
+}
+
+template <class WT, int M>
+static hipError_t launch_merged_rw(int rw, const GemmArgs& a, const MergeArgs& mg, hipStream_t s) {
+  const dim3 block(gemv_threads<WT>(a, rw, M));
+  if (block.x == 0) return hipErrorInvalidValue;
+  const dim3 grid(mg.nwg + a.n_groups);
+  const int u = a.gv_u > 0 ? a.gv_u : 2;
+  if (rw == 6) return launch_merged_u<WT, M, 6>(u, grid, block, a, mg, s);
+  if (rw == 7) return launch_merged_u<WT, M, 7>(u, grid, block, a, mg, s);
+  if (rw == 8) return launch_merged_u<WT, M, 8>(u, grid, block, a, mg, s);
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_gemv_merged(int dtype, int rw, const GemmArgs& a, const MergeArgs& mg, hipStream_t s) {
+  if (a.gain != nullptr || a.ksplit > 1 || a.row_map || a.M < 1 || a.M > 2 || mg.nwg != a.M * mg.hq ||
+      (mg.hd != 64 && mg.hd != 128) || mg.nslots < 1 || mg.nslots > kAttnMaxWG || mg.cnt == nullptr ||
+      a.ldx != mg.hq * mg.hd || (size_t)a.M * a.ldx * 4 > mg.o_bytes || a.K != a.ldx || mg.max_rows < a.M)
+    return hipErrorInvalidValue;
+  if (dtype == 1) return a.M == 1 ? launch_merged_rw<bf16_t, 1>(rw, a, mg, s) : launch_merged_rw<bf16_t, 2>(rw, a, mg, s);
+  return a.M == 1 ? launch_merged_rw<float, 1>(rw, a, mg, s) : launch_merged_rw<float, 2>(rw, a, mg, s);
 }
 
 hipError_t launch_gemm(int dtype, int mode, int epi, int rw, const GemmArgs& a, hipStream_t s) {

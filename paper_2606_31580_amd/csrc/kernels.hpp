@@ -69,6 +69,9 @@ struct PlanIO {
 // part of each array).
 struct alignas(16) Plan {  // (16-byte aligned arrays: k_plan_fetch copies 16-byte chunks)
   int M, n_groups, n_out, n_bt, n_items;
+  // split merge carried by the O-projection's launch: the value every layer's merge counter
+  // reaches once this forward's merge workgroups of that layer have stored their outputs
+  unsigned merge_target;
   PlanIO io;
   RowDesc rows[kMaxRows];
   int row_nslots[kMaxRows];  // attention partial slots of each row (over all its groups)
@@ -183,6 +186,25 @@ inline hipError_t launch_k(K kernel, dim3 grid, dim3 block, hipStream_t s, Args.
 // rw: rows per workgroup (VALU: QKV 6 or 8, residual 6, 7 or 8, others 8; MFMA: 16).
 hipError_t launch_gemm(int dtype, int mode, int epi, int rw, const GemmArgs& a, hipStream_t s);
 hipError_t launch_ksplit_reduce(const GemmArgs& a, hipStream_t s);
+
+// The attention split merge carried by the first workgroups of the O-projection's launch
+// (VALU path, 1-2 rows): merge workgroup b < nwg combines the partials of (row b / hq, head
+// b % hq) like k_attn_merge, stores o with device-scope stores and bumps the layer's counter;
+// the projection's workgroups issue their weight loads, wait (bounded) until the counter
+// reaches plan->merge_target, then read o with device-scope loads.  The counter only grows:
+// each forward adds nwg per layer and the host carries the running total in the plan.  The
+// counter has kMgReplicas copies (kKsCntStride apart), each merge workgroup bumps all of them
+// and projection workgroup g polls copy g mod kMgReplicas (7B shape, 512 projection
+// workgroups: the projection with the merge took 13.1-13.4 us with one copy, 11.5 us with 16).
+constexpr int kMgReplicas = 64;
+struct MergeArgs {
+  const float* part;  // attention partials [hkv][kAttnMaxWG][max_rows * G][hd]
+  const float* ml;    // their (m, l) pairs, same index
+  unsigned* cnt;      // this layer's counter replicas
+  uint32_t o_bytes;   // bytes of o (the projection's activation rows, GemmArgs::x)
+  int hq, G, hd, max_rows, nslots, nwg;  // nslots: bound on every row's slot count; nwg = M * hq
+};
+hipError_t launch_gemv_merged(int dtype, int rw, const GemmArgs& a, const MergeArgs& mg, hipStream_t s);
 // QKV of a wide forward (bf16 weights; a.M of 33 to 64 rows) over K slices of kQSliceSteps
 // 32-column steps, kQSliceGroups row groups per workgroup: partial sums per slice in qpart
 // [ceil(K / (32 kQSliceSteps))][M][N], the rows' sums of squares per slice in sqpart [slices][M],

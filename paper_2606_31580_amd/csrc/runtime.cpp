@@ -88,11 +88,16 @@ constexpr int kMaxPagesPerWave = LASER_ATTN_MAX_PPS;
 #define LASER_ATTN_FUSED_SPLITS 56
 #endif
 constexpr int kFusedMaxSplits = LASER_ATTN_FUSED_SPLITS;
+// The split merge runs in the O-projection's launch (mode 1) when the projection's weights
+// take at least this many bytes: their stream has to outlast the merge for the merge to be
+// hidden (7B shape, 25.7 MB: attention + O-proj 19.7 against 20.1 us per layer with the merge
+// kernel; 1.5B shape, 4.7 MB: 15.9 against 15.2 us).
+constexpr size_t kMergeMinOBytes = (size_t)16 << 20;
 
 struct Layout {
-  size_t rope, h, q, o, act, kpart, kcnt, qpart, sqpart, lm_part, attn_part, attn_ml, attn_cnt, plans, probe_p, tok_buf, p_buf,
-      total;
-  size_t attn_part_bytes, attn_ml_bytes, attn_cnt_bytes, kcnt_bytes;
+  size_t rope, h, q, o, act, kpart, kcnt, mcnt, qpart, sqpart, lm_part, attn_part, attn_ml, attn_cnt, plans, probe_p, tok_buf,
+      p_buf, total;
+  size_t attn_part_bytes, attn_ml_bytes, attn_cnt_bytes, kcnt_bytes, mcnt_bytes;
 };
 
 // Launch signature of a forward.  With the plan in its fixed device slot and the caller's
@@ -100,10 +105,11 @@ struct Layout {
 // its arguments, so one captured graph serves every forward with the same key.
 struct FwdKey {
   int M, n_out, agx, mslots, merge;  // agx: attention work items (grid width)
+  int mo;                              // the split merge runs in the O-projection's launch
   uint64_t kv_id;
   // same launches apart from the attention grid width
   bool same_shape(const FwdKey& o) const {
-    return M == o.M && n_out == o.n_out && mslots == o.mslots && merge == o.merge && kv_id == o.kv_id;
+    return M == o.M && n_out == o.n_out && mslots == o.mslots && merge == o.merge && mo == o.mo && kv_id == o.kv_id;
   }
 };
 
@@ -181,6 +187,14 @@ struct laser_model {
   // off by default: measured slower than the merge kernel at the 7B shape, batch 1)
   int attn_fuse = 0;
   int attn_fuse_max = kFusedMaxSplits;
+  // where the split merge of 1-2 row forwards runs (laser_model_set_oproj_merge): 0 the merge
+  // kernel, 1 the O-projection's launch when its weights hide the merge, 2 the O-projection's
+  // launch always; merge_cum: the value each layer's merge counter reaches once
+  // every forward launched so far has run; merge_resync: a forward failed after adding to it,
+  // so the counters are cleared before the next one
+  int oproj_merge = 1;
+  unsigned merge_cum = 0;
+  bool merge_resync = false;
   // laser_decode_step_static: this device's address of the static scratch array (resolved at
   // finalize) and a host plan buffer, so that the call allocates nothing
   void* static_scratch = nullptr;
@@ -414,6 +428,8 @@ static Layout make_layout(const laser_model_desc& d, int max_rows) {
   L.kpart = take((size_t)kMaxKsplit * max_rows * d.d_model * 4);  // K-share partials of O-proj / down
   L.kcnt_bytes = ks_cnt_bytes(d);
   L.kcnt = take(L.kcnt_bytes);  // their arrival counters (zero between kernels)
+  L.mcnt_bytes = (size_t)d.n_layers * kMgReplicas * kKsCntStride * 4;
+  L.mcnt = take(L.mcnt_bytes);  // merge counters of the O-projection's launch (replicas per layer)
   if (qkv_slices_fit(d, max_rows)) {  // K-slice partials of the QKV projection of wide forwards
     const size_t nsl = ceil_div(d.d_model, kQSliceSteps * 32);
     L.qpart = take(nsl * max_rows * (size_t)(d.n_q_heads + 2 * d.n_kv_heads) * hd * 4);
@@ -619,6 +635,7 @@ extern "C" laser_status laser_model_finalize(laser_model* m, int max_rows, void*
   HIP_TRY(hipMemcpyAsync(ws + L.rope, rope.data(), rope.size() * sizeof(float2), hipMemcpyHostToDevice, s));
   HIP_TRY(hipMemsetAsync(ws + L.attn_cnt, 0, L.attn_cnt_bytes, s));
   HIP_TRY(hipMemsetAsync(ws + L.kcnt, 0, L.kcnt_bytes, s));
+  HIP_TRY(hipMemsetAsync(ws + L.mcnt, 0, L.mcnt_bytes, s));
   HIP_TRY(hipStreamSynchronize(s));  // the host rope table goes out of scope
   m->static_plan = new (std::nothrow) Plan;
   if (static_scratch_address(m->device, &m->static_scratch) != LASER_OK) m->static_scratch = nullptr;
@@ -1113,6 +1130,7 @@ static void pad_items(Plan& p, int n) {
 struct Scratch {
   float *attn_part, *attn_ml, *kpart;
   unsigned* kcnt;  // K-share arrival counters
+  unsigned* mcnt;  // merge counters of the O-projection's launch (null: the merge kernel is used)
   float *qpart, *sqpart;  // QKV K-slice partials (null: that kernel is not used)
   unsigned* attn_cnt;
   LmPart* lm_part;
@@ -1127,6 +1145,7 @@ static Scratch workspace_scratch(const laser_model* m) {
                  m->wsp<float>(L.attn_ml),
                  m->wsp<float>(L.kpart),
                  m->wsp<unsigned>(L.kcnt),
+                 m->wsp<unsigned>(L.mcnt),
                  L.qpart ? m->wsp<float>(L.qpart) : nullptr,
                  L.sqpart ? m->wsp<float>(L.sqpart) : nullptr,
                  m->wsp<unsigned>(L.attn_cnt), m->wsp<LmPart>(L.lm_part), L.attn_part_bytes, L.attn_ml_bytes,
@@ -1155,7 +1174,31 @@ static laser_status run_forward(laser_model* m, laser_kv* kv, Plan& p, const Pla
   // while (the merge reads the row's own count)
   key.mslots = std::min(kAttnMaxWG, ceil_div(max_slots, 8) * 8);
   key.merge = merge;
+  const laser_model_desc& d = m->desc;
+  key.mo = merge && sc.mcnt != nullptr && p.M <= kValuMaxRows && (d.head_dim == 64 || d.head_dim == 128) &&
+           (m->oproj_merge == 2 ||
+            (m->oproj_merge == 1 && (size_t)d.d_model * d.n_q_heads * d.head_dim * m->es >= kMergeMinOBytes));
   key.kv_id = kv->id;
+  // The merge in the O-projection's launch: every layer's counter grows by the forward's
+  // merge workgroups, and the O-projection waits for the running total.  After a forward that
+  // failed part way the counters no longer match it, so they are cleared first.
+  struct Resync {
+    laser_model* m;
+    bool armed;
+    ~Resync() {
+      if (armed) m->merge_resync = true;
+    }
+  } resync{m, false};
+  if (key.mo) {
+    if (m->merge_resync) {
+      HIP_TRY(launch_fill_u32(sc.mcnt, (int)(m->lay.mcnt_bytes / 4), 0u, s));
+      m->merge_cum = 0;
+      m->merge_resync = false;
+    }
+    m->merge_cum += (unsigned)(p.M * d.n_q_heads);
+    resync.armed = true;
+  }
+  p.merge_target = m->merge_cum;
   // The attention grid is at least the item count, a multiple of 8 (so that item i runs on
   // XCD i mod 8), padded with empty items.  A captured forward of the same shape whose grid
   // is at most 1/4 (+8) wider is reused; a new one is captured 1/8 wider, so a growing
@@ -1180,6 +1223,7 @@ static laser_status run_forward(laser_model* m, laser_kv* kv, Plan& p, const Pla
       TimingScope scope(m);
       st = launch_forward(m, kv, key, s, sc, hp);
     }
+    resync.armed = resync.armed && st != LASER_OK;
     const laser_status sd = staged_done(m, slot, s);
     return st != LASER_OK ? st : sd;
   }
@@ -1242,6 +1286,7 @@ static laser_status run_forward(laser_model* m, laser_kv* kv, Plan& p, const Pla
     HIP_TRY(hipEventRecord(ge->done, s));
     ge->unrecorded = 0;
   }
+  resync.armed = false;
   return staged_done(m, slot, s);
 }
 
@@ -1282,7 +1327,10 @@ static laser_status launch_forward(laser_model* m, laser_kv* kv, const FwdKey& k
 
   // rows: output rows of the projection (SwiGLU: gate and up rows together)
   // tile: the projection's tile-order weights (used on the MFMA path when tiles are on)
-  auto gemm = [&](int cls, int epi, GemmArgs a, int K, int N, int rows, int M, const char* tile) -> laser_status {
+  // mg: the split merge that produces the activation rows runs in this launch (residual
+  // projection, VALU path)
+  auto gemm = [&](int cls, int epi, GemmArgs a, int K, int N, int rows, int M, const char* tile,
+                  const MergeArgs* mg = nullptr) -> laser_status {
     int rw = proj_rw(epi, rows, M, m->cus);
     if (epi == EPI_QKV && gemv_short_rows(K, (int)m->es, M)) rw = qkv_short_rw(rows, m->cus, rw);
     a.K = K;
@@ -1310,6 +1358,11 @@ static laser_status launch_forward(laser_model* m, laser_kv* kv, const FwdKey& k
       return LASER_OK;
     }
     const int mode = gemm_mode(M);
+    if (mg != nullptr) {
+      if (epi != EPI_RESID || mode > kValuMaxRows) return laser_fail(LASER_ERR_STATE, "merged projection off the VALU path");
+      HIP_TRY(timed(m, cls, s, [&] { return launch_gemv_merged(dt, rw, a, *mg, s); }));
+      return LASER_OK;
+    }
     HIP_TRY(timed(m, cls, s, [&] {
       hipError_t e = launch_gemm(dt, mode, epi, rw, a, s);
       if (e == hipSuccess && a.ksplit > 1 && a.kcnt == nullptr) e = launch_ksplit_reduce(a, s);
@@ -1360,7 +1413,7 @@ static laser_status launch_forward(laser_model* m, laser_kv* kv, const FwdKey& k
     aa.layer = li;
     HIP_TRY(timed(m, LASER_K_ATTN, s, [&] {
       hipError_t e = launch_attn(m->kv_fp8 ? 2 : dt, hd, aa, agrid, s);
-      if (e == hipSuccess && key.merge) e = launch_attn_merge(aa, key.M, hd, key.mslots, s);
+      if (e == hipSuccess && key.merge && !key.mo) e = launch_attn_merge(aa, key.M, hd, key.mslots, s);
       return e;
     }));
 
@@ -1369,7 +1422,21 @@ static laser_status launch_forward(laser_model* m, laser_kv* kv, const FwdKey& k
     a.x = m->wsp<float>(L.o);
     a.ldx = d.n_q_heads * hd;
     a.gain = nullptr;
-    st = gemm(LASER_K_OPROJ, EPI_RESID, a, d.n_q_heads * hd, d.d_model, d.d_model, key.M, T ? T->o : nullptr);
+    MergeArgs mg{};
+    if (key.mo) {
+      mg.part = aa.part;
+      mg.ml = aa.ml;
+      mg.cnt = sc.mcnt + (size_t)li * kMgReplicas * kKsCntStride;
+      mg.o_bytes = (uint32_t)((size_t)key.M * d.n_q_heads * hd * 4);
+      mg.hq = d.n_q_heads;
+      mg.G = G;
+      mg.hd = hd;
+      mg.max_rows = sc.rows;
+      mg.nslots = key.mslots;
+      mg.nwg = key.M * d.n_q_heads;
+    }
+    st = gemm(LASER_K_OPROJ, EPI_RESID, a, d.n_q_heads * hd, d.d_model, d.d_model, key.M, T ? T->o : nullptr,
+              key.mo ? &mg : nullptr);
     if (st != LASER_OK) return st;
 
     a = base;
@@ -1554,7 +1621,7 @@ extern "C" laser_status laser_decode_step_static(laser_model* m, laser_kv* kv, i
                       off, kStaticScratchBytes);
   char* base = (char*)m->static_scratch;
   const Scratch sc{(float*)(base + o_part), (float*)(base + o_ml), (float*)(base + o_kpart), (unsigned*)(base + o_kcnt),
-                   nullptr, nullptr,
+                   nullptr /* the merge kernel */, nullptr, nullptr,
                    (unsigned*)(base + o_cnt), (LmPart*)(base + o_lm), part_bytes, ml_bytes, batch};
   std::vector<int> seqs(seq_ids, seq_ids + batch), grow(batch, 1);
   st = check_growth(m, kv, seqs, grow);
@@ -1913,6 +1980,13 @@ extern "C" laser_status laser_model_set_attn_merge(laser_model* m, int fused, in
     return laser_fail(LASER_ERR_INVALID_ARG, "fused must be 0 or 1 and max_splits in [2, %d]", kAttnMaxWG);
   m->attn_fuse = fused;
   m->attn_fuse_max = max_splits;
+  return LASER_OK;
+}
+
+extern "C" laser_status laser_model_set_oproj_merge(laser_model* m, int mode) {
+  if (!model_of(m)) return laser_fail(LASER_ERR_STATE, "invalid or destroyed model");
+  if (mode < 0 || mode > 2) return laser_fail(LASER_ERR_INVALID_ARG, "mode must be 0, 1 or 2");
+  m->oproj_merge = mode;  // (captured forwards are keyed on where the merge runs)
   return LASER_OK;
 }
 

@@ -116,6 +116,7 @@ _SIGS = {
     "laser_model_set_graphs": (_I, [_P, _I]),
     "laser_model_set_gemm_kernel": (_I, [_P, _I]),
     "laser_model_set_attn_merge": (_I, [_P, _I, _I]),
+    "laser_model_set_oproj_merge": (_I, [_P, _I]),
     "laser_model_graph_stats": (_I, [_P, C.POINTER(C.c_longlong), C.POINTER(C.c_int)]),
     "laser_model_tile_bytes": (_I, [_P, C.POINTER(C.c_size_t)]),
     "laser_model_set_tiles": (_I, [_P, _P, C.c_size_t, _P]),
@@ -313,6 +314,11 @@ class Model:
     def set_attn_merge(self, fused: bool, max_splits: int = 56):
         """One-row attention groups merged inside the attention kernel (fused) or by the merge kernel (default)."""
         _call("laser_model_set_attn_merge", self.h, int(fused), int(max_splits))
+
+    def set_oproj_merge(self, mode: int):
+        """Where the split merge of 1-2 row forwards runs: 0 the merge kernel, 1 (default) the
+        O-projection's launch for projections of at least 16 MiB of weights, 2 that launch always."""
+        _call("laser_model_set_oproj_merge", self.h, int(mode))
 
     def set_gemm_kernel(self, mode: int):
         """Matrix-core projection kernel: 0 by cost (default), 1 K-split waves, 2 row waves."""
