@@ -9,7 +9,8 @@ other, and the appended K/V agree to one rounding step of their largest values. 
 of two requests, replayed graphs, and switching back and forth on one model (the merge
 counters keep counting across forwards that do not use them).  Oracle parity of the default
 path is covered by the end-to-end tests.  Shapes: tiny (fp32, head dim 64), 1.5B (3-wave
-projection workgroups, one round of partials for 96 splits), 7B (4 waves, up to 112 splits).
+projection workgroups, one round of partials for 96 splits), 7B (4 waves, up to 112 splits,
+GQA group 7), 8B (group 4; the default takes this path there too).
 """
 import numpy as np
 import pytest
@@ -18,7 +19,7 @@ import torch
 from gpu_helpers import export_seq, require_gpu
 from paper_2606_31580_amd import laser as L
 from paper_2606_31580_amd import synth
-from paper_2606_31580_amd.configs import QWEN_1P5B, QWEN_7B, TINY
+from paper_2606_31580_amd.configs import LLAMA_8B, QWEN_1P5B, QWEN_7B, TINY
 
 pytestmark = pytest.mark.gpu
 
@@ -92,3 +93,7 @@ def test_oproj_merge_1p5b():
 
 def test_oproj_merge_7b():
     _run(QWEN_7B, [14336, 3000], [[0], [1, 0]], 3, 2e-3)
+
+
+def test_oproj_merge_8b():
+    _run(LLAMA_8B, [6000, 1500], [[0], [0, 1]], 2, 2e-3)
