@@ -92,7 +92,9 @@ def test_oproj_merge_1p5b():
 
 
 def test_oproj_merge_7b():
-    _run(QWEN_7B, [14336, 3000], [[0], [1, 0]], 3, 2e-3)
+    # request 2 (24 positions) fits one attention workgroup, whose output needs no merge: its
+    # merge workgroups only count their arrival, beside request 0's 112 splits
+    _run(QWEN_7B, [14336, 3000, 24], [[0], [1, 0], [2, 0]], 3, 2e-3)
 
 
 def test_oproj_merge_8b():
